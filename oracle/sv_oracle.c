@@ -1,0 +1,567 @@
+/*
+ * sv_oracle.c -- CPU test oracle: seeded synthesis, candidate derivation and
+ * the elementwise check of Eq. (1) with its report.
+ *
+ * TEST INFRASTRUCTURE ONLY (see sv_oracle.h).  Plain serial C, one element at
+ * a time, no vectorisation, no blocking, no threads.  Built with
+ * -O2 -ffp-contract=off so that every float operation written below is one
+ * IEEE-754 operation rounded to nearest-even, exactly as written.
+ *
+ * What the paper fixes and what this file adds:
+ *  - Sec. 4.2.1, Eq. (1): V = I[ |K(x) - y| <= atol + rtol*|y| ], rtol scaling
+ *    the magnitude of the reference y.  or_compare() evaluates it per element.
+ *  - Sec. 4.2.1 asks for test inputs drawn from a broad numeric range (a
+ *    Gaussian with mean 5 and standard deviation 10 is its example); that is
+ *    the normal distribution with explicit mean and std below.
+ *  - The generator, the word-to-element mapping and the transforms are not in
+ *    the paper (it names only "standard numerical libraries").  They follow the
+ *    conventions recorded in the design notes: Philox4x32-10 (Salmon, Moraes,
+ *    Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11) keyed
+ *    by the seed with counter (block, stream); uniform from the top 24 bits;
+ *    Box-Muller (1958) with ln, sin and cos written as fixed sequences of fp32
+ *    operations (Taylor series whose coefficients are the fp32 roundings of
+ *    exact rationals and powers of pi/2 over factorials); Lemire's
+ *    multiply-shift for integer ranges; a class-threshold mix for special values.
+ */
+#include "sv_oracle.h"
+
+#include <math.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------- */
+/* Bit views                                                                  */
+/* ------------------------------------------------------------------------- */
+static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+
+/* ------------------------------------------------------------------------- */
+/* Philox4x32-10 (Salmon et al., SC'11).                                      */
+/* One round multiplies counter words 0 and 2 by the two round multipliers;   */
+/* the high halves are mixed with the other two words and the round key, the  */
+/* low halves pass through.  The key is bumped by the two Weyl constants      */
+/* (golden ratio and sqrt(3)-1, scaled by 2^32) between rounds.               */
+/* ------------------------------------------------------------------------- */
+#define PHILOX_M0 0xD2511F53u
+#define PHILOX_M1 0xCD9E8D57u
+#define PHILOX_W0 0x9E3779B9u
+#define PHILOX_W1 0xBB67AE85u
+
+void or_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; round++) {
+    if (round > 0) {
+      k0 += PHILOX_W0;
+      k1 += PHILOX_W1;
+    }
+    uint64_t p0 = (uint64_t)PHILOX_M0 * (uint64_t)x0;
+    uint64_t p1 = (uint64_t)PHILOX_M1 * (uint64_t)x2;
+    uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+    uint32_t y1 = (uint32_t)p1;
+    uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+    uint32_t y3 = (uint32_t)p0;
+    x0 = y0; x1 = y1; x2 = y2; x3 = y3;
+  }
+  out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+/* key = (low, high) words of the seed; counter = (low, high) words of the
+ * block index c followed by (low, high) words of the substream id. */
+void or_philox_block(uint64_t seed, uint64_t stream, uint64_t c, uint32_t out[4]) {
+  uint32_t ctr[4] = {(uint32_t)c, (uint32_t)(c >> 32), (uint32_t)stream, (uint32_t)(stream >> 32)};
+  uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  or_philox4x32_10(ctr, key, out);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Natural logarithm for positive normal fp32 x.                              */
+/* x = 2^e * m with m in [sqrt(1/2), sqrt(2)); with s = (m-1)/(m+1),          */
+/* ln m = 2 atanh(s) = 2s + 2s^3/3 + 2s^5/5 + 2s^7/7 + 2s^9/9 + ...           */
+/* (|s| <= 0.1716, so the first omitted term is below 2e-9 relative).         */
+/* ln x = e*ln2_hi + (ln m + e*ln2_lo), with ln2_hi = ln 2 rounded to 16 bits */
+/* (so e*ln2_hi is exact for |e| < 2^8) and ln2_lo = fp32(ln 2 - ln2_hi).     */
+/* ------------------------------------------------------------------------- */
+static const float LN_SQRT2 = 0x1.6a09e6p+0f;      /* fp32(sqrt 2)                */
+static const float LN_C3 = 0x1.555556p-1f;         /* fp32(2/3)                   */
+static const float LN_C5 = 0x1.99999ap-2f;         /* fp32(2/5)                   */
+static const float LN_C7 = 0x1.24924ap-2f;         /* fp32(2/7)                   */
+static const float LN_C9 = 0x1.c71c72p-3f;         /* fp32(2/9)                   */
+static const float LN2_HI = 0x1.62e4p-1f;          /* 45426 / 2^16                */
+static const float LN2_LO = 0x1.7f7d1cp-20f;       /* fp32(ln 2 - 45426 / 2^16)   */
+
+float or_ln_f32(float x) {
+  uint32_t bits = f2u(x);
+  int e = (int)((bits >> 23) & 0xFFu) - 127;
+  float m = u2f((bits & 0x007FFFFFu) | 0x3F800000u); /* m in [1, 2) */
+  if (m > LN_SQRT2) {
+    m = m * 0.5f;                                    /* exact */
+    e = e + 1;
+  }
+  float f = m - 1.0f;                                /* exact (Sterbenz) */
+  float den = 2.0f + f;
+  float s = f / den;
+  float z = s * s;
+  float poly = LN_C9;
+  poly = LN_C7 + z * poly;
+  poly = LN_C5 + z * poly;
+  poly = LN_C3 + z * poly;
+  poly = 2.0f + z * poly;
+  float ln_m = s * poly;
+  float ef = (float)e;
+  float hi = ef * LN2_HI;
+  float lo = ef * LN2_LO;
+  return hi + (ln_m + lo);
+}
+
+/* ------------------------------------------------------------------------- */
+/* sin and cos of the angle 2*pi*j/2^24, j < 2^24.                            */
+/* The angle is (pi/2)(q + f) with quadrant q = j >> 22 and f = (j mod 2^22)  */
+/* / 2^22, both exact.  S(f) = sin(pi f/2) and C(f) = cos(pi f/2) come from   */
+/* Taylor series in f with coefficients (-1)^k (pi/2)^n / n! rounded to fp32; */
+/* for f > 1/2 the complement g = 1 - f (exact) is used instead, since        */
+/* sin(pi f/2) = cos(pi g/2), so that both series run on f in [0, 1/2] and    */
+/* keep relative accuracy near the zeros.  The quadrant then rotates (S, C).  */
+/* ------------------------------------------------------------------------- */
+static const float SIN_1 = 0x1.921fb6p+0f;    /*  (pi/2)^1 / 1!  */
+static const float SIN_3 = -0x1.4abbcep-1f;   /* -(pi/2)^3 / 3!  */
+static const float SIN_5 = 0x1.466bc6p-4f;    /*  (pi/2)^5 / 5!  */
+static const float SIN_7 = -0x1.32d2ccp-8f;   /* -(pi/2)^7 / 7!  */
+static const float SIN_9 = 0x1.507834p-13f;   /*  (pi/2)^9 / 9!  */
+static const float COS_2 = -0x1.3bd3ccp+0f;   /* -(pi/2)^2 / 2!  */
+static const float COS_4 = 0x1.03c1f0p-2f;    /*  (pi/2)^4 / 4!  */
+static const float COS_6 = -0x1.55d3c8p-6f;   /* -(pi/2)^6 / 6!  */
+static const float COS_8 = 0x1.e1f506p-11f;   /*  (pi/2)^8 / 8!  */
+static const float COS_10 = -0x1.a6d1f2p-16f; /* -(pi/2)^10 / 10! */
+
+static float sin_quarter(float f) {   /* sin(pi f / 2), f in [0, 1/2] */
+  float f2 = f * f;
+  float p = SIN_9;
+  p = SIN_7 + f2 * p;
+  p = SIN_5 + f2 * p;
+  p = SIN_3 + f2 * p;
+  p = SIN_1 + f2 * p;
+  return f * p;
+}
+
+static float cos_quarter(float f) {   /* cos(pi f / 2), f in [0, 1/2] */
+  float f2 = f * f;
+  float p = COS_10;
+  p = COS_8 + f2 * p;
+  p = COS_6 + f2 * p;
+  p = COS_4 + f2 * p;
+  p = COS_2 + f2 * p;
+  return 1.0f + f2 * p;
+}
+
+void or_sincos_2pi_f32(uint32_t j24, float *s_out, float *c_out) {
+  uint32_t j = j24 & 0x00FFFFFFu;
+  uint32_t q = j >> 22;
+  uint32_t fj = j & 0x003FFFFFu;
+  float S, C;
+  if (fj <= 0x00200000u) {
+    float f = (float)fj * 0x1p-22f;
+    S = sin_quarter(f);
+    C = cos_quarter(f);
+  } else {
+    float g = (float)(0x00400000u - fj) * 0x1p-22f;
+    S = cos_quarter(g);
+    C = sin_quarter(g);
+  }
+  float s, c;
+  if (q == 0) { s = S; c = C; }
+  else if (q == 1) { s = C; c = -S; }
+  else if (q == 2) { s = -S; c = -C; }
+  else { s = -C; c = S; }
+  *s_out = s;
+  *c_out = c;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Box-Muller: u1 = ((wa >> 8) + 1) 2^-24 in (0, 1], u2 = (wb >> 8) 2^-24 in  */
+/* [0, 1); r = sqrt(-2 ln u1); z_cos = r cos(2 pi u2), z_sin = r sin(2 pi u2) */
+/* ------------------------------------------------------------------------- */
+void or_box_muller_f32(uint32_t wa, uint32_t wb, float *zc, float *zs) {
+  float u1 = (float)((wa >> 8) + 1u) * 0x1p-24f;
+  float lnu = or_ln_f32(u1);
+  float r = sqrtf(-2.0f * lnu);
+  float s, c;
+  or_sincos_2pi_f32(wb >> 8, &s, &c);
+  *zc = r * c;
+  *zs = r * s;
+}
+
+/* ------------------------------------------------------------------------- */
+/* fp32 -> bf16, round to nearest even; NaN stays NaN (quiet bit forced).     */
+/* ------------------------------------------------------------------------- */
+uint16_t or_bf16_rne(uint32_t x) {
+  if ((x & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((x >> 16) | 0x0040u);
+  uint32_t lsb = (x >> 16) & 1u;
+  return (uint16_t)((x + 0x7FFFu + lsb) >> 16);
+}
+
+static float bf16_to_f32(uint16_t h) { return u2f((uint32_t)h << 16); }
+
+/* ------------------------------------------------------------------------- */
+/* One step to the next representable value up (up != 0) or down.            */
+/* ------------------------------------------------------------------------- */
+uint32_t or_next_f32(uint32_t x, int up) {
+  uint32_t mag = x & 0x7FFFFFFFu;
+  if (mag > 0x7F800000u) return x;                          /* NaN */
+  if (mag == 0) return up ? 0x00000001u : 0x80000001u;      /* +-0 */
+  if (x == 0x7F800000u && up) return x;                     /* +Inf up */
+  if (x == 0xFF800000u && !up) return x;                    /* -Inf down */
+  int neg = (int)(x >> 31);
+  return (up != neg) ? x + 1u : x - 1u;   /* magnitude grows when moving away from 0 */
+}
+
+uint16_t or_next_bf16(uint16_t x, int up) {
+  uint16_t mag = x & 0x7FFFu;
+  if (mag > 0x7F80u) return x;
+  if (mag == 0) return up ? (uint16_t)0x0001u : (uint16_t)0x8001u;
+  if (x == 0x7F80u && up) return x;
+  if (x == 0xFF80u && !up) return x;
+  int neg = (int)(x >> 15);
+  return (uint16_t)((up != neg) ? x + 1u : x - 1u);
+}
+
+/* Array forms, one call per element. */
+void or_philox_blocks(uint64_t seed, uint64_t stream, uint64_t c0, uint64_t n, uint32_t *out) {
+  for (uint64_t k = 0; k < n; k++) or_philox_block(seed, stream, c0 + k, out + 4 * k);
+}
+
+void or_ln_f32_n(const float *x, float *y, uint64_t n) {
+  for (uint64_t k = 0; k < n; k++) y[k] = or_ln_f32(x[k]);
+}
+
+void or_sincos_2pi_f32_n(const uint32_t *j24, float *s, float *c, uint64_t n) {
+  for (uint64_t k = 0; k < n; k++) or_sincos_2pi_f32(j24[k], &s[k], &c[k]);
+}
+
+void or_bf16_rne_n(const uint32_t *x, uint16_t *y, uint64_t n) {
+  for (uint64_t k = 0; k < n; k++) y[k] = or_bf16_rne(x[k]);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Synthesis                                                                  */
+/* ------------------------------------------------------------------------- */
+typedef struct {
+  float a, span;           /* uniform: a + span * U                      */
+  float mean, std;         /* normal                                     */
+  int64_t lo;              /* integer range                              */
+  uint64_t range;          /* hi - lo + 1                                */
+  uint64_t t_nan, t_inf, t_den, t_zero;   /* cumulative class thresholds */
+} prepared;
+
+static uint64_t width32(double p) { return (uint64_t)floor(p * 4294967296.0); }
+
+static int prepare(int32_t dtype, int32_t dist, const or_dist_params *p, prepared *q) {
+  memset(q, 0, sizeof(*q));
+  if (dtype != OR_F32 && dtype != OR_BF16 && dtype != OR_I32) return -2;
+  if (!p) return -1;
+  switch (dist) {
+  case OR_UNIFORM: {
+    if (dtype == OR_I32) return -2;
+    float a = (float)p->a, b = (float)p->b;
+    float span = b - a;
+    if (!(a < b) || isinf(a) || isinf(b) || isinf(span)) return -1;
+    q->a = a;
+    q->span = span;
+    return 0;
+  }
+  case OR_NORMAL:
+  case OR_SPECIAL: {
+    if (dtype == OR_I32) return -2;
+    q->mean = (float)p->mean;
+    q->std = (float)p->std;
+    if (!isfinite(q->mean) || !isfinite(q->std) || !(q->std >= 0.0f)) return -1;
+    if (dist == OR_SPECIAL) {
+      double ps[4] = {p->p_nan, p->p_inf, p->p_denorm, p->p_zero};
+      double tot = 0.0;
+      for (int k = 0; k < 4; k++) {
+        if (!(ps[k] >= 0.0 && ps[k] <= 1.0)) return -1;
+        tot += ps[k];
+      }
+      if (!(tot <= 1.0)) return -1;
+      q->t_nan = width32(p->p_nan);
+      q->t_inf = q->t_nan + width32(p->p_inf);
+      q->t_den = q->t_inf + width32(p->p_denorm);
+      q->t_zero = q->t_den + width32(p->p_zero);
+    }
+    return 0;
+  }
+  case OR_INT_RANGE:
+    if (dtype != OR_I32) return -2;
+    if (p->lo > p->hi || p->lo < INT32_MIN || p->hi > INT32_MAX) return -1;
+    q->lo = p->lo;
+    q->range = (uint64_t)(p->hi - p->lo) + 1u;
+    return 0;
+  default:
+    return -2;
+  }
+}
+
+/* Value of element i as fp32 bits (UNIFORM, NORMAL, SPECIAL) or int32 bits. */
+static uint32_t element_bits(uint64_t seed, uint64_t stream, int32_t dist,
+                             const prepared *q, uint64_t i) {
+  uint32_t w[4];
+  if (dist == OR_UNIFORM) {
+    /* four elements per block: element i takes word i mod 4 of block i / 4 */
+    or_philox_block(seed, stream, i / 4u, w);
+    float U = (float)(w[i % 4u] >> 8) * 0x1p-24f;
+    float t = q->span * U;
+    return f2u(q->a + t);
+  }
+  if (dist == OR_NORMAL) {
+    /* words (w0, w1) give elements 4c (cos) and 4c+1 (sin); (w2, w3) give
+     * elements 4c+2 (cos) and 4c+3 (sin) */
+    or_philox_block(seed, stream, i / 4u, w);
+    unsigned pair = (unsigned)((i % 4u) / 2u);
+    float zc, zs;
+    or_box_muller_f32(w[2 * pair], w[2 * pair + 1], &zc, &zs);
+    float z = (i % 2u == 0u) ? zc : zs;
+    float t = q->std * z;
+    return f2u(q->mean + t);
+  }
+  if (dist == OR_INT_RANGE) {
+    /* two elements per block: R = (w1:w0) for even i, (w3:w2) for odd i;
+     * value = lo + floor(R * range / 2^64) (Lemire's multiply-shift) */
+    or_philox_block(seed, stream, i / 2u, w);
+    unsigned h = (unsigned)(i % 2u);
+    uint64_t R = ((uint64_t)w[2 * h + 1] << 32) | (uint64_t)w[2 * h];
+    unsigned __int128 prod = (unsigned __int128)R * (unsigned __int128)q->range;
+    int64_t v = q->lo + (int64_t)(uint64_t)(prod >> 64);
+    return (uint32_t)(int32_t)v;
+  }
+  /* SPECIAL: one element per block.  w0 picks the class against cumulative
+   * thresholds in the order NaN, Inf, denormal, zero, normal; w1 supplies the
+   * sign and the payload / mantissa; (w2, w3) feed Box-Muller, cos branch. */
+  or_philox_block(seed, stream, i, w);
+  uint32_t sign = w[1] & 0x80000000u;
+  uint64_t x = w[0];
+  if (x < q->t_nan) return sign | 0x7FC00000u | (w[1] & 0x003FFFFFu);
+  if (x < q->t_inf) return sign | 0x7F800000u;
+  if (x < q->t_den) {
+    uint32_t m = w[1] & 0x007FFFFFu;
+    return sign | (m ? m : 1u);
+  }
+  if (x < q->t_zero) return sign;
+  float zc, zs;
+  or_box_muller_f32(w[2], w[3], &zc, &zs);
+  float t = q->std * zc;
+  return f2u(q->mean + t);
+}
+
+static void store(int32_t dtype, void *out, uint64_t k, uint32_t bits) {
+  if (dtype == OR_BF16)
+    ((uint16_t *)out)[k] = or_bf16_rne(bits);
+  else
+    ((uint32_t *)out)[k] = bits;
+}
+
+int or_synth(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
+             const or_dist_params *p, uint64_t offset, uint64_t n, void *out) {
+  prepared q;
+  int rc = prepare(dtype, dist, p, &q);
+  if (rc) return rc;
+  if (n && !out) return -1;
+  for (uint64_t k = 0; k < n; k++)
+    store(dtype, out, k, element_bits(seed, stream, dist, &q, offset + k));
+  return 0;
+}
+
+int or_synth_at(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
+                const or_dist_params *p, const uint64_t *idx, uint64_t n, void *out) {
+  prepared q;
+  int rc = prepare(dtype, dist, p, &q);
+  if (rc) return rc;
+  if (n && (!out || !idx)) return -1;
+  for (uint64_t k = 0; k < n; k++)
+    store(dtype, out, k, element_bits(seed, stream, dist, &q, idx[k]));
+  return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Candidate derivation                                                       */
+/* ------------------------------------------------------------------------- */
+static uint32_t load_bits(int32_t dtype, const void *a, uint64_t k) {
+  return dtype == OR_BF16 ? (uint32_t)((const uint16_t *)a)[k] : ((const uint32_t *)a)[k];
+}
+
+static void store_bits(int32_t dtype, void *a, uint64_t k, uint32_t bits) {
+  if (dtype == OR_BF16)
+    ((uint16_t *)a)[k] = (uint16_t)bits;
+  else
+    ((uint32_t *)a)[k] = bits;
+}
+
+/* value of a float-typed element as fp32 (bf16 widens exactly) */
+static float as_f32(int32_t dtype, uint32_t bits) {
+  return dtype == OR_BF16 ? bf16_to_f32((uint16_t)bits) : u2f(bits);
+}
+
+/* fp32 result back to the element format */
+static uint32_t from_f32(int32_t dtype, float v) {
+  return dtype == OR_BF16 ? (uint32_t)or_bf16_rne(f2u(v)) : f2u(v);
+}
+
+static uint32_t perturb_element(uint64_t seed, uint64_t stream, int32_t dtype,
+                                const or_perturb_plan *plan, uint64_t i, uint32_t b) {
+  if (plan->op == OR_OP_COPY) return b;
+  /* one Philox block per element: w0 selects (w0 < floor(p 2^32)), the top
+   * bit of w1 chooses the direction, w1 gives the NaN payload mask, the top
+   * 24 bits of w2 give the uniform variate of SCALE */
+  uint32_t w[4];
+  or_philox_block(seed, stream, i, w);
+  if (!((uint64_t)w[0] < width32(plan->p))) return b;
+  int up = (int)(w[1] >> 31);
+  if (plan->op == OR_OP_ULP)
+    return dtype == OR_BF16 ? (uint32_t)or_next_bf16((uint16_t)b, up) : or_next_f32(b, up);
+  if (plan->op == OR_OP_SCALE) {
+    float U = (float)(w[2] >> 8) * 0x1p-24f;
+    float amp = (float)plan->value;
+    float two_amp = 2.0f * amp;
+    float t = two_amp * U;
+    float u = t - amp;
+    float s = 1.0f + u;
+    return from_f32(dtype, as_f32(dtype, b) * s);
+  }
+  /* SPECIAL_FLIP: zeros change sign, NaNs get their payload XOR-ed with a
+   * nonzero mask below the quiet bit; everything else is left alone */
+  if (dtype == OR_BF16) {
+    uint32_t mag = b & 0x7FFFu;
+    if (mag == 0) return b ^ 0x8000u;
+    if (mag > 0x7F80u) {
+      uint32_t m = w[1] & 0x003Fu;
+      return b ^ (m ? m : 1u);
+    }
+    return b;
+  }
+  uint32_t mag = b & 0x7FFFFFFFu;
+  if (mag == 0) return b ^ 0x80000000u;
+  if (mag > 0x7F800000u) {
+    uint32_t m = w[1] & 0x003FFFFFu;
+    return b ^ (m ? m : 1u);
+  }
+  return b;
+}
+
+static uint32_t index_op(int32_t dtype, const or_perturb_plan *plan, uint32_t b) {
+  if (plan->op == OR_OP_SET_AT)
+    return dtype == OR_BF16 ? (plan->bits & 0xFFFFu) : plan->bits;
+  if (plan->op == OR_OP_ADD_AT) {
+    float v = (float)plan->value;
+    return from_f32(dtype, as_f32(dtype, b) + v);
+  }
+  /* FAULT_AT */
+  if (dtype == OR_I32) return b + 1u;
+  float x = as_f32(dtype, b);
+  float t = 1.0f + fabsf(x);
+  return from_f32(dtype, x + t);
+}
+
+int or_perturb(uint64_t seed, uint64_t stream, int32_t dtype,
+               const or_perturb_plan *plan, uint64_t offset, uint64_t n,
+               const void *ref, void *cand) {
+  if (!plan) return -1;
+  if (dtype != OR_F32 && dtype != OR_BF16 && dtype != OR_I32) return -2;
+  if (n && (!ref || !cand)) return -1;
+  int op = plan->op;
+  if (op < OR_OP_COPY || op > OR_OP_FAULT_AT) return -2;
+  if (dtype == OR_I32 && op != OR_OP_COPY && op != OR_OP_SET_AT && op != OR_OP_FAULT_AT) return -2;
+  if (op <= OR_OP_SPECIAL_FLIP) {
+    if (op != OR_OP_COPY && !(plan->p >= 0.0 && plan->p <= 1.0)) return -1;
+    for (uint64_t k = 0; k < n; k++)
+      store_bits(dtype, cand, k,
+                 perturb_element(seed, stream, dtype, plan, offset + k, load_bits(dtype, ref, k)));
+    return 0;
+  }
+  if (plan->nidx && !plan->idx) return -1;
+  for (uint64_t j = 0; j < plan->nidx; j++) {
+    uint64_t i = plan->idx[j];
+    if (i < offset || i - offset >= n) continue;
+    uint64_t k = i - offset;
+    store_bits(dtype, cand, k, index_op(dtype, plan, load_bits(dtype, ref, k)));
+  }
+  return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Eq. (1) and the report                                                     */
+/* ------------------------------------------------------------------------- */
+static double load_value(int32_t dtype, const void *a, uint64_t k) {
+  if (dtype == OR_F32) return (double)((const float *)a)[k];
+  if (dtype == OR_BF16) return (double)bf16_to_f32(((const uint16_t *)a)[k]);
+  return (double)((const int32_t *)a)[k];
+}
+
+int or_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
+               double rtol, double atol, int32_t equal_nan, or_report *r) {
+  if (!r) return -1;
+  if (dtype != OR_F32 && dtype != OR_BF16 && dtype != OR_I32) return -2;
+  if (n && (!ref || !cand)) return -1;
+  if (!(rtol >= 0.0) || !(atol >= 0.0) || isinf(rtol) || isinf(atol)) return -1;
+  memset(r, 0, sizeof(*r));
+  r->n = n;
+  r->first_mismatch = -1;
+  double sum = 0.0, comp = 0.0;   /* Neumaier (1974) compensated summation */
+  for (uint64_t k = 0; k < n; k++) {
+    double y = load_value(dtype, ref, k);    /* reference output y     */
+    double a = load_value(dtype, cand, k);   /* kernel output K(x)     */
+    int match, finite;
+    double d = 0.0;
+    if (dtype == OR_I32) {
+      /* integers are checked exactly; the tolerances do not apply */
+      d = fabs(a - y);
+      match = (a == y);
+      finite = 1;
+    } else {
+      /* isnan / isinf may return any nonzero value (glibc's isinf gives -1 for
+       * -Inf), so normalise to 0 / 1 before counting */
+      int nan_y = isnan(y) != 0, nan_a = isnan(a) != 0;
+      int inf_y = isinf(y) != 0, inf_a = isinf(a) != 0;
+      r->nan_ref += (uint64_t)nan_y;
+      r->nan_cand += (uint64_t)nan_a;
+      r->inf_ref += (uint64_t)inf_y;
+      r->inf_cand += (uint64_t)inf_a;
+      if (nan_y || nan_a) {
+        match = equal_nan && nan_y && nan_a;
+        finite = 0;
+      } else if (inf_y || inf_a) {
+        match = (a == y);   /* identical infinities agree */
+        finite = 0;
+      } else {
+        d = fabs(a - y);
+        double t = atol + rtol * fabs(y);
+        match = (d <= t);
+        finite = 1;
+      }
+    }
+    if (!match) {
+      if (r->mismatches == 0) r->first_mismatch = (int64_t)k;
+      r->mismatches++;
+    }
+    if (finite) {
+      if (d > r->max_abs_err) r->max_abs_err = d;
+      double rel = (d == 0.0) ? 0.0 : d / fabs(y);   /* y = 0, d > 0 gives +Inf */
+      if (rel > r->max_rel_err) r->max_rel_err = rel;
+      double t = sum + d;
+      if (fabs(sum) >= fabs(d))
+        comp += (sum - t) + d;
+      else
+        comp += (d - t) + sum;
+      sum = t;
+    }
+  }
+  r->err_sum = sum + comp;
+  return 0;
+}
+
+int or_compare_batched(const or_segment *segs, uint32_t nseg, or_report *reports) {
+  if (nseg && (!segs || !reports)) return -1;
+  for (uint32_t s = 0; s < nseg; s++) {
+    const or_segment *g = &segs[s];
+    int rc = or_compare(g->ref, g->cand, g->n, g->dtype, g->rtol, g->atol, g->equal_nan, &reports[s]);
+    if (rc) return rc;
+  }
+  return 0;
+}

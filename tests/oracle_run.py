@@ -1,0 +1,48 @@
+"""Run a workload case through the CPU oracle (test helper).
+
+Builds the reference tensor and the candidate exactly as the case describes,
+using only the oracle; the GPU tests call this to get expected values.
+"""
+import numpy as np
+
+import oracle as O
+
+
+def params_of(spec):
+    return O.dist_params(**spec.params)
+
+
+def oracle_ref(spec, offset=0, n=None):
+    n = spec.n - offset if n is None else n
+    return O.synth(spec.seed, spec.stream, spec.dtype, spec.dist, params_of(spec), n, offset=offset)
+
+
+def oracle_cand(case, ref, offset=0):
+    """Apply the case's derivation steps to the window [offset, offset+len(ref))."""
+    cand = ref.copy()
+    for s in case.steps:
+        if s.op in ("copy", "ulp", "scale", "special_flip"):
+            cand = O.perturb(s.seed, s.stream, case.ref.dtype, s.op, ref, np.empty_like(ref),
+                             p=s.p, value=s.value, offset=offset)
+        else:
+            cand = O.perturb(s.seed, s.stream, case.ref.dtype, s.op, ref, cand, value=s.value,
+                             bits=s.bits, idx=s.idx, offset=offset)
+    return cand
+
+
+def oracle_case(case):
+    ref = oracle_ref(case.ref)
+    cand = oracle_cand(case, ref)
+    rep = O.compare(ref, cand, case.ref.dtype, case.rtol, case.atol, case.equal_nan)
+    return ref, cand, rep
+
+
+def oracle_elements(case, idx):
+    """Reference and candidate values at global indices idx, one element at a time."""
+    idx = np.asarray(idx, dtype=np.uint64)
+    ref = O.synth_at(case.ref.seed, case.ref.stream, case.ref.dtype, case.ref.dist,
+                     params_of(case.ref), idx)
+    cand = np.empty_like(ref)
+    for k, i in enumerate(idx):
+        cand[k] = oracle_cand(case, ref[k:k + 1], offset=int(i))[0]
+    return ref, cand

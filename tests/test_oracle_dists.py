@@ -1,0 +1,285 @@
+"""Pins of the oracle's distribution transforms.
+
+Sec. 4.2.1 asks that test inputs come from a broad numeric range (a Gaussian
+with mean 5 and standard deviation 10 is its example).  The transforms below
+are conventions the paper leaves open; each is pinned against mathematics
+that does not depend on the oracle: exact closed forms, exhaustive error
+bounds against float64 / mpmath, special cases, moments and Kolmogorov-Smirnov
+statistics, and library routines (torch's bf16 rounding).
+"""
+import math
+import os
+import re
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.stats as st
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def f32(bits):
+    return np.asarray(bits, dtype=np.uint32).view(np.float32)
+
+
+def ulp32(x):
+    x = np.abs(np.asarray(x, np.float64))
+    e = np.floor(np.log2(np.maximum(x, 2.0 ** -126)))
+    return 2.0 ** (e - 23)
+
+
+# --------------------------------------------------------------- constants
+def _oracle_constants():
+    src = open(os.path.join(ROOT, "oracle", "sv_oracle.c")).read()
+    return {m.group(1): float.fromhex(m.group(2))
+            for m in re.finditer(r"static const float (\w+) = (-?0x[0-9a-fA-F.]+p[-+]?\d+)f;", src)}
+
+
+def test_transform_constants_are_the_fp32_roundings_of_their_definitions():
+    mp = pytest.importorskip("mpmath")
+    mp.mp.prec = 300
+
+    def rne32(x):
+        # fp32 round-to-nearest-even of an mpf, exactly
+        v = float(x)                       # correctly rounded to fp64 first is not enough;
+        lo = np.float32(v)                 # so check the neighbours explicitly
+        cands = [np.nextafter(lo, np.float32(-np.inf)), lo, np.nextafter(lo, np.float32(np.inf))]
+        best = min(cands, key=lambda c: (abs(mp.mpf(float(c)) - x),
+                                         int(np.float32(c).view(np.uint32)) & 1))
+        return float(best)
+
+    half_pi = mp.pi / 2
+    ln2 = mp.log(2)
+    ln2_hi = mp.floor(ln2 * 2 ** 16) / 2 ** 16
+    want = {
+        "LN_SQRT2": mp.sqrt(2), "LN_C3": mp.mpf(2) / 3, "LN_C5": mp.mpf(2) / 5,
+        "LN_C7": mp.mpf(2) / 7, "LN_C9": mp.mpf(2) / 9,
+        "LN2_HI": ln2_hi, "LN2_LO": ln2 - ln2_hi,
+    }
+    for k in (1, 3, 5, 7, 9):
+        want["SIN_%d" % k] = (-1) ** ((k - 1) // 2) * half_pi ** k / mp.factorial(k)
+    for k in (2, 4, 6, 8, 10):
+        want["COS_%d" % k] = (-1) ** (k // 2) * half_pi ** k / mp.factorial(k)
+    got = _oracle_constants()
+    assert set(want) <= set(got)
+    for name, x in want.items():
+        assert got[name] == rne32(x), name
+    assert float(ln2_hi) == 45426 / 2 ** 16
+
+
+# --------------------------------------------------------------- uniform
+@pytest.mark.parametrize("a,b", [(-1.0, 1.0), (-4.0, 4.0), (0.0, 1.0)])
+def test_uniform_closed_form_on_power_of_two_spans(oracle, a, b):
+    # element i = a + (b - a) * k * 2^-24 exactly, k = top 24 bits of word i%4 of block i/4
+    n = 4096
+    v = f32(oracle.synth(2, 5, "f32", "uniform", oracle.dist_params(a=a, b=b), n))
+    w = oracle.philox_blocks(2, 5, 0, n // 4).reshape(-1)
+    k = w >> 8
+    for i in range(n):
+        assert Fraction(float(v[i])) == Fraction(a) + Fraction(b - a) * Fraction(int(k[i]), 2 ** 24)
+
+
+def test_uniform_half_open_and_moments(oracle):
+    n = 1 << 20
+    a, b = -3.0, 7.5
+    v = f32(oracle.synth(0, 1, "f32", "uniform", oracle.dist_params(a=a, b=b), n)).astype(np.float64)
+    assert v.min() >= a and v.max() < b
+    mean_sigma = (b - a) / math.sqrt(12 * n)
+    assert abs(v.mean() - (a + b) / 2) < 5 * mean_sigma
+    var = (b - a) ** 2 / 12
+    assert abs(v.var() - var) < 5 * var * math.sqrt(0.8 / n)   # var of sample var: (4/5) var^2 / n
+    d = st.kstest(v, "uniform", args=(a, b - a)).statistic
+    assert d < 1.95 / math.sqrt(n)
+
+
+def test_uniform_bf16_is_rne_of_fp32(oracle):
+    import torch
+    p = oracle.dist_params(a=-4.0, b=4.0)
+    n = 1 << 16
+    v32 = oracle.synth(9, 3, "f32", "uniform", p, n)
+    v16 = oracle.synth(9, 3, "bf16", "uniform", p, n)
+    want = torch.from_numpy(v32.view(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(v16, want)
+    # bf16 rounding may reach the closed end b = 4 (the interval is [a, b] after rounding)
+    assert f32(v16.astype(np.uint32) << 16).max() <= 4.0
+
+
+# --------------------------------------------------------------- ln / sincos / Box-Muller
+def test_ln_exhaustive_on_all_box_muller_inputs(oracle):
+    # every u1 = k 2^-24, k = 1 .. 2^24, within 2.6 ulp of float64 log (measured max 2.51)
+    k = np.arange(1, (1 << 24) + 1, dtype=np.float64)
+    u1 = (k * 2.0 ** -24).astype(np.float32)
+    got = oracle.ln_f32_n(u1).astype(np.float64)
+    want = np.log(u1.astype(np.float64))
+    assert got[-1] == 0.0                      # ln 1 = 0 exactly
+    nz = want != 0
+    err = np.abs(got[nz] - want[nz]) / ulp32(want[nz])
+    assert err.max() <= 2.6
+    assert np.all(got[:-1] < 0)
+
+
+def test_ln_at_powers_of_two_is_e_ln2_within_one_ulp(oracle):
+    for e in range(-24, 0):
+        want = e * math.log(2)
+        assert abs(float(oracle.ln_f32(2.0 ** e)) - want) <= float(ulp32(want))
+
+
+def test_sincos_exhaustive(oracle):
+    # all 2^24 angles 2 pi j / 2^24 within 1.75 ulp (measured max 1.72), exact at the axes
+    j = np.arange(1 << 24, dtype=np.uint32)
+    s, c = oracle.sincos_2pi_f32_n(j)
+    q = j >> 22
+    f = (j & 0x3FFFFF).astype(np.float64) * 2.0 ** -22
+    S, C = np.sin(np.pi / 2 * f), np.cos(np.pi / 2 * f)   # quarter-turn reduction is exact
+    sref = np.select([q == 0, q == 1, q == 2, q == 3], [S, C, -S, -C])
+    cref = np.select([q == 0, q == 1, q == 2, q == 3], [C, -S, -C, S])
+    for got, want in ((s, sref), (c, cref)):
+        nz = want != 0
+        assert np.all(got[~nz] == 0)
+        err = np.abs(got[nz].astype(np.float64) - want[nz]) / ulp32(want[nz])
+        assert err.max() <= 1.75
+    axes = np.array([0, 1 << 22, 2 << 22, 3 << 22], dtype=np.uint32)
+    s, c = oracle.sincos_2pi_f32_n(axes)
+    assert list(s) == [0.0, 1.0, 0.0, -1.0] and list(c) == [1.0, 0.0, -1.0, 0.0]
+    assert np.all(s * s + c * c <= 1.0 + 4e-7)
+
+
+def test_box_muller_accuracy_and_special_cases(oracle):
+    w = oracle.philox_blocks(0, 0, 0, 1 << 17)
+    zc = np.empty(w.shape[0]); zs = np.empty(w.shape[0])
+    for k in range(w.shape[0]):
+        zc[k], zs[k] = oracle.box_muller_f32(int(w[k, 0]), int(w[k, 1]))
+    u1 = ((w[:, 0] >> 8).astype(np.float64) + 1) * 2.0 ** -24
+    u2 = (w[:, 1] >> 8).astype(np.float64) * 2.0 ** -24
+    r = np.sqrt(-2 * np.log(u1))
+    for got, want in ((zc, r * np.cos(2 * np.pi * u2)), (zs, r * np.sin(2 * np.pi * u2))):
+        nz = np.abs(want) > 1e-30
+        assert (np.abs(got[nz] - want[nz]) / ulp32(want[nz])).max() <= 4.5
+    # u1 = 1 gives r = 0; u2 = 0 gives (r, 0); the largest radius is sqrt(48 ln 2)
+    assert all(z == 0 for z in oracle.box_muller_f32(0xFFFFFFFF, 12345 << 8))
+    zc0, zs0 = oracle.box_muller_f32(0, 0)
+    assert zs0 == 0.0 and abs(float(zc0) - math.sqrt(48 * math.log(2))) <= 4 * float(ulp32(5.77))
+
+
+def test_normal_element_order(oracle):
+    p = oracle.dist_params(mean=0.0, std=1.0)
+    v = f32(oracle.synth(4, 2, "f32", "normal", p, 64))
+    w = oracle.philox_blocks(4, 2, 0, 16)
+    for c in range(16):
+        a = oracle.box_muller_f32(int(w[c, 0]), int(w[c, 1]))
+        b = oracle.box_muller_f32(int(w[c, 2]), int(w[c, 3]))
+        assert list(v[4 * c:4 * c + 4]) == [a[0], a[1], b[0], b[1]]
+
+
+@pytest.mark.parametrize("mean,std", [(0.0, 1.0), (5.0, 10.0)])
+def test_normal_moments_and_ks(oracle, mean, std):
+    n = 1 << 20
+    v = f32(oracle.synth(0, 7, "f32", "normal", oracle.dist_params(mean=mean, std=std), n)).astype(np.float64)
+    z = (v - mean) / std
+    assert abs(z.mean()) < 5 / math.sqrt(n)
+    assert abs(z.var() - 1) < 5 * math.sqrt(2 / n)
+    assert abs(st.skew(z)) < 5 * math.sqrt(6 / n)
+    assert abs(st.kurtosis(z)) < 5 * math.sqrt(24 / n)
+    assert st.kstest(z, "norm").statistic < 1.95 / math.sqrt(n)
+    assert np.abs(z).max() <= math.sqrt(48 * math.log(2)) * (1 + 1e-6)
+
+
+# --------------------------------------------------------------- integer range
+def test_int_range_power_of_two_closed_form(oracle):
+    # range = 2^k: value = lo + top k bits of R, R = (w1:w0) for even i, (w3:w2) for odd i
+    n = 2048
+    for lo, k in [(0, 1), (-(1 << 20), 21), (-(2 ** 31), 32), (100, 7)]:
+        v = oracle.synth(1, 1, "i32", "int_range", oracle.dist_params(lo=lo, hi=lo + 2 ** k - 1), n)
+        v = v.view(np.int32).astype(np.int64)
+        w = oracle.philox_blocks(1, 1, 0, n // 2).astype(np.uint64)
+        R = np.empty(n, dtype=np.uint64)
+        R[0::2] = (w[:, 1] << np.uint64(32)) | w[:, 0]
+        R[1::2] = (w[:, 3] << np.uint64(32)) | w[:, 2]
+        want = lo + (R >> np.uint64(64 - k)).astype(np.int64)
+        assert np.array_equal(v, want)
+
+
+def test_int_range_general_is_floor_of_exact_product(oracle):
+    lo, hi = -(1 << 20), 1 << 20            # 2^21 + 1 values, inclusive
+    n = 4096
+    v = oracle.synth(0, 3, "i32", "int_range", oracle.dist_params(lo=lo, hi=hi), n).view(np.int32)
+    w = oracle.philox_blocks(0, 3, 0, n // 2)
+    for i in range(n):
+        h = i % 2
+        R = (int(w[i // 2, 2 * h + 1]) << 32) | int(w[i // 2, 2 * h])
+        assert int(v[i]) == lo + (R * (hi - lo + 1)) // 2 ** 64
+
+
+def test_int_range_bounds_endpoints_and_chi_square(oracle):
+    v = oracle.synth(0, 0, "i32", "int_range", oracle.dist_params(lo=-3, hi=6), 1 << 20).view(np.int32)
+    assert v.min() == -3 and v.max() == 6
+    counts = np.bincount(v + 3, minlength=10)
+    assert st.chisquare(counts).pvalue > 1e-4
+    big = oracle.synth(0, 1, "i32", "int_range", oracle.dist_params(lo=-(1 << 20), hi=1 << 20),
+                       1 << 20).view(np.int32)
+    assert big.min() >= -(1 << 20) and big.max() <= (1 << 20)
+    one = oracle.synth(0, 1, "i32", "int_range", oracle.dist_params(lo=42, hi=42), 100).view(np.int32)
+    assert np.all(one == 42)
+
+
+# --------------------------------------------------------------- special values
+SPECIAL = dict(mean=0.0, std=1e3, p_nan=0.01, p_inf=0.005, p_denorm=0.01, p_zero=0.01)
+
+
+def test_special_classes_follow_thresholds_and_bit_rules(oracle):
+    n = 1 << 16
+    bits = oracle.synth(0, 0, "f32", "special", oracle.dist_params(**SPECIAL), n)
+    w = oracle.philox_blocks(0, 0, 0, n)
+    widths = [math.floor(p * 2 ** 32) for p in (0.01, 0.005, 0.01, 0.01)]
+    assert widths == [42949672, 21474836, 42949672, 42949672]
+    t = np.cumsum(widths)
+    sign = w[:, 1] & 0x80000000
+    cls = np.searchsorted(t, w[:, 0].astype(np.int64), side="right")   # 0 nan 1 inf 2 den 3 zero 4 normal
+    mag = bits & 0x7FFFFFFF
+    spec = cls < 4
+    assert np.all((bits[spec] & 0x80000000) == sign[spec])
+    nan = cls == 0
+    assert np.all(bits[nan] == (sign[nan] | 0x7FC00000 | (w[nan, 1] & 0x3FFFFF)))
+    inf = cls == 1
+    assert np.all(mag[inf] == 0x7F800000)
+    den = cls == 2
+    m = w[den, 1] & 0x7FFFFF
+    assert np.all(mag[den] == np.where(m == 0, 1, m))
+    assert np.all(mag[cls == 3] == 0)
+    nor = np.nonzero(cls == 4)[0]
+    for i in nor[:2000]:
+        zc, _ = oracle.box_muller_f32(int(w[i, 2]), int(w[i, 3]))
+        assert f32(bits[i]) == np.float32(np.float32(1e3) * zc)
+    x = f32(bits)
+    assert np.all(np.isnan(x[nan])) and np.all(np.isinf(x[inf]))
+    assert np.all(np.isfinite(x[cls >= 2]))
+    assert np.all(np.abs(x[den]) < np.finfo(np.float32).tiny) and np.all(x[den] != 0)
+
+
+def test_special_class_frequencies(oracle):
+    n = 1 << 20
+    x = f32(oracle.synth(0, 0, "f32", "special", oracle.dist_params(**SPECIAL), n))
+    ax = np.abs(x)
+    got = [np.isnan(x).sum(), np.isinf(x).sum(),
+           ((ax > 0) & (ax < np.finfo(np.float32).tiny)).sum(), (x == 0).sum()]
+    for cnt, p in zip(got, (0.01, 0.005, 0.01, 0.01)):
+        assert abs(cnt - n * p) < 5 * math.sqrt(n * p * (1 - p))
+    normal = x[np.isfinite(x) & (ax >= np.finfo(np.float32).tiny)].astype(np.float64) / 1e3
+    assert st.kstest(normal, "norm").statistic < 1.95 / math.sqrt(normal.size)
+
+
+# --------------------------------------------------------------- bf16 rounding
+def test_bf16_rne_matches_torch(oracle):
+    import torch
+    rng = np.random.default_rng(0)
+    edge = np.array([0, 0x80000000, 1, 0x80000001, 0x007FFFFF, 0x00800000, 0x7F7FFFFF, 0xFF7FFFFF,
+                     0x7F800000, 0xFF800000, 0x3F808000, 0x3F818000, 0x3F807FFF, 0x3F808001,
+                     0x7F7F8000, 0x7F7F7FFF, 0x00008000, 0x00018000], dtype=np.uint32)
+    bits = np.concatenate([edge, rng.integers(0, 2 ** 32, 1 << 20, dtype=np.uint64).astype(np.uint32)])
+    finite = (bits & 0x7FFFFFFF) <= 0x7F800000
+    got = oracle.bf16_rne_n(bits)
+    want = torch.from_numpy(bits.view(np.float32).copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(got[finite], want[finite])
+    nanb = bits[~finite]
+    assert np.all(got[~finite] == ((nanb >> 16) | 0x40).astype(np.uint16))
