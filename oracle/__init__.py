@@ -104,6 +104,9 @@ def lib():
         L.or_synth_at.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32,
                                   ctypes.POINTER(DistParams), ctypes.c_void_p, ctypes.c_uint64,
                                   ctypes.c_void_p]
+        L.or_special_class_counts.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.POINTER(DistParams),
+                                              ctypes.c_uint64, ctypes.c_uint64, vp]
+        L.or_special_class_counts.restype = ctypes.c_int
         L.or_perturb.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32,
                                  ctypes.POINTER(PerturbPlan), ctypes.c_uint64, ctypes.c_uint64,
                                  ctypes.c_void_p, ctypes.c_void_p]
@@ -225,6 +228,14 @@ def synth_at(seed, stream, dtype, dist, params: DistParams, idx) -> np.ndarray:
     out = np.empty(idx.size, dtype=NP_STORAGE[dtype])
     _check(lib().or_synth_at(seed, stream, DTYPES[dtype], DISTS[dist], ctypes.byref(params),
                              _ptr(idx), idx.size, _ptr(out)), "or_synth_at")
+    return out
+
+
+def special_class_counts(seed, stream, params: DistParams, n, offset=0) -> np.ndarray:
+    """[NaN, Inf, denormal, zero, normal] counts of SPECIAL elements [offset, offset+n)."""
+    out = np.zeros(5, dtype=np.uint64)
+    _check(lib().or_special_class_counts(seed, stream, ctypes.byref(params), offset, n, _ptr(out)),
+           "or_special_class_counts")
     return out
 
 

@@ -380,6 +380,22 @@ int or_synth_at(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
   return 0;
 }
 
+int or_special_class_counts(uint64_t seed, uint64_t stream, const or_dist_params *p,
+                            uint64_t offset, uint64_t n, uint64_t counts[5]) {
+  prepared q;
+  int rc = prepare(OR_F32, OR_SPECIAL, p, &q);
+  if (rc) return rc;
+  for (int k = 0; k < 5; k++) counts[k] = 0;
+  for (uint64_t i = offset; i < offset + n; i++) {
+    uint32_t w[4];
+    or_philox_block(seed, stream, i, w);
+    uint64_t x = w[0];
+    int cls = x < q.t_nan ? 0 : x < q.t_inf ? 1 : x < q.t_den ? 2 : x < q.t_zero ? 3 : 4;
+    counts[cls]++;
+  }
+  return 0;
+}
+
 /* ------------------------------------------------------------------------- */
 /* Candidate derivation                                                       */
 /* ------------------------------------------------------------------------- */

@@ -95,6 +95,11 @@ int or_synth(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
 int or_synth_at(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
                 const or_dist_params *p, const uint64_t *idx, uint64_t n, void *out);
 
+/* Class counts of SPECIAL elements [offset, offset + n): counts[0..4] =
+ * NaN, Inf, denormal, zero, normal (the class depends on the first word only). */
+int or_special_class_counts(uint64_t seed, uint64_t stream, const or_dist_params *p,
+                            uint64_t offset, uint64_t n, uint64_t counts[5]);
+
 /* Candidate derivation over the window [offset, offset + n): ref and cand
  * hold that window; index lists carry global indices and entries outside the
  * window are skipped. */

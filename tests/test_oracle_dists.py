@@ -283,3 +283,16 @@ def test_bf16_rne_matches_torch(oracle):
     assert np.array_equal(got[finite], want[finite])
     nanb = bits[~finite]
     assert np.all(got[~finite] == ((nanb >> 16) | 0x40).astype(np.uint16))
+
+
+def test_special_class_counts_agree_with_synthesized_classes(oracle):
+    n = 1 << 18
+    p = oracle.dist_params(**SPECIAL)
+    c = oracle.special_class_counts(0, 5, p, n)
+    x = f32(oracle.synth(0, 5, "f32", "special", p, n))
+    ax = np.abs(x)
+    tiny = np.finfo(np.float32).tiny
+    assert list(c) == [np.isnan(x).sum(), np.isinf(x).sum(), ((ax > 0) & (ax < tiny)).sum(),
+                       (x == 0).sum(), (np.isfinite(x) & (ax >= tiny)).sum()]
+    half = oracle.special_class_counts(0, 5, p, n // 2) + oracle.special_class_counts(0, 5, p, n // 2, offset=n // 2)
+    assert np.array_equal(half, c)
