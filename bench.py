@@ -1,0 +1,155 @@
+"""Throughput of the synthesis + check path on one MI355X.
+
+A step is one pass of the whole path over one batch of synthetic input:
+synthesize the reference tensor(s) (sv_synth), check the candidate against
+it under Eq. (1) (sv_compare, or sv_compare_batched for the batched
+workloads), and bring the report(s) to the host.  Candidates are derived
+once before timing (workload support, untimed).  Inputs are resident in HBM
+when the timed region starts.
+
+value = (bytes synthesized + bytes checked) / time per step, in GB/s
+(1e9 bytes/s): synthesis writes n * itemsize bytes, the check reads
+2 * n * itemsize bytes (algorithmic bytes).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, AMD public figure
+ELEMENTWISE = ("copy", "ulp", "scale", "special_flip")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="normal_ulp")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(wl):
+    """The oracle, as it stands (serial C, one thread), on one step of the
+    workload: synthesis + check of the full tensor (the first two segments of
+    a batched workload); the candidate is derived untimed."""
+    import numpy as np
+    import oracle as O
+    cases = wl.cases if not wl.batched else wl.cases[:2]
+    nbytes, secs, elems = 0, 0.0, 0
+    for case in cases:
+        spec = case.ref
+        p = O.dist_params(**spec.params)
+        t0 = time.perf_counter()
+        ref = O.synth(spec.seed, spec.stream, spec.dtype, spec.dist, p, spec.n)
+        t1 = time.perf_counter()
+        cand = ref.copy()
+        for s in case.steps:
+            if s.op in ELEMENTWISE:
+                cand = O.perturb(s.seed, s.stream, spec.dtype, s.op, ref, np.empty_like(ref), p=s.p,
+                                 value=s.value)
+            else:
+                cand = O.perturb(s.seed, s.stream, spec.dtype, s.op, ref, cand, value=s.value, bits=s.bits,
+                                 idx=s.idx)
+        t2 = time.perf_counter()
+        O.compare(ref, cand, spec.dtype, case.rtol, case.atol, case.equal_nan)
+        t3 = time.perf_counter()
+        secs += (t1 - t0) + (t3 - t2)
+        nbytes += 3 * spec.nbytes
+        elems += spec.n
+    return {"value": round(nbytes / secs / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "one full step (%d elements, %d tensor(s)): synth + check" % (elems, len(cases)),
+            "seconds": round(secs, 3), "cpu": platform.processor() or platform.machine()}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the path runs on a single MI355X and this build has no "
+              "multi-GPU execution; rerun with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_00058_amd as sv
+    import workloads as W
+
+    torch.cuda.set_device(0)
+    wl = W.WORKLOADS[args.workload]()
+    tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "i32": torch.int32}
+    refs, cands = [], []
+    for case in wl.cases:
+        r = torch.empty(case.ref.n, dtype=tdt[case.ref.dtype], device="cuda")
+        sv.synth(r, case.ref.seed, case.ref.stream, case.ref.dist, **case.ref.params)
+        c = torch.empty_like(r)
+        for s in case.steps:
+            if s.op in ELEMENTWISE:
+                sv.perturb(r, c, s.seed, s.stream, s.op, p=s.p, value=s.value)
+            else:
+                sv.perturb(r, c, s.seed, s.stream, s.op, value=s.value, bits=s.bits, idx=s.idx)
+        refs.append(r)
+        cands.append(c)
+    segs = [(r, c, k.rtol, k.atol, k.equal_nan) for r, c, k in zip(refs, cands, wl.cases)]
+    torch.cuda.synchronize()
+
+    def step():
+        for c, r in zip(wl.cases, refs):
+            sv.synth(r, c.ref.seed, c.ref.stream, c.ref.dist, **c.ref.params)
+        return sv.compare_batched(segs) if wl.batched else [sv.compare(*segs[0])]
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    sv.profile_enable(True)
+    for k in ("synth", "compare", "finalize"):
+        sv.profile_read(k)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        reps = step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    sv.profile_enable(False)
+    kt = {k: sv.profile_read(k) for k in ("synth", "compare", "finalize")}
+
+    ms = (t1 - t0) / args.steps * 1e3
+    sbytes, cbytes = wl.synth_bytes, wl.compare_bytes
+    value = (sbytes + cbytes) / (ms / 1e3) / 1e9
+    kernels = {}
+    for k, nbytes in (("synth", sbytes), ("compare", cbytes), ("finalize", 0)):
+        cnt, tot = kt[k]
+        kernels[k] = {"launches": cnt, "avg_ms": round(tot / max(cnt, 1), 6),
+                      "ms_per_step": round(tot / args.steps, 6)}
+        if nbytes:
+            kernels[k]["GBps"] = round(nbytes / (tot / args.steps / 1e3) / 1e9, 1)
+    dom = max(("synth", "compare"), key=lambda k: kernels[k]["ms_per_step"])
+    achieved = kernels[dom]["GBps"]
+    out = {
+        "metric": "synth+check throughput (GB/s of algorithmic HBM traffic) on 1 MI355X",
+        "value": round(value, 1), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "+".join(sorted(set({"f32": "f32", "bf16": "bf16", "i32": "int32"}[c.ref.dtype]
+                                     for c in wl.cases))),
+        "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.description, "tensors": len(wl.cases),
+                   "elements": wl.total_elems, "synth_bytes": sbytes, "check_bytes": cbytes,
+                   "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
+                   "tensors_per_s": round(len(wl.cases) / (ms / 1e3), 1)},
+        "kernels": kernels,
+        "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None},
+        "mismatches": [int(r["mismatches"]) for r in reps][:8],
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

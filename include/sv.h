@@ -1,0 +1,197 @@
+/*
+ * sv.h -- C ABI of libsynthverify: seeded synthesis of test inputs and the
+ * elementwise functional check of candidate-kernel outputs, on one AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The operations are the data-parallel core of Synthesis-Based Verification
+ * in "CUDA-Harness" (arXiv 2609.00058), Sec. 4.2:
+ *   - sv_synth produces isolated, reproducible test data (Sec. 4.2.1: test
+ *     inputs are synthesized apart from kernel generation, from a broad numeric
+ *     range);
+ *   - sv_compare evaluates the functional validation rule, Eq. (1),
+ *       V(K, x, y) = I[ |K(x) - y| <= atol + rtol * |y| ],
+ *     element by element, y being the reference output and K(x) the candidate;
+ *   - sv_compare_batched checks many outputs in one launch, one report each,
+ *     for the progressive, fail-fast validation of Sec. 4.2.2.
+ *
+ * Conventions.  All functions return an sv_status (0 on success).  On error
+ * nothing is launched and sv_last_error() returns a message for the calling
+ * thread.  No C++ exception crosses this interface.  Device pointers are
+ * caller-owned HIP device memory on the current device; the library never
+ * frees them.  Host pointers are read or written only during the call.
+ * Work is issued on the stream set by sv_set_stream() for the calling thread
+ * (the null stream by default).  The library owns a per-device scratch area
+ * (partial reductions, segment table, report staging) that it allocates on
+ * first use, grows when needed and releases in sv_shutdown(); calls that use
+ * it on the same device are serialised by a lock.
+ */
+#ifndef SV_H
+#define SV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SV_ABI_VERSION 1
+
+enum {
+  SV_OK = 0,
+  SV_ERR_INVALID_ARG = -1, /* null pointer with n > 0, bad tolerance or parameter, size overflow */
+  SV_ERR_UNSUPPORTED = -2, /* unknown dtype / dist / op, or an unsupported combination          */
+  SV_ERR_HIP = -3,         /* a HIP runtime call failed; the message carries hipGetErrorString  */
+  SV_ERR_ALLOC = -4        /* scratch allocation failed                                         */
+};
+
+/* Element types.  Storage is contiguous, little-endian, 1-D. */
+enum { SV_F32 = 0, SV_BF16 = 1, SV_I32 = 2 };
+
+/* Distributions of sv_synth. */
+enum {
+  SV_UNIFORM = 0,   /* [a, b): fp32, bf16                                       */
+  SV_NORMAL = 1,    /* N(mean, std^2) by Box-Muller: fp32, bf16                 */
+  SV_INT_RANGE = 2, /* integers uniform on [lo, hi] inclusive: int32            */
+  SV_SPECIAL = 3    /* NaN / +-Inf / denormal / +-0 mix, else N(mean, std^2): fp32, bf16 */
+};
+
+typedef struct {
+  double a, b;                            /* SV_UNIFORM                             */
+  double mean, std;                       /* SV_NORMAL and the normal part of SPECIAL */
+  int64_t lo, hi;                         /* SV_INT_RANGE, within int32              */
+  double p_nan, p_inf, p_denorm, p_zero;  /* SV_SPECIAL class probabilities, sum <= 1 */
+} sv_dist_params;
+
+/* Result of the check of one tensor (or one segment of a batch). */
+typedef struct {
+  uint64_t n;              /* elements checked                                        */
+  uint64_t mismatches;     /* elements failing Eq. (1)                                */
+  int64_t first_mismatch;  /* smallest failing index, -1 if none                      */
+  double max_abs_err;      /* max |K(x) - y| over pairs where both are finite, else 0 */
+  double max_rel_err;      /* max |K(x) - y| / |y| over those pairs (0/0 -> 0, d/0 -> +Inf) */
+  double err_sum;          /* fp64 sum of |K(x) - y| over those pairs                 */
+  uint64_t nan_ref, nan_cand, inf_ref, inf_cand;  /* NaN / Inf counts on each side    */
+} sv_report;
+
+/* One tensor pair of a batched check. */
+typedef struct {
+  const void *ref;    /* device: reference output y                    */
+  const void *cand;   /* device: candidate output K(x), same dtype and n */
+  uint64_t n;         /* elements; 0 allowed                           */
+  int32_t dtype;      /* SV_F32 / SV_BF16 / SV_I32                      */
+  double rtol, atol;  /* finite, >= 0; ignored for SV_I32              */
+  int32_t equal_nan;  /* nonzero: NaN vs NaN agrees                     */
+} sv_segment;
+
+/*
+ * sv_synth -- fill out[0..n) with element i of the seeded sequence.
+ *
+ * Element i is a function of (seed, stream_id, i) only: Philox4x32-10
+ * (Salmon et al., SC'11) keyed by the seed, with counter (block index,
+ * stream_id), where block = i / E and E = 4 (uniform, normal), 2 (integer
+ * range) or 1 (special).  Uniform: a + (b - a) * (top 24 bits) * 2^-24 in
+ * fp32.  Normal: Box-Muller with ln, sin, cos evaluated as fixed fp32
+ * operation sequences, so the bits are reproducible on any IEEE-754 machine.
+ * Integer range: lo + floor(R * (hi - lo + 1) / 2^64), R a 64-bit word.
+ * Special: class by thresholds floor(p * 2^32) on the first word; bit
+ * patterns for NaN (quiet, random payload), Inf, denormals and zeros.  bf16
+ * outputs are the round-to-nearest-even of the fp32 value.  Any slice of a
+ * tensor can be regenerated alone.
+ *
+ * seed, stream_id : generator key and substream (stream_id is not a HIP stream).
+ * dtype, dist     : see the enums; other pairs return SV_ERR_UNSUPPORTED.
+ * params          : host pointer, read during the call.
+ * n, out          : element count and device output (any alignment of the
+ *                   element type; 16-byte aligned outputs take the fast path).
+ * Asynchronous: returns after the launch.
+ */
+int sv_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist,
+             const sv_dist_params *params, uint64_t n, void *out);
+
+/*
+ * sv_compare -- evaluate Eq. (1) on every element and reduce into *report.
+ *
+ * Both values are widened exactly to fp64.  If either is NaN the pair agrees
+ * only when equal_nan is set and both are NaN; otherwise if either is
+ * infinite the pair agrees only when the values are equal; otherwise it
+ * agrees when |K(x) - y| <= atol + rtol * |y|, each operation rounded to
+ * nearest in fp64 (no fused multiply-add).  SV_I32 pairs agree only when
+ * equal.  V(K, x, y) = 1 exactly when report->mismatches == 0.
+ *
+ * ref, cand : device pointers to n elements of dtype (any element alignment).
+ * report    : host pointer, written on success.
+ * Synchronous: returns after the report has reached the host.
+ */
+int sv_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
+               double rtol, double atol, int32_t equal_nan, sv_report *report);
+
+/*
+ * sv_compare_batched -- sv_compare on nseg independent segments in one launch.
+ *
+ * Each segment carries its own dtype, tolerances and equal_nan; indices in
+ * its report are local to the segment; zero-length segments are allowed and
+ * segments may alias.  Work is balanced by bytes across the whole batch.
+ * segs, reports : host arrays of nseg entries.  Synchronous.
+ */
+int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports);
+
+/* Candidate derivation steps of sv_perturb (workload support, not part of the check). */
+enum {
+  SV_OP_COPY = 0,         /* cand[i] = ref[i]                                              */
+  SV_OP_ULP = 1,          /* selected: next value up or down (fp32, bf16)                   */
+  SV_OP_SCALE = 2,        /* selected: fmt(fp32(y * fp32(1 + u))), u in [-value, value)     */
+  SV_OP_SPECIAL_FLIP = 3, /* selected zeros change sign, selected NaNs change payload       */
+  SV_OP_ADD_AT = 4,       /* cand[idx] = fmt(fp32(y) + fp32(value))        (fp32, bf16)     */
+  SV_OP_SET_AT = 5,       /* cand[idx] = bits (low 16 bits for bf16)                       */
+  SV_OP_FAULT_AT = 6      /* cand[idx] = fmt(y + (1 + |y|)); int32: y + 1 (wrapping)        */
+};
+
+typedef struct {
+  int32_t op;
+  double p;             /* selection probability of ops 1..3, in [0, 1]           */
+  double value;         /* ADD_AT delta; SCALE half-width                         */
+  uint32_t bits;        /* SET_AT pattern                                         */
+  const uint64_t *idx;  /* host: element indices of ops 4..6, each < n            */
+  uint64_t nidx;
+} sv_perturb_plan;
+
+/*
+ * sv_perturb -- derive a candidate from a reference (test-workload support).
+ *
+ * Ops 0..3 write every cand[i] from ref[i]; element i is selected when the
+ * first word of Philox(seed, stream_id, block i) is below floor(p * 2^32), the
+ * top bit of the second word gives the ulp direction (1 = up) and the NaN
+ * payload mask, the top 24 bits of the third word give u.  Ops 4..6 write only
+ * the listed elements, from ref.  ref may equal cand.  Synchronous for ops
+ * 4..6 (the index list is staged through the scratch area), asynchronous
+ * otherwise.
+ */
+int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_perturb_plan *plan,
+               uint64_t n, const void *ref, void *cand);
+
+/* HIP stream (hipStream_t) for the calling thread's later calls; NULL = null stream. */
+int sv_set_stream(void *hip_stream);
+
+/* Message of the calling thread's last failed call ("" if none).  Valid until its next call. */
+const char *sv_last_error(void);
+
+/*
+ * Kernel timing.  While enabled (per process), every launch of a main kernel
+ * is bracketed by HIP events on its stream.  sv_profile_read() waits for the
+ * recorded events of one kind, returns their count and total milliseconds,
+ * and forgets them.  Kinds: 0 synthesis, 1 check (single and batched main
+ * kernels), 2 finalize, 3 candidate derivation.
+ */
+enum { SV_PROF_SYNTH = 0, SV_PROF_COMPARE = 1, SV_PROF_FINALIZE = 2, SV_PROF_PERTURB = 3 };
+int sv_profile_enable(int32_t on);
+int sv_profile_read(int32_t kind, uint64_t *count, double *total_ms);
+
+/* Frees the scratch areas of every device.  Later calls allocate again. */
+int sv_shutdown(void);
+
+int sv_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SV_H */

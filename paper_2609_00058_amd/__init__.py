@@ -1,0 +1,202 @@
+"""Python binding of libsynthverify (argument marshalling only).
+
+Seeded synthesis of test inputs and the elementwise check of Eq. (1) of
+"CUDA-Harness" (arXiv 2609.00058, Sec. 4.2) on an MI355X.  Every step runs in
+the HIP kernels of libsynthverify.so; this module turns torch tensors into
+device pointers, passes torch's current HIP stream to the library, and
+returns reports as dicts.  It never computes anything itself and has no CPU
+fallback: if the library is missing, importing this package fails.
+"""
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsynthverify.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libsynthverify.so is not built (run paper_2609_00058_amd/build.py or "
+                      "__graft_entry__.build())")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+SV_OK, SV_ERR_INVALID_ARG, SV_ERR_UNSUPPORTED, SV_ERR_HIP, SV_ERR_ALLOC = 0, -1, -2, -3, -4
+DTYPE_CODES = {"f32": 0, "bf16": 1, "i32": 2}
+DIST_CODES = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3}
+OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
+            "add_at": 4, "set_at": 5, "fault_at": 6}
+PROF_KINDS = {"synth": 0, "compare": 1, "finalize": 2, "perturb": 3}
+
+# every symbol include/sv.h declares
+SYMBOLS = ("sv_synth", "sv_compare", "sv_compare_batched", "sv_perturb", "sv_set_stream",
+           "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
+
+
+class DistParams(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_double), ("b", ctypes.c_double),
+                ("mean", ctypes.c_double), ("std", ctypes.c_double),
+                ("lo", ctypes.c_int64), ("hi", ctypes.c_int64),
+                ("p_nan", ctypes.c_double), ("p_inf", ctypes.c_double),
+                ("p_denorm", ctypes.c_double), ("p_zero", ctypes.c_double)]
+
+
+class Report(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_uint64), ("mismatches", ctypes.c_uint64),
+                ("first_mismatch", ctypes.c_int64),
+                ("max_abs_err", ctypes.c_double), ("max_rel_err", ctypes.c_double),
+                ("err_sum", ctypes.c_double),
+                ("nan_ref", ctypes.c_uint64), ("nan_cand", ctypes.c_uint64),
+                ("inf_ref", ctypes.c_uint64), ("inf_cand", ctypes.c_uint64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class Segment(ctypes.Structure):
+    _fields_ = [("ref", ctypes.c_void_p), ("cand", ctypes.c_void_p),
+                ("n", ctypes.c_uint64), ("dtype", ctypes.c_int32),
+                ("rtol", ctypes.c_double), ("atol", ctypes.c_double),
+                ("equal_nan", ctypes.c_int32)]
+
+
+class PerturbPlan(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("p", ctypes.c_double),
+                ("value", ctypes.c_double), ("bits", ctypes.c_uint32),
+                ("idx", ctypes.POINTER(ctypes.c_uint64)), ("nidx", ctypes.c_uint64)]
+
+
+_u64, _i32, _vp, _dbl = ctypes.c_uint64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_double
+_lib.sv_synth.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u64, _vp]
+_lib.sv_compare.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(Report)]
+_lib.sv_compare_batched.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, ctypes.POINTER(Report)]
+_lib.sv_perturb.argtypes = [_u64, _u64, _i32, ctypes.POINTER(PerturbPlan), _u64, _vp, _vp]
+_lib.sv_set_stream.argtypes = [_vp]
+_lib.sv_last_error.restype = ctypes.c_char_p
+_lib.sv_profile_enable.argtypes = [_i32]
+_lib.sv_profile_read.argtypes = [_i32, ctypes.POINTER(_u64), ctypes.POINTER(_dbl)]
+for _name in SYMBOLS:
+    if _name != "sv_last_error":
+        getattr(_lib, _name).restype = ctypes.c_int
+
+
+class SVError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("libsynthverify error %d: %s" % (code, msg))
+        self.code = code
+
+
+def _check(rc):
+    if rc != SV_OK:
+        raise SVError(rc, _lib.sv_last_error().decode(errors="replace"))
+
+
+def lib():
+    return _lib
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def dtype_code(t) -> int:
+    torch = _torch()
+    m = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32"}
+    if t.dtype not in m:
+        raise SVError(SV_ERR_UNSUPPORTED, "unsupported tensor dtype %s" % t.dtype)
+    return DTYPE_CODES[m[t.dtype]]
+
+
+def _dev_ptr(t, name):
+    if not t.is_cuda:
+        raise SVError(SV_ERR_INVALID_ARG, "%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise SVError(SV_ERR_INVALID_ARG, "%s must be contiguous" % name)
+    return t.data_ptr()
+
+
+def _use_current_stream(t):
+    torch = _torch()
+    with torch.cuda.device(t.device):
+        _check(_lib.sv_set_stream(torch.cuda.current_stream().cuda_stream))
+
+
+def dist_params(**kw) -> DistParams:
+    p = DistParams()
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+def synth(out, seed: int, stream_id: int, dist: str, **params):
+    """Fill `out` (contiguous device tensor) with the seeded sequence (asynchronous)."""
+    _use_current_stream(out)
+    torch = _torch()
+    with torch.cuda.device(out.device):
+        _check(_lib.sv_synth(seed, stream_id, dtype_code(out), DIST_CODES[dist],
+                             ctypes.byref(dist_params(**params)), out.numel(), _dev_ptr(out, "out")))
+    return out
+
+
+def compare(ref, cand, rtol: float, atol: float, equal_nan: bool = False) -> dict:
+    """Eq. (1) on every element of (ref, cand) -> report dict (synchronous)."""
+    if ref.dtype != cand.dtype or ref.numel() != cand.numel():
+        raise SVError(SV_ERR_INVALID_ARG, "ref and cand must have the same dtype and size")
+    _use_current_stream(ref)
+    rep = Report()
+    torch = _torch()
+    with torch.cuda.device(ref.device):
+        _check(_lib.sv_compare(_dev_ptr(ref, "ref"), _dev_ptr(cand, "cand"), ref.numel(), dtype_code(ref),
+                               rtol, atol, int(bool(equal_nan)), ctypes.byref(rep)))
+    return rep.as_dict()
+
+
+def compare_batched(segments) -> list:
+    """segments: list of (ref, cand, rtol, atol, equal_nan); one launch, one report each."""
+    if not segments:
+        return []
+    arr = (Segment * len(segments))()
+    for k, (ref, cand, rtol, atol, eqn) in enumerate(segments):
+        if ref.dtype != cand.dtype or ref.numel() != cand.numel():
+            raise SVError(SV_ERR_INVALID_ARG, "segment %d: ref and cand differ in dtype or size" % k)
+        arr[k] = Segment(_dev_ptr(ref, "ref") if ref.numel() else None,
+                         _dev_ptr(cand, "cand") if cand.numel() else None,
+                         ref.numel(), dtype_code(ref), rtol, atol, int(bool(eqn)))
+    reps = (Report * len(segments))()
+    dev = segments[0][0].device
+    _use_current_stream(segments[0][0])
+    torch = _torch()
+    with torch.cuda.device(dev):
+        _check(_lib.sv_compare_batched(arr, len(segments), reps))
+    return [reps[k].as_dict() for k in range(len(segments))]
+
+
+def perturb(ref, cand, seed: int, stream_id: int, op: str, p: float = 0.0, value: float = 0.0,
+            bits: int = 0, idx=None):
+    """One candidate-derivation step from ref into cand (workload support)."""
+    import numpy as np
+    if ref.dtype != cand.dtype or ref.numel() != cand.numel():
+        raise SVError(SV_ERR_INVALID_ARG, "ref and cand must have the same dtype and size")
+    idx_arr = np.ascontiguousarray(idx if idx is not None else [], dtype=np.uint64)
+    plan = PerturbPlan(OP_CODES[op], p, value, bits & 0xFFFFFFFF,
+                       idx_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), idx_arr.size)
+    _use_current_stream(ref)
+    torch = _torch()
+    with torch.cuda.device(ref.device):
+        _check(_lib.sv_perturb(seed, stream_id, dtype_code(ref), ctypes.byref(plan), ref.numel(),
+                               _dev_ptr(ref, "ref"), _dev_ptr(cand, "cand")))
+    return cand
+
+
+def profile_enable(on: bool = True):
+    _check(_lib.sv_profile_enable(int(bool(on))))
+
+
+def profile_read(kind: str):
+    """(count, total_ms) of the main-kernel events of `kind` recorded since the last read."""
+    c, ms = ctypes.c_uint64(), ctypes.c_double()
+    _check(_lib.sv_profile_read(PROF_KINDS[kind], ctypes.byref(c), ctypes.byref(ms)))
+    return c.value, ms.value
+
+
+def shutdown():
+    _check(_lib.sv_shutdown())

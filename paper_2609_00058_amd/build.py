@@ -1,0 +1,47 @@
+"""Build libsynthverify.so (gfx950) in-tree with hipcc.
+
+Flags that the numerics depend on:
+  -ffp-contract=off                      every a + b * c stays two roundings
+  -fno-gpu-flush-denormals-to-zero       fp32 denormals survive synthesis and checks
+  -fhip-fp32-correctly-rounded-divide-sqrt  IEEE fp32 division and square root
+  no -ffast-math
+Packed fp32 instructions are disabled for the device code.
+"""
+import os
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+CSRC = os.path.join(HERE, "csrc")
+SOURCES = ["sv_api.hip", "sv_synth.hip", "sv_perturb.hip", "sv_compare.hip"]
+LIB = os.path.join(HERE, "libsynthverify.so")
+ARCH = os.environ.get("SV_OFFLOAD_ARCH", "gfx950")
+
+FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", "--offload-arch=" + ARCH,
+         "-ffp-contract=off", "-fno-gpu-flush-denormals-to-zero",
+         "-fhip-fp32-correctly-rounded-divide-sqrt",
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-Wall", "-Wno-unused-function",
+         "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
+
+
+def build(verbose: bool = False) -> str:
+    tmp = LIB + ".tmp%d" % os.getpid()
+    cmd = ["hipcc", *FLAGS, *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    # hipcc's host pass does not know the packed-fp32 feature; that warning is noise
+    noise = "is not a recognized feature for this target"
+    err = "\n".join(l for l in res.stderr.splitlines() if noise not in l)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc failed (%d):\n%s" % (res.returncode, err))
+    if verbose and err.strip():
+        print(err, file=sys.stderr)
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

@@ -1,0 +1,86 @@
+// sv_internal.h -- structures shared by the host entry points and the kernels
+// of libsynthverify.  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sv.h"
+
+namespace sv {
+
+constexpr int kBlock = 256;          // threads per workgroup of every streaming kernel
+constexpr int kWave = 64;            // CDNA wavefront
+constexpr uint64_t kNone = ~0ull;    // "no mismatch yet"
+
+// ----------------------------------------------------------------- synthesis
+struct SynthParams {
+  uint32_t k0, k1, s0, s1;      // Philox key (seed) and substream words
+  float a, span;                // uniform: a + span * U
+  float mean, std;              // normal and the normal part of SPECIAL
+  int64_t lo;                   // integer range
+  uint64_t range;               // hi - lo + 1 (<= 2^32)
+  uint64_t t_nan, t_inf, t_den, t_zero;   // cumulative class thresholds on w0
+};
+
+hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint64_t n, void *out,
+                        int cus, hipStream_t stream);
+
+// ----------------------------------------------------------------- candidates
+struct PerturbParams {
+  uint32_t k0, k1, s0, s1;
+  uint64_t threshold;           // selected iff w0 < threshold (floor(p 2^32))
+  float value;                  // ADD_AT delta, SCALE half-width
+  uint32_t bits;                // SET_AT pattern
+  int32_t op;
+};
+
+hipError_t launch_perturb_elementwise(int32_t dtype, const PerturbParams &p, uint64_t n,
+                                      const void *ref, void *cand, int cus, hipStream_t stream);
+hipError_t launch_perturb_indexed(int32_t dtype, const PerturbParams &p, const uint64_t *idx_dev,
+                                  uint64_t nidx, const void *ref, void *cand, hipStream_t stream);
+
+// ----------------------------------------------------------------- checking
+// A "unit" is 16 bytes of one segment: 4 fp32 / int32 or 8 bf16 elements.
+// Segments are laid end to end in unit space; workgroup b owns the units
+// [b * chunk, (b + 1) * chunk) of that space and writes one partial per
+// segment piece it touches, into slot b + s (distinct for every (b, s) pair
+// that occurs, because both b and s grow along the unit space).
+struct SegDesc {
+  const void *ref;
+  const void *cand;
+  uint64_t n;
+  uint64_t unit_begin;          // first unit of this segment in the batch's unit space
+  double rtol, atol;
+  int32_t dtype;
+  int32_t equal_nan;
+  int32_t vec_ok;               // both pointers 16-byte aligned
+  int32_t pad;
+};
+
+struct Partial {
+  uint64_t mism;
+  uint64_t first;               // kNone if no mismatch
+  double maxabs, maxrel, sum;
+  uint64_t nan_r, nan_c, inf_r, inf_c;
+};
+
+struct CompareArgs {
+  const SegDesc *segs;          // device table (batched) or nullptr (single)
+  SegDesc single;               // the segment of a single-tensor check
+  uint32_t nseg;
+  uint64_t total_units;
+  uint64_t chunk;               // units per workgroup
+  Partial *partials;            // nblocks + nseg slots
+  sv_report *reports;           // nseg device reports
+};
+
+__host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
+  const uint64_t per = dtype == SV_BF16 ? 8 : 4;
+  return (n + per - 1) / per;
+}
+
+hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, hipStream_t stream,
+                          hipEvent_t ev_start, hipEvent_t ev_mid, hipEvent_t ev_stop);
+
+}  // namespace sv

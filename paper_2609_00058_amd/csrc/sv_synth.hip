@@ -1,0 +1,151 @@
+// sv_synth.hip -- seeded synthesis of test inputs (sv_synth).
+//
+// Element i of a tensor is a pure function of (seed, stream, i), so any
+// thread can produce any element and any slice can be regenerated alone.  The
+// fast path gives every thread one 16-byte output vector per iteration (4
+// fp32 / int32 or 8 bf16 elements), computes the Philox blocks that cover it
+// (one block for uniform / normal fp32, two for bf16 and the integer range,
+// four or eight for the special mix) and writes it with one non-temporal
+// dwordx4 store: the output is streamed once and never read back by this
+// kernel, so it should not displace anything in L2.  The grid is a fixed
+// multiple of the CU count with a grid-stride loop.  Outputs that are not
+// 16-byte aligned, and the ragged tail, go through a one-element-per-thread
+// kernel.
+#include "sv_device.h"
+#include "sv_internal.h"
+
+namespace sv {
+
+template <int DIST> struct DistTraits;
+template <> struct DistTraits<SV_UNIFORM> { static constexpr int E = 4; };
+template <> struct DistTraits<SV_NORMAL> { static constexpr int E = 4; };
+template <> struct DistTraits<SV_INT_RANGE> { static constexpr int E = 2; };
+template <> struct DistTraits<SV_SPECIAL> { static constexpr int E = 1; };
+
+// The E element values (fp32 bits or int32 bits) of Philox block `block`.
+template <int DIST>
+__device__ __forceinline__ void block_values(const SynthParams &p, uint64_t block, uint32_t *v) {
+  const Key key{p.k0, p.k1, p.s0, p.s1};
+  const u32x4 w = philox_block(key, block);
+  if constexpr (DIST == SV_UNIFORM) {
+    v[0] = as_u32(p.a + p.span * unit24(w.x));
+    v[1] = as_u32(p.a + p.span * unit24(w.y));
+    v[2] = as_u32(p.a + p.span * unit24(w.z));
+    v[3] = as_u32(p.a + p.span * unit24(w.w));
+  } else if constexpr (DIST == SV_NORMAL) {
+    float c0, s0, c1, s1;
+    box_muller(w.x, w.y, c0, s0);
+    box_muller(w.z, w.w, c1, s1);
+    v[0] = as_u32(p.mean + p.std * c0);
+    v[1] = as_u32(p.mean + p.std * s0);
+    v[2] = as_u32(p.mean + p.std * c1);
+    v[3] = as_u32(p.mean + p.std * s1);
+  } else if constexpr (DIST == SV_INT_RANGE) {
+    // Lemire's multiply-shift: lo + floor(R * range / 2^64), R a 64-bit word
+    const uint64_t r0 = ((uint64_t)w.y << 32) | w.x;
+    const uint64_t r1 = ((uint64_t)w.w << 32) | w.z;
+    v[0] = (uint32_t)(int32_t)(p.lo + (int64_t)__umul64hi(r0, p.range));
+    v[1] = (uint32_t)(int32_t)(p.lo + (int64_t)__umul64hi(r1, p.range));
+  } else {
+    // class by cumulative thresholds on w0 (NaN, Inf, denormal, zero, normal);
+    // w1 carries the sign and the payload / mantissa; (w2, w3) feed Box-Muller
+    const uint32_t sign = w.y & 0x80000000u;
+    const uint64_t x = w.x;
+    uint32_t out;
+    if (x < p.t_nan) {
+      out = sign | 0x7FC00000u | (w.y & 0x003FFFFFu);
+    } else if (x < p.t_inf) {
+      out = sign | 0x7F800000u;
+    } else if (x < p.t_den) {
+      const uint32_t m = w.y & 0x007FFFFFu;
+      out = sign | (m ? m : 1u);
+    } else if (x < p.t_zero) {
+      out = sign;
+    } else {
+      float zc, zs;
+      box_muller(w.z, w.w, zc, zs);
+      out = as_u32(p.mean + p.std * zc);
+    }
+    v[0] = out;
+  }
+}
+
+template <int DIST, int DT>
+__global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64_t nvec,
+                                                           u32x4 *__restrict__ out) {
+  constexpr int E = DistTraits<DIST>::E;
+  constexpr int V = DT == SV_BF16 ? 8 : 4;   // elements per 16-byte vector
+  constexpr int B = V / E;                   // Philox blocks per vector
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t u = (uint64_t)blockIdx.x * kBlock + threadIdx.x; u < nvec; u += stride) {
+    uint32_t v[V];
+#pragma unroll
+    for (int b = 0; b < B; ++b) block_values<DIST>(p, u * B + b, v + b * E);
+    u32x4 o;
+    if constexpr (DT == SV_BF16) {
+      o.x = bf16_rne(v[0]) | (bf16_rne(v[1]) << 16);
+      o.y = bf16_rne(v[2]) | (bf16_rne(v[3]) << 16);
+      o.z = bf16_rne(v[4]) | (bf16_rne(v[5]) << 16);
+      o.w = bf16_rne(v[6]) | (bf16_rne(v[7]) << 16);
+    } else {
+      o = u32x4{v[0], v[1], v[2], v[3]};
+    }
+    __builtin_nontemporal_store(o, out + u);
+  }
+}
+
+// Elements [first, n), one per thread (tails and unaligned outputs).
+template <int DIST, int DT>
+__global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint64_t first, uint64_t n,
+                                                            void *__restrict__ out) {
+  constexpr int E = DistTraits<DIST>::E;
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t i = first + (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
+    uint32_t v[E];
+    block_values<DIST>(p, i / E, v);
+    const uint32_t x = v[i % E];
+    if constexpr (DT == SV_BF16)
+      ((uint16_t *)out)[i] = (uint16_t)bf16_rne(x);
+    else
+      ((uint32_t *)out)[i] = x;
+  }
+}
+
+template <int DIST, int DT>
+static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
+  constexpr uint64_t V = DT == SV_BF16 ? 8 : 4;
+  const uint64_t max_blocks = (uint64_t)cus * 8;
+  uint64_t first = 0;
+  if (((uintptr_t)out & 15u) == 0) {
+    const uint64_t nvec = n / V;
+    if (nvec) {
+      const uint64_t blocks = std::min<uint64_t>((nvec + kBlock - 1) / kBlock, max_blocks);
+      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
+                         nvec, (u32x4 *)out);
+    }
+    first = nvec * V;
+  }
+  if (first < n) {
+    const uint64_t rest = n - first;
+    const uint64_t blocks = std::min<uint64_t>((rest + kBlock - 1) / kBlock, max_blocks);
+    hipLaunchKernelGGL((synth_elem_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
+                       first, n, out);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint64_t n, void *out, int cus,
+                        hipStream_t stream) {
+  switch (dist * 4 + dtype) {
+    case SV_UNIFORM * 4 + SV_F32: return launch_typed<SV_UNIFORM, SV_F32>(p, n, out, cus, stream);
+    case SV_UNIFORM * 4 + SV_BF16: return launch_typed<SV_UNIFORM, SV_BF16>(p, n, out, cus, stream);
+    case SV_NORMAL * 4 + SV_F32: return launch_typed<SV_NORMAL, SV_F32>(p, n, out, cus, stream);
+    case SV_NORMAL * 4 + SV_BF16: return launch_typed<SV_NORMAL, SV_BF16>(p, n, out, cus, stream);
+    case SV_INT_RANGE * 4 + SV_I32: return launch_typed<SV_INT_RANGE, SV_I32>(p, n, out, cus, stream);
+    case SV_SPECIAL * 4 + SV_F32: return launch_typed<SV_SPECIAL, SV_F32>(p, n, out, cus, stream);
+    case SV_SPECIAL * 4 + SV_BF16: return launch_typed<SV_SPECIAL, SV_BF16>(p, n, out, cus, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace sv

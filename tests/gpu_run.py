@@ -1,0 +1,52 @@
+"""Run a workload case through libsynthverify on the GPU (test helper)."""
+import numpy as np
+import torch
+
+import paper_2609_00058_amd as sv
+
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16, "i32": torch.int32}
+STORAGE = {"f32": np.uint32, "bf16": np.uint16, "i32": np.uint32}
+
+
+def empty(n, dtype, device="cuda"):
+    return torch.empty(n, dtype=TORCH_DTYPE[dtype], device=device)
+
+
+def gpu_ref(spec, out=None):
+    out = empty(spec.n, spec.dtype) if out is None else out
+    sv.synth(out, spec.seed, spec.stream, spec.dist, **spec.params)
+    return out
+
+
+def gpu_cand(case, ref, cand=None):
+    cand = torch.empty_like(ref) if cand is None else cand
+    for s in case.steps:
+        if s.op in ("copy", "ulp", "scale", "special_flip"):
+            sv.perturb(ref, cand, s.seed, s.stream, s.op, p=s.p, value=s.value)
+        else:
+            sv.perturb(ref, cand, s.seed, s.stream, s.op, value=s.value, bits=s.bits, idx=s.idx)
+    return cand
+
+
+def bits(t):
+    """Raw storage of a device tensor as a host numpy array."""
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    return t.view(torch.int32).cpu().numpy().view(np.uint32)
+
+
+def bits_at(t, idx):
+    ii = torch.as_tensor(np.asarray(idx, dtype=np.int64), device=t.device)
+    return bits(t.index_select(0, ii))
+
+
+def same_report(got, want, sum_rel=1e-12):
+    """Bit-exact on every field except err_sum (within sum_rel relative)."""
+    for k in want:
+        if k == "err_sum":
+            if want[k] == 0.0:
+                assert got[k] == 0.0, (k, got[k], want[k])
+            else:
+                assert abs(got[k] - want[k]) <= sum_rel * abs(want[k]), (k, got[k], want[k])
+        else:
+            assert got[k] == want[k], (k, got[k], want[k])

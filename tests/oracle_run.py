@@ -46,3 +46,55 @@ def oracle_elements(case, idx):
     for k, i in enumerate(idx):
         cand[k] = oracle_cand(case, ref[k:k + 1], offset=int(i))[0]
     return ref, cand
+
+
+# ------------------------------------------------------------ chunked runs
+# The oracle is serial; these helpers only split a large tensor into windows
+# and run the serial oracle on each window from a thread pool (ctypes releases
+# the GIL), to keep full-size parity tests within seconds.
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+
+def workers():
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def _windows(n, parts):
+    step = max(1, -(-n // parts))
+    return [(o, min(step, n - o)) for o in range(0, n, step)]
+
+
+def oracle_ref_parallel(spec):
+    out = np.empty(spec.n, dtype=O.NP_STORAGE[spec.dtype])
+    def run(w):
+        o, m = w
+        out[o:o + m] = oracle_ref(spec, o, m)
+    with ThreadPoolExecutor(workers()) as ex:
+        list(ex.map(run, _windows(spec.n, 4 * workers())))
+    return out
+
+
+def oracle_cand_parallel(case, ref):
+    cand = np.empty_like(ref)
+    def run(w):
+        o, m = w
+        cand[o:o + m] = oracle_cand(case, ref[o:o + m], offset=o)
+    with ThreadPoolExecutor(workers()) as ex:
+        list(ex.map(run, _windows(ref.size, 4 * workers())))
+    return cand
+
+
+def oracle_case_parallel(case):
+    ref = oracle_ref_parallel(case.ref)
+    cand = oracle_cand_parallel(case, ref)
+    rep = O.compare(ref, cand, case.ref.dtype, case.rtol, case.atol, case.equal_nan)
+    return ref, cand, rep
+
+
+def special_counts_parallel(spec):
+    p = params_of(spec)
+    with ThreadPoolExecutor(workers()) as ex:
+        parts = list(ex.map(lambda w: O.special_class_counts(spec.seed, spec.stream, p, w[1], offset=w[0]),
+                            _windows(spec.n, 4 * workers())))
+    return np.sum(parts, axis=0)

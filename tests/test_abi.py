@@ -1,0 +1,151 @@
+"""The C-ABI library loads, exports every symbol include/sv.h declares, and
+rejects bad arguments with the documented status before any HIP call (no
+GPU is needed for any of this)."""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sv.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(sv_\w+)\s*\(", src, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def svlib():
+    import paper_2609_00058_amd as sv
+    return sv
+
+
+def test_every_declared_symbol_is_exported(svlib):
+    names = declared_functions()
+    assert len(names) >= 10
+    assert set(names) == set(svlib.SYMBOLS)
+    out = subprocess.run(["nm", "-D", "--defined-only", svlib.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    for name in names:
+        assert name in exported, name
+        assert getattr(svlib.lib(), name) is not None
+
+
+def test_abi_version_and_enums_match_header(svlib):
+    L = svlib.lib()
+    L.sv_abi_version.restype = ctypes.c_int
+    assert L.sv_abi_version() == 1
+    src = open(HEADER).read()
+    for name, code in [("SV_F32", 0), ("SV_BF16", 1), ("SV_I32", 2), ("SV_UNIFORM", 0), ("SV_NORMAL", 1),
+                       ("SV_INT_RANGE", 2), ("SV_SPECIAL", 3), ("SV_OP_FAULT_AT", 6)]:
+        assert re.search(r"\b%s = %d\b" % (name, code), src), name
+    assert svlib.DTYPE_CODES == {"f32": 0, "bf16": 1, "i32": 2}
+
+
+def test_struct_layouts_match_the_c_compiler(svlib, tmp_path):
+    # sizes and field offsets of every ABI struct, as gcc lays them out from include/sv.h
+    mirrors = {"sv_report": svlib.Report, "sv_segment": svlib.Segment,
+               "sv_dist_params": svlib.DistParams, "sv_perturb_plan": svlib.PerturbPlan}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "sv.h"', "int main(void) {"]
+    for cname, mirror in mirrors.items():
+        lines.append('printf("%s %%zu\\n", sizeof(%s));' % (cname, cname))
+        for field, _ in mirror._fields_:
+            lines.append('printf("%s.%s %%zu\\n", offsetof(%s, %s));' % (cname, field, cname, field))
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    got = dict(l.split() for l in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                   check=True).stdout.splitlines())
+    for cname, mirror in mirrors.items():
+        assert int(got[cname]) == ctypes.sizeof(mirror), cname
+        for field, _ in mirror._fields_:
+            assert int(got["%s.%s" % (cname, field)]) == getattr(mirror, field).offset, (cname, field)
+
+
+def _synth(L, svlib, dtype, dist, n=16, out=0x1000, params=True, **kw):
+    p = svlib.dist_params(**kw)
+    return L.sv_synth(0, 0, dtype, dist, ctypes.byref(p) if params else None, n, out)
+
+
+def test_synth_argument_errors_before_any_device_work(svlib):
+    L = svlib.lib()
+    INV, UNS = svlib.SV_ERR_INVALID_ARG, svlib.SV_ERR_UNSUPPORTED
+    assert _synth(L, svlib, 7, 0, a=0.0, b=1.0) == UNS                      # unknown dtype
+    assert _synth(L, svlib, 0, 9, a=0.0, b=1.0) == UNS                      # unknown dist
+    assert _synth(L, svlib, 0, 2, lo=0, hi=3) == UNS                        # int range into fp32
+    assert _synth(L, svlib, 2, 0, a=0.0, b=1.0) == UNS                      # uniform into int32
+    assert _synth(L, svlib, 0, 0, params=False) == INV
+    assert _synth(L, svlib, 0, 0, out=0, a=0.0, b=1.0) == INV               # NULL with n > 0
+    assert _synth(L, svlib, 0, 0, out=0x1002, a=0.0, b=1.0) == INV          # misaligned fp32
+    assert _synth(L, svlib, 0, 0, n=1 << 61, a=0.0, b=1.0) == INV           # size overflow
+    assert _synth(L, svlib, 0, 0, a=1.0, b=1.0) == INV                      # empty interval
+    assert _synth(L, svlib, 0, 0, a=-3e38, b=3e38) == INV                   # span overflows fp32
+    assert _synth(L, svlib, 0, 1, mean=0.0, std=-1.0) == INV
+    assert _synth(L, svlib, 0, 1, mean=math.nan, std=1.0) == INV
+    assert _synth(L, svlib, 0, 3, std=1.0, p_nan=0.6, p_inf=0.6) == INV     # probabilities sum > 1
+    assert _synth(L, svlib, 0, 3, std=1.0, p_zero=-0.1) == INV
+    assert _synth(L, svlib, 2, 2, lo=5, hi=4) == INV
+    assert _synth(L, svlib, 2, 2, lo=0, hi=1 << 31) == INV                  # beyond int32
+    assert "int32" in L.sv_last_error().decode()
+    assert _synth(L, svlib, 0, 0, n=0, out=0, a=0.0, b=1.0) == svlib.SV_OK  # nothing to do
+
+
+def test_compare_argument_errors_and_empty(svlib):
+    L = svlib.lib()
+    INV = svlib.SV_ERR_INVALID_ARG
+    rep = svlib.Report()
+    assert L.sv_compare(0x1000, 0x2000, 4, 0, 1e-5, 1e-8, 0, None) == INV
+    assert L.sv_compare(0, 0x2000, 4, 0, 1e-5, 1e-8, 0, ctypes.byref(rep)) == INV
+    assert L.sv_compare(0x1000, 0x2000, 4, 0, -1e-5, 0.0, 0, ctypes.byref(rep)) == INV
+    assert L.sv_compare(0x1000, 0x2000, 4, 0, math.inf, 0.0, 0, ctypes.byref(rep)) == INV
+    assert L.sv_compare(0x1000, 0x2000, 4, 0, 0.0, math.nan, 0, ctypes.byref(rep)) == INV
+    assert L.sv_compare(0x1001, 0x2000, 4, 1, 0.0, 0.0, 0, ctypes.byref(rep)) == INV   # misaligned bf16
+    assert L.sv_compare(0x1000, 0x2000, 4, 5, 0.0, 0.0, 0, ctypes.byref(rep)) == svlib.SV_ERR_UNSUPPORTED
+    assert "rtol" in L.sv_last_error().decode() or "dtype" in L.sv_last_error().decode()
+    assert L.sv_compare(0, 0, 0, 0, 1e-5, 1e-8, 0, ctypes.byref(rep)) == svlib.SV_OK
+    assert rep.n == 0 and rep.mismatches == 0 and rep.first_mismatch == -1 and rep.err_sum == 0.0
+    # int32 ignores its tolerances, so even invalid values are accepted for it (n = 0 here)
+    assert L.sv_compare(0, 0, 0, 2, -1.0, math.nan, 0, ctypes.byref(rep)) == svlib.SV_OK
+
+
+def test_batched_argument_errors_and_empty(svlib):
+    L = svlib.lib()
+    segs = (svlib.Segment * 3)()
+    reps = (svlib.Report * 3)()
+    assert L.sv_compare_batched(None, 0, None) == svlib.SV_OK
+    assert L.sv_compare_batched(None, 3, reps) == svlib.SV_ERR_INVALID_ARG
+    for k in range(3):
+        segs[k] = svlib.Segment(None, None, 0, 0, 1e-5, 1e-8, 0)
+    assert L.sv_compare_batched(segs, 3, reps) == svlib.SV_OK
+    assert all(reps[k].first_mismatch == -1 for k in range(3))
+    segs[1] = svlib.Segment(0x1000, None, 8, 0, 1e-5, 1e-8, 0)
+    assert L.sv_compare_batched(segs, 3, reps) == svlib.SV_ERR_INVALID_ARG
+    assert "segment 1" in L.sv_last_error().decode()
+
+
+def test_perturb_argument_errors(svlib):
+    L = svlib.lib()
+    plan = svlib.PerturbPlan(9, 0.5, 0.0, 0, None, 0)
+    assert L.sv_perturb(0, 0, 0, ctypes.byref(plan), 4, 0x1000, 0x2000) == svlib.SV_ERR_UNSUPPORTED
+    plan = svlib.PerturbPlan(1, 1.5, 0.0, 0, None, 0)
+    assert L.sv_perturb(0, 0, 0, ctypes.byref(plan), 4, 0x1000, 0x2000) == svlib.SV_ERR_INVALID_ARG
+    plan = svlib.PerturbPlan(1, 0.5, 0.0, 0, None, 0)
+    assert L.sv_perturb(0, 0, 2, ctypes.byref(plan), 4, 0x1000, 0x2000) == svlib.SV_ERR_UNSUPPORTED
+    idx = (ctypes.c_uint64 * 2)(1, 4)
+    plan = svlib.PerturbPlan(5, 0.0, 0.0, 0, idx, 2)
+    assert L.sv_perturb(0, 0, 0, ctypes.byref(plan), 4, 0x1000, 0x2000) == svlib.SV_ERR_INVALID_ARG
+    assert "out of range" in L.sv_last_error().decode()
+    assert L.sv_perturb(0, 0, 0, None, 4, 0x1000, 0x2000) == svlib.SV_ERR_INVALID_ARG
+
+
+def test_profile_read_with_nothing_recorded(svlib):
+    c, ms = svlib.profile_read("synth")
+    assert c == 0 and ms == 0.0

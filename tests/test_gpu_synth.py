@@ -1,0 +1,157 @@
+"""GPU parity of sv_synth and sv_perturb against the CPU oracle (bit-exact).
+
+Sizes span several workgroup tiles and ragged tails; outputs that are not
+16-byte aligned exercise the one-element-per-thread path; full-size tensors
+are checked on sampled elements the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_00058_amd as sv
+from gpu_run import bits, bits_at, empty
+
+pytestmark = pytest.mark.gpu
+
+SPECIAL = dict(mean=0.0, std=1e3, p_nan=0.01, p_inf=0.005, p_denorm=0.01, p_zero=0.01)
+SPECIAL_HEAVY = dict(mean=5.0, std=10.0, p_nan=0.2, p_inf=0.1, p_denorm=0.2, p_zero=0.2)
+CASES = [
+    ("uniform", "f32", dict(a=-1.0, b=1.0)),
+    ("uniform", "f32", dict(a=-3.0, b=7.5)),
+    ("uniform", "bf16", dict(a=-4.0, b=4.0)),
+    ("normal", "f32", dict(mean=0.0, std=1.0)),
+    ("normal", "f32", dict(mean=5.0, std=10.0)),
+    ("normal", "bf16", dict(mean=5.0, std=10.0)),
+    ("int_range", "i32", dict(lo=-(1 << 20), hi=1 << 20)),
+    ("int_range", "i32", dict(lo=-2 ** 31, hi=2 ** 31 - 1)),
+    ("int_range", "i32", dict(lo=7, hi=7)),
+    ("special", "f32", SPECIAL),
+    ("special", "f32", SPECIAL_HEAVY),
+    ("special", "bf16", SPECIAL_HEAVY),
+]
+SIZES = [1, 3, 4, 5, 8, 17, 1000, 4099, 65543, (1 << 20) + 3]
+
+
+def _diff(got, want):
+    bad = np.nonzero(got != want)[0]
+    return "first diff at %d of %d: got %#x want %#x" % (bad[0], bad.size, got[bad[0]], want[bad[0]]) \
+        if bad.size else ""
+
+
+@pytest.mark.parametrize("dist,dtype,params", CASES)
+def test_synth_bit_exact(oracle, dist, dtype, params):
+    for n in SIZES:
+        seed, stream = 0xDEADBEEF12345678, (1 << 63) | n
+        print("synth", dist, dtype, n, flush=True)
+        g = empty(n, dtype)
+        sv.synth(g, seed, stream, dist, **params)
+        want = oracle.synth(seed, stream, dtype, dist, oracle.dist_params(**params), n)
+        got = bits(g)
+        assert np.array_equal(got, want), _diff(got, want)
+
+
+@pytest.mark.parametrize("dist,dtype,params", [CASES[0], CASES[2], CASES[4], CASES[6], CASES[10], CASES[11]])
+def test_synth_unaligned_outputs_and_guard(oracle, dist, dtype, params):
+    n = 5003
+    per = 8 if dtype == "bf16" else 4
+    for off in range(1, per):
+        big = empty(n + 2 * per, dtype)
+        big.view(torch.int16 if dtype == "bf16" else torch.int32).fill_(0x5A5A)
+        view = big[off:off + n]
+        print("synth unaligned", dist, dtype, off, flush=True)
+        sv.synth(view, 9, 4, dist, **params)
+        want = oracle.synth(9, 4, dtype, dist, oracle.dist_params(**params), n)
+        allb = bits(big)
+        assert np.array_equal(allb[off:off + n], want), _diff(allb[off:off + n], want)
+        assert np.all(allb[:off] == 0x5A5A) and np.all(allb[off + n:] == 0x5A5A)
+
+
+def test_synth_is_deterministic_and_empty_ok():
+    a, b = empty(1 << 20, "f32"), empty(1 << 20, "f32")
+    sv.synth(a, 1, 2, "normal", mean=0.0, std=1.0)
+    sv.synth(b, 1, 2, "normal", mean=0.0, std=1.0)
+    assert torch.equal(a.view(torch.int32), b.view(torch.int32))
+    sv.synth(empty(0, "f32"), 1, 2, "normal", mean=0.0, std=1.0)
+
+
+def test_synth_rejects_bad_arguments():
+    g = empty(16, "f32")
+    with pytest.raises(sv.SVError) as e:
+        sv.synth(g, 0, 0, "int_range", lo=0, hi=5)
+    assert e.value.code == sv.SV_ERR_UNSUPPORTED
+    with pytest.raises(sv.SVError) as e:
+        sv.synth(g, 0, 0, "uniform", a=1.0, b=1.0)
+    assert e.value.code == sv.SV_ERR_INVALID_ARG
+    with pytest.raises(sv.SVError):
+        sv.synth(g, 0, 0, "special", p_nan=0.7, p_inf=0.7)
+
+
+@pytest.mark.parametrize("dist,dtype,n,params", [
+    ("normal", "f32", 1 << 26, dict(mean=0.0, std=1.0)),
+    ("special", "f32", 1 << 30, SPECIAL),
+    ("uniform", "bf16", 1 << 24, dict(a=-4.0, b=4.0)),
+])
+def test_synth_full_size_sampled(oracle, dist, dtype, n, params):
+    print("synth full", dist, dtype, n, flush=True)
+    g = empty(n, dtype)
+    sv.synth(g, 0, 0, dist, **params)
+    rng = np.random.default_rng(n)
+    idx = np.unique(np.concatenate([np.arange(4096), np.arange(n - 4096, n),
+                                    rng.integers(0, n, 60000)])).astype(np.uint64)
+    got = bits_at(g, idx)
+    want = oracle.synth_at(0, 0, dtype, dist, oracle.dist_params(**params), idx)
+    assert np.array_equal(got, want), _diff(got, want)
+    del g
+    torch.cuda.empty_cache()
+
+
+PERTURB = [
+    ("f32", "uniform", dict(a=-1.0, b=1.0), "copy", {}),
+    ("f32", "normal", dict(mean=0.0, std=1.0), "ulp", dict(p=0.3)),
+    ("bf16", "normal", dict(mean=5.0, std=10.0), "ulp", dict(p=0.3)),
+    ("f32", "special", SPECIAL_HEAVY, "ulp", dict(p=0.5)),
+    ("bf16", "uniform", dict(a=-4.0, b=4.0), "scale", dict(p=1.0, value=2.0 ** -9)),
+    ("f32", "normal", dict(mean=5.0, std=10.0), "scale", dict(p=0.7, value=0.25)),
+    ("f32", "special", SPECIAL_HEAVY, "special_flip", dict(p=0.5)),
+    ("bf16", "special", SPECIAL_HEAVY, "special_flip", dict(p=0.5)),
+    ("i32", "int_range", dict(lo=-100, hi=100), "copy", {}),
+]
+
+
+@pytest.mark.parametrize("dtype,dist,params,op,kw", PERTURB)
+def test_perturb_elementwise_bit_exact(oracle, dtype, dist, params, op, kw):
+    for n in (1, 7, 4099, (1 << 20) + 3):
+        print("perturb", op, dtype, n, flush=True)
+        ref = empty(n, dtype)
+        sv.synth(ref, 3, 1, dist, **params)
+        cand = empty(n, dtype)
+        stream = (1 << 63) | (5 << 32) | n
+        sv.perturb(ref, cand, 11, stream, op, **kw)
+        r = oracle.synth(3, 1, dtype, dist, oracle.dist_params(**params), n)
+        want = oracle.perturb(11, stream, dtype, op, r, np.empty_like(r), **kw)
+        got = bits(cand)
+        assert np.array_equal(got, want), _diff(got, want)
+
+
+@pytest.mark.parametrize("dtype,dist,params", [("f32", "normal", dict(mean=5.0, std=10.0)),
+                                               ("bf16", "uniform", dict(a=-4.0, b=4.0)),
+                                               ("i32", "int_range", dict(lo=-(1 << 20), hi=1 << 20))])
+def test_perturb_index_ops_bit_exact(oracle, dtype, dist, params):
+    n = 100003
+    rng = np.random.default_rng(4)
+    idx = np.concatenate([[0, n - 1], rng.choice(n, 300, replace=False)]).astype(np.uint64)
+    ref = empty(n, dtype)
+    sv.synth(ref, 0, 7, dist, **params)
+    r = oracle.synth(0, 7, dtype, dist, oracle.dist_params(**params), n)
+    ops = [("set_at", dict(bits=0x7FC00000)), ("fault_at", {})]
+    if dtype != "i32":
+        ops.append(("add_at", dict(value=1e-3)))
+    for op, kw in ops:
+        print("perturb index", op, dtype, flush=True)
+        cand = ref.clone()
+        sv.perturb(ref, cand, 0, 0, op, idx=idx, **kw)
+        want = oracle.perturb(0, 0, dtype, op, r, r.copy(), idx=idx, **kw)
+        got = bits(cand)
+        assert np.array_equal(got, want), _diff(got, want)
+    with pytest.raises(sv.SVError):
+        sv.perturb(ref, ref.clone(), 0, 0, "set_at", idx=[n])
