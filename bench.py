@@ -12,7 +12,7 @@ value = (bytes synthesized + bytes checked) / time per step, in GB/s
 2 * n * itemsize bytes (algorithmic bytes).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--no-cpu-baseline]
+                       [--no-cpu-baseline] [--copy-probe]
 """
 import argparse
 import json
@@ -26,6 +26,36 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, AMD public figure
 ELEMENTWISE = ("copy", "ulp", "scale", "special_flip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+KERNEL_NAMES = {"synth": "void sv::synth_vec_kernel<1, 0>", "compare": "void sv::compare_kernel<true, 1>"}
+
+
+def kernel_source_hash():
+    """Hash of the library sources and build flags: the HBM-traffic counters in
+    profiles/ are reported only while the kernels they were taken on are unchanged."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_00058_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + f.read())
+    with open(os.path.join(ROOT, "paper_2609_00058_amd", "build.py"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary, or None when it was taken on other sources or another workload."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_hash") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    k = t["kernels"].get(KERNEL_NAMES.get(kernel, ""))
+    return k["hbm_bytes"] if k else None
 
 
 def parse():
@@ -35,6 +65,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="normal_ulp")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="copy 256 MiB device-to-device once before timing (known-size kernel for "
+                         "calibrating the FETCH_SIZE / WRITE_SIZE counters)")
     return ap.parse_args()
 
 
@@ -97,6 +130,13 @@ def main():
         refs.append(r)
         cands.append(c)
     segs = [(r, c, k.rtol, k.atol, k.equal_nan) for r, c, k in zip(refs, cands, wl.cases)]
+    if args.copy_probe:
+        src = torch.ones(1 << 26, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     torch.cuda.synchronize()
 
     def step():
@@ -106,17 +146,26 @@ def main():
 
     for _ in range(args.warmup):
         step()
+    # timed region: K steps, no event markers
     torch.cuda.synchronize()
-    sv.profile_enable(True)
-    for k in ("synth", "compare", "finalize"):
-        sv.profile_read(k)
     t0 = time.perf_counter()
     for _ in range(args.steps):
         reps = step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    # the same K steps again with HIP events around every kernel (on the stream
+    # the kernels run on), for the per-kernel durations
+    kinds = ("synth", "compare", "finalize")
+    sv.profile_enable(True)
+    for k in kinds:
+        sv.profile_read(k)
+    t2 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
     sv.profile_enable(False)
-    kt = {k: sv.profile_read(k) for k in ("synth", "compare", "finalize")}
+    kt = {k: sv.profile_read(k) for k in kinds}
 
     ms = (t1 - t0) / args.steps * 1e3
     sbytes, cbytes = wl.synth_bytes, wl.compare_bytes
@@ -128,6 +177,7 @@ def main():
                       "ms_per_step": round(tot / args.steps, 6)}
         if nbytes:
             kernels[k]["GBps"] = round(nbytes / (tot / args.steps / 1e3) / 1e9, 1)
+    kernels["profiled_ms_per_step"] = round((t3 - t2) / args.steps * 1e3, 4)
     dom = max(("synth", "compare"), key=lambda k: kernels[k]["ms_per_step"])
     achieved = kernels[dom]["GBps"]
     out = {
@@ -143,7 +193,8 @@ def main():
                    "tensors_per_s": round(len(wl.cases) / (ms / 1e3), 1)},
         "kernels": kernels,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None},
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(wl.name, dom) if not wl.batched else None},
         "mismatches": [int(r["mismatches"]) for r in reps][:8],
     }
     if not args.no_cpu_baseline:

@@ -176,13 +176,15 @@ int sv_set_stream(void *hip_stream);
 const char *sv_last_error(void);
 
 /*
- * Kernel timing.  While enabled (per process), every launch of a main kernel
- * is bracketed by HIP events on its stream.  sv_profile_read() waits for the
+ * Kernel timing.  While enabled (per process), every kernel launch of the
+ * library is bracketed by HIP events on its stream (the markers themselves
+ * add a few microseconds between launches).  sv_profile_read() waits for the
  * recorded events of one kind, returns their count and total milliseconds,
- * and forgets them.  Kinds: 0 synthesis, 1 check (single and batched main
- * kernels), 2 finalize, 3 candidate derivation.
+ * and forgets them.  Kinds: 0 synthesis, 1 check (the streaming kernel of
+ * sv_compare / sv_compare_batched), 2 candidate derivation, 3 the check's
+ * finalize kernel (per-segment reduction and report).
  */
-enum { SV_PROF_SYNTH = 0, SV_PROF_COMPARE = 1, SV_PROF_FINALIZE = 2, SV_PROF_PERTURB = 3 };
+enum { SV_PROF_SYNTH = 0, SV_PROF_COMPARE = 1, SV_PROF_PERTURB = 2, SV_PROF_FINALIZE = 3 };
 int sv_profile_enable(int32_t on);
 int sv_profile_read(int32_t kind, uint64_t *count, double *total_ms);
 

@@ -24,7 +24,7 @@ DTYPE_CODES = {"f32": 0, "bf16": 1, "i32": 2}
 DIST_CODES = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3}
 OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
             "add_at": 4, "set_at": 5, "fault_at": 6}
-PROF_KINDS = {"synth": 0, "compare": 1, "finalize": 2, "perturb": 3}
+PROF_KINDS = {"synth": 0, "compare": 1, "perturb": 2, "finalize": 3}
 
 # every symbol include/sv.h declares
 SYMBOLS = ("sv_synth", "sv_compare", "sv_compare_batched", "sv_perturb", "sv_set_stream",

@@ -46,17 +46,16 @@ int hip_fail(hipError_t e, const char *what) {
 struct DeviceState {
   std::mutex mu;                 // serialises calls that use the scratch below
   int cus = 0;
-  Partial *partials = nullptr;
+  Partial *partials = nullptr;   // one per (workgroup, segment piece)
   size_t partials_cap = 0;
-  SegDesc *table = nullptr;
+  SegDesc *table = nullptr;      // batched segment table
   size_t table_cap = 0;
-  sv_report *reports = nullptr;
-  size_t reports_cap = 0;
   uint64_t *idx = nullptr;
   size_t idx_cap = 0;
   SegDesc *h_table = nullptr;    // pinned staging
   size_t h_table_cap = 0;
-  sv_report *h_reports = nullptr;
+  sv_report *h_reports = nullptr;  // pinned, host-mapped, coherent: the kernel writes reports here
+  sv_report *d_reports = nullptr;  // the device address of h_reports
   size_t h_reports_cap = 0;
   uint64_t *h_idx = nullptr;
   size_t h_idx_cap = 0;
@@ -103,6 +102,30 @@ int ensure_device(T *&ptr, size_t &cap, size_t need, const char *what) {
     return fail(SV_ERR_ALLOC, "hipMalloc of %zu bytes for %s: %s", want * sizeof(T), what, hipGetErrorString(e));
   }
   cap = want;
+  return SV_OK;
+}
+
+int ensure_reports(DeviceState *ds, size_t need) {
+  if (need <= ds->h_reports_cap) return SV_OK;
+  const size_t want = std::max(need, ds->h_reports_cap + ds->h_reports_cap / 2);
+  if (ds->h_reports) (void)hipHostFree(ds->h_reports);
+  ds->h_reports = nullptr;
+  ds->d_reports = nullptr;
+  ds->h_reports_cap = 0;
+  hipError_t e = hipHostMalloc((void **)&ds->h_reports, want * sizeof(sv_report),
+                               hipHostMallocMapped | hipHostMallocCoherent);
+  if (e != hipSuccess) {
+    ds->h_reports = nullptr;
+    return fail(SV_ERR_ALLOC, "hipHostMalloc of %zu bytes for reports: %s", want * sizeof(sv_report),
+                hipGetErrorString(e));
+  }
+  e = hipHostGetDevicePointer((void **)&ds->d_reports, ds->h_reports, 0);
+  if (e != hipSuccess) {
+    (void)hipHostFree(ds->h_reports);
+    ds->h_reports = nullptr;
+    return hip_fail(e, "hipHostGetDevicePointer(reports)");
+  }
+  ds->h_reports_cap = want;
   return SV_OK;
 }
 
@@ -202,10 +225,11 @@ void zero_report(sv_report *r, uint64_t n) {
   r->first_mismatch = -1;
 }
 
-// grid for a check over `units` 16-byte units
+// grid for a check over `units` 16-byte units: at most SV_CMP_BLOCKS_PER_CU
+// workgroups per CU, each owning whole waves of units
 void compare_grid(uint64_t units, int cus, uint32_t *nblocks, uint64_t *chunk) {
-  const uint64_t per_iter = (uint64_t)kBlock * 4;
-  uint64_t nb = std::min<uint64_t>((units + per_iter - 1) / per_iter, (uint64_t)cus * 8);
+  const uint64_t per_iter = (uint64_t)kBlock;
+  uint64_t nb = std::min<uint64_t>((units + per_iter - 1) / per_iter, (uint64_t)cus * SV_CMP_BLOCKS_PER_CU);
   if (nb == 0) nb = 1;
   uint64_t c = (units + nb - 1) / nb;
   c = (c + kWave - 1) / kWave * kWave;       // whole waves of units per workgroup
@@ -213,29 +237,46 @@ void compare_grid(uint64_t units, int cus, uint32_t *nblocks, uint64_t *chunk) {
   *nblocks = (uint32_t)((units + c - 1) / c);
 }
 
-int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, uint32_t nseg, sv_report *out) {
+// The check kernel and its finalize kernel (which writes the reports into
+// host-mapped memory), then a stream synchronisation.  Segments with no
+// elements get their (empty) report here.
+int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_segment *segs, uint32_t nseg,
+                sv_report *out) {
   hipStream_t st = t_stream;
   int rc = ensure_device(ds->partials, ds->partials_cap, (size_t)nblocks + nseg, "partials");
-  if (!rc) rc = ensure_device(ds->reports, ds->reports_cap, nseg, "reports");
-  if (!rc) rc = ensure_pinned(ds->h_reports, ds->h_reports_cap, nseg, "report staging");
+  if (!rc) rc = ensure_reports(ds, nseg);
   if (rc) return rc;
   args.partials = ds->partials;
-  args.reports = ds->reports;
+  args.reports = ds->d_reports;
   hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
   if (g_prof_on.load()) {
     e0 = take_event();
     e1 = take_event();
     e2 = take_event();
+    if (e0) (void)hipEventRecord(e0, st);
   }
-  SV_HIP(launch_compare(args, nblocks, st, e0, e1, e2), "check kernel launch");
-  if (e0) {
+  uint32_t mask = 0;
+  for (uint32_t k = 0; k < nseg; ++k) {
+    const sv_segment *g = segs ? &segs[k] : nullptr;
+    const uint64_t n = g ? g->n : args.single.n;
+    if (n) mask |= 1u << (g ? g->dtype : args.single.dtype);
+  }
+  hipError_t e = launch_compare(args, nblocks, mask, st, e0 ? e1 : nullptr);
+  if (e != hipSuccess) return hip_fail(e, "check kernel launch");
+  if (e0 && e1 && e2) {
+    (void)hipEventRecord(e2, st);
     push_record(SV_PROF_COMPARE, e0, e1);
     push_record(SV_PROF_FINALIZE, e1, e2);
   }
-  SV_HIP(hipMemcpyAsync(ds->h_reports, ds->reports, nseg * sizeof(sv_report), hipMemcpyDeviceToHost, st),
-         "report copy to host");
-  SV_HIP(hipStreamSynchronize(st), "hipStreamSynchronize after the check");
-  std::memcpy(out, ds->h_reports, nseg * sizeof(sv_report));
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize after the check");
+  for (uint32_t k = 0; k < nseg; ++k) {
+    const uint64_t n = segs ? segs[k].n : args.single.n;
+    if (n)
+      out[k] = ds->h_reports[k];
+    else
+      zero_report(&out[k], 0);
+  }
   return SV_OK;
 }
 
@@ -344,7 +385,7 @@ int sv_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype, dou
   args.total_units = units_of(dtype, n);
   uint32_t nblocks;
   compare_grid(args.total_units, ds->cus, &nblocks, &args.chunk);
-  return run_compare(ds, args, nblocks, 1, report);
+  return run_compare(ds, args, nblocks, nullptr, 1, report);
 }
 
 int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports) {
@@ -382,7 +423,7 @@ int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports
   args.total_units = total;
   uint32_t nblocks;
   compare_grid(total, ds->cus, &nblocks, &args.chunk);
-  return run_compare(ds, args, nblocks, nseg, reports);
+  return run_compare(ds, args, nblocks, segs, nseg, reports);
 }
 
 int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_perturb_plan *plan, uint64_t n,
@@ -495,14 +536,13 @@ int sv_shutdown(void) {
     (void)hipDeviceSynchronize();
     if (s->partials) (void)hipFree(s->partials);
     if (s->table) (void)hipFree(s->table);
-    if (s->reports) (void)hipFree(s->reports);
     if (s->idx) (void)hipFree(s->idx);
     if (s->h_table) (void)hipHostFree(s->h_table);
     if (s->h_reports) (void)hipHostFree(s->h_reports);
     if (s->h_idx) (void)hipHostFree(s->h_idx);
-    s->partials = nullptr; s->table = nullptr; s->reports = nullptr; s->idx = nullptr;
-    s->h_table = nullptr; s->h_reports = nullptr; s->h_idx = nullptr;
-    s->partials_cap = s->table_cap = s->reports_cap = s->idx_cap = 0;
+    s->partials = nullptr; s->table = nullptr; s->idx = nullptr;
+    s->h_table = nullptr; s->h_reports = nullptr; s->d_reports = nullptr; s->h_idx = nullptr;
+    s->partials_cap = s->table_cap = s->idx_cap = 0;
     s->h_table_cap = s->h_reports_cap = s->h_idx_cap = 0;
   }
   (void)hipSetDevice(prev);

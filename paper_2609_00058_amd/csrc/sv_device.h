@@ -30,11 +30,19 @@ struct Key {
   uint32_t s0, s1;   // substream words
 };
 
+// a ^ b ^ k in one VALU instruction: CDNA4's three-input bitwise operation
+// with truth table 0x96 (odd parity).  k is wave-uniform (a round key).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t k) {
+  uint32_t r;
+  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "s"(k));
+  return r;
+}
+
 __device__ __forceinline__ u32x4 philox_block(const Key &key, uint64_t block) {
   uint32_t x0 = (uint32_t)block, x1 = (uint32_t)(block >> 32), x2 = key.s0, x3 = key.s1;
   uint32_t k0 = key.k0, k1 = key.k1;
-#pragma unroll
-  for (int r = 0; r < 10; ++r) {
+  {
+    // first round: words 2 and 3 are the (uniform) substream, left to the compiler
     const uint64_t a = (uint64_t)0xD2511F53u * x0;
     const uint64_t b = (uint64_t)0xCD9E8D57u * x2;
     const uint32_t n0 = (uint32_t)(b >> 32) ^ x1 ^ k0;
@@ -43,8 +51,19 @@ __device__ __forceinline__ u32x4 philox_block(const Key &key, uint64_t block) {
     x3 = (uint32_t)a;
     x0 = n0;
     x2 = n2;
+  }
+#pragma unroll
+  for (int r = 1; r < 10; ++r) {
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
+    const uint64_t a = (uint64_t)0xD2511F53u * x0;
+    const uint64_t b = (uint64_t)0xCD9E8D57u * x2;
+    const uint32_t n0 = xor3((uint32_t)(b >> 32), x1, k0);
+    const uint32_t n2 = xor3((uint32_t)(a >> 32), x3, k1);
+    x1 = (uint32_t)b;
+    x3 = (uint32_t)a;
+    x0 = n0;
+    x2 = n2;
   }
   return u32x4{x0, x1, x2, x3};
 }

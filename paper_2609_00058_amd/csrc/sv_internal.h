@@ -9,6 +9,20 @@
 
 namespace sv {
 
+// Launch shape (compile-time tunables, defaults chosen by measurement on MI355X).
+#ifndef SV_CMP_UNROLL
+#define SV_CMP_UNROLL 4              // 16-byte units per thread in flight in the check
+#endif
+#ifndef SV_CMP_BLOCKS_PER_CU
+#define SV_CMP_BLOCKS_PER_CU 16      // check workgroups per CU
+#endif
+#ifndef SV_SYNTH_BLOCKS_PER_CU
+#define SV_SYNTH_BLOCKS_PER_CU 64    // synthesis workgroups per CU
+#endif
+#ifndef SV_SYNTH_NT_STORE
+#define SV_SYNTH_NT_STORE 0          // 1: non-temporal output stores
+#endif
+
 constexpr int kBlock = 256;          // threads per workgroup of every streaming kernel
 constexpr int kWave = 64;            // CDNA wavefront
 constexpr uint64_t kNone = ~0ull;    // "no mismatch yet"
@@ -72,7 +86,7 @@ struct CompareArgs {
   uint64_t total_units;
   uint64_t chunk;               // units per workgroup
   Partial *partials;            // nblocks + nseg slots
-  sv_report *reports;           // nseg device reports
+  sv_report *reports;           // nseg reports, in host-mapped pinned memory
 };
 
 __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
@@ -80,7 +94,9 @@ __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
   return (n + per - 1) / per;
 }
 
-hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, hipStream_t stream,
-                          hipEvent_t ev_start, hipEvent_t ev_mid, hipEvent_t ev_stop);
+// dtype_mask: OR of (1 << dtype) over the segments with elements
+// ev_mid (optional) is recorded between the check kernel and its finalize kernel.
+hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream,
+                          hipEvent_t ev_mid);
 
 }  // namespace sv

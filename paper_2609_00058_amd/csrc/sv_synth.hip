@@ -5,12 +5,13 @@
 // fast path gives every thread one 16-byte output vector per iteration (4
 // fp32 / int32 or 8 bf16 elements), computes the Philox blocks that cover it
 // (one block for uniform / normal fp32, two for bf16 and the integer range,
-// four or eight for the special mix) and writes it with one non-temporal
-// dwordx4 store: the output is streamed once and never read back by this
-// kernel, so it should not displace anything in L2.  The grid is a fixed
-// multiple of the CU count with a grid-stride loop.  Outputs that are not
-// 16-byte aligned, and the ragged tail, go through a one-element-per-thread
-// kernel.
+// four or eight for the special mix) and writes it with one dwordx4 store.
+// The grid is a fixed multiple of the CU count with a grid-stride loop; the
+// ragged tail (fewer than one vector) is written element by element by the
+// first threads of the same launch.  Outputs that are not 16-byte aligned go
+// through a one-element-per-thread kernel.  The path is ALU-bound (Philox is
+// 20 64-bit multiply-adds and 20 three-input XORs per block; Box-Muller adds a
+// logarithm, a square root and a sine / cosine pair per two elements).
 #include "sv_device.h"
 #include "sv_internal.h"
 
@@ -71,13 +72,24 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
 }
 
 template <int DIST, int DT>
-__global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64_t nvec,
+__device__ __forceinline__ void store_elem(void *out, uint64_t i, uint32_t x) {
+  if constexpr (DT == SV_BF16)
+    ((uint16_t *)out)[i] = (uint16_t)bf16_rne(x);
+  else
+    ((uint32_t *)out)[i] = x;
+}
+
+// Vectors [0, nvec) of a 16-byte aligned output, then the n - nvec V ragged
+// tail elements, one per thread of the first threads of the grid.
+template <int DIST, int DT>
+__global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                            u32x4 *__restrict__ out) {
   constexpr int E = DistTraits<DIST>::E;
   constexpr int V = DT == SV_BF16 ? 8 : 4;   // elements per 16-byte vector
   constexpr int B = V / E;                   // Philox blocks per vector
+  const uint64_t gid = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t u = (uint64_t)blockIdx.x * kBlock + threadIdx.x; u < nvec; u += stride) {
+  for (uint64_t u = gid; u < nvec; u += stride) {
     uint32_t v[V];
 #pragma unroll
     for (int b = 0; b < B; ++b) block_values<DIST>(p, u * B + b, v + b * E);
@@ -90,46 +102,44 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
     } else {
       o = u32x4{v[0], v[1], v[2], v[3]};
     }
-    __builtin_nontemporal_store(o, out + u);
+    if constexpr (SV_SYNTH_NT_STORE)
+      __builtin_nontemporal_store(o, out + u);
+    else
+      out[u] = o;
+  }
+  const uint64_t i = nvec * V + gid;
+  if (i < n) {
+    uint32_t v[E];
+    block_values<DIST>(p, i / E, v);
+    store_elem<DIST, DT>(out, i, v[i % E]);
   }
 }
 
-// Elements [first, n), one per thread (tails and unaligned outputs).
+// Every element, one per thread (outputs that are not 16-byte aligned).
 template <int DIST, int DT>
-__global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint64_t first, uint64_t n,
-                                                            void *__restrict__ out) {
+__global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint64_t n, void *__restrict__ out) {
   constexpr int E = DistTraits<DIST>::E;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t i = first + (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
     uint32_t v[E];
     block_values<DIST>(p, i / E, v);
-    const uint32_t x = v[i % E];
-    if constexpr (DT == SV_BF16)
-      ((uint16_t *)out)[i] = (uint16_t)bf16_rne(x);
-    else
-      ((uint32_t *)out)[i] = x;
+    store_elem<DIST, DT>(out, i, v[i % E]);
   }
 }
 
 template <int DIST, int DT>
 static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
   constexpr uint64_t V = DT == SV_BF16 ? 8 : 4;
-  const uint64_t max_blocks = (uint64_t)cus * 8;
-  uint64_t first = 0;
+  const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
   if (((uintptr_t)out & 15u) == 0) {
     const uint64_t nvec = n / V;
-    if (nvec) {
-      const uint64_t blocks = std::min<uint64_t>((nvec + kBlock - 1) / kBlock, max_blocks);
-      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
-                         nvec, (u32x4 *)out);
-    }
-    first = nvec * V;
-  }
-  if (first < n) {
-    const uint64_t rest = n - first;
-    const uint64_t blocks = std::min<uint64_t>((rest + kBlock - 1) / kBlock, max_blocks);
-    hipLaunchKernelGGL((synth_elem_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
-                       first, n, out);
+    const uint64_t threads = std::max<uint64_t>(nvec, n - nvec * V);   // the tail needs n - nvec V < V threads
+    const uint64_t blocks = std::min<uint64_t>((threads + kBlock - 1) / kBlock, max_blocks);
+    hipLaunchKernelGGL((synth_vec_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, nvec, n,
+                       (u32x4 *)out);
+  } else {
+    const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, max_blocks);
+    hipLaunchKernelGGL((synth_elem_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n, out);
   }
   return hipGetLastError();
 }
