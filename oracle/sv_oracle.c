@@ -5,7 +5,8 @@
  * TEST INFRASTRUCTURE ONLY (see sv_oracle.h).  Plain serial C, one element at
  * a time, no vectorisation, no blocking, no threads.  Built with
  * -O2 -ffp-contract=off so that every float operation written below is one
- * IEEE-754 operation rounded to nearest-even, exactly as written.
+ * IEEE-754 operation rounded to nearest-even, exactly as written; fmaf() is
+ * the IEEE fused multiply-add (one rounding).
  *
  * What the paper fixes and what this file adds:
  *  - Sec. 4.2.1, Eq. (1): V = I[ |K(x) - y| <= atol + rtol*|y| ], rtol scaling
@@ -19,9 +20,10 @@
  *    Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11) keyed
  *    by the seed with counter (block, stream); uniform from the top 24 bits;
  *    Box-Muller (1958) with ln, sin and cos written as fixed sequences of fp32
- *    operations (Taylor series whose coefficients are the fp32 roundings of
- *    exact rationals and powers of pi/2 over factorials); Lemire's
- *    multiply-shift for integer ranges; a class-threshold mix for special values.
+ *    operations (a Chebyshev polynomial for ln, Taylor series in powers of
+ *    pi/2 over factorials for sin and cos, coefficients rounded to fp32,
+ *    Horner steps fused multiply-adds); Lemire's multiply-shift for integer
+ *    ranges; a class-threshold mix for special values.
  */
 #include "sv_oracle.h"
 
@@ -75,17 +77,25 @@ void or_philox_block(uint64_t seed, uint64_t stream, uint64_t c, uint32_t out[4]
 
 /* ------------------------------------------------------------------------- */
 /* Natural logarithm for positive normal fp32 x.                              */
-/* x = 2^e * m with m in [sqrt(1/2), sqrt(2)); with s = (m-1)/(m+1),          */
-/* ln m = 2 atanh(s) = 2s + 2s^3/3 + 2s^5/5 + 2s^7/7 + 2s^9/9 + ...           */
-/* (|s| <= 0.1716, so the first omitted term is below 2e-9 relative).         */
+/* x = 2^e * m with m in [sqrt(1/2), sqrt(2)); with f = m - 1 (exact),        */
+/* ln m = f * P(f) where P is the degree-9 Chebyshev approximation of         */
+/* ln(1 + f) / f on [sqrt(1/2) - 1, sqrt(2) - 1] (interpolation at the 10     */
+/* Chebyshev nodes of that interval, coefficients rounded to fp32), evaluated */
+/* by Horner steps that are each one fused multiply-add.                      */
 /* ln x = e*ln2_hi + (ln m + e*ln2_lo), with ln2_hi = ln 2 rounded to 16 bits */
-/* (so e*ln2_hi is exact for |e| < 2^8) and ln2_lo = fp32(ln 2 - ln2_hi).     */
+/* (so e*ln2_hi is exact for |e| < 2^8) and ln2_lo = fp32(ln 2 - ln2_hi),     */
+/* both additions fused with their products.                                  */
 /* ------------------------------------------------------------------------- */
 static const float LN_SQRT2 = 0x1.6a09e6p+0f;      /* fp32(sqrt 2)                */
-static const float LN_C3 = 0x1.555556p-1f;         /* fp32(2/3)                   */
-static const float LN_C5 = 0x1.99999ap-2f;         /* fp32(2/5)                   */
-static const float LN_C7 = 0x1.24924ap-2f;         /* fp32(2/7)                   */
-static const float LN_C9 = 0x1.c71c72p-3f;         /* fp32(2/9)                   */
+static const float LN_P1 = -0x1.fffff8p-2f;        /* Chebyshev fit, degree 1     */
+static const float LN_P2 = 0x1.55555ep-2f;
+static const float LN_P3 = -0x1.000424p-2f;
+static const float LN_P4 = 0x1.999e86p-3f;
+static const float LN_P5 = -0x1.5423b0p-3f;
+static const float LN_P6 = 0x1.22cf10p-3f;
+static const float LN_P7 = -0x1.0fb036p-3f;
+static const float LN_P8 = 0x1.064786p-3f;
+static const float LN_P9 = -0x1.31335ap-4f;        /* Chebyshev fit, degree 9     */
 static const float LN2_HI = 0x1.62e4p-1f;          /* 45426 / 2^16                */
 static const float LN2_LO = 0x1.7f7d1cp-20f;       /* fp32(ln 2 - 45426 / 2^16)   */
 
@@ -98,29 +108,30 @@ float or_ln_f32(float x) {
     e = e + 1;
   }
   float f = m - 1.0f;                                /* exact (Sterbenz) */
-  float den = 2.0f + f;
-  float s = f / den;
-  float z = s * s;
-  float poly = LN_C9;
-  poly = LN_C7 + z * poly;
-  poly = LN_C5 + z * poly;
-  poly = LN_C3 + z * poly;
-  poly = 2.0f + z * poly;
-  float ln_m = s * poly;
+  float p = LN_P9;
+  p = fmaf(p, f, LN_P8);
+  p = fmaf(p, f, LN_P7);
+  p = fmaf(p, f, LN_P6);
+  p = fmaf(p, f, LN_P5);
+  p = fmaf(p, f, LN_P4);
+  p = fmaf(p, f, LN_P3);
+  p = fmaf(p, f, LN_P2);
+  p = fmaf(p, f, LN_P1);
+  p = fmaf(p, f, 1.0f);
+  float ln_m = f * p;
   float ef = (float)e;
-  float hi = ef * LN2_HI;
-  float lo = ef * LN2_LO;
-  return hi + (ln_m + lo);
+  return fmaf(ef, LN2_HI, fmaf(ef, LN2_LO, ln_m));
 }
 
 /* ------------------------------------------------------------------------- */
 /* sin and cos of the angle 2*pi*j/2^24, j < 2^24.                            */
 /* The angle is (pi/2)(q + f) with quadrant q = j >> 22 and f = (j mod 2^22)  */
 /* / 2^22, both exact.  S(f) = sin(pi f/2) and C(f) = cos(pi f/2) come from   */
-/* Taylor series in f with coefficients (-1)^k (pi/2)^n / n! rounded to fp32; */
-/* for f > 1/2 the complement g = 1 - f (exact) is used instead, since        */
-/* sin(pi f/2) = cos(pi g/2), so that both series run on f in [0, 1/2] and    */
-/* keep relative accuracy near the zeros.  The quadrant then rotates (S, C).  */
+/* Taylor series in f with coefficients (-1)^k (pi/2)^n / n! rounded to fp32, */
+/* in f^2 by fused multiply-add Horner steps; for f > 1/2 the complement      */
+/* g = 1 - f (exact) is used instead, since sin(pi f/2) = cos(pi g/2), so     */
+/* that both series run on f in [0, 1/2] and keep relative accuracy near the  */
+/* zeros.  The quadrant then rotates (S, C).                                  */
 /* ------------------------------------------------------------------------- */
 static const float SIN_1 = 0x1.921fb6p+0f;    /*  (pi/2)^1 / 1!  */
 static const float SIN_3 = -0x1.4abbcep-1f;   /* -(pi/2)^3 / 3!  */
@@ -136,21 +147,21 @@ static const float COS_10 = -0x1.a6d1f2p-16f; /* -(pi/2)^10 / 10! */
 static float sin_quarter(float f) {   /* sin(pi f / 2), f in [0, 1/2] */
   float f2 = f * f;
   float p = SIN_9;
-  p = SIN_7 + f2 * p;
-  p = SIN_5 + f2 * p;
-  p = SIN_3 + f2 * p;
-  p = SIN_1 + f2 * p;
+  p = fmaf(p, f2, SIN_7);
+  p = fmaf(p, f2, SIN_5);
+  p = fmaf(p, f2, SIN_3);
+  p = fmaf(p, f2, SIN_1);
   return f * p;
 }
 
 static float cos_quarter(float f) {   /* cos(pi f / 2), f in [0, 1/2] */
   float f2 = f * f;
   float p = COS_10;
-  p = COS_8 + f2 * p;
-  p = COS_6 + f2 * p;
-  p = COS_4 + f2 * p;
-  p = COS_2 + f2 * p;
-  return 1.0f + f2 * p;
+  p = fmaf(p, f2, COS_8);
+  p = fmaf(p, f2, COS_6);
+  p = fmaf(p, f2, COS_4);
+  p = fmaf(p, f2, COS_2);
+  return fmaf(f2, p, 1.0f);
 }
 
 void or_sincos_2pi_f32(uint32_t j24, float *s_out, float *c_out) {
@@ -319,8 +330,7 @@ static uint32_t element_bits(uint64_t seed, uint64_t stream, int32_t dist,
     float zc, zs;
     or_box_muller_f32(w[2 * pair], w[2 * pair + 1], &zc, &zs);
     float z = (i % 2u == 0u) ? zc : zs;
-    float t = q->std * z;
-    return f2u(q->mean + t);
+    return f2u(fmaf(q->std, z, q->mean));           /* mean + std z, one rounding */
   }
   if (dist == OR_INT_RANGE) {
     /* two elements per block: R = (w1:w0) for even i, (w3:w2) for odd i;
@@ -347,8 +357,7 @@ static uint32_t element_bits(uint64_t seed, uint64_t stream, int32_t dist,
   if (x < q->t_zero) return sign;
   float zc, zs;
   or_box_muller_f32(w[2], w[3], &zc, &zs);
-  float t = q->std * zc;
-  return f2u(q->mean + t);
+  return f2u(fmaf(q->std, zc, q->mean));
 }
 
 static void store(int32_t dtype, void *out, uint64_t k, uint32_t bits) {
