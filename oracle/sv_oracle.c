@@ -77,7 +77,8 @@ void or_philox_block(uint64_t seed, uint64_t stream, uint64_t c, uint32_t out[4]
 
 /* ------------------------------------------------------------------------- */
 /* Natural logarithm for positive normal fp32 x.                              */
-/* x = 2^e * m with m in [sqrt(1/2), sqrt(2)); with f = m - 1 (exact),        */
+/* x = 2^e * m with m in [sqrt(1/2), sqrt(2)): m is x's mantissa as 1.M,      */
+/* halved (and e raised) when 1.M >= fp32(sqrt 2); with f = m - 1 (exact),    */
 /* ln m = f * P(f) where P is the degree-9 Chebyshev approximation of         */
 /* ln(1 + f) / f on [sqrt(1/2) - 1, sqrt(2) - 1] (interpolation at the 10     */
 /* Chebyshev nodes of that interval, coefficients rounded to fp32), evaluated */
@@ -103,7 +104,7 @@ float or_ln_f32(float x) {
   uint32_t bits = f2u(x);
   int e = (int)((bits >> 23) & 0xFFu) - 127;
   float m = u2f((bits & 0x007FFFFFu) | 0x3F800000u); /* m in [1, 2) */
-  if (m > LN_SQRT2) {
+  if (m >= LN_SQRT2) {
     m = m * 0.5f;                                    /* exact */
     e = e + 1;
   }
