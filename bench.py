@@ -1,9 +1,9 @@
 """Throughput of the synthesis + check path on one MI355X.
 
 A step is one pass of the whole path over one batch of synthetic input:
-synthesize the reference tensor(s) (sv_synth), check the candidate against
-it under Eq. (1) (sv_compare, or sv_compare_batched for the batched
-workloads), and bring the report(s) to the host.  Candidates are derived
+synthesize the reference tensor(s) (sv_synth; sv_synth_batched for the
+batched workloads), check the candidates against them under Eq. (1)
+(sv_compare; sv_compare_batched), and bring the report(s) to the host.  Candidates are derived
 once before timing (workload support, untimed).  Inputs are resident in HBM
 when the timed region starts.
 
@@ -139,10 +139,15 @@ def main():
         del src, dst
     torch.cuda.synchronize()
 
+    jobs = [(r, c.ref.seed, c.ref.stream, c.ref.dist, c.ref.params) for c, r in zip(wl.cases, refs)]
+
     def step():
-        for c, r in zip(wl.cases, refs):
-            sv.synth(r, c.ref.seed, c.ref.stream, c.ref.dist, **c.ref.params)
-        return sv.compare_batched(segs) if wl.batched else [sv.compare(*segs[0])]
+        if wl.batched:
+            sv.synth_batched(jobs)
+            return sv.compare_batched(segs)
+        c = wl.cases[0]
+        sv.synth(refs[0], c.ref.seed, c.ref.stream, c.ref.dist, **c.ref.params)
+        return [sv.compare(*segs[0])]
 
     for _ in range(args.warmup):
         step()

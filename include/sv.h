@@ -108,6 +108,28 @@ typedef struct {
 int sv_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist,
              const sv_dist_params *params, uint64_t n, void *out);
 
+/* One tensor of a batched synthesis: the arguments of one sv_synth call. */
+typedef struct {
+  uint64_t seed, stream_id;
+  int32_t dtype, dist;
+  sv_dist_params params;
+  uint64_t n;
+  void *out;            /* device; outputs of one batch must not overlap */
+} sv_synth_job;
+
+/*
+ * sv_synth_batched -- njobs sv_synth calls in one launch.
+ *
+ * Job k writes exactly what sv_synth(jobs[k].seed, jobs[k].stream_id,
+ * jobs[k].dtype, jobs[k].dist, &jobs[k].params, jobs[k].n, jobs[k].out)
+ * writes.  The work is cut into tiles of 256 16-byte output vectors spread
+ * over the whole grid, so many small tensors cost one launch.  jobs is a host
+ * array read during the call; its device copy goes through the library's
+ * scratch on the calling thread's stream.  Asynchronous: returns after the
+ * launch.  Any invalid job fails the whole call before anything is launched.
+ */
+int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs);
+
 /*
  * sv_compare -- evaluate Eq. (1) on every element and reduce into *report.
  *
@@ -168,6 +190,19 @@ typedef struct {
  */
 int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_perturb_plan *plan,
                uint64_t n, const void *ref, void *cand);
+
+/*
+ * sv_eval_transform -- diagnostics: evaluate one building block of the normal
+ * transform of sv_synth on caller-given 24-bit inputs, so that it can be
+ * compared exhaustively with an independent implementation.
+ *   which = SV_EVAL_LN     : out[i] = bits of ln(u1),        u1 = ((in[i] & 0xFFFFFF) + 1) 2^-24
+ *   which = SV_EVAL_RADIUS : out[i] = bits of sqrt(-2 ln u1)  (the Box-Muller radius)
+ *   which = SV_EVAL_SIN    : out[i] = bits of sin(2 pi (in[i] & 0xFFFFFF) 2^-24)
+ *   which = SV_EVAL_COS    : out[i] = bits of cos(2 pi (in[i] & 0xFFFFFF) 2^-24)
+ * in, out: device arrays of n uint32.  Asynchronous.
+ */
+enum { SV_EVAL_LN = 0, SV_EVAL_RADIUS = 1, SV_EVAL_SIN = 2, SV_EVAL_COS = 3 };
+int sv_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out);
 
 /* HIP stream (hipStream_t) for the calling thread's later calls; NULL = null stream. */
 int sv_set_stream(void *hip_stream);

@@ -98,6 +98,7 @@ def lib():
         L.or_ln_f32_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_sincos_2pi_f32_n.argtypes = [vp, vp, vp, ctypes.c_uint64]
         L.or_bf16_rne_n.argtypes = [vp, vp, ctypes.c_uint64]
+        L.or_radius_f32_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_synth.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32,
                                ctypes.POINTER(DistParams), ctypes.c_uint64, ctypes.c_uint64,
                                ctypes.c_void_p]
@@ -177,6 +178,14 @@ def sincos_2pi_f32_n(j24):
     c = np.empty(j.size, np.float32)
     lib().or_sincos_2pi_f32_n(_ptr(j), _ptr(s), _ptr(c), j.size)
     return s, c
+
+
+def radius_f32_n(k24) -> np.ndarray:
+    """Box-Muller radius sqrt(-2 ln u1), u1 = (k24 + 1) 2^-24."""
+    k = np.ascontiguousarray(k24, dtype=np.uint32)
+    r = np.empty(k.size, np.float32)
+    lib().or_radius_f32_n(_ptr(k), _ptr(r), k.size)
+    return r
 
 
 def bf16_rne_n(bits) -> np.ndarray:

@@ -192,10 +192,14 @@ void or_sincos_2pi_f32(uint32_t j24, float *s_out, float *c_out) {
 /* Box-Muller: u1 = ((wa >> 8) + 1) 2^-24 in (0, 1], u2 = (wb >> 8) 2^-24 in  */
 /* [0, 1); r = sqrt(-2 ln u1); z_cos = r cos(2 pi u2), z_sin = r sin(2 pi u2) */
 /* ------------------------------------------------------------------------- */
-void or_box_muller_f32(uint32_t wa, uint32_t wb, float *zc, float *zs) {
-  float u1 = (float)((wa >> 8) + 1u) * 0x1p-24f;
+float or_radius_f32(uint32_t k24) {   /* u1 = (k24 + 1) 2^-24 */
+  float u1 = (float)((k24 & 0x00FFFFFFu) + 1u) * 0x1p-24f;
   float lnu = or_ln_f32(u1);
-  float r = sqrtf(-2.0f * lnu);
+  return sqrtf(-2.0f * lnu);
+}
+
+void or_box_muller_f32(uint32_t wa, uint32_t wb, float *zc, float *zs) {
+  float r = or_radius_f32(wa >> 8);
   float s, c;
   or_sincos_2pi_f32(wb >> 8, &s, &c);
   *zc = r * c;
@@ -247,6 +251,10 @@ void or_ln_f32_n(const float *x, float *y, uint64_t n) {
 
 void or_sincos_2pi_f32_n(const uint32_t *j24, float *s, float *c, uint64_t n) {
   for (uint64_t k = 0; k < n; k++) or_sincos_2pi_f32(j24[k], &s[k], &c[k]);
+}
+
+void or_radius_f32_n(const uint32_t *k24, float *r, uint64_t n) {
+  for (uint64_t k = 0; k < n; k++) r[k] = or_radius_f32(k24[k]);
 }
 
 void or_bf16_rne_n(const uint32_t *x, uint16_t *y, uint64_t n) {

@@ -78,6 +78,7 @@ void or_philox_block(uint64_t seed, uint64_t stream, uint64_t c, uint32_t out[4]
 /* Building blocks exposed so that tests can pin them one at a time. */
 float or_ln_f32(float x);
 void or_sincos_2pi_f32(uint32_t j24, float *s, float *c);
+float or_radius_f32(uint32_t k24);   /* Box-Muller radius for u1 = (k24 + 1) 2^-24 */
 void or_box_muller_f32(uint32_t wa, uint32_t wb, float *zc, float *zs);
 uint16_t or_bf16_rne(uint32_t f32_bits);
 uint32_t or_next_f32(uint32_t bits, int up);
@@ -86,6 +87,7 @@ uint16_t or_next_bf16(uint16_t bits, int up);
 void or_philox_blocks(uint64_t seed, uint64_t stream, uint64_t c0, uint64_t n, uint32_t *out);
 void or_ln_f32_n(const float *x, float *y, uint64_t n);
 void or_sincos_2pi_f32_n(const uint32_t *j24, float *s, float *c, uint64_t n);
+void or_radius_f32_n(const uint32_t *k24, float *r, uint64_t n);
 void or_bf16_rne_n(const uint32_t *x, uint16_t *y, uint64_t n);
 
 /* Synthesis of elements [offset, offset + n) into out (host memory). */

@@ -9,6 +9,7 @@ fallback: if the library is missing, importing this package fails.
 """
 import ctypes
 import os
+import threading
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsynthverify.so")
@@ -27,8 +28,8 @@ OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
 PROF_KINDS = {"synth": 0, "compare": 1, "perturb": 2, "finalize": 3}
 
 # every symbol include/sv.h declares
-SYMBOLS = ("sv_synth", "sv_compare", "sv_compare_batched", "sv_perturb", "sv_set_stream",
-           "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
+SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_compare", "sv_compare_batched", "sv_perturb",
+           "sv_eval_transform", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
 
 
 class DistParams(ctypes.Structure):
@@ -37,6 +38,12 @@ class DistParams(ctypes.Structure):
                 ("lo", ctypes.c_int64), ("hi", ctypes.c_int64),
                 ("p_nan", ctypes.c_double), ("p_inf", ctypes.c_double),
                 ("p_denorm", ctypes.c_double), ("p_zero", ctypes.c_double)]
+
+
+class SynthJob(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("stream_id", ctypes.c_uint64),
+                ("dtype", ctypes.c_int32), ("dist", ctypes.c_int32),
+                ("params", DistParams), ("n", ctypes.c_uint64), ("out", ctypes.c_void_p)]
 
 
 class Report(ctypes.Structure):
@@ -66,9 +73,11 @@ class PerturbPlan(ctypes.Structure):
 
 _u64, _i32, _vp, _dbl = ctypes.c_uint64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_double
 _lib.sv_synth.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u64, _vp]
+_lib.sv_synth_batched.argtypes = [ctypes.POINTER(SynthJob), ctypes.c_uint32]
 _lib.sv_compare.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(Report)]
 _lib.sv_compare_batched.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, ctypes.POINTER(Report)]
 _lib.sv_perturb.argtypes = [_u64, _u64, _i32, ctypes.POINTER(PerturbPlan), _u64, _vp, _vp]
+_lib.sv_eval_transform.argtypes = [_i32, _vp, _u64, _vp]
 _lib.sv_set_stream.argtypes = [_vp]
 _lib.sv_last_error.restype = ctypes.c_char_p
 _lib.sv_profile_enable.argtypes = [_i32]
@@ -93,17 +102,26 @@ def lib():
     return _lib
 
 
+_torch_mod = None
+_tdtype_codes = None
+_tls = threading.local()
+
+
 def _torch():
-    import torch
-    return torch
+    global _torch_mod, _tdtype_codes
+    if _torch_mod is None:
+        import torch
+        _torch_mod = torch
+        _tdtype_codes = {torch.float32: 0, torch.bfloat16: 1, torch.int32: 2}
+    return _torch_mod
 
 
 def dtype_code(t) -> int:
-    torch = _torch()
-    m = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32"}
-    if t.dtype not in m:
+    _torch()
+    code = _tdtype_codes.get(t.dtype)
+    if code is None:
         raise SVError(SV_ERR_UNSUPPORTED, "unsupported tensor dtype %s" % t.dtype)
-    return DTYPE_CODES[m[t.dtype]]
+    return code
 
 
 def _dev_ptr(t, name):
@@ -114,10 +132,25 @@ def _dev_ptr(t, name):
     return t.data_ptr()
 
 
-def _use_current_stream(t):
+def _run(t, fn, *args):
+    """Call fn(*args) with t's device current and torch's current stream of
+    that device handed to the library (only when it changed)."""
     torch = _torch()
-    with torch.cuda.device(t.device):
-        _check(_lib.sv_set_stream(torch.cuda.current_stream().cuda_stream))
+    dev = t.get_device()
+    if dev < 0:
+        raise SVError(SV_ERR_INVALID_ARG, "tensors must be on the GPU")
+    prev = torch._C._cuda_getDevice()
+    if prev != dev:
+        torch.cuda.set_device(dev)
+    try:
+        stream = torch._C._cuda_getCurrentRawStream(dev)
+        if getattr(_tls, "stream", None) != (dev, stream):
+            _check(_lib.sv_set_stream(stream))
+            _tls.stream = (dev, stream)
+        _check(fn(*args))
+    finally:
+        if prev != dev:
+            torch.cuda.set_device(prev)
 
 
 def dist_params(**kw) -> DistParams:
@@ -129,24 +162,29 @@ def dist_params(**kw) -> DistParams:
 
 def synth(out, seed: int, stream_id: int, dist: str, **params):
     """Fill `out` (contiguous device tensor) with the seeded sequence (asynchronous)."""
-    _use_current_stream(out)
-    torch = _torch()
-    with torch.cuda.device(out.device):
-        _check(_lib.sv_synth(seed, stream_id, dtype_code(out), DIST_CODES[dist],
-                             ctypes.byref(dist_params(**params)), out.numel(), _dev_ptr(out, "out")))
+    _run(out, _lib.sv_synth, seed, stream_id, dtype_code(out), DIST_CODES[dist],
+         ctypes.byref(dist_params(**params)), out.numel(), _dev_ptr(out, "out"))
     return out
+
+
+def synth_batched(jobs):
+    """jobs: list of (out, seed, stream_id, dist, params dict); one launch (asynchronous)."""
+    if not jobs:
+        return
+    arr = (SynthJob * len(jobs))()
+    for k, (out, seed, stream_id, dist, params) in enumerate(jobs):
+        arr[k] = SynthJob(seed, stream_id, dtype_code(out), DIST_CODES[dist], dist_params(**params),
+                          out.numel(), _dev_ptr(out, "out") if out.numel() else None)
+    _run(jobs[0][0], _lib.sv_synth_batched, arr, len(jobs))
 
 
 def compare(ref, cand, rtol: float, atol: float, equal_nan: bool = False) -> dict:
     """Eq. (1) on every element of (ref, cand) -> report dict (synchronous)."""
     if ref.dtype != cand.dtype or ref.numel() != cand.numel():
         raise SVError(SV_ERR_INVALID_ARG, "ref and cand must have the same dtype and size")
-    _use_current_stream(ref)
     rep = Report()
-    torch = _torch()
-    with torch.cuda.device(ref.device):
-        _check(_lib.sv_compare(_dev_ptr(ref, "ref"), _dev_ptr(cand, "cand"), ref.numel(), dtype_code(ref),
-                               rtol, atol, int(bool(equal_nan)), ctypes.byref(rep)))
+    _run(ref, _lib.sv_compare, _dev_ptr(ref, "ref"), _dev_ptr(cand, "cand"), ref.numel(), dtype_code(ref),
+         rtol, atol, int(bool(equal_nan)), ctypes.byref(rep))
     return rep.as_dict()
 
 
@@ -162,11 +200,7 @@ def compare_batched(segments) -> list:
                          _dev_ptr(cand, "cand") if cand.numel() else None,
                          ref.numel(), dtype_code(ref), rtol, atol, int(bool(eqn)))
     reps = (Report * len(segments))()
-    dev = segments[0][0].device
-    _use_current_stream(segments[0][0])
-    torch = _torch()
-    with torch.cuda.device(dev):
-        _check(_lib.sv_compare_batched(arr, len(segments), reps))
+    _run(segments[0][0], _lib.sv_compare_batched, arr, len(segments), reps)
     return [reps[k].as_dict() for k in range(len(segments))]
 
 
@@ -179,12 +213,20 @@ def perturb(ref, cand, seed: int, stream_id: int, op: str, p: float = 0.0, value
     idx_arr = np.ascontiguousarray(idx if idx is not None else [], dtype=np.uint64)
     plan = PerturbPlan(OP_CODES[op], p, value, bits & 0xFFFFFFFF,
                        idx_arr.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)), idx_arr.size)
-    _use_current_stream(ref)
-    torch = _torch()
-    with torch.cuda.device(ref.device):
-        _check(_lib.sv_perturb(seed, stream_id, dtype_code(ref), ctypes.byref(plan), ref.numel(),
-                               _dev_ptr(ref, "ref"), _dev_ptr(cand, "cand")))
+    _run(ref, _lib.sv_perturb, seed, stream_id, dtype_code(ref), ctypes.byref(plan), ref.numel(),
+         _dev_ptr(ref, "ref"), _dev_ptr(cand, "cand"))
     return cand
+
+
+EVAL = {"ln": 0, "radius": 1, "sin": 2, "cos": 3}
+
+
+def eval_transform(which: str, inp, out):
+    """Diagnostics: one building block of the normal transform on int32 device tensors (asynchronous)."""
+    if inp.numel() != out.numel():
+        raise SVError(SV_ERR_INVALID_ARG, "in and out differ in size")
+    _run(inp, _lib.sv_eval_transform, EVAL[which], _dev_ptr(inp, "in"), inp.numel(), _dev_ptr(out, "out"))
+    return out
 
 
 def profile_enable(on: bool = True):

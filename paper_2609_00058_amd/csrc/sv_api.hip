@@ -59,6 +59,13 @@ struct DeviceState {
   size_t h_reports_cap = 0;
   uint64_t *h_idx = nullptr;
   size_t h_idx_cap = 0;
+  SynthJob *synth_table = nullptr;   // batched synthesis job table
+  size_t synth_table_cap = 0;
+  SynthJob *h_synth = nullptr;       // its pinned staging
+  size_t h_synth_cap = 0;
+  hipEvent_t synth_copied = nullptr; // staging -> table copy of the last batch done
+  hipEvent_t synth_done = nullptr;   // last batch kernel done (table free to overwrite)
+  bool synth_pending = false;        // the two events above have been recorded
 };
 
 std::mutex g_devices_mu;
@@ -269,7 +276,7 @@ int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_s
     push_record(SV_PROF_FINALIZE, e1, e2);
   }
   e = hipStreamSynchronize(st);
-  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize after the check");
+  if (e != hipSuccess) return hip_fail(e, "waiting for the check");
   for (uint32_t k = 0; k < nseg; ++k) {
     const uint64_t n = segs ? segs[k].n : args.single.n;
     if (n)
@@ -280,23 +287,10 @@ int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_s
   return SV_OK;
 }
 
-}  // namespace
-
-// =================================================================== C ABI
-extern "C" {
-
-int sv_abi_version(void) { return SV_ABI_VERSION; }
-
-const char *sv_last_error(void) { return t_error.c_str(); }
-
-int sv_set_stream(void *hip_stream) {
-  t_stream = (hipStream_t)hip_stream;
-  return SV_OK;
-}
-
-int sv_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, const sv_dist_params *params,
-             uint64_t n, void *out) {
-  t_error.clear();
+// Validates the arguments of one synthesis and prepares its kernel
+// parameters; issues no HIP call.
+int prepare_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, const sv_dist_params *params,
+                  uint64_t n, void *out, SynthParams *pp) {
   if (!valid_dtype(dtype)) return fail(SV_ERR_UNSUPPORTED, "sv_synth: unknown dtype %d", dtype);
   if (dist < SV_UNIFORM || dist > SV_SPECIAL) return fail(SV_ERR_UNSUPPORTED, "sv_synth: unknown dist %d", dist);
   if ((dist == SV_INT_RANGE) != (dtype == SV_I32))
@@ -304,7 +298,7 @@ int sv_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, con
   if (!params) return fail(SV_ERR_INVALID_ARG, "sv_synth: params is NULL");
   int rc = check_tensor(out, n, dtype, "sv_synth out");
   if (rc) return rc;
-  SynthParams p;
+  SynthParams &p = *pp;
   std::memset(&p, 0, sizeof p);
   p.k0 = (uint32_t)seed;
   p.k1 = (uint32_t)(seed >> 32);
@@ -344,6 +338,29 @@ int sv_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, con
     p.lo = params->lo;
     p.range = (uint64_t)(params->hi - params->lo) + 1u;
   }
+  return SV_OK;
+}
+
+}  // namespace
+
+// =================================================================== C ABI
+extern "C" {
+
+int sv_abi_version(void) { return SV_ABI_VERSION; }
+
+const char *sv_last_error(void) { return t_error.c_str(); }
+
+int sv_set_stream(void *hip_stream) {
+  t_stream = (hipStream_t)hip_stream;
+  return SV_OK;
+}
+
+int sv_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, const sv_dist_params *params,
+             uint64_t n, void *out) {
+  t_error.clear();
+  SynthParams p;
+  int rc = prepare_synth(seed, stream_id, dtype, dist, params, n, out, &p);
+  if (rc) return rc;
   if (!n) return SV_OK;
   int cus;
   rc = cu_count(&cus);
@@ -359,6 +376,74 @@ int sv_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, con
     (void)hipEventRecord(e1, t_stream);
     push_record(SV_PROF_SYNTH, e0, e1);
   }
+  return SV_OK;
+}
+
+int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
+  t_error.clear();
+  if (njobs == 0) return SV_OK;
+  if (!jobs) return fail(SV_ERR_INVALID_ARG, "sv_synth_batched: jobs is NULL");
+  std::vector<SynthParams> params(njobs);
+  uint64_t tiles = 0;
+  for (uint32_t k = 0; k < njobs; ++k) {
+    const sv_synth_job &j = jobs[k];
+    int rc = prepare_synth(j.seed, j.stream_id, j.dtype, j.dist, &j.params, j.n, j.out, &params[k]);
+    if (rc) {
+      t_error = "job " + std::to_string(k) + ": " + t_error;
+      return rc;
+    }
+    const uint64_t per = j.dtype == SV_BF16 ? 8 : 4;
+    tiles += ((j.n + per - 1) / per + kBlock - 1) / kBlock;
+  }
+  if (tiles == 0) return SV_OK;
+  DeviceState *ds;
+  int rc = current_device(&ds);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lock(ds->mu);
+  hipStream_t st = t_stream;
+  if (!ds->synth_copied) {
+    SV_HIP(hipEventCreateWithFlags(&ds->synth_copied, hipEventDisableTiming), "hipEventCreate");
+    SV_HIP(hipEventCreateWithFlags(&ds->synth_done, hipEventDisableTiming), "hipEventCreate");
+  }
+  if (ds->synth_pending) {
+    // the staging buffer is rewritten below: its last copy must have left it;
+    // the device table is rewritten on this stream after the last batch read it
+    SV_HIP(hipEventSynchronize(ds->synth_copied), "wait for the previous job-table copy");
+    SV_HIP(hipStreamWaitEvent(st, ds->synth_done, 0), "order after the previous batch");
+  }
+  rc = ensure_pinned(ds->h_synth, ds->h_synth_cap, njobs, "job table staging");
+  if (!rc) rc = ensure_device(ds->synth_table, ds->synth_table_cap, njobs, "job table");
+  if (rc) return rc;
+  uint64_t begin = 0;
+  for (uint32_t k = 0; k < njobs; ++k) {
+    const sv_synth_job &j = jobs[k];
+    const uint64_t per = j.dtype == SV_BF16 ? 8 : 4;
+    SynthJob &d = ds->h_synth[k];
+    d.p = params[k];
+    d.out = j.out;
+    d.n = j.n;
+    d.nvec = (j.n + per - 1) / per;
+    d.tile_begin = begin;
+    d.kind = j.dist * 4 + j.dtype;
+    d.vec_ok = ((uintptr_t)j.out & 15u) == 0 ? 1 : 0;
+    begin += (d.nvec + kBlock - 1) / kBlock;
+  }
+  SV_HIP(hipMemcpyAsync(ds->synth_table, ds->h_synth, njobs * sizeof(SynthJob), hipMemcpyHostToDevice, st),
+         "job table copy to device");
+  SV_HIP(hipEventRecord(ds->synth_copied, st), "hipEventRecord");
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (g_prof_on.load()) {
+    e0 = take_event();
+    e1 = take_event();
+    if (e0) (void)hipEventRecord(e0, st);
+  }
+  SV_HIP(launch_synth_batched(ds->synth_table, njobs, tiles, ds->cus, st), "batched synthesis kernel launch");
+  if (e0 && e1) {
+    (void)hipEventRecord(e1, st);
+    push_record(SV_PROF_SYNTH, e0, e1);
+  }
+  SV_HIP(hipEventRecord(ds->synth_done, st), "hipEventRecord");
+  ds->synth_pending = true;
   return SV_OK;
 }
 
@@ -490,6 +575,20 @@ int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_pertur
   return SV_OK;
 }
 
+int sv_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out) {
+  t_error.clear();
+  if (which < SV_EVAL_LN || which > SV_EVAL_COS)
+    return fail(SV_ERR_UNSUPPORTED, "sv_eval_transform: unknown transform %d", which);
+  int rc = check_tensor(in, n, SV_F32, "sv_eval_transform in");
+  if (!rc) rc = check_tensor(out, n, SV_F32, "sv_eval_transform out");
+  if (rc || !n) return rc;
+  int cus;
+  rc = cu_count(&cus);
+  if (rc) return rc;
+  SV_HIP(launch_eval_transform(which, in, n, out, cus, t_stream), "transform kernel launch");
+  return SV_OK;
+}
+
 int sv_profile_enable(int32_t on) {
   g_prof_on.store(on ? 1 : 0);
   return SV_OK;
@@ -540,6 +639,13 @@ int sv_shutdown(void) {
     if (s->h_table) (void)hipHostFree(s->h_table);
     if (s->h_reports) (void)hipHostFree(s->h_reports);
     if (s->h_idx) (void)hipHostFree(s->h_idx);
+    if (s->synth_table) (void)hipFree(s->synth_table);
+    if (s->h_synth) (void)hipHostFree(s->h_synth);
+    if (s->synth_copied) (void)hipEventDestroy(s->synth_copied);
+    if (s->synth_done) (void)hipEventDestroy(s->synth_done);
+    s->synth_table = nullptr; s->h_synth = nullptr; s->synth_copied = nullptr; s->synth_done = nullptr;
+    s->synth_table_cap = s->h_synth_cap = 0;
+    s->synth_pending = false;
     s->partials = nullptr; s->table = nullptr; s->idx = nullptr;
     s->h_table = nullptr; s->h_reports = nullptr; s->d_reports = nullptr; s->h_idx = nullptr;
     s->partials_cap = s->table_cap = s->idx_cap = 0;

@@ -296,30 +296,42 @@ __device__ __forceinline__ uint32_t find_segment(const SegDesc *segs, uint32_t n
 }
 
 // One workgroup per segment: combine the partials of the workgroups that
-// touched it (thread t takes slots b0 + t, b0 + t + 256, ... in order, then a
+// touched it (thread t takes slots b0 + t, b0 + t + 1024, ... in order, then a
 // fixed shuffle tree and the waves in order) and write the report into
 // host-mapped memory.  Running after the check kernel, it sees every partial
 // without any device-scope fence inside the check (on gfx950 such a fence
 // writes back the L2 of the issuing XCD, which thousands of workgroups cannot
 // afford).
+constexpr int kFinBlock = 1024;                  // finalize threads per segment
+constexpr int kFinWaves = kFinBlock / kWave;
+
 template <bool kSingle>
-__global__ __launch_bounds__(kBlock) void finalize_kernel(CompareArgs args) {
-  __shared__ Partial lds[kWavesPerBlock];
+__global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
+  __shared__ Partial lds[kFinWaves];
   const uint32_t s = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const SegDesc sd = kSingle ? args.single : args.segs[s];
   const uint64_t units = units_of(sd.dtype, sd.n);
   if (units == 0) return;            // empty segments are reported by the host
   const uint64_t b0 = sd.unit_begin / args.chunk;
   const uint64_t b1 = (sd.unit_begin + units - 1) / args.chunk;
+  const Partial *P = args.partials + s;
   Partial acc = empty_partial();
-  for (uint64_t b = b0 + tid; b <= b1; b += kBlock) merge(acc, args.partials[b + s]);
+  uint64_t b = b0 + tid;
+  for (; b + 3 * kFinBlock <= b1; b += 4 * kFinBlock) {   // four partials in flight, merged in slot order
+    const Partial p0 = P[b], p1 = P[b + kFinBlock], p2 = P[b + 2 * kFinBlock], p3 = P[b + 3 * kFinBlock];
+    merge(acc, p0);
+    merge(acc, p1);
+    merge(acc, p2);
+    merge(acc, p3);
+  }
+  for (; b <= b1; b += kFinBlock) merge(acc, P[b]);
   wave_merge(acc);
   if (lane == 0) lds[wave] = acc;
   __syncthreads();
   if (tid == 0) {
     Partial r = lds[0];
 #pragma unroll
-    for (int w = 1; w < kWavesPerBlock; ++w) merge(r, lds[w]);
+    for (int w = 1; w < kFinWaves; ++w) merge(r, lds[w]);
     sv_report rep;
     rep.n = sd.n;
     rep.mismatches = r.mism;
@@ -383,9 +395,9 @@ static void launch_masked(const CompareArgs &args, uint32_t nblocks, hipStream_t
     hipLaunchKernelGGL((compare_kernel<false, kMask>), dim3(nblocks), dim3(kBlock), 0, stream, args);
   if (ev_mid) (void)hipEventRecord(ev_mid, stream);
   if (single)
-    hipLaunchKernelGGL(finalize_kernel<true>, dim3(1), dim3(kBlock), 0, stream, args);
+    hipLaunchKernelGGL(finalize_kernel<true>, dim3(1), dim3(kFinBlock), 0, stream, args);
   else
-    hipLaunchKernelGGL(finalize_kernel<false>, dim3(args.nseg), dim3(kBlock), 0, stream, args);
+    hipLaunchKernelGGL(finalize_kernel<false>, dim3(args.nseg), dim3(kFinBlock), 0, stream, args);
 }
 
 hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream,

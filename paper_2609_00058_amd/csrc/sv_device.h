@@ -2,10 +2,11 @@
 //
 // Counter-based generation and the distribution transforms behind sv_synth
 // and sv_perturb.  Every floating-point step is one IEEE-754 fp32 operation
-// rounded to nearest-even: the library is compiled with -ffp-contract=off, no
-// fast-math, fp32 denormals kept, and correctly rounded fp32 division and
-// square root, so a value depends only on (seed, stream, index) and is the same
-// bits on any machine that performs the same operation sequence.
+// rounded to nearest-even (a fused multiply-add where written as one): the
+// library is compiled with -ffp-contract=off, no fast-math, fp32 denormals
+// kept, and correctly rounded fp32 division and square root, so a value
+// depends only on (seed, stream, index) and is the same bits on any machine
+// that performs the same operation sequence.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -86,80 +87,96 @@ __device__ __forceinline__ uint32_t bf16_rne(uint32_t x) {
 __device__ __forceinline__ float unit24(uint32_t w) { return (float)(w >> 8) * 0x1p-24f; }
 
 // ---------------------------------------------------------------------------
-// ln of a positive normal fp32 value.  Write x = 2^e m, m in [1, 2), and
-// halve m (raising e) when it exceeds sqrt(2), so m lies in [sqrt(1/2),
-// sqrt(2)).  Then ln m = 2 atanh(s) with s = (m - 1)/(m + 1), |s| < 0.172,
-// summed as s (2 + s^2 (2/3 + s^2 (2/5 + s^2 (2/7 + s^2 2/9)))), and
-// ln x = e ln2_hi + (ln m + e ln2_lo) where ln2_hi = 45426/2^16 (so e ln2_hi
-// is exact) and ln2_lo is the fp32 rounding of ln 2 - ln2_hi.  Constants are
-// the fp32 roundings of the stated exact values.
+// ln of a positive normal fp32 value.  x = 2^e 1.M; when 1.M >= fp32(sqrt 2)
+// the mantissa is halved and e raised, so m lies in [sqrt(1/2), sqrt(2)) and
+// f = m - 1 is exact.  Both follow from one integer offset: subtracting the
+// bits of fp32(sqrt(1/2)) = 0x3F3504F3 leaves e in the bits above the
+// mantissa field (arithmetic shift) and m - fp32(sqrt(1/2)) below it.
+// ln m = f P(f), P the degree-9 Chebyshev interpolant of ln(1 + f) / f on
+// [sqrt(1/2) - 1, sqrt(2) - 1] with coefficients rounded to fp32, by fused
+// multiply-add Horner steps; then ln x = e ln2_hi + (ln m + e ln2_lo),
+// ln2_hi = 45426/2^16 (e ln2_hi exact), ln2_lo the fp32 rounding of
+// ln 2 - ln2_hi, both sums fused with their products.  No division.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float ln_f32(float x) {
-  const uint32_t bits = as_u32(x);
-  int e = (int)(bits >> 23) - 127;                      // x > 0
-  float m = as_f32((bits & 0x007FFFFFu) | 0x3F800000u);
-  if (m > 0x1.6a09e6p+0f) {                            // sqrt(2)
-    m = m * 0.5f;
-    e = e + 1;
-  }
+  const int32_t ix = (int32_t)as_u32(x) - 0x3F3504F3;
+  const float ef = (float)(ix >> 23);
+  const float m = as_f32((uint32_t)(ix & 0x007FFFFF) + 0x3F3504F3u);
   const float f = m - 1.0f;
-  const float s = f / (2.0f + f);
-  const float z = s * s;
-  float p = 0x1.c71c72p-3f;                              // 2/9
-  p = 0x1.24924ap-2f + z * p;                            // 2/7
-  p = 0x1.99999ap-2f + z * p;                            // 2/5
-  p = 0x1.555556p-1f + z * p;                            // 2/3
-  p = 2.0f + z * p;
-  const float lnm = s * p;
-  const float ef = (float)e;
-  return ef * 0x1.62e4p-1f + (lnm + ef * 0x1.7f7d1cp-20f);   // ln2 hi, lo
+  float p = -0x1.31335ap-4f;                             // degree 9
+  p = __builtin_fmaf(p, f, 0x1.064786p-3f);
+  p = __builtin_fmaf(p, f, -0x1.0fb036p-3f);
+  p = __builtin_fmaf(p, f, 0x1.22cf10p-3f);
+  p = __builtin_fmaf(p, f, -0x1.5423b0p-3f);
+  p = __builtin_fmaf(p, f, 0x1.999e86p-3f);
+  p = __builtin_fmaf(p, f, -0x1.000424p-2f);
+  p = __builtin_fmaf(p, f, 0x1.55555ep-2f);
+  p = __builtin_fmaf(p, f, -0x1.fffff8p-2f);
+  p = __builtin_fmaf(p, f, 1.0f);                        // degree 0
+  const float lnm = f * p;
+  return __builtin_fmaf(ef, 0x1.62e4p-1f, __builtin_fmaf(ef, 0x1.7f7d1cp-20f, lnm));   // ln2 hi, lo
 }
 
-// sin(pi f / 2) and cos(pi f / 2) for f in [0, 1/2], Taylor series in f whose
-// coefficients are (-1)^k (pi/2)^n / n! rounded to fp32.
-__device__ __forceinline__ float sin_q(float f) {
-  const float f2 = f * f;
-  float p = 0x1.507834p-13f;           //  (pi/2)^9 / 9!
-  p = -0x1.32d2ccp-8f + f2 * p;        // -(pi/2)^7 / 7!
-  p = 0x1.466bc6p-4f + f2 * p;         //  (pi/2)^5 / 5!
-  p = -0x1.4abbcep-1f + f2 * p;        // -(pi/2)^3 / 3!
-  p = 0x1.921fb6p+0f + f2 * p;         //  pi/2
+// IEEE (correctly rounded) square root of v in {0} and [2^-126, 2^126]: the
+// hardware square root is within one ulp, and of it and its two neighbours
+// the one whose fused residual v - s' s has the right sign is the rounded
+// root (no input here is denormal, infinite or negative, so no scaling).
+__device__ __forceinline__ float sqrt_rn(float v) {
+  float s = __builtin_amdgcn_sqrtf(v);
+  const float sd = as_f32(as_u32(s) - 1u), su = as_f32(as_u32(s) + 1u);
+  const float rd = __builtin_fmaf(-sd, s, v), ru = __builtin_fmaf(-su, s, v);
+  s = (rd <= 0.0f) ? sd : s;
+  s = (ru > 0.0f) ? su : s;
+  return s;
+}
+
+// sin(pi f / 2) and cos(pi f / 2) for f in [0, 1/2]: Taylor series in f whose
+// coefficients are (-1)^k (pi/2)^n / n! rounded to fp32, Horner in f^2 with
+// fused multiply-adds.
+__device__ __forceinline__ float sin_q(float f, float f2) {
+  float p = 0x1.507834p-13f;                     //  (pi/2)^9 / 9!
+  p = __builtin_fmaf(p, f2, -0x1.32d2ccp-8f);    // -(pi/2)^7 / 7!
+  p = __builtin_fmaf(p, f2, 0x1.466bc6p-4f);     //  (pi/2)^5 / 5!
+  p = __builtin_fmaf(p, f2, -0x1.4abbcep-1f);    // -(pi/2)^3 / 3!
+  p = __builtin_fmaf(p, f2, 0x1.921fb6p+0f);     //  pi/2
   return f * p;
 }
 
-__device__ __forceinline__ float cos_q(float f) {
-  const float f2 = f * f;
-  float p = -0x1.a6d1f2p-16f;          // -(pi/2)^10 / 10!
-  p = 0x1.e1f506p-11f + f2 * p;        //  (pi/2)^8 / 8!
-  p = -0x1.55d3c8p-6f + f2 * p;        // -(pi/2)^6 / 6!
-  p = 0x1.03c1f0p-2f + f2 * p;         //  (pi/2)^4 / 4!
-  p = -0x1.3bd3ccp+0f + f2 * p;        // -(pi/2)^2 / 2!
-  return 1.0f + f2 * p;
+__device__ __forceinline__ float cos_q(float f2) {
+  float p = -0x1.a6d1f2p-16f;                    // -(pi/2)^10 / 10!
+  p = __builtin_fmaf(p, f2, 0x1.e1f506p-11f);    //  (pi/2)^8 / 8!
+  p = __builtin_fmaf(p, f2, -0x1.55d3c8p-6f);    // -(pi/2)^6 / 6!
+  p = __builtin_fmaf(p, f2, 0x1.03c1f0p-2f);     //  (pi/2)^4 / 4!
+  p = __builtin_fmaf(p, f2, -0x1.3bd3ccp+0f);    // -(pi/2)^2 / 2!
+  return __builtin_fmaf(f2, p, 1.0f);
 }
 
 // sin and cos of 2 pi j / 2^24 for j < 2^24: quadrant q = j >> 22, fraction
 // f = (j mod 2^22) / 2^22; above f = 1/2 the series run on the exact
-// complement 1 - f with sine and cosine exchanged; the quadrant rotates the
-// pair (negation is exact).
+// complement 1 - f.  The magnitudes are the two series values, exchanged when
+// exactly one of "odd quadrant" and "complement" holds; sine is negative in
+// quadrants 2 and 3, cosine in 1 and 2 (sign bits set by XOR, as negation).
 __device__ __forceinline__ void sincos_2pi(uint32_t j, float &s, float &c) {
   const uint32_t q = j >> 22;
   const uint32_t fj = j & 0x003FFFFFu;
-  const bool lower = fj <= 0x00200000u;
-  const float f = (float)(lower ? fj : 0x00400000u - fj) * 0x1p-22f;
-  const float a = sin_q(f), b = cos_q(f);
-  const float S = lower ? a : b;       // sin(pi fj / 2^23)
-  const float C = lower ? b : a;       // cos(pi fj / 2^23)
-  const float sq = (q & 1u) ? C : S;
-  const float cq = (q & 1u) ? -S : C;
-  s = (q & 2u) ? -sq : sq;
-  c = (q & 2u) ? -cq : cq;
+  const bool upper = fj > 0x00200000u;
+  const float f = (float)(upper ? 0x00400000u - fj : fj) * 0x1p-22f;
+  const float f2 = f * f;
+  const float a = sin_q(f, f2), b = cos_q(f2);
+  const bool swap = ((q & 1u) != 0u) != upper;
+  s = as_f32(as_u32(swap ? b : a) ^ ((q & 2u) << 30));
+  c = as_f32(as_u32(swap ? a : b) ^ (((q + 1u) & 2u) << 30));
 }
 
 // Box-Muller pair from two words: u1 = ((wa >> 8) + 1) 2^-24 in (0, 1],
 // u2 = (wb >> 8) 2^-24; r = sqrt(-2 ln u1); (r cos 2 pi u2, r sin 2 pi u2).
+__device__ __forceinline__ float bm_radius(uint32_t k24) {   // u1 = (k24 + 1) 2^-24
+  const float u1 = (float)(k24 + 1u) * 0x1p-24f;
+  return sqrt_rn(-2.0f * ln_f32(u1));
+}
+
 __device__ __forceinline__ void box_muller(uint32_t wa, uint32_t wb, float &zc, float &zs) {
-  const float u1 = (float)((wa >> 8) + 1u) * 0x1p-24f;
-  const float r = sqrtf(-2.0f * ln_f32(u1));
+  const float r = bm_radius(wa >> 8);
   float s, c;
   sincos_2pi(wb >> 8, s, c);
   zc = r * c;

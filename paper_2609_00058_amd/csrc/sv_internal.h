@@ -40,6 +40,25 @@ struct SynthParams {
 hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint64_t n, void *out,
                         int cus, hipStream_t stream);
 
+hipError_t launch_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out, int cus,
+                                 hipStream_t stream);
+
+// One job of a batched synthesis (device table).  Output vector u of a job
+// (16 bytes, V elements) covers elements [u V, u V + V); tiles of kBlock
+// vectors are laid end to end over the jobs.
+struct SynthJob {
+  SynthParams p;
+  void *out;
+  uint64_t n;
+  uint64_t nvec;                // ceil(n / V)
+  uint64_t tile_begin;          // first tile of this job
+  int32_t kind;                 // dist * 4 + dtype
+  int32_t vec_ok;               // out is 16-byte aligned
+};
+
+hipError_t launch_synth_batched(const SynthJob *jobs, uint32_t njobs, uint64_t total_tiles, int cus,
+                                hipStream_t stream);
+
 // ----------------------------------------------------------------- candidates
 struct PerturbParams {
   uint32_t k0, k1, s0, s1;

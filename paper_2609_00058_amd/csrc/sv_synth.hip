@@ -37,10 +37,10 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
     float c0, s0, c1, s1;
     box_muller(w.x, w.y, c0, s0);
     box_muller(w.z, w.w, c1, s1);
-    v[0] = as_u32(p.mean + p.std * c0);
-    v[1] = as_u32(p.mean + p.std * s0);
-    v[2] = as_u32(p.mean + p.std * c1);
-    v[3] = as_u32(p.mean + p.std * s1);
+    v[0] = as_u32(__builtin_fmaf(p.std, c0, p.mean));   // mean + std z, one rounding
+    v[1] = as_u32(__builtin_fmaf(p.std, s0, p.mean));
+    v[2] = as_u32(__builtin_fmaf(p.std, c1, p.mean));
+    v[3] = as_u32(__builtin_fmaf(p.std, s1, p.mean));
   } else if constexpr (DIST == SV_INT_RANGE) {
     // Lemire's multiply-shift: lo + floor(R * range / 2^64), R a 64-bit word
     const uint64_t r0 = ((uint64_t)w.y << 32) | w.x;
@@ -65,7 +65,7 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
     } else {
       float zc, zs;
       box_muller(w.z, w.w, zc, zs);
-      out = as_u32(p.mean + p.std * zc);
+      out = as_u32(__builtin_fmaf(p.std, zc, p.mean));
     }
     v[0] = out;
   }
@@ -156,6 +156,102 @@ hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint6
     case SV_SPECIAL * 4 + SV_BF16: return launch_typed<SV_SPECIAL, SV_BF16>(p, n, out, cus, stream);
     default: return hipErrorInvalidValue;
   }
+}
+
+// ------------------------------------------------------------ diagnostics
+__global__ __launch_bounds__(kBlock) void eval_transform_kernel(int32_t which, const uint32_t *__restrict__ in,
+                                                                uint64_t n, uint32_t *__restrict__ out) {
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
+    const uint32_t k = in[i] & 0x00FFFFFFu;
+    float v;
+    if (which == SV_EVAL_LN) {
+      v = ln_f32((float)(k + 1u) * 0x1p-24f);
+    } else if (which == SV_EVAL_RADIUS) {
+      v = bm_radius(k);
+    } else {
+      float sn, cs;
+      sincos_2pi(k, sn, cs);
+      v = which == SV_EVAL_SIN ? sn : cs;
+    }
+    out[i] = as_u32(v);
+  }
+}
+
+hipError_t launch_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out, int cus,
+                                 hipStream_t stream) {
+  const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, (uint64_t)cus * 8);
+  hipLaunchKernelGGL(eval_transform_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, stream, which, in, n, out);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ batched
+// Output vector u of one job: the B Philox blocks that cover it, then one
+// 16-byte store, or element stores where the vector is partial or the
+// output is not 16-byte aligned.
+template <int DIST, int DT>
+__device__ __forceinline__ void synth_vector(const SynthParams &p, void *out, uint64_t n, uint64_t u,
+                                             bool vec_ok) {
+  constexpr int E = DistTraits<DIST>::E;
+  constexpr int V = DT == SV_BF16 ? 8 : 4;
+  constexpr int B = V / E;
+  uint32_t v[V];
+#pragma unroll
+  for (int b = 0; b < B; ++b) block_values<DIST>(p, u * B + b, v + b * E);
+  if (vec_ok && (u + 1) * V <= n) {
+    u32x4 o;
+    if constexpr (DT == SV_BF16) {
+      o.x = bf16_rne(v[0]) | (bf16_rne(v[1]) << 16);
+      o.y = bf16_rne(v[2]) | (bf16_rne(v[3]) << 16);
+      o.z = bf16_rne(v[4]) | (bf16_rne(v[5]) << 16);
+      o.w = bf16_rne(v[6]) | (bf16_rne(v[7]) << 16);
+    } else {
+      o = u32x4{v[0], v[1], v[2], v[3]};
+    }
+    ((u32x4 *)out)[u] = o;
+  } else {
+#pragma unroll
+    for (int j = 0; j < V; ++j)
+      if (u * V + j < n) store_elem<DIST, DT>(out, u * V + j, v[j]);
+  }
+}
+
+// Job holding tile t: the last job whose first tile is <= t (jobs without
+// elements share their successor's first tile and are skipped by this rule).
+__device__ __forceinline__ uint32_t find_job(const SynthJob *jobs, uint32_t njobs, uint64_t t) {
+  uint32_t lo = 0, hi = njobs;
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) / 2;
+    if (jobs[mid].tile_begin <= t) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(kBlock) void synth_batched_kernel(const SynthJob *__restrict__ jobs, uint32_t njobs,
+                                                               uint64_t total_tiles) {
+  for (uint64_t t = blockIdx.x; t < total_tiles; t += gridDim.x) {
+    const SynthJob &job = jobs[find_job(jobs, njobs, t)];
+    const uint64_t u = (t - job.tile_begin) * kBlock + threadIdx.x;
+    if (u >= job.nvec) continue;
+    const bool ok = job.vec_ok != 0;
+    switch (job.kind) {
+      case SV_UNIFORM * 4 + SV_F32: synth_vector<SV_UNIFORM, SV_F32>(job.p, job.out, job.n, u, ok); break;
+      case SV_UNIFORM * 4 + SV_BF16: synth_vector<SV_UNIFORM, SV_BF16>(job.p, job.out, job.n, u, ok); break;
+      case SV_NORMAL * 4 + SV_F32: synth_vector<SV_NORMAL, SV_F32>(job.p, job.out, job.n, u, ok); break;
+      case SV_NORMAL * 4 + SV_BF16: synth_vector<SV_NORMAL, SV_BF16>(job.p, job.out, job.n, u, ok); break;
+      case SV_INT_RANGE * 4 + SV_I32: synth_vector<SV_INT_RANGE, SV_I32>(job.p, job.out, job.n, u, ok); break;
+      case SV_SPECIAL * 4 + SV_F32: synth_vector<SV_SPECIAL, SV_F32>(job.p, job.out, job.n, u, ok); break;
+      default: synth_vector<SV_SPECIAL, SV_BF16>(job.p, job.out, job.n, u, ok); break;
+    }
+  }
+}
+
+hipError_t launch_synth_batched(const SynthJob *jobs, uint32_t njobs, uint64_t total_tiles, int cus,
+                                hipStream_t stream) {
+  const uint64_t blocks = std::min<uint64_t>(total_tiles, (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU);
+  hipLaunchKernelGGL(synth_batched_kernel, dim3((unsigned)blocks), dim3(kBlock), 0, stream, jobs, njobs,
+                     total_tiles);
+  return hipGetLastError();
 }
 
 }  // namespace sv

@@ -51,7 +51,8 @@ def test_abi_version_and_enums_match_header(svlib):
 def test_struct_layouts_match_the_c_compiler(svlib, tmp_path):
     # sizes and field offsets of every ABI struct, as gcc lays them out from include/sv.h
     mirrors = {"sv_report": svlib.Report, "sv_segment": svlib.Segment,
-               "sv_dist_params": svlib.DistParams, "sv_perturb_plan": svlib.PerturbPlan}
+               "sv_dist_params": svlib.DistParams, "sv_perturb_plan": svlib.PerturbPlan,
+               "sv_synth_job": svlib.SynthJob}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "sv.h"', "int main(void) {"]
     for cname, mirror in mirrors.items():
         lines.append('printf("%s %%zu\\n", sizeof(%s));' % (cname, cname))
@@ -96,6 +97,22 @@ def test_synth_argument_errors_before_any_device_work(svlib):
     assert _synth(L, svlib, 2, 2, lo=0, hi=1 << 31) == INV                  # beyond int32
     assert "int32" in L.sv_last_error().decode()
     assert _synth(L, svlib, 0, 0, n=0, out=0, a=0.0, b=1.0) == svlib.SV_OK  # nothing to do
+
+
+def test_synth_batched_argument_errors(svlib):
+    L = svlib.lib()
+    jobs = (svlib.SynthJob * 3)()
+    assert L.sv_synth_batched(None, 0) == svlib.SV_OK
+    assert L.sv_synth_batched(None, 2) == svlib.SV_ERR_INVALID_ARG
+    ok = svlib.dist_params(a=0.0, b=1.0)
+    for k in range(3):
+        jobs[k] = svlib.SynthJob(1, k, 0, 0, ok, 0, None)          # empty jobs: nothing to launch
+    assert L.sv_synth_batched(jobs, 3) == svlib.SV_OK
+    jobs[2] = svlib.SynthJob(1, 2, 0, 1, svlib.dist_params(mean=0.0, std=-2.0), 16, 0x1000)
+    assert L.sv_synth_batched(jobs, 3) == svlib.SV_ERR_INVALID_ARG
+    assert L.sv_last_error().decode().startswith("job 2:")
+    jobs[1] = svlib.SynthJob(1, 1, 2, 0, ok, 16, 0x1000)              # uniform into int32
+    assert L.sv_synth_batched(jobs, 3) == svlib.SV_ERR_UNSUPPORTED
 
 
 def test_compare_argument_errors_and_empty(svlib):
@@ -149,3 +166,12 @@ def test_perturb_argument_errors(svlib):
 def test_profile_read_with_nothing_recorded(svlib):
     c, ms = svlib.profile_read("synth")
     assert c == 0 and ms == 0.0
+
+
+def test_eval_transform_argument_errors(svlib):
+    L = svlib._lib
+    assert L.sv_eval_transform(4, 0x1000, 4, 0x2000) == svlib.SV_ERR_UNSUPPORTED
+    assert L.sv_eval_transform(-1, 0x1000, 4, 0x2000) == svlib.SV_ERR_UNSUPPORTED
+    assert L.sv_eval_transform(0, None, 4, 0x2000) == svlib.SV_ERR_INVALID_ARG
+    assert L.sv_eval_transform(0, 0x1002, 4, 0x2000) == svlib.SV_ERR_INVALID_ARG   # misaligned
+    assert L.sv_eval_transform(1, None, 0, None) == svlib.SV_OK

@@ -105,6 +105,38 @@ def test_synth_full_size_sampled(oracle, dist, dtype, n, params):
     torch.cuda.empty_cache()
 
 
+def test_synth_batched_matches_single_calls_and_oracle(oracle):
+    rng = np.random.default_rng(12)
+    jobs, singles = [], []
+    keep = []
+    for k, (dist, dtype, params) in enumerate(CASES * 3):
+        n = int(rng.choice([0, 1, 3, 8, 255, 256 * 4 + 1, 70001, 1 << 20]))
+        off = int(rng.integers(0, 3)) if k % 4 == 0 else 0          # some outputs not 16-byte aligned
+        big = empty(n + 8, dtype)
+        out = big[off:off + n]
+        ref = empty(n, dtype)
+        keep += [big, ref]
+        jobs.append((out, 5 + k, (1 << 63) | k, dist, params))
+        singles.append((ref, 5 + k, (1 << 63) | k, dist, params))
+    print("synth batched", len(jobs), flush=True)
+    sv.synth_batched(jobs)
+    for ref, seed, stream, dist, params in singles:
+        sv.synth(ref, seed, stream, dist, **params)
+    for (out, seed, stream, dist, params), (ref, *_rest) in zip(jobs, singles):
+        assert torch.equal(out.view(torch.int16 if out.dtype == torch.bfloat16 else torch.int32),
+                           ref.view(torch.int16 if ref.dtype == torch.bfloat16 else torch.int32))
+    for out, seed, stream, dist, params in jobs[:12]:
+        dtype = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32"}[out.dtype]
+        want = oracle.synth(seed, stream, dtype, dist, oracle.dist_params(**params), out.numel())
+        assert np.array_equal(bits(out), want)
+    # back-to-back batches reuse the job table: the second must not see the first's jobs
+    a, b = empty(5000, "f32"), empty(7000, "bf16")
+    sv.synth_batched([(a, 1, 1, "normal", dict(mean=0.0, std=1.0))])
+    sv.synth_batched([(b, 2, 2, "uniform", dict(a=-1.0, b=1.0))])
+    assert np.array_equal(bits(a), oracle.synth(1, 1, "f32", "normal", oracle.dist_params(mean=0.0, std=1.0), 5000))
+    assert np.array_equal(bits(b), oracle.synth(2, 2, "bf16", "uniform", oracle.dist_params(a=-1.0, b=1.0), 7000))
+
+
 PERTURB = [
     ("f32", "uniform", dict(a=-1.0, b=1.0), "copy", {}),
     ("f32", "normal", dict(mean=0.0, std=1.0), "ulp", dict(p=0.3)),
@@ -155,3 +187,21 @@ def test_perturb_index_ops_bit_exact(oracle, dtype, dist, params):
         assert np.array_equal(got, want), _diff(got, want)
     with pytest.raises(sv.SVError):
         sv.perturb(ref, ref.clone(), 0, 0, "set_at", idx=[n])
+
+
+def test_normal_transform_building_blocks_exhaustive(oracle):
+    # every 24-bit input of ln, the Box-Muller radius, sin and cos: GPU bits == oracle bits
+    k = np.arange(1 << 24, dtype=np.uint32)
+    kin = torch.from_numpy(k.view(np.int32)).to("cuda")
+    out = torch.empty_like(kin)
+    want = {
+        "ln": oracle.ln_f32_n(((k.astype(np.float64) + 1) * 2.0 ** -24).astype(np.float32)).view(np.uint32),
+        "radius": oracle.radius_f32_n(k).view(np.uint32),
+    }
+    s, c = oracle.sincos_2pi_f32_n(k)
+    want["sin"], want["cos"] = s.view(np.uint32), c.view(np.uint32)
+    for which in ("ln", "radius", "sin", "cos"):
+        print("transform", which, flush=True)
+        sv.eval_transform(which, kin, out)
+        got = out.cpu().numpy().view(np.uint32)
+        assert np.array_equal(got, want[which]), (which, _diff(got, want[which]))
