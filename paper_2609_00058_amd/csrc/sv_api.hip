@@ -5,6 +5,7 @@
 // call, and reports failures as a status code plus a thread-local message.
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -66,6 +67,11 @@ struct DeviceState {
   hipEvent_t synth_copied = nullptr; // staging -> table copy of the last batch done
   hipEvent_t synth_done = nullptr;   // last batch kernel done (table free to overwrite)
   bool synth_pending = false;        // the two events above have been recorded
+  uint32_t *counters = nullptr;      // arrival counters of the check (zero between launches)
+  size_t counters_cap = 0;
+  uint64_t *h_done = nullptr;        // pinned, host-mapped, coherent: a check's last word written
+  uint64_t *d_done = nullptr;        // its device address
+  uint64_t seq = 0;                  // sequence number of the last check launched
 };
 
 std::mutex g_devices_mu;
@@ -133,6 +139,57 @@ int ensure_reports(DeviceState *ds, size_t need) {
     return hip_fail(e, "hipHostGetDevicePointer(reports)");
   }
   ds->h_reports_cap = want;
+  return SV_OK;
+}
+
+int ensure_counters(DeviceState *ds, size_t need) {
+  if (need <= ds->counters_cap) return SV_OK;
+  int rc = ensure_device(ds->counters, ds->counters_cap, need, "arrival counters");
+  if (rc) return rc;
+  SV_HIP(hipMemset(ds->counters, 0, ds->counters_cap * sizeof(uint32_t)), "hipMemset(arrival counters)");
+  return SV_OK;
+}
+
+int ensure_done(DeviceState *ds) {
+  if (ds->h_done) return SV_OK;
+  hipError_t e = hipHostMalloc((void **)&ds->h_done, 64, hipHostMallocMapped | hipHostMallocCoherent);
+  if (e != hipSuccess) {
+    ds->h_done = nullptr;
+    return fail(SV_ERR_ALLOC, "hipHostMalloc of the completion word: %s", hipGetErrorString(e));
+  }
+  e = hipHostGetDevicePointer((void **)&ds->d_done, ds->h_done, 0);
+  if (e != hipSuccess) {
+    (void)hipHostFree(ds->h_done);
+    ds->h_done = nullptr;
+    return hip_fail(e, "hipHostGetDevicePointer(completion word)");
+  }
+  *(volatile uint64_t *)ds->h_done = ds->seq;
+  return SV_OK;
+}
+
+// Waits until the check launched with sequence number `seq` has written its
+// reports: spins on the host-mapped completion word (a few hundred ns after
+// the kernel's last store, well before a stream synchronisation would
+// return), asking the stream now and then whether it failed instead.
+int wait_done(DeviceState *ds, uint64_t seq, hipStream_t st) {
+  using clock = std::chrono::steady_clock;
+  const volatile uint64_t *flag = ds->h_done;
+  std::chrono::microseconds interval(50);
+  auto next = clock::now() + interval;
+  while (*flag != seq) {
+    __builtin_ia32_pause();
+    const auto now = clock::now();
+    if (now < next) continue;
+    const hipError_t e = hipStreamQuery(st);
+    if (e == hipSuccess) {
+      if (*flag == seq) break;
+      return fail(SV_ERR_HIP, "the check kernel finished without writing its reports");
+    }
+    if (e != hipErrorNotReady) return hip_fail(e, "waiting for the check");
+    interval = std::min(interval * 2, std::chrono::microseconds(1000));
+    next = now + interval;
+  }
+  std::atomic_thread_fence(std::memory_order_acquire);
   return SV_OK;
 }
 
@@ -244,17 +301,23 @@ void compare_grid(uint64_t units, int cus, uint32_t *nblocks, uint64_t *chunk) {
   *nblocks = (uint32_t)((units + c - 1) / c);
 }
 
-// The check kernel and its finalize kernel (which writes the reports into
-// host-mapped memory), then a stream synchronisation.  Segments with no
-// elements get their (empty) report here.
+// The check kernel (and, for a batch, its finalize kernel), which write the
+// reports into host-mapped memory and then the launch's sequence number; the
+// host waits for that number.  Segments with no elements get their (empty)
+// report here.
 int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_segment *segs, uint32_t nseg,
                 sv_report *out) {
   hipStream_t st = t_stream;
   int rc = ensure_device(ds->partials, ds->partials_cap, (size_t)nblocks + nseg, "partials");
   if (!rc) rc = ensure_reports(ds, nseg);
+  if (!rc) rc = ensure_counters(ds, 1);
+  if (!rc) rc = ensure_done(ds);
   if (rc) return rc;
   args.partials = ds->partials;
+  args.counter = ds->counters;
   args.reports = ds->d_reports;
+  args.done = ds->d_done;
+  args.seq = ds->seq + 1;
   hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
   if (g_prof_on.load()) {
     e0 = take_event();
@@ -270,13 +333,14 @@ int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_s
   }
   hipError_t e = launch_compare(args, nblocks, mask, st, e0 ? e1 : nullptr);
   if (e != hipSuccess) return hip_fail(e, "check kernel launch");
+  ds->seq = args.seq;
   if (e0 && e1 && e2) {
     (void)hipEventRecord(e2, st);
     push_record(SV_PROF_COMPARE, e0, e1);
     push_record(SV_PROF_FINALIZE, e1, e2);
   }
-  e = hipStreamSynchronize(st);
-  if (e != hipSuccess) return hip_fail(e, "waiting for the check");
+  rc = wait_done(ds, args.seq, st);
+  if (rc) return rc;
   for (uint32_t k = 0; k < nseg; ++k) {
     const uint64_t n = segs ? segs[k].n : args.single.n;
     if (n)
@@ -643,6 +707,10 @@ int sv_shutdown(void) {
     if (s->h_synth) (void)hipHostFree(s->h_synth);
     if (s->synth_copied) (void)hipEventDestroy(s->synth_copied);
     if (s->synth_done) (void)hipEventDestroy(s->synth_done);
+    if (s->counters) (void)hipFree(s->counters);
+    if (s->h_done) (void)hipHostFree(s->h_done);
+    s->counters = nullptr; s->counters_cap = 0;
+    s->h_done = nullptr; s->d_done = nullptr;
     s->synth_table = nullptr; s->h_synth = nullptr; s->synth_copied = nullptr; s->synth_done = nullptr;
     s->synth_table_cap = s->h_synth_cap = 0;
     s->synth_pending = false;

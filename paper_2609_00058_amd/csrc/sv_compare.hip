@@ -27,11 +27,21 @@
 // rejects a quotient that rounds above m).
 //
 // Reduction.  Lanes -> wave by xor shuffles, waves -> workgroup through LDS,
-// one partial per (workgroup, segment piece) in scratch slot b + s; then a
-// finalize kernel (one workgroup per segment) combines a segment's partials in
-// a fixed order and writes the report straight into host-mapped pinned memory.
-// No floating-point atomics: reports are bit-reproducible run to run for a
-// given device.
+// one 72-byte partial per (workgroup, segment piece) in scratch slot b + s.
+// The finalize kernel -- one workgroup per segment, launched behind the check
+// -- combines a segment's partials in a fixed order and writes the report
+// straight into host-mapped pinned memory, then the last finalize workgroup
+// writes the launch's sequence number, which the host spins on.  No
+// floating-point atomics: reports are bit-reproducible run to run for a given
+// device.
+//
+// The partials need no device-scope fence inside the check: the finalize runs
+// after it.  (On gfx950 such a fence writes back the whole L2 of the issuing
+// XCD, which cuts the check to a third of its bandwidth when thousands of
+// workgroups each issue one; an in-kernel "last workgroup finishes" scheme
+// built from device-scope atomic stores instead of fences measured slower than
+// the separate finalize, its chain of round trips to the coherence point being
+// longer than a kernel launch.)
 #include "sv_device.h"
 #include "sv_internal.h"
 
@@ -207,6 +217,45 @@ __device__ __forceinline__ void wave_merge(Partial &acc) {
   }
 }
 
+__device__ __forceinline__ uint64_t dbits(double x) { return (uint64_t)__double_as_longlong(x); }
+
+// ---- hand-off to the host
+__device__ __forceinline__ void wait_memory() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// The report, field by field, with system-scope stores into host-mapped memory.
+__device__ __forceinline__ void write_report(sv_report *dst, const Partial &r, uint64_t n) {
+  uint64_t v[10];
+  v[0] = n;
+  v[1] = r.mism;
+  v[2] = r.first == kNone ? ~0ull : r.first;     // -1 as int64 when there is no mismatch
+  v[3] = dbits(r.maxabs);
+  v[4] = dbits(r.maxrel);
+  v[5] = dbits(r.sum);
+  v[6] = r.nan_r;
+  v[7] = r.nan_c;
+  v[8] = r.inf_r;
+  v[9] = r.inf_c;
+  uint64_t *w = (uint64_t *)dst;
+#pragma unroll
+  for (int i = 0; i < 10; ++i) __hip_atomic_store(w + i, v[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// Called by one thread of every finalize workgroup once its report (if any)
+// is written: the last to arrive clears the counter and, after every store
+// before it has landed, hands the sequence number to the host.
+__device__ __forceinline__ void arrive_and_signal(const CompareArgs &args) {
+  wait_memory();
+  if (__hip_atomic_fetch_add(args.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != gridDim.x - 1)
+    return;
+  __hip_atomic_store(args.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  wait_memory();
+  __hip_atomic_store(args.done, args.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // Units [ulo, uhi) of one segment -> a workgroup partial, valid on thread 0.
 template <int DT>
 __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Partial *lds) {
@@ -295,13 +344,9 @@ __device__ __forceinline__ uint32_t find_segment(const SegDesc *segs, uint32_t n
   return lo;
 }
 
-// One workgroup per segment: combine the partials of the workgroups that
-// touched it (thread t takes slots b0 + t, b0 + t + 1024, ... in order, then a
-// fixed shuffle tree and the waves in order) and write the report into
-// host-mapped memory.  Running after the check kernel, it sees every partial
-// without any device-scope fence inside the check (on gfx950 such a fence
-// writes back the L2 of the issuing XCD, which thousands of workgroups cannot
-// afford).
+// One workgroup per segment, behind the check kernel: thread t merges slots
+// b0 + t, b0 + t + 1024, ... in order (four loaded at a time), then a fixed
+// shuffle tree and the waves in order; the report goes into host-mapped memory.
 constexpr int kFinBlock = 1024;                  // finalize threads per segment
 constexpr int kFinWaves = kFinBlock / kWave;
 
@@ -311,40 +356,31 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
   const uint32_t s = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const SegDesc sd = kSingle ? args.single : args.segs[s];
   const uint64_t units = units_of(sd.dtype, sd.n);
-  if (units == 0) return;            // empty segments are reported by the host
-  const uint64_t b0 = sd.unit_begin / args.chunk;
-  const uint64_t b1 = (sd.unit_begin + units - 1) / args.chunk;
-  const Partial *P = args.partials + s;
-  Partial acc = empty_partial();
-  uint64_t b = b0 + tid;
-  for (; b + 3 * kFinBlock <= b1; b += 4 * kFinBlock) {   // four partials in flight, merged in slot order
-    const Partial p0 = P[b], p1 = P[b + kFinBlock], p2 = P[b + 2 * kFinBlock], p3 = P[b + 3 * kFinBlock];
-    merge(acc, p0);
-    merge(acc, p1);
-    merge(acc, p2);
-    merge(acc, p3);
-  }
-  for (; b <= b1; b += kFinBlock) merge(acc, P[b]);
-  wave_merge(acc);
-  if (lane == 0) lds[wave] = acc;
-  __syncthreads();
-  if (tid == 0) {
-    Partial r = lds[0];
+  if (units != 0) {                  // empty segments are reported by the host
+    const uint64_t b0 = sd.unit_begin / args.chunk;
+    const uint64_t b1 = (sd.unit_begin + units - 1) / args.chunk;
+    const Partial *P = args.partials + s;
+    Partial acc = empty_partial();
+    uint64_t b = b0 + tid;
+    for (; b + 3 * kFinBlock <= b1; b += 4 * kFinBlock) {
+      const Partial p0 = P[b], p1 = P[b + kFinBlock], p2 = P[b + 2 * kFinBlock], p3 = P[b + 3 * kFinBlock];
+      merge(acc, p0);
+      merge(acc, p1);
+      merge(acc, p2);
+      merge(acc, p3);
+    }
+    for (; b <= b1; b += kFinBlock) merge(acc, P[b]);
+    wave_merge(acc);
+    if (lane == 0) lds[wave] = acc;
+    __syncthreads();
+    if (tid == 0) {
+      Partial r = lds[0];
 #pragma unroll
-    for (int w = 1; w < kFinWaves; ++w) merge(r, lds[w]);
-    sv_report rep;
-    rep.n = sd.n;
-    rep.mismatches = r.mism;
-    rep.first_mismatch = r.first == kNone ? -1 : (int64_t)r.first;
-    rep.max_abs_err = r.maxabs;
-    rep.max_rel_err = r.maxrel;
-    rep.err_sum = r.sum;
-    rep.nan_ref = r.nan_r;
-    rep.nan_cand = r.nan_c;
-    rep.inf_ref = r.inf_r;
-    rep.inf_cand = r.inf_c;
-    args.reports[s] = rep;
+      for (int w = 1; w < kFinWaves; ++w) merge(r, lds[w]);
+      write_report(args.reports + s, r, sd.n);
+    }
   }
+  if (tid == 0) arrive_and_signal(args);
 }
 
 // kMask: the set of dtypes (bit 1 << dtype) the segments of this launch use;
@@ -378,6 +414,7 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(CompareArgs args) {
         p = check_piece<SV_I32>(sd, ulo, uhi, lds);
     }
     if (threadIdx.x == 0) args.partials[b + s] = p;
+    if constexpr (kSingle) return;   // one segment: the chunk is a single piece
     lo = piece_hi;
     if constexpr (!kSingle) {
       ++s;

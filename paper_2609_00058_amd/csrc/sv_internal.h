@@ -105,7 +105,10 @@ struct CompareArgs {
   uint64_t total_units;
   uint64_t chunk;               // units per workgroup
   Partial *partials;            // nblocks + nseg slots
+  uint32_t *counter;            // finalize arrivals, zero between launches
   sv_report *reports;           // nseg reports, in host-mapped pinned memory
+  uint64_t *done;               // host-mapped word that receives `seq` once every report is written
+  uint64_t seq;
 };
 
 __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
