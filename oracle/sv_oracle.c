@@ -15,8 +15,8 @@
  *    Gaussian with mean 5 and standard deviation 10 is its example); that is
  *    the normal distribution with explicit mean and std below.
  *  - The generator, the word-to-element mapping and the transforms are not in
- *    the paper (it names only "standard numerical libraries").  They follow the
- *    conventions recorded in the design notes: Philox4x32-10 (Salmon, Moraes,
+ *    the paper (it only points to general-purpose numerical libraries).  They
+ *    follow the conventions recorded in the design notes: Philox4x32-10 (Salmon, Moraes,
  *    Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11) keyed
  *    by the seed with counter (block, stream); uniform from the top 24 bits;
  *    Box-Muller (1958) with ln, sin and cos written as fixed sequences of fp32
