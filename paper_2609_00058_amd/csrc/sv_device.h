@@ -118,9 +118,10 @@ __device__ __forceinline__ float ln_f32(float x) {
 }
 
 // IEEE (correctly rounded) square root of v in {0} and [2^-126, 2^126]: the
-// hardware square root is within one ulp, and of it and its two neighbours
-// the one whose fused residual v - s' s has the right sign is the rounded
-// root (no input here is denormal, infinite or negative, so no scaling).
+// hardware square root is within one ulp (and not always rounded correctly on
+// the Box-Muller radicands), and of it and its two neighbours the one whose
+// fused residual v - s' s has the right sign is the rounded root (no input
+// here is denormal, infinite or negative, so no scaling).
 __device__ __forceinline__ float sqrt_rn(float v) {
   float s = __builtin_amdgcn_sqrtf(v);
   const float sd = as_f32(as_u32(s) - 1u), su = as_f32(as_u32(s) + 1u);
