@@ -12,7 +12,7 @@ value = (bytes synthesized + bytes checked) / time per step, in GB/s
 2 * n * itemsize bytes (algorithmic bytes).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--no-cpu-baseline] [--copy-probe]
+                       [--no-cpu-baseline] [--copy-probe] [--perf-stage]
 """
 import argparse
 import json
@@ -65,6 +65,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="normal_ulp")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--perf-stage", action="store_true",
+                    help="time the fail-fast sequence on a synthetic candidate kernel instead (Eq. 3-4)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="copy 256 MiB device-to-device once before timing (known-size kernel for "
                          "calibrating the FETCH_SIZE / WRITE_SIZE counters)")
@@ -104,12 +106,58 @@ def cpu_baseline(wl):
             "seconds": round(secs, 3), "cpu": platform.processor() or platform.machine()}
 
 
+def perf_stage(args):
+    """The stages after the functional check (Eq. 3-4) on a synthetic candidate:
+    z = a x + y over 2^26 fp32 elements (768 MiB of traffic per run), loaded
+    from the test candidates' code object.  Functional check against a
+    reference computed by torch, then the performance stage warm (back-to-back
+    runs) and cold (Infinity Cache and L2 evicted before each run), then the
+    reward.  `value` is P = 1 / mean latency of the warm runs."""
+    import struct
+    import torch
+    import paper_2609_00058_amd as sv
+    torch.cuda.set_device(0)
+    with open(os.path.join(ROOT, "tests", "kernels", "candidates.hsaco"), "rb") as f:
+        code = f.read()
+    n = 1 << 26
+    g = torch.Generator().manual_seed(0)
+    x = torch.randn(n, generator=g).cuda()
+    y = torch.randn(n, generator=g).cuda()
+    z = torch.empty_like(x)
+    a = 1.7
+    ref = torch.tensor(a, device="cuda") * x + y
+    argbuf = struct.pack("<QQQfxxxxQ", z.data_ptr(), x.data_ptr(), y.data_ptr(), a, n)
+    grid, block = ((n + 255) // 256,), (256,)
+    k = sv.kernel_load(code, "sv_test_axpy")
+    k.launch(grid, block, argbuf)
+    rep = sv.compare(ref, z, 0.0, 0.0)
+    valid = rep["mismatches"] == 0
+    warm = k.time(grid, block, argbuf, warmup=args.warmup, reps=args.steps)
+    cold = k.time(grid, block, argbuf, warmup=1, reps=args.steps, flush_bytes=512 << 20)
+    nbytes = 3 * 4 * n
+    out = {"metric": "performance stage: P = 1 / mean latency of a candidate kernel (Eq. 3)",
+           "value": round(warm["perf"], 4), "unit": "1/ms", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(warm["mean_ms"], 5), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": "axpy_f32_67108864", "candidate": "sv_test_axpy", "bytes_per_run": nbytes},
+           "functional_check": {"mismatches": rep["mismatches"], "valid": valid},
+           "timing_warm": {k_: round(v, 6) for k_, v in warm.items()},
+           "timing_cold": {k_: round(v, 6) for k_, v in cold.items()},
+           "candidate_GBps_warm": round(nbytes / (warm["mean_ms"] * 1e-3) / 1e9, 1),
+           "candidate_GBps_cold": round(nbytes / (cold["mean_ms"] * 1e-3) / 1e9, 1),
+           "reward": sv.reward(True, valid, warm["perf"])}
+    k.free()
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print("bench.py measures one GPU: the path runs on a single MI355X and this build has no "
               "multi-GPU execution; rerun with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.perf_stage:
+        return perf_stage(args)
     import torch
     import paper_2609_00058_amd as sv
     import workloads as W

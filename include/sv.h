@@ -204,6 +204,77 @@ int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_pertur
 enum { SV_EVAL_LN = 0, SV_EVAL_RADIUS = 1, SV_EVAL_SIN = 2, SV_EVAL_COS = 3 };
 int sv_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out);
 
+/*
+ * ---- Performance stage and reward (Sec. 4.2.2, Eq. (3); Sec. 4.3, Eq. (4)) ----
+ *
+ * After a candidate kernel compiles (C of Eq. (2)) and passes the functional
+ * check (V, sv_compare), its runtime performance is measured as
+ * P_latency = 1 / Latency (Eq. (3)), the latency being the mean over repeated
+ * runs (Sec. 5.1), and the three stages combine into the reward
+ * r = -1 + C + C V P (Eq. (4)).
+ *
+ * sv_kernel_load -- load a candidate: a gfx950 code object (an .hsaco image in
+ * host memory, `size` bytes, as produced by `hipcc --genco`) and the name of a
+ * kernel in it.  On success *out owns the module; release it with
+ * sv_kernel_free.  The kernel belongs to the device current at load time.
+ * Errors: INVALID_ARG for NULL arguments or size 0; HIP for a code object the
+ * runtime rejects or a name it does not contain.
+ */
+typedef struct sv_kernel sv_kernel;
+int sv_kernel_load(const void *code_object, uint64_t size, const char *name, sv_kernel **out);
+int sv_kernel_free(sv_kernel *k);
+
+/*
+ * One launch of a candidate: grid (in workgroups) and workgroup dimensions,
+ * dynamic LDS bytes, and the kernel's arguments packed into one buffer as the
+ * kernel's parameter list lays them out (each parameter at its natural
+ * alignment).  `args` is host memory read during the call.
+ */
+typedef struct {
+  uint32_t grid[3];
+  uint32_t block[3];
+  uint32_t shared_bytes;
+  uint32_t reserved;            /* 0 */
+  const void *args;
+  uint64_t args_size;
+} sv_launch;
+
+/* Launches the candidate once on the calling thread's stream (asynchronous). */
+int sv_kernel_launch(const sv_kernel *k, const sv_launch *launch);
+
+typedef struct {
+  uint32_t reps;
+  uint32_t reserved;
+  double mean_ms;               /* Latency of Eq. (3): mean of the timed runs */
+  double median_ms, min_ms, max_ms;
+  double perf;                  /* P = 1 / mean_ms, in 1/ms */
+} sv_timing;
+
+/*
+ * sv_kernel_time -- the performance stage: `warmup` untimed launches, then
+ * `reps` launches each bracketed by HIP events on the calling thread's stream.
+ * With flush_bytes > 0, a fill of that many bytes of library scratch runs
+ * before every timed launch, outside its events, so each run starts with the
+ * L2 and Infinity Cache holding none of the candidate's data (256 MiB or more
+ * evicts both on MI355X); at most 2^34 bytes.  Waits for the runs; fills *out
+ * and, if rep_ms is not NULL, rep_ms[0..reps) with each run's milliseconds.
+ * Errors: INVALID_ARG for NULL k / launch / out, reps == 0 or > 2^20, a zero
+ * grid or block dimension, more than 1024 threads per workgroup, args NULL
+ * with args_size > 0, a kernel loaded on another device; HIP for launch or
+ * event failures (a faulting candidate surfaces here); ALLOC for the flush.
+ */
+int sv_kernel_time(const sv_kernel *k, const sv_launch *launch, uint32_t warmup, uint32_t reps,
+                   uint64_t flush_bytes, float *rep_ms, sv_timing *out);
+
+/*
+ * Eq. (4): r = -1 + C + C V P, with C = (compiled != 0), V = (valid != 0) and
+ * P >= 0 the performance of Eq. (3) (ignored unless C and V hold).  So a
+ * kernel that does not compile gets -1, one that compiles but fails the check
+ * 0, and a correct one its performance.  Returns NaN for a NaN or negative P
+ * when C and V hold.  Pure host arithmetic.
+ */
+double sv_reward(int32_t compiled, int32_t valid, double perf);
+
 /* HIP stream (hipStream_t) for the calling thread's later calls; NULL = null stream. */
 int sv_set_stream(void *hip_stream);
 

@@ -99,6 +99,10 @@ def lib():
         L.or_sincos_2pi_f32_n.argtypes = [vp, vp, vp, ctypes.c_uint64]
         L.or_bf16_rne_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_radius_f32_n.argtypes = [vp, vp, ctypes.c_uint64]
+        L.or_performance.argtypes = [ctypes.c_double]
+        L.or_performance.restype = ctypes.c_double
+        L.or_reward.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_double]
+        L.or_reward.restype = ctypes.c_double
         L.or_synth.argtypes = [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int32, ctypes.c_int32,
                                ctypes.POINTER(DistParams), ctypes.c_uint64, ctypes.c_uint64,
                                ctypes.c_void_p]
@@ -295,3 +299,14 @@ def compare_batched(segments) -> list:
     reps = (Report * max(1, len(segments)))()
     _check(lib().or_compare_batched(arr, len(segments), reps), "or_compare_batched")
     return [reps[k].as_dict() for k in range(len(segments))]
+
+
+# ---------------------------------------------------------------- Eq. (3), Eq. (4)
+def performance(mean_latency_ms: float) -> float:
+    """Eq. (3): P = 1 / latency (latency in ms, P in 1/ms)."""
+    return lib().or_performance(mean_latency_ms)
+
+
+def reward(compiled: int, valid: int, p: float) -> float:
+    """Eq. (4): r = -1 + C + C V P."""
+    return lib().or_reward(int(compiled), int(valid), float(p))

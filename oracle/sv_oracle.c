@@ -599,3 +599,20 @@ int or_compare_batched(const or_segment *segs, uint32_t nseg, or_report *reports
   }
   return 0;
 }
+
+/* ------------------------------------------------------------ Eq. (3), Eq. (4)
+ * Performance of a candidate from its mean latency in milliseconds, Eq. (3)
+ * (the latency averaged over repeated runs, Sec. 5.1; the unit is that of the
+ * paper's RScore, 1 / ms).  Reward, Eq. (4): r = -1 + C + C V P with C = 1 when
+ * the kernel compiled (Eq. (2)), V = 1 when it passed the functional check
+ * (Eq. (1)).  The fail-fast order of Sec. 4.2.2 never profiles a kernel that
+ * failed an earlier stage, so its performance term is absent (0) whatever p
+ * holds; for a profiled kernel p must be a number >= 0, else the result is NaN. */
+double or_performance(double mean_latency_ms) { return 1.0 / mean_latency_ms; }
+
+double or_reward(int compiled, int valid, double p) {
+  const double c = compiled ? 1.0 : 0.0, v = valid ? 1.0 : 0.0;
+  if (c * v == 0.0) return -1.0 + c;
+  if (!(p >= 0.0)) return NAN;
+  return -1.0 + c + c * v * p;
+}

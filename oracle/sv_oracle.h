@@ -114,6 +114,9 @@ int or_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
                double rtol, double atol, int32_t equal_nan, or_report *r);
 int or_compare_batched(const or_segment *segs, uint32_t nseg, or_report *reports);
 
+double or_performance(double mean_latency_ms);          /* Eq. (3) */
+double or_reward(int compiled, int valid, double p);    /* Eq. (4) */
+
 #ifdef __cplusplus
 }
 #endif

@@ -29,7 +29,8 @@ PROF_KINDS = {"synth": 0, "compare": 1, "perturb": 2, "finalize": 3}
 
 # every symbol include/sv.h declares
 SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_compare", "sv_compare_batched", "sv_perturb",
-           "sv_eval_transform", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
+           "sv_eval_transform", "sv_kernel_load", "sv_kernel_free", "sv_kernel_launch", "sv_kernel_time",
+           "sv_reward", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
 
 
 class DistParams(ctypes.Structure):
@@ -71,6 +72,21 @@ class PerturbPlan(ctypes.Structure):
                 ("idx", ctypes.POINTER(ctypes.c_uint64)), ("nidx", ctypes.c_uint64)]
 
 
+class Launch(ctypes.Structure):
+    _fields_ = [("grid", ctypes.c_uint32 * 3), ("block", ctypes.c_uint32 * 3),
+                ("shared_bytes", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("args", ctypes.c_void_p), ("args_size", ctypes.c_uint64)]
+
+
+class Timing(ctypes.Structure):
+    _fields_ = [("reps", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("mean_ms", ctypes.c_double), ("median_ms", ctypes.c_double),
+                ("min_ms", ctypes.c_double), ("max_ms", ctypes.c_double), ("perf", ctypes.c_double)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_ if name != "reserved"}
+
+
 _u64, _i32, _vp, _dbl = ctypes.c_uint64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_double
 _lib.sv_synth.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u64, _vp]
 _lib.sv_synth_batched.argtypes = [ctypes.POINTER(SynthJob), ctypes.c_uint32]
@@ -78,13 +94,20 @@ _lib.sv_compare.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINT
 _lib.sv_compare_batched.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, ctypes.POINTER(Report)]
 _lib.sv_perturb.argtypes = [_u64, _u64, _i32, ctypes.POINTER(PerturbPlan), _u64, _vp, _vp]
 _lib.sv_eval_transform.argtypes = [_i32, _vp, _u64, _vp]
+_lib.sv_kernel_load.argtypes = [ctypes.c_char_p, _u64, ctypes.c_char_p, ctypes.POINTER(_vp)]
+_lib.sv_kernel_free.argtypes = [_vp]
+_lib.sv_kernel_launch.argtypes = [_vp, ctypes.POINTER(Launch)]
+_lib.sv_kernel_time.argtypes = [_vp, ctypes.POINTER(Launch), ctypes.c_uint32, ctypes.c_uint32, _u64,
+                                ctypes.POINTER(ctypes.c_float), ctypes.POINTER(Timing)]
 _lib.sv_set_stream.argtypes = [_vp]
 _lib.sv_last_error.restype = ctypes.c_char_p
 _lib.sv_profile_enable.argtypes = [_i32]
 _lib.sv_profile_read.argtypes = [_i32, ctypes.POINTER(_u64), ctypes.POINTER(_dbl)]
 for _name in SYMBOLS:
-    if _name != "sv_last_error":
+    if _name not in ("sv_last_error", "sv_reward"):
         getattr(_lib, _name).restype = ctypes.c_int
+_lib.sv_reward.argtypes = [_i32, _i32, _dbl]
+_lib.sv_reward.restype = _dbl
 
 
 class SVError(RuntimeError):
@@ -135,10 +158,14 @@ def _dev_ptr(t, name):
 def _run(t, fn, *args):
     """Call fn(*args) with t's device current and torch's current stream of
     that device handed to the library (only when it changed)."""
-    torch = _torch()
     dev = t.get_device()
     if dev < 0:
         raise SVError(SV_ERR_INVALID_ARG, "tensors must be on the GPU")
+    _run_on(dev, fn, *args)
+
+
+def _run_on(dev, fn, *args):
+    torch = _torch()
     prev = torch._C._cuda_getDevice()
     if prev != dev:
         torch.cuda.set_device(dev)
@@ -227,6 +254,65 @@ def eval_transform(which: str, inp, out):
         raise SVError(SV_ERR_INVALID_ARG, "in and out differ in size")
     _run(inp, _lib.sv_eval_transform, EVAL[which], _dev_ptr(inp, "in"), inp.numel(), _dev_ptr(out, "out"))
     return out
+
+
+class Kernel:
+    """A candidate kernel loaded from a gfx950 code object (sv_kernel_load)."""
+
+    def __init__(self, code_object: bytes, name: str, device: int = None):
+        torch = _torch()
+        self.device = torch._C._cuda_getDevice() if device is None else device
+        self._code = bytes(code_object)
+        self.name = name
+        h = _vp()
+        _run_on(self.device, _lib.sv_kernel_load, self._code, len(self._code), name.encode(), ctypes.byref(h))
+        self._h = h
+
+    def free(self):
+        if getattr(self, "_h", None):
+            _check(_lib.sv_kernel_free(self._h))
+            self._h = None
+
+    def _launch_struct(self, grid, block, args, shared_bytes):
+        grid = tuple(grid) + (1,) * (3 - len(grid))
+        block = tuple(block) + (1,) * (3 - len(block))
+        buf = ctypes.create_string_buffer(bytes(args), len(args)) if args else None
+        l = Launch((ctypes.c_uint32 * 3)(*grid), (ctypes.c_uint32 * 3)(*block), shared_bytes, 0,
+                   ctypes.cast(buf, _vp) if buf is not None else None, len(args) if args else 0)
+        return l, buf
+
+    def launch(self, grid, block, args: bytes = b"", shared_bytes: int = 0):
+        """One launch on torch's current stream (asynchronous)."""
+        l, buf = self._launch_struct(grid, block, args, shared_bytes)
+        _run_on(self.device, _lib.sv_kernel_launch, self._h, ctypes.byref(l))
+
+    def time(self, grid, block, args: bytes = b"", shared_bytes: int = 0, warmup: int = 3, reps: int = 20,
+             flush_bytes: int = 0, per_rep: bool = False) -> dict:
+        """The performance stage: latency statistics and P = 1 / mean latency (1/ms)."""
+        l, buf = self._launch_struct(grid, block, args, shared_bytes)
+        out = Timing()
+        arr = (ctypes.c_float * reps)() if per_rep else None
+        _run_on(self.device, _lib.sv_kernel_time, self._h, ctypes.byref(l), warmup, reps, flush_bytes, arr,
+                ctypes.byref(out))
+        d = out.as_dict()
+        if per_rep:
+            d["rep_ms"] = list(arr)
+        return d
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def kernel_load(code_object: bytes, name: str) -> Kernel:
+    return Kernel(code_object, name)
+
+
+def reward(compiled: bool, valid: bool, perf: float) -> float:
+    """Eq. (4): r = -1 + C + C V P."""
+    return _lib.sv_reward(1 if compiled else 0, 1 if valid else 0, float(perf))
 
 
 def profile_enable(on: bool = True):

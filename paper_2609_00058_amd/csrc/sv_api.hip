@@ -33,7 +33,11 @@ int fail(int code, const char *fmt, ...) {
   return code;
 }
 
+// The status and message carry the error to the caller, so the runtime's
+// per-thread last error is cleared: a later hipGetLastError() of the caller
+// (torch checks it after its own launches) must not see the library's failure.
 int hip_fail(hipError_t e, const char *what) {
+  (void)hipGetLastError();
   return fail(SV_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
 }
 
@@ -407,6 +411,13 @@ int prepare_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist
 
 }  // namespace
 
+namespace sv {
+hipStream_t api_stream() { return t_stream; }
+void api_clear_error() { t_error.clear(); }
+int api_fail(int code, const char *msg) { return fail(code, "%s", msg); }
+int api_hip_fail(hipError_t e, const char *what) { return hip_fail(e, what); }
+}  // namespace sv
+
 // =================================================================== C ABI
 extern "C" {
 
@@ -719,6 +730,7 @@ int sv_shutdown(void) {
     s->partials_cap = s->table_cap = s->idx_cap = 0;
     s->h_table_cap = s->h_reports_cap = s->h_idx_cap = 0;
   }
+  perf_shutdown();
   (void)hipSetDevice(prev);
   return SV_OK;
 }

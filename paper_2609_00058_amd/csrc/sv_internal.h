@@ -111,6 +111,14 @@ struct CompareArgs {
   uint64_t seq;
 };
 
+// ----------------------------------------------------------------- host helpers
+// Shared by the entry-point files; defined in sv_api.hip.
+hipStream_t api_stream();                         // the calling thread's stream
+void api_clear_error();
+int api_fail(int code, const char *msg);          // records msg, returns code
+int api_hip_fail(hipError_t e, const char *what);
+void perf_shutdown();                             // sv_perf.hip: frees its per-device state
+
 __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
   const uint64_t per = dtype == SV_BF16 ? 8 : 4;
   return (n + per - 1) / per;

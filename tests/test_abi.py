@@ -52,7 +52,7 @@ def test_struct_layouts_match_the_c_compiler(svlib, tmp_path):
     # sizes and field offsets of every ABI struct, as gcc lays them out from include/sv.h
     mirrors = {"sv_report": svlib.Report, "sv_segment": svlib.Segment,
                "sv_dist_params": svlib.DistParams, "sv_perturb_plan": svlib.PerturbPlan,
-               "sv_synth_job": svlib.SynthJob}
+               "sv_synth_job": svlib.SynthJob, "sv_launch": svlib.Launch, "sv_timing": svlib.Timing}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "sv.h"', "int main(void) {"]
     for cname, mirror in mirrors.items():
         lines.append('printf("%s %%zu\\n", sizeof(%s));' % (cname, cname))
@@ -175,3 +175,43 @@ def test_eval_transform_argument_errors(svlib):
     assert L.sv_eval_transform(0, None, 4, 0x2000) == svlib.SV_ERR_INVALID_ARG
     assert L.sv_eval_transform(0, 0x1002, 4, 0x2000) == svlib.SV_ERR_INVALID_ARG   # misaligned
     assert L.sv_eval_transform(1, None, 0, None) == svlib.SV_OK
+
+
+def test_kernel_harness_argument_errors_before_any_device_work(svlib):
+    L = svlib.lib()
+    INV = svlib.SV_ERR_INVALID_ARG
+    h = ctypes.c_void_p()
+    assert L.sv_kernel_load(None, 100, b"k", ctypes.byref(h)) == INV
+    assert L.sv_kernel_load(b"\x7fELF" + b"\0" * 60, 0, b"k", ctypes.byref(h)) == INV
+    assert L.sv_kernel_load(b"\x7fELF" + b"\0" * 60, 64, None, ctypes.byref(h)) == INV
+    assert L.sv_kernel_load(b"not a code object at all", 24, b"k", ctypes.byref(h)) == INV
+    assert "code object" in L.sv_last_error().decode()
+    l = svlib.Launch((ctypes.c_uint32 * 3)(1, 1, 1), (ctypes.c_uint32 * 3)(64, 1, 1), 0, 0, None, 0)
+    t = svlib.Timing()
+    assert L.sv_kernel_launch(None, ctypes.byref(l)) == INV
+    assert L.sv_kernel_time(None, ctypes.byref(l), 0, 10, 0, None, ctypes.byref(t)) == INV
+    assert L.sv_kernel_free(None) == svlib.SV_OK
+
+
+def test_reward_matches_the_oracle_on_every_case(svlib, oracle):
+    L = svlib.lib()
+    for c in (0, 1):
+        for v in (0, 1):
+            for p in (0.0, 0.5, 2.0, 1e6, math.inf):
+                want = oracle.reward(c, v, p)
+                got = L.sv_reward(c, v, p)
+                assert got == want, (c, v, p, got, want)
+    assert math.isnan(L.sv_reward(1, 1, -1.0)) and math.isnan(L.sv_reward(1, 1, math.nan))
+    assert L.sv_reward(0, 1, math.nan) == -1.0 and L.sv_reward(1, 0, math.nan) == 0.0
+    assert svlib.reward(True, True, 4.0) == 4.0
+
+
+def test_wall_clock_attribute_value_used_by_the_gpu_tests(tmp_path):
+    src = tmp_path / "wc.cpp"
+    src.write_text('#include <hip/hip_runtime_api.h>\n#include <cstdio>\n'
+                   'int main() { printf("%d", (int)hipDeviceAttributeWallClockRate); return 0; }\n')
+    exe = tmp_path / "wc"
+    subprocess.run(["g++", "-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", str(src), "-o", str(exe)], check=True)
+    import test_gpu_perf
+    assert int(subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout) == \
+        test_gpu_perf.WALL_CLOCK_RATE_ATTR
