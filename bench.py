@@ -9,7 +9,9 @@ when the timed region starts.
 
 value = (bytes synthesized + bytes checked) / time per step, in GB/s
 (1e9 bytes/s): synthesis writes n * itemsize bytes, the check reads
-2 * n * itemsize bytes (algorithmic bytes).
+2 * n * itemsize bytes (algorithmic bytes); with an early-exit check
+(candidates_round) a failing segment counts only the bytes up to and
+including its first mismatch.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--no-cpu-baseline] [--copy-probe] [--perf-stage]
@@ -65,6 +67,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="normal_ulp")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--full-check", action="store_true",
+                    help="check failing segments in full even where the workload stops at the first mismatch")
     ap.add_argument("--perf-stage", action="store_true",
                     help="time the fail-fast sequence on a synthetic candidate kernel instead (Eq. 3-4)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -164,20 +168,26 @@ def main():
 
     torch.cuda.set_device(0)
     wl = W.WORKLOADS[args.workload]()
+    if args.full_check:
+        wl.stop_at_first = False
     tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "i32": torch.int32}
-    refs, cands = [], []
-    for case in wl.cases:
-        r = torch.empty(case.ref.n, dtype=tdt[case.ref.dtype], device="cuda")
-        sv.synth(r, case.ref.seed, case.ref.stream, case.ref.dist, **case.ref.params)
+    uniq, which = wl.ref_groups()
+    refs = []
+    for spec in uniq:
+        r = torch.empty(spec.n, dtype=tdt[spec.dtype], device="cuda")
+        sv.synth(r, spec.seed, spec.stream, spec.dist, **spec.params)
+        refs.append(r)
+    cands = []
+    for case, j in zip(wl.cases, which):
+        r = refs[j]
         c = torch.empty_like(r)
         for s in case.steps:
             if s.op in ELEMENTWISE:
                 sv.perturb(r, c, s.seed, s.stream, s.op, p=s.p, value=s.value)
             else:
                 sv.perturb(r, c, s.seed, s.stream, s.op, value=s.value, bits=s.bits, idx=s.idx)
-        refs.append(r)
         cands.append(c)
-    segs = [(r, c, k.rtol, k.atol, k.equal_nan) for r, c, k in zip(refs, cands, wl.cases)]
+    segs = [(refs[j], c, k.rtol, k.atol, k.equal_nan) for c, k, j in zip(cands, wl.cases, which)]
     if args.copy_probe:
         src = torch.ones(1 << 26, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -187,12 +197,12 @@ def main():
         del src, dst
     torch.cuda.synchronize()
 
-    jobs = [(r, c.ref.seed, c.ref.stream, c.ref.dist, c.ref.params) for c, r in zip(wl.cases, refs)]
+    jobs = [(r, spec.seed, spec.stream, spec.dist, spec.params) for spec, r in zip(uniq, refs)]
 
     def step():
         if wl.batched:
             sv.synth_batched(jobs)
-            return sv.compare_batched(segs)
+            return sv.compare_batched(segs, stop_at_first=wl.stop_at_first)
         c = wl.cases[0]
         sv.synth(refs[0], c.ref.seed, c.ref.stream, c.ref.dist, **c.ref.params)
         return [sv.compare(*segs[0])]
@@ -222,6 +232,11 @@ def main():
 
     ms = (t1 - t0) / args.steps * 1e3
     sbytes, cbytes = wl.synth_bytes, wl.compare_bytes
+    if wl.stop_at_first:
+        # bytes a check must read to settle each verdict: a passing segment in full, a failing one
+        # up to and including its first mismatch
+        cbytes = sum(2 * (r["n"] if r["mismatches"] == 0 else r["first_mismatch"] + 1) * k.ref.itemsize
+                     for r, k in zip(reps, wl.cases))
     value = (sbytes + cbytes) / (ms / 1e3) / 1e9
     kernels = {}
     for k, nbytes in (("synth", sbytes), ("compare", cbytes), ("finalize", 0)):
@@ -249,6 +264,7 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(wl.name, dom) if not wl.batched else None},
         "mismatches": [int(r["mismatches"]) for r in reps][:8],
+        "failing_segments": sum(1 for r in reps if r["mismatches"]),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)

@@ -157,6 +157,23 @@ int sv_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
  */
 int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports);
 
+/*
+ * sv_compare_batched_mode -- sv_compare_batched with a choice of how far to
+ * check a failing output, for the fail-fast validation of Sec. 4.2.2 (where a
+ * failing output ends its candidate's validation, e.g. G candidates x their
+ * outputs of one round in one call).
+ *   mode = SV_CHECK_FULL (0): exactly sv_compare_batched.
+ *   mode = SV_CHECK_STOP_AT_FIRST (1): the check of a segment stops where
+ *     it first meets a mismatch (each part of the segment checked in parallel
+ *     stops at its own first one), but every element before the segment's
+ *     first mismatch is still checked.  A passing segment gets its full
+ *     report.  A failing one gets n, mismatches = 1 (meaning "at least one")
+ *     and the exact first_mismatch; its other fields are 0.
+ * Errors as sv_compare_batched; UNSUPPORTED for another mode.
+ */
+enum { SV_CHECK_FULL = 0, SV_CHECK_STOP_AT_FIRST = 1 };
+int sv_compare_batched_mode(const sv_segment *segs, uint32_t nseg, int32_t mode, sv_report *reports);
+
 /* Candidate derivation steps of sv_perturb (workload support, not part of the check). */
 enum {
   SV_OP_COPY = 0,         /* cand[i] = ref[i]                                              */

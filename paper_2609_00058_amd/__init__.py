@@ -28,7 +28,8 @@ OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
 PROF_KINDS = {"synth": 0, "compare": 1, "perturb": 2, "finalize": 3}
 
 # every symbol include/sv.h declares
-SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_compare", "sv_compare_batched", "sv_perturb",
+SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_compare", "sv_compare_batched", "sv_compare_batched_mode",
+           "sv_perturb",
            "sv_eval_transform", "sv_kernel_load", "sv_kernel_free", "sv_kernel_launch", "sv_kernel_time",
            "sv_reward", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
 
@@ -92,6 +93,7 @@ _lib.sv_synth.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u
 _lib.sv_synth_batched.argtypes = [ctypes.POINTER(SynthJob), ctypes.c_uint32]
 _lib.sv_compare.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(Report)]
 _lib.sv_compare_batched.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, ctypes.POINTER(Report)]
+_lib.sv_compare_batched_mode.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, _i32, ctypes.POINTER(Report)]
 _lib.sv_perturb.argtypes = [_u64, _u64, _i32, ctypes.POINTER(PerturbPlan), _u64, _vp, _vp]
 _lib.sv_eval_transform.argtypes = [_i32, _vp, _u64, _vp]
 _lib.sv_kernel_load.argtypes = [ctypes.c_char_p, _u64, ctypes.c_char_p, ctypes.POINTER(_vp)]
@@ -215,8 +217,11 @@ def compare(ref, cand, rtol: float, atol: float, equal_nan: bool = False) -> dic
     return rep.as_dict()
 
 
-def compare_batched(segments) -> list:
-    """segments: list of (ref, cand, rtol, atol, equal_nan); one launch, one report each."""
+def compare_batched(segments, stop_at_first: bool = False) -> list:
+    """segments: list of (ref, cand, rtol, atol, equal_nan); one launch, one report each.
+    stop_at_first: a failing segment is checked only as far as needed to know
+    its first mismatch exactly; its report then holds n, mismatches = 1 and
+    first_mismatch, everything else 0."""
     if not segments:
         return []
     arr = (Segment * len(segments))()
@@ -227,7 +232,7 @@ def compare_batched(segments) -> list:
                          _dev_ptr(cand, "cand") if cand.numel() else None,
                          ref.numel(), dtype_code(ref), rtol, atol, int(bool(eqn)))
     reps = (Report * len(segments))()
-    _run(segments[0][0], _lib.sv_compare_batched, arr, len(segments), reps)
+    _run(segments[0][0], _lib.sv_compare_batched_mode, arr, len(segments), 1 if stop_at_first else 0, reps)
     return [reps[k].as_dict() for k in range(len(segments))]
 
 

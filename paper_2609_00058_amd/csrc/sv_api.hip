@@ -310,13 +310,14 @@ void compare_grid(uint64_t units, int cus, uint32_t *nblocks, uint64_t *chunk) {
 // host waits for that number.  Segments with no elements get their (empty)
 // report here.
 int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_segment *segs, uint32_t nseg,
-                sv_report *out) {
+                sv_report *out, bool stop_at_first = false) {
   hipStream_t st = t_stream;
   int rc = ensure_device(ds->partials, ds->partials_cap, (size_t)nblocks + nseg, "partials");
   if (!rc) rc = ensure_reports(ds, nseg);
   if (!rc) rc = ensure_counters(ds, 1);
   if (!rc) rc = ensure_done(ds);
   if (rc) return rc;
+  args.stop_at_first = stop_at_first ? 1 : 0;
   args.partials = ds->partials;
   args.counter = ds->counters;
   args.reports = ds->d_reports;
@@ -351,6 +352,12 @@ int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_s
       out[k] = ds->h_reports[k];
     else
       zero_report(&out[k], 0);
+    if (stop_at_first && out[k].mismatches) {   // only the verdict and the first index are defined
+      const int64_t first = out[k].first_mismatch;
+      zero_report(&out[k], n);
+      out[k].mismatches = 1;
+      out[k].first_mismatch = first;
+    }
   }
   return SV_OK;
 }
@@ -549,7 +556,13 @@ int sv_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype, dou
 }
 
 int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports) {
+  return sv_compare_batched_mode(segs, nseg, SV_CHECK_FULL, reports);
+}
+
+int sv_compare_batched_mode(const sv_segment *segs, uint32_t nseg, int32_t mode, sv_report *reports) {
   t_error.clear();
+  if (mode != SV_CHECK_FULL && mode != SV_CHECK_STOP_AT_FIRST)
+    return fail(SV_ERR_UNSUPPORTED, "sv_compare_batched_mode: unknown mode %d", mode);
   if (nseg == 0) return SV_OK;
   if (!segs || !reports) return fail(SV_ERR_INVALID_ARG, "sv_compare_batched: segs or reports is NULL");
   uint64_t total = 0;
@@ -583,7 +596,7 @@ int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports
   args.total_units = total;
   uint32_t nblocks;
   compare_grid(total, ds->cus, &nblocks, &args.chunk);
-  return run_compare(ds, args, nblocks, segs, nseg, reports);
+  return run_compare(ds, args, nblocks, segs, nseg, reports, mode == SV_CHECK_STOP_AT_FIRST);
 }
 
 int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_perturb_plan *plan, uint64_t n,

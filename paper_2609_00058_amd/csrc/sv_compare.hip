@@ -256,8 +256,15 @@ __device__ __forceinline__ void arrive_and_signal(const CompareArgs &args) {
   __hip_atomic_store(args.done, args.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// Early exit (kStop): a wave leaves its piece once its next tile starts past
+// its own first mismatch.  Every unit below a wave's first mismatch is still
+// checked, so the segment's first mismatch (the smallest over its waves) stays
+// exact; the other statistics cover a timing-independent but partial set.  A
+// shared "first mismatch so far" word that every wave could poll was measured
+// slower: thousands of device-scope atomics and uncached reads on a few words
+// queue up at their memory channels.
 // Units [ulo, uhi) of one segment -> a workgroup partial, valid on thread 0.
-template <int DT>
+template <int DT, bool kStop = false>
 __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Partial *lds) {
   constexpr int V = Elem<DT>::V;
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
@@ -273,6 +280,7 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
   uint64_t base = ulo + wave * kWave;
   // whole tiles: kUnroll sub-iterations of kBlock units, every unit full
   for (; base + (uint64_t)(kUnroll - 1) * kBlock + kWave <= full_end; base += (uint64_t)kBlock * kUnroll) {
+    if (kStop && base * V > W.first) break;
     u32x4 yv[kUnroll], av[kUnroll];
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k) {
@@ -286,6 +294,7 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
   }
   // the rest, one sub-iteration at a time, guarded (same unit order)
   for (; base < uhi; base += kBlock) {
+    if (kStop && base * V > W.first) break;
     const uint64_t u = base + lane;
     u32x4 yv = u32x4{0, 0, 0, 0}, av = u32x4{0, 0, 0, 0};
     if (u < full_end) {
@@ -386,7 +395,7 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
 // kMask: the set of dtypes (bit 1 << dtype) the segments of this launch use;
 // only their code paths are compiled in, which keeps register pressure at
 // what the widest of them needs.
-template <bool kSingle, int kMask>
+template <bool kSingle, int kMask, bool kStop = false>
 __global__ __launch_bounds__(kBlock) void compare_kernel(CompareArgs args) {
   __shared__ Partial lds[kWavesPerBlock];
   const uint64_t b = blockIdx.x;
@@ -400,18 +409,18 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(CompareArgs args) {
     const uint64_t ulo = lo - sd.unit_begin, uhi = piece_hi - sd.unit_begin;
     Partial p;
     if constexpr (kMask == (1 << SV_F32)) {
-      p = check_piece<SV_F32>(sd, ulo, uhi, lds);
+      p = check_piece<SV_F32, kStop>(sd, ulo, uhi, lds);
     } else if constexpr (kMask == (1 << SV_BF16)) {
-      p = check_piece<SV_BF16>(sd, ulo, uhi, lds);
+      p = check_piece<SV_BF16, kStop>(sd, ulo, uhi, lds);
     } else if constexpr (kMask == (1 << SV_I32)) {
-      p = check_piece<SV_I32>(sd, ulo, uhi, lds);
+      p = check_piece<SV_I32, kStop>(sd, ulo, uhi, lds);
     } else {
       if ((kMask & (1 << SV_F32)) && sd.dtype == SV_F32)
-        p = check_piece<SV_F32>(sd, ulo, uhi, lds);
+        p = check_piece<SV_F32, kStop>(sd, ulo, uhi, lds);
       else if ((kMask & (1 << SV_BF16)) && sd.dtype == SV_BF16)
-        p = check_piece<SV_BF16>(sd, ulo, uhi, lds);
+        p = check_piece<SV_BF16, kStop>(sd, ulo, uhi, lds);
       else
-        p = check_piece<SV_I32>(sd, ulo, uhi, lds);
+        p = check_piece<SV_I32, kStop>(sd, ulo, uhi, lds);
     }
     if (threadIdx.x == 0) args.partials[b + s] = p;
     if constexpr (kSingle) return;   // one segment: the chunk is a single piece
@@ -428,6 +437,8 @@ static void launch_masked(const CompareArgs &args, uint32_t nblocks, hipStream_t
   const bool single = args.segs == nullptr;
   if (single)
     hipLaunchKernelGGL((compare_kernel<true, kMask>), dim3(nblocks), dim3(kBlock), 0, stream, args);
+  else if (args.stop_at_first)
+    hipLaunchKernelGGL((compare_kernel<false, kMask, true>), dim3(nblocks), dim3(kBlock), 0, stream, args);
   else
     hipLaunchKernelGGL((compare_kernel<false, kMask>), dim3(nblocks), dim3(kBlock), 0, stream, args);
   if (ev_mid) (void)hipEventRecord(ev_mid, stream);

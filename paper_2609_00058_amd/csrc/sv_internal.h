@@ -106,6 +106,7 @@ struct CompareArgs {
   uint64_t chunk;               // units per workgroup
   Partial *partials;            // nblocks + nseg slots
   uint32_t *counter;            // finalize arrivals, zero between launches
+  int32_t stop_at_first;        // batched: each wave stops at its first mismatch
   sv_report *reports;           // nseg reports, in host-mapped pinned memory
   uint64_t *done;               // host-mapped word that receives `seq` once every report is written
   uint64_t seq;

@@ -167,3 +167,61 @@ def test_indices_beyond_2_pow_32():
     assert rep["max_abs_err"] == abs(a - y) and rep["err_sum"] == abs(a - y)
     del ref, cand
     torch.cuda.empty_cache()
+
+
+def _stop_expect(full):
+    if full["mismatches"] == 0:
+        return full
+    out = {k: (0 if isinstance(v, int) else 0.0) for k, v in full.items()}
+    out.update(n=full["n"], mismatches=1, first_mismatch=full["first_mismatch"])
+    return out
+
+
+def test_batched_stop_at_first(oracle):
+    # G candidates x outputs: clean, wrong from the start, wrong at the very end, one fault in the middle,
+    # a NaN against a number, 1 % wrong; the early exit must keep the first index exact
+    rng = np.random.default_rng(33)
+    segs, want, keep = [], [], []
+    for k, n in enumerate([1, 7, 1000, 65537, (1 << 20) + 3, 1 << 22, (1 << 22) + 5, 12345]):
+        dtype = ["f32", "bf16", "i32"][k % 3]
+        ref, cand = random_pair(rng, n, dtype, special_frac=0.0)
+        if dtype == "i32":
+            ref_vals = ref.view(np.int32)
+        tol = (1e-5, 1e-8, False) if dtype != "bf16" else (1e-2, 1e-2, False)
+        R = dev(ref, dtype)
+        keep.append(R)
+        variants = [ref.copy()]                                  # passes
+        bad = ref.copy()
+        bad_pos = [0, n - 1, n // 2]
+        for pos in bad_pos:                                      # a wrong value at pos
+            c = ref.copy()
+            if dtype == "i32":
+                c.view(np.int32)[pos] += 1
+            elif dtype == "bf16":
+                c[pos] = 0x7FC0                                  # NaN against a number
+            else:
+                c[pos] = np.float32(c.view(np.float32)[pos] * 2 + 1).view(np.uint32)
+            variants.append(c)
+        if n >= 100:
+            c = ref.copy()
+            idx = rng.choice(n, n // 100, replace=False)
+            c[idx] = ref[(idx + 1) % n] if dtype != "i32" else (ref.view(np.int32)[idx] + 7).view(np.uint32)
+            variants.append(c)
+        for c in variants:
+            C = dev(c, dtype)
+            keep.append(C)
+            segs.append((R, C, *tol))
+            want.append(oracle.compare(ref, c, dtype, *tol))
+    print("stop-at-first batch", len(segs), flush=True)
+    for rep in range(2):                                         # the early-exit words reset between calls
+        got = sv.compare_batched(segs, stop_at_first=True)
+        for g, w in zip(got, want):
+            same_report(g, _stop_expect(w))
+    got = sv.compare_batched(segs)                               # and the full check is unaffected
+    for g, w in zip(got, want):
+        same_report(g, w)
+    with pytest.raises(sv.SVError) as e:
+        arr = (sv.Segment * 1)()
+        reps = (sv.Report * 1)()
+        sv._check(sv.lib().sv_compare_batched_mode(arr, 1, 2, reps))
+    assert e.value.code == sv.SV_ERR_UNSUPPORTED

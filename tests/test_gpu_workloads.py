@@ -110,3 +110,38 @@ def test_special_stream_full(oracle):
     assert np.array_equal(bits_at(ref, idx), r) and np.array_equal(bits_at(cand, idx), c)
     del ref, cand
     torch.cuda.empty_cache()
+
+
+def test_candidates_round_full(oracle):
+    wl = W.candidates_round()
+    uniq, which = wl.ref_groups()
+    print("candidates round: gpu", flush=True)
+    refs = [gpu_ref(s) for s in uniq]
+    cands = [gpu_cand(c, refs[j]) for c, j in zip(wl.cases, which)]
+    segs = [(refs[j], c, k.rtol, k.atol, k.equal_nan) for c, k, j in zip(cands, wl.cases, which)]
+    stop = sv.compare_batched(segs, stop_at_first=True)
+    full = sv.compare_batched(segs)
+    for k, case in enumerate(wl.cases):
+        g = k % 3
+        if g == 0:
+            assert full[k]["mismatches"] == 0 and full[k]["err_sum"] == 0.0 and stop[k] == full[k]
+            continue
+        f = full[k]["first_mismatch"]
+        assert stop[k]["mismatches"] == 1 and stop[k]["first_mismatch"] == f and stop[k]["err_sum"] == 0.0
+        if g == 2:
+            assert full[k]["mismatches"] == 1 and f == wl.expect["faults"][k]
+        else:
+            assert full[k]["mismatches"] > 0.99 * case.ref.n
+        # the first mismatch is exact: the oracle, element by element up to it, finds nothing earlier
+        lo = 0 if f < 4096 else f - 64
+        idx = np.arange(lo, f + 1, dtype=np.uint64)
+        r, c = oracle_elements(case, idx)
+        assert np.array_equal(bits_at(refs[which[k]], idx), r) and np.array_equal(bits_at(cands[k], idx), c)
+        rep = oracle.compare(r, c, "f32", case.rtol, case.atol, case.equal_nan)
+        assert rep["first_mismatch"] == f - lo
+    print("candidates round: oracle on two whole segments", flush=True)
+    for k in (1, 5):
+        r, c, want = oracle_case_parallel(wl.cases[k])
+        same_report(full[k], want)
+    del refs, cands, segs
+    torch.cuda.empty_cache()

@@ -104,3 +104,22 @@ def test_reference_synthesis_windows_compose():
     case = W.normal_ulp(4096).cases[0]
     full = oracle_ref(case.ref)
     assert np.array_equal(np.concatenate([oracle_ref(case.ref, 0, 1000), oracle_ref(case.ref, 1000)]), full)
+
+
+def test_candidates_round_verdicts_at_reduced_size():
+    from oracle_run import oracle_case
+    n = 1 << 14
+    wl = W.candidates_round(outputs=2, n=n)
+    assert W.candidates_round(outputs=2, n=n).expect == wl.expect and wl.stop_at_first
+    uniq, which = wl.ref_groups()
+    assert len(uniq) == 2 and which == [0, 0, 0, 1, 1, 1]
+    assert wl.synth_bytes == 2 * 4 * n and wl.compare_bytes == 6 * 2 * 4 * n
+    for k, case in enumerate(wl.cases):
+        _, _, rep = oracle_case(case)
+        g = k % 3
+        if g == 0:       # reproduces the reference
+            assert rep["mismatches"] == 0 and rep["err_sum"] == 0.0 and rep["first_mismatch"] == -1
+        elif g == 1:     # |u| <= 1e-2 against rtol 1e-5: wrong almost everywhere
+            assert rep["mismatches"] > 0.99 * n and rep["first_mismatch"] < 100
+        else:            # exactly the seeded fault
+            assert rep["mismatches"] == 1 and rep["first_mismatch"] == wl.expect["faults"][k]

@@ -79,6 +79,20 @@ class Workload:
     batched: bool
     description: str = ""
     expect: dict = field(default_factory=dict)
+    stop_at_first: bool = False     # batched check stops each failing segment at its first mismatch
+
+    def ref_groups(self):
+        """The distinct reference tensors (cases may share one: several
+        candidates checked against the same output) and, per case, the index
+        of its reference among them."""
+        uniq, which, seen = [], [], {}
+        for c in self.cases:
+            key = (c.ref.n, c.ref.dtype, c.ref.dist, tuple(sorted(c.ref.params.items())), c.ref.seed, c.ref.stream)
+            if key not in seen:
+                seen[key] = len(uniq)
+                uniq.append(c.ref)
+            which.append(seen[key])
+        return uniq, which
 
     @property
     def total_elems(self) -> int:
@@ -86,11 +100,11 @@ class Workload:
 
     @property
     def synth_bytes(self) -> int:
-        return sum(c.ref.nbytes for c in self.cases)
+        return sum(r.nbytes for r in self.ref_groups()[0])
 
     @property
     def compare_bytes(self) -> int:
-        return 2 * self.synth_bytes
+        return 2 * sum(c.ref.nbytes for c in self.cases)
 
 
 def _distinct(rng: np.random.Generator, n: int, k: int) -> np.ndarray:
@@ -182,10 +196,39 @@ def special_stream(n: int = 1 << 30) -> Workload:
                     expect=dict(mismatches=0, err_sum=0.0))
 
 
+def candidates_round(outputs: int = 8, n: int = 1 << 24, G: int = 3) -> Workload:
+    """One round of the generation loop (Sec. 5.1: G = 3 kernels per round)
+    validated in one batched check: 8 outputs of 2^24 fp32 normal(5, 10)
+    (streams 0..7), each checked against 3 candidates -- the first reproduces
+    the reference, the second is off everywhere (x(1+u), |u| <= 1e-2), the
+    third has one wrong element at a seeded index; rtol 1e-5, atol 1e-6.  The
+    check stops each failing segment at its first mismatch (fail-fast,
+    Sec. 4.2.2)."""
+    rng = np.random.Generator(np.random.PCG64(1006))
+    cases, faults = [], {}
+    for j in range(outputs):
+        ref = TensorSpec(n, "f32", "normal", dict(mean=5.0, std=10.0), stream=j)
+        for g in range(G):
+            if g % 3 == 0:
+                steps = [Step("copy")]
+            elif g % 3 == 1:
+                steps = [Step("scale", p=1.0, value=1e-2, stream=harness_stream(TAG_SCALE, 1000 + G * j + g))]
+            else:
+                pos = np.array([rng.integers(0, n)], dtype=np.uint64)
+                faults[len(cases)] = int(pos[0])
+                steps = [Step("copy"), Step("fault_at", idx=pos)]
+            cases.append(Case(ref, steps, 1e-5, 1e-6, False))
+    return Workload("candidates_round_%dx%dx%d" % (outputs, G, n), cases, True,
+                    "%d fp32 outputs of %d elements x %d candidates (exact, off everywhere, one fault); "
+                    "stop at first mismatch" % (outputs, n, G),
+                    expect=dict(faults=faults), stop_at_first=True)
+
+
 WORKLOADS = {
     "uniform_small": uniform_small,
     "normal_ulp": normal_ulp,
     "bf16_batch": bf16_batch,
     "ragged_batch": ragged_batch,
     "special_stream": special_stream,
+    "candidates_round": candidates_round,
 }
