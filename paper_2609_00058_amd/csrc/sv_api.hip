@@ -295,9 +295,10 @@ void zero_report(sv_report *r, uint64_t n) {
 
 // grid for a check over `units` 16-byte units: at most SV_CMP_BLOCKS_PER_CU
 // workgroups per CU, each owning whole waves of units
-void compare_grid(uint64_t units, int cus, uint32_t *nblocks, uint64_t *chunk) {
+void compare_grid(uint64_t units, int cus, bool batched, uint32_t *nblocks, uint64_t *chunk) {
   const uint64_t per_iter = (uint64_t)kBlock;
-  uint64_t nb = std::min<uint64_t>((units + per_iter - 1) / per_iter, (uint64_t)cus * SV_CMP_BLOCKS_PER_CU);
+  const uint64_t per_cu = batched ? SV_CMP_BATCH_BLOCKS_PER_CU : SV_CMP_BLOCKS_PER_CU;
+  uint64_t nb = std::min<uint64_t>((units + per_iter - 1) / per_iter, (uint64_t)cus * per_cu);
   if (nb == 0) nb = 1;
   uint64_t c = (units + nb - 1) / nb;
   c = (c + kWave - 1) / kWave * kWave;       // whole waves of units per workgroup
@@ -551,7 +552,7 @@ int sv_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype, dou
   args.nseg = 1;
   args.total_units = units_of(dtype, n);
   uint32_t nblocks;
-  compare_grid(args.total_units, ds->cus, &nblocks, &args.chunk);
+  compare_grid(args.total_units, ds->cus, false, &nblocks, &args.chunk);
   return run_compare(ds, args, nblocks, nullptr, 1, report);
 }
 
@@ -595,7 +596,7 @@ int sv_compare_batched_mode(const sv_segment *segs, uint32_t nseg, int32_t mode,
   args.nseg = nseg;
   args.total_units = total;
   uint32_t nblocks;
-  compare_grid(total, ds->cus, &nblocks, &args.chunk);
+  compare_grid(total, ds->cus, true, &nblocks, &args.chunk);
   return run_compare(ds, args, nblocks, segs, nseg, reports, mode == SV_CHECK_STOP_AT_FIRST);
 }
 

@@ -179,7 +179,36 @@ __device__ __forceinline__ void check_unit(const u32x4 &yv, const u32x4 &av, uin
   }
 }
 
-__device__ __forceinline__ double shfl_xor_d(double v, int m) { return __shfl_xor(v, m, kWave); }
+// ---- cross-lane steps of the wave reductions
+// Step k pairs each lane with one holding the other half of its 2^(k+1)-lane
+// group: for groups of 2, 4, 8 and 16 lanes through DPP moves inside the VALU
+// (quad permutes, then the half-row and row mirrors, whose partner lies in the
+// other half of the group, which after the earlier steps holds one uniform
+// value), for 32 and 64 lanes through the LDS crossbar.  Every merge is
+// commutative, so the result is one fixed tree, identical on every lane.
+constexpr int kDppXor1 = 0xB1;       // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+
+template <int kStep>
+__device__ __forceinline__ uint32_t lane_pair32(uint32_t v) {
+  if constexpr (kStep == 0) return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kDppXor1, 0xF, 0xF, false);
+  else if constexpr (kStep == 1) return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kDppXor2, 0xF, 0xF, false);
+  else if constexpr (kStep == 2) return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kDppHalfMirror, 0xF, 0xF, false);
+  else if constexpr (kStep == 3) return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, kDppMirror, 0xF, 0xF, false);
+  else return (uint32_t)__shfl_xor((int)v, kStep == 4 ? 16 : 32, kWave);
+}
+
+template <int kStep>
+__device__ __forceinline__ uint64_t lane_pair(uint64_t v) {
+  return ((uint64_t)lane_pair32<kStep>((uint32_t)(v >> 32)) << 32) | lane_pair32<kStep>((uint32_t)v);
+}
+
+template <int kStep>
+__device__ __forceinline__ double lane_pair(double v) {
+  return __longlong_as_double((long long)lane_pair<kStep>((uint64_t)__double_as_longlong(v)));
+}
 
 __device__ __forceinline__ void merge(Partial &a, const Partial &b) {
   a.mism += b.mism;
@@ -200,21 +229,28 @@ __device__ __forceinline__ Partial empty_partial() {
   return p;
 }
 
+template <int kStep>
+__device__ __forceinline__ void merge_step(Partial &acc) {
+  Partial o;
+  o.mism = lane_pair<kStep>(acc.mism);
+  o.first = lane_pair<kStep>(acc.first);
+  o.maxabs = lane_pair<kStep>(acc.maxabs);
+  o.maxrel = lane_pair<kStep>(acc.maxrel);
+  o.sum = lane_pair<kStep>(acc.sum);
+  o.nan_r = lane_pair<kStep>(acc.nan_r);
+  o.nan_c = lane_pair<kStep>(acc.nan_c);
+  o.inf_r = lane_pair<kStep>(acc.inf_r);
+  o.inf_c = lane_pair<kStep>(acc.inf_c);
+  merge(acc, o);
+}
+
 __device__ __forceinline__ void wave_merge(Partial &acc) {
-#pragma unroll
-  for (int m = kWave / 2; m >= 1; m >>= 1) {
-    Partial o;
-    o.mism = __shfl_xor(acc.mism, m, kWave);
-    o.first = __shfl_xor(acc.first, m, kWave);
-    o.maxabs = shfl_xor_d(acc.maxabs, m);
-    o.maxrel = shfl_xor_d(acc.maxrel, m);
-    o.sum = shfl_xor_d(acc.sum, m);
-    o.nan_r = __shfl_xor(acc.nan_r, m, kWave);
-    o.nan_c = __shfl_xor(acc.nan_c, m, kWave);
-    o.inf_r = __shfl_xor(acc.inf_r, m, kWave);
-    o.inf_c = __shfl_xor(acc.inf_c, m, kWave);
-    merge(acc, o);
-  }
+  merge_step<0>(acc);
+  merge_step<1>(acc);
+  merge_step<2>(acc);
+  merge_step<3>(acc);
+  merge_step<4>(acc);
+  merge_step<5>(acc);
 }
 
 __device__ __forceinline__ uint64_t dbits(double x) { return (uint64_t)__double_as_longlong(x); }
@@ -226,9 +262,8 @@ __device__ __forceinline__ void wait_memory() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// The report, field by field, with system-scope stores into host-mapped memory.
-__device__ __forceinline__ void write_report(sv_report *dst, const Partial &r, uint64_t n) {
-  uint64_t v[10];
+// The report as ten 64-bit words, in sv_report's field order.
+__device__ __forceinline__ void report_words(const Partial &r, uint64_t n, uint64_t *v) {
   v[0] = n;
   v[1] = r.mism;
   v[2] = r.first == kNone ? ~0ull : r.first;     // -1 as int64 when there is no mismatch
@@ -239,10 +274,8 @@ __device__ __forceinline__ void write_report(sv_report *dst, const Partial &r, u
   v[7] = r.nan_c;
   v[8] = r.inf_r;
   v[9] = r.inf_c;
-  uint64_t *w = (uint64_t *)dst;
-#pragma unroll
-  for (int i = 0; i < 10; ++i) __hip_atomic_store(w + i, v[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
+constexpr int kReportWords = 10;
 
 // Called by one thread of every finalize workgroup once its report (if any)
 // is written: the last to arrive clears the counter and, after every store
@@ -254,6 +287,13 @@ __device__ __forceinline__ void arrive_and_signal(const CompareArgs &args) {
   __hip_atomic_store(args.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   wait_memory();
   __hip_atomic_store(args.done, args.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+template <int kStep>
+__device__ __forceinline__ void lane_step(LaneAcc &L) {
+  L.sum += lane_pair<kStep>(L.sum);
+  L.maxabs = fmax(L.maxabs, lane_pair<kStep>(L.maxabs));
+  L.maxrel = fmax(L.maxrel, lane_pair<kStep>(L.maxrel));
 }
 
 // Early exit (kStop): a wave leaves its piece once its next tile starts past
@@ -319,12 +359,12 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
     check_unit<DT>(yv, av, base * V, rtol, atol, eqn, L, W);
   }
   // lanes -> wave -> workgroup
-#pragma unroll
-  for (int m = kWave / 2; m >= 1; m >>= 1) {
-    L.sum += shfl_xor_d(L.sum, m);
-    L.maxabs = fmax(L.maxabs, shfl_xor_d(L.maxabs, m));
-    L.maxrel = fmax(L.maxrel, shfl_xor_d(L.maxrel, m));
-  }
+  lane_step<0>(L);
+  lane_step<1>(L);
+  lane_step<2>(L);
+  lane_step<3>(L);
+  lane_step<4>(L);
+  lane_step<5>(L);
   if (lane == 0) {
     Partial p;
     p.mism = W.mism; p.first = W.first;
@@ -382,12 +422,18 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
     wave_merge(acc);
     if (lane == 0) lds[wave] = acc;
     __syncthreads();
+    __shared__ uint64_t words[kReportWords];
     if (tid == 0) {
       Partial r = lds[0];
 #pragma unroll
       for (int w = 1; w < kFinWaves; ++w) merge(r, lds[w]);
-      write_report(args.reports + s, r, sd.n);
+      report_words(r, sd.n, words);
     }
+    __syncthreads();
+    // ten lanes of wave 0 write the report together, with system-scope stores
+    if (tid < kReportWords)
+      __hip_atomic_store((uint64_t *)(args.reports + s) + tid, words[tid], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_SYSTEM);
   }
   if (tid == 0) arrive_and_signal(args);
 }

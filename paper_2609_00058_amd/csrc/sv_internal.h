@@ -14,7 +14,10 @@ namespace sv {
 #define SV_CMP_UNROLL 4              // 16-byte units per thread in flight in the check
 #endif
 #ifndef SV_CMP_BLOCKS_PER_CU
-#define SV_CMP_BLOCKS_PER_CU 16      // check workgroups per CU
+#define SV_CMP_BLOCKS_PER_CU 16      // check workgroups per CU, single tensor
+#endif
+#ifndef SV_CMP_BATCH_BLOCKS_PER_CU
+#define SV_CMP_BATCH_BLOCKS_PER_CU 12   // check workgroups per CU, batched
 #endif
 #ifndef SV_SYNTH_BLOCKS_PER_CU
 #define SV_SYNTH_BLOCKS_PER_CU 64    // synthesis workgroups per CU
