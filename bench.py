@@ -69,6 +69,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--full-check", action="store_true",
                     help="check failing segments in full even where the workload stops at the first mismatch")
+    ap.add_argument("--files", action="store_true",
+                    help="time synthesis into a file and the check of two files instead (1 GiB fp32 each)")
     ap.add_argument("--perf-stage", action="store_true",
                     help="time the fail-fast sequence on a synthetic candidate kernel instead (Eq. 3-4)")
     ap.add_argument("--copy-probe", action="store_true",
@@ -154,6 +156,76 @@ def perf_stage(args):
     print(json.dumps(out), flush=True)
 
 
+def files_stage(args):
+    """Test data as files: sv_synth_file writes 2^28 fp32 normal(5, 10) values
+    (1 GiB) to a file; sv_compare_file checks that file against a candidate
+    file (the reference with +-1 ulp on 0.1 % of elements, written untimed).
+    Each is timed over `steps` runs after one untimed run (synthesis into a
+    new file each time), next to the rates of a plain 1 GiB write into a new
+    file and a single-threaded 2 GiB read of the same files (page cache warm),
+    which bound them.  `value` is the file check's GB/s."""
+    import shutil
+    import tempfile
+    import numpy as np
+    import torch
+    import paper_2609_00058_amd as sv
+    torch.cuda.set_device(0)
+    n = 1 << 28
+    d = tempfile.mkdtemp(prefix="sv_bench_", dir=os.environ.get("SV_BENCH_DIR", "/tmp"))
+    try:
+        rp, cp = os.path.join(d, "ref.bin"), os.path.join(d, "cand.bin")
+        prm = dict(mean=5.0, std=10.0)
+        sv.synth_file(rp, n, 0, 0, "f32", "normal", **prm)
+        ref = torch.empty(n, device="cuda")
+        sv.synth(ref, 0, 0, "normal", **prm)
+        cand = torch.empty_like(ref)
+        sv.perturb(ref, cand, 0, 1, "ulp", p=1e-3)
+        cand.cpu().numpy().tofile(cp)
+        del ref, cand
+        torch.cuda.empty_cache()
+        t = []
+        for k in range(args.steps):
+            sp = os.path.join(d, "synth%d.bin" % k)   # a new file: overwriting one first frees its cached pages
+            t0 = time.perf_counter()
+            sv.synth_file(sp, n, 0, 0, "f32", "normal", **prm)
+            t.append(time.perf_counter() - t0)
+            os.unlink(sp)
+        synth_s = sorted(t)[len(t) // 2]
+        sv.compare_file(rp, cp, n, "f32", 1e-6, 0.0)
+        t = []
+        for _ in range(args.steps):
+            t0 = time.perf_counter()
+            rep = sv.compare_file(rp, cp, n, "f32", 1e-6, 0.0)
+            t.append(time.perf_counter() - t0)
+        cmp_s = sorted(t)[len(t) // 2]
+        buf = np.fromfile(rp, dtype=np.uint8)
+        t0 = time.perf_counter()
+        with open(os.path.join(d, "plain.bin"), "wb") as f:
+            f.write(memoryview(buf))
+        write_s = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        for path in (rp, cp):
+            with open(path, "rb") as f:
+                while f.readinto(memoryview(buf)[: 64 << 20]):
+                    pass
+        read_s = time.perf_counter() - t0
+        st = os.statvfs(d)
+        nbytes = 4 * n
+        out = {"metric": "file check throughput (GB/s of file bytes read)", "value": round(2 * nbytes / cmp_s / 1e9, 2),
+               "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": 1, "ms_per_step": round(cmp_s * 1e3, 2),
+               "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+               "data": "synthetic", "config": {"workload": "files_f32_268435456", "dir": d,
+                                               "dir_free_GB": round(st.f_bavail * st.f_frsize / 1e9, 1)},
+               "synth_file_GBps": round(nbytes / synth_s / 1e9, 2),
+               "compare_file_GBps": round(2 * nbytes / cmp_s / 1e9, 2),
+               "plain_write_GBps": round(nbytes / write_s / 1e9, 2),
+               "plain_read_GBps": round(2 * nbytes / read_s / 1e9, 2),
+               "report": {k: rep[k] for k in ("mismatches", "first_mismatch", "max_rel_err")}}
+        print(json.dumps(out), flush=True)
+    finally:
+        shutil.rmtree(d, ignore_errors=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -162,6 +234,8 @@ def main():
         sys.exit(2)
     if args.perf_stage:
         return perf_stage(args)
+    if args.files:
+        return files_stage(args)
     import torch
     import paper_2609_00058_amd as sv
     import workloads as W

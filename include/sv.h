@@ -41,7 +41,8 @@ enum {
   SV_ERR_INVALID_ARG = -1, /* null pointer with n > 0, bad tolerance or parameter, size overflow */
   SV_ERR_UNSUPPORTED = -2, /* unknown dtype / dist / op, or an unsupported combination          */
   SV_ERR_HIP = -3,         /* a HIP runtime call failed; the message carries hipGetErrorString  */
-  SV_ERR_ALLOC = -4        /* scratch allocation failed                                         */
+  SV_ERR_ALLOC = -4,       /* scratch allocation failed                                         */
+  SV_ERR_IO = -5           /* a file could not be opened, read or written (sv_*_file)           */
 };
 
 /* Element types.  Storage is contiguous, little-endian, 1-D. */
@@ -129,6 +130,18 @@ typedef struct {
  * launch.  Any invalid job fails the whole call before anything is launched.
  */
 int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs);
+
+/*
+ * sv_synth_window -- elements [offset, offset + n) of the tensor that
+ * sv_synth(seed, stream_id, dtype, dist, params, N, .) produces for any
+ * N >= offset + n, written to out[0 .. n): the same bits as that slice (the
+ * counter-based generator needs no state from the elements before it), so a
+ * tensor can be produced in pieces, on several devices or straight into a file.
+ * Arguments and errors as sv_synth; INVALID_ARG if offset + n > 2^60.
+ * Asynchronous.
+ */
+int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, const sv_dist_params *params,
+                    uint64_t offset, uint64_t n, void *out);
 
 /*
  * sv_compare -- evaluate Eq. (1) on every element and reduce into *report.
@@ -220,6 +233,31 @@ int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_pertur
  */
 enum { SV_EVAL_LN = 0, SV_EVAL_RADIUS = 1, SV_EVAL_SIN = 2, SV_EVAL_COS = 3 };
 int sv_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out);
+
+/*
+ * ---- Test data as files (Sec. 4.1: the generated program reads its inputs
+ * from binary files and writes its outputs to binary files) ----
+ *
+ * sv_synth_file -- writes the n elements sv_synth would produce to `path`
+ * (created or truncated) as raw little-endian values of `dtype`, n * itemsize
+ * bytes, nothing else.  Generated on the current device in 64 MiB chunks, the
+ * copy of each to the host overlapping the file write of the one before.
+ * Synchronous.  Errors: as sv_synth for the distribution arguments; IO when
+ * the file cannot be created or written (a partial file may remain); ALLOC.
+ *
+ * sv_compare_file -- the check of sv_compare between two files that each hold
+ * exactly n raw little-endian values of `dtype` (read as that type: an int32
+ * file is compared as integers, never reinterpreted as fp32).  Read in 64 MiB
+ * chunks by a reader thread ahead of the device; the chunk reports are merged
+ * exactly except for err_sum, which adds the chunks' sums in order (within
+ * 1e-12 relative of a one-launch check).  Synchronous.  Errors: as sv_compare
+ * for dtype and tolerances; IO when a file cannot be opened or read;
+ * INVALID_ARG when a file's size is not n * itemsize.
+ */
+int sv_synth_file(const char *path, uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist,
+                  const sv_dist_params *params, uint64_t n);
+int sv_compare_file(const char *ref_path, const char *cand_path, uint64_t n, int32_t dtype, double rtol,
+                    double atol, int32_t equal_nan, sv_report *report);
 
 /*
  * ---- Performance stage and reward (Sec. 4.2.2, Eq. (3); Sec. 4.3, Eq. (4)) ----

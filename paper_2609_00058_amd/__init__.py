@@ -20,7 +20,7 @@ if not os.path.exists(LIB_PATH):
 
 _lib = ctypes.CDLL(LIB_PATH)
 
-SV_OK, SV_ERR_INVALID_ARG, SV_ERR_UNSUPPORTED, SV_ERR_HIP, SV_ERR_ALLOC = 0, -1, -2, -3, -4
+SV_OK, SV_ERR_INVALID_ARG, SV_ERR_UNSUPPORTED, SV_ERR_HIP, SV_ERR_ALLOC, SV_ERR_IO = 0, -1, -2, -3, -4, -5
 DTYPE_CODES = {"f32": 0, "bf16": 1, "i32": 2}
 DIST_CODES = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3}
 OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
@@ -28,9 +28,9 @@ OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
 PROF_KINDS = {"synth": 0, "compare": 1, "perturb": 2, "finalize": 3}
 
 # every symbol include/sv.h declares
-SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_compare", "sv_compare_batched", "sv_compare_batched_mode",
+SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_synth_window", "sv_compare", "sv_compare_batched", "sv_compare_batched_mode",
            "sv_perturb",
-           "sv_eval_transform", "sv_kernel_load", "sv_kernel_free", "sv_kernel_launch", "sv_kernel_time",
+           "sv_eval_transform", "sv_synth_file", "sv_compare_file", "sv_kernel_load", "sv_kernel_free", "sv_kernel_launch", "sv_kernel_time",
            "sv_reward", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
 
 
@@ -91,6 +91,7 @@ class Timing(ctypes.Structure):
 _u64, _i32, _vp, _dbl = ctypes.c_uint64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_double
 _lib.sv_synth.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u64, _vp]
 _lib.sv_synth_batched.argtypes = [ctypes.POINTER(SynthJob), ctypes.c_uint32]
+_lib.sv_synth_window.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u64, _u64, _vp]
 _lib.sv_compare.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(Report)]
 _lib.sv_compare_batched.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, ctypes.POINTER(Report)]
 _lib.sv_compare_batched_mode.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, _i32, ctypes.POINTER(Report)]
@@ -101,6 +102,9 @@ _lib.sv_kernel_free.argtypes = [_vp]
 _lib.sv_kernel_launch.argtypes = [_vp, ctypes.POINTER(Launch)]
 _lib.sv_kernel_time.argtypes = [_vp, ctypes.POINTER(Launch), ctypes.c_uint32, ctypes.c_uint32, _u64,
                                 ctypes.POINTER(ctypes.c_float), ctypes.POINTER(Timing)]
+_lib.sv_synth_file.argtypes = [ctypes.c_char_p, _u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u64]
+_lib.sv_compare_file.argtypes = [ctypes.c_char_p, ctypes.c_char_p, _u64, _i32, _dbl, _dbl, _i32,
+                                 ctypes.POINTER(Report)]
 _lib.sv_set_stream.argtypes = [_vp]
 _lib.sv_last_error.restype = ctypes.c_char_p
 _lib.sv_profile_enable.argtypes = [_i32]
@@ -194,6 +198,34 @@ def synth(out, seed: int, stream_id: int, dist: str, **params):
     _run(out, _lib.sv_synth, seed, stream_id, dtype_code(out), DIST_CODES[dist],
          ctypes.byref(dist_params(**params)), out.numel(), _dev_ptr(out, "out"))
     return out
+
+
+def synth_window(out, seed: int, stream_id: int, dist: str, offset: int, **params):
+    """Fill `out` with elements [offset, offset + out.numel()) of the tensor synth() would produce."""
+    p = dist_params(**params)
+    _run(out, _lib.sv_synth_window, seed, stream_id, dtype_code(out), DIST_CODES[dist], ctypes.byref(p), offset,
+         out.numel(), _dev_ptr(out, "out"))
+    return out
+
+
+def _run_current(fn, *args):
+    torch = _torch()
+    _run_on(torch._C._cuda_getDevice(), fn, *args)
+
+
+def synth_file(path: str, n: int, seed: int, stream_id: int, dtype: str, dist: str, **params):
+    """Write the n elements synth() would produce, raw, to `path` (on the current device; synchronous)."""
+    _run_current(_lib.sv_synth_file, os.fsencode(path), seed, stream_id, DTYPE_CODES[dtype], DIST_CODES[dist],
+                 ctypes.byref(dist_params(**params)), n)
+
+
+def compare_file(ref_path: str, cand_path: str, n: int, dtype: str, rtol: float, atol: float,
+                 equal_nan: bool = False) -> dict:
+    """Eq. (1) between two raw files of n elements of `dtype` (on the current device)."""
+    r = Report()
+    _run_current(_lib.sv_compare_file, os.fsencode(ref_path), os.fsencode(cand_path), n, DTYPE_CODES[dtype],
+                 rtol, atol, int(bool(equal_nan)), ctypes.byref(r))
+    return r.as_dict()
 
 
 def synth_batched(jobs):

@@ -14,7 +14,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["sv_api.hip", "sv_synth.hip", "sv_perturb.hip", "sv_compare.hip", "sv_perf.hip"]
+SOURCES = ["sv_api.hip", "sv_synth.hip", "sv_perturb.hip", "sv_compare.hip", "sv_perf.hip", "sv_files.hip"]
 LIB = os.path.join(HERE, "libsynthverify.so")
 ARCH = os.environ.get("SV_OFFLOAD_ARCH", "gfx950")
 

@@ -440,10 +440,20 @@ int sv_set_stream(void *hip_stream) {
 
 int sv_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, const sv_dist_params *params,
              uint64_t n, void *out) {
+  return sv_synth_window(seed, stream_id, dtype, dist, params, 0, n, out);
+}
+
+int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, const sv_dist_params *params,
+                    uint64_t offset, uint64_t n, void *out) {
   t_error.clear();
   SynthParams p;
   int rc = prepare_synth(seed, stream_id, dtype, dist, params, n, out, &p);
   if (rc) return rc;
+  if (offset > kMaxElems || n > kMaxElems - offset)
+    return fail(SV_ERR_INVALID_ARG, "sv_synth_window: offset + n exceeds 2^60");
+  const uint64_t per_block = dist == SV_SPECIAL ? 1 : dist == SV_INT_RANGE ? 2 : 4;
+  p.e0 = offset;
+  p.c0 = offset / per_block;
   if (!n) return SV_OK;
   int cus;
   rc = cu_count(&cus);
@@ -745,6 +755,7 @@ int sv_shutdown(void) {
     s->h_table_cap = s->h_reports_cap = s->h_idx_cap = 0;
   }
   perf_shutdown();
+  files_shutdown();
   (void)hipSetDevice(prev);
   return SV_OK;
 }

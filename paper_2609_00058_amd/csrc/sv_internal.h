@@ -38,6 +38,8 @@ struct SynthParams {
   int64_t lo;                   // integer range
   uint64_t range;               // hi - lo + 1 (<= 2^32)
   uint64_t t_nan, t_inf, t_den, t_zero;   // cumulative class thresholds on w0
+  uint64_t e0;                  // tensor index of out[0] (a window of the tensor; 0 for a whole tensor)
+  uint64_t c0;                  // e0 / E, the first Philox block (used when E divides e0)
 };
 
 hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint64_t n, void *out,
@@ -122,6 +124,7 @@ void api_clear_error();
 int api_fail(int code, const char *msg);          // records msg, returns code
 int api_hip_fail(hipError_t e, const char *what);
 void perf_shutdown();                             // sv_perf.hip: frees its per-device state
+void files_shutdown();                            // sv_files.hip: frees its staging buffers
 
 __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
   const uint64_t per = dtype == SV_BF16 ? 8 : 4;

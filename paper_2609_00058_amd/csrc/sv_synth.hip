@@ -8,8 +8,10 @@
 // four or eight for the special mix) and writes it with one dwordx4 store.
 // The grid is a fixed multiple of the CU count with a grid-stride loop; the
 // ragged tail (fewer than one vector) is written element by element by the
-// first threads of the same launch.  Outputs that are not 16-byte aligned go
-// through a one-element-per-thread kernel.  The path is ALU-bound (Philox is
+// first threads of the same launch.  Outputs that are not 16-byte aligned, and
+// windows that start inside a Philox block, go through a one-element-per-thread
+// kernel.  A window of a tensor (out[0] = element e0) is the same bits as the
+// slice of the whole tensor: only the counter base moves.  The path is ALU-bound (Philox is
 // 20 64-bit multiply-adds and 20 three-input XORs per block; Box-Muller adds a
 // logarithm, a square root and a sine / cosine pair per two elements).
 #include "sv_device.h"
@@ -92,7 +94,7 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
   for (uint64_t u = gid; u < nvec; u += stride) {
     uint32_t v[V];
 #pragma unroll
-    for (int b = 0; b < B; ++b) block_values<DIST>(p, u * B + b, v + b * E);
+    for (int b = 0; b < B; ++b) block_values<DIST>(p, p.c0 + u * B + b, v + b * E);
     u32x4 o;
     if constexpr (DT == SV_BF16) {
       o.x = bf16_rne(v[0]) | (bf16_rne(v[1]) << 16);
@@ -109,9 +111,10 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
   }
   const uint64_t i = nvec * V + gid;
   if (i < n) {
+    const uint64_t g = p.e0 + i;
     uint32_t v[E];
-    block_values<DIST>(p, i / E, v);
-    store_elem<DIST, DT>(out, i, v[i % E]);
+    block_values<DIST>(p, g / E, v);
+    store_elem<DIST, DT>(out, i, v[g % E]);
   }
 }
 
@@ -121,9 +124,10 @@ __global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint6
   constexpr int E = DistTraits<DIST>::E;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
+    const uint64_t g = p.e0 + i;
     uint32_t v[E];
-    block_values<DIST>(p, i / E, v);
-    store_elem<DIST, DT>(out, i, v[i % E]);
+    block_values<DIST>(p, g / E, v);
+    store_elem<DIST, DT>(out, i, v[g % E]);
   }
 }
 
@@ -131,7 +135,7 @@ template <int DIST, int DT>
 static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
   constexpr uint64_t V = DT == SV_BF16 ? 8 : 4;
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
-  if (((uintptr_t)out & 15u) == 0) {
+  if (((uintptr_t)out & 15u) == 0 && p.e0 % DistTraits<DIST>::E == 0) {
     const uint64_t nvec = n / V;
     const uint64_t threads = std::max<uint64_t>(nvec, n - nvec * V);   // the tail needs n - nvec V < V threads
     const uint64_t blocks = std::min<uint64_t>((threads + kBlock - 1) / kBlock, max_blocks);

@@ -215,3 +215,28 @@ def test_wall_clock_attribute_value_used_by_the_gpu_tests(tmp_path):
     import test_gpu_perf
     assert int(subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout) == \
         test_gpu_perf.WALL_CLOCK_RATE_ATTR
+
+
+def test_file_entry_points_reject_bad_arguments_without_a_device(svlib, tmp_path):
+    L = svlib.lib()
+    p = svlib.dist_params(a=-1.0, b=1.0)
+    assert L.sv_synth_file(None, 0, 0, 0, 0, ctypes.byref(p), 10) == svlib.SV_ERR_INVALID_ARG
+    assert L.sv_synth_file(str(tmp_path / "x").encode(), 0, 0, 2, 0, ctypes.byref(p), 10) == \
+        svlib.SV_ERR_UNSUPPORTED                      # int32 from a uniform distribution
+    assert not (tmp_path / "x").exists()              # nothing created for invalid arguments
+    r = svlib.Report()
+    assert L.sv_compare_file(b"/nonexistent/ref", b"/nonexistent/cand", 4, 0, 0.0, 0.0, 0,
+                             ctypes.byref(r)) == svlib.SV_ERR_IO
+    assert "cannot open" in L.sv_last_error().decode()
+    a, b = tmp_path / "a.bin", tmp_path / "b.bin"
+    a.write_bytes(b"\0" * 16)
+    b.write_bytes(b"\0" * 12)
+    assert L.sv_compare_file(str(a).encode(), str(b).encode(), 4, 0, 0.0, 0.0, 0, ctypes.byref(r)) == \
+        svlib.SV_ERR_INVALID_ARG                      # 12 bytes are not 4 fp32 values
+    assert "holds 12 bytes" in L.sv_last_error().decode()
+    assert L.sv_compare_file(str(a).encode(), str(a).encode(), 4, 0, -1.0, 0.0, 0, ctypes.byref(r)) == \
+        svlib.SV_ERR_INVALID_ARG                      # tolerance checked as in sv_compare
+    assert L.sv_compare_file(str(a).encode(), str(a).encode(), 0, 0, 0.0, 0.0, 0, ctypes.byref(r)) == \
+        svlib.SV_ERR_INVALID_ARG                      # 16 bytes are not 0 values
+    q = svlib.dist_params(a=-1.0, b=1.0)
+    assert L.sv_synth_window(0, 0, 0, 0, ctypes.byref(q), 1 << 60, 1, 0x1000) == svlib.SV_ERR_INVALID_ARG
