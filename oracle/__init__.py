@@ -26,8 +26,9 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsvoracle.so")
 
-DTYPES = {"f32": 0, "bf16": 1, "i32": 2}
-NP_STORAGE = {"f32": np.uint32, "bf16": np.uint16, "i32": np.uint32}
+DTYPES = {"f32": 0, "bf16": 1, "i32": 2, "f16": 3, "f64": 4, "u8": 5, "i64": 6}
+NP_STORAGE = {"f32": np.uint32, "bf16": np.uint16, "i32": np.uint32, "f16": np.uint16, "f64": np.uint64,
+              "u8": np.uint8, "i64": np.uint64}
 DISTS = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3}
 OPS = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
        "add_at": 4, "set_at": 5, "fault_at": 6}
@@ -98,6 +99,7 @@ def lib():
         L.or_ln_f32_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_sincos_2pi_f32_n.argtypes = [vp, vp, vp, ctypes.c_uint64]
         L.or_bf16_rne_n.argtypes = [vp, vp, ctypes.c_uint64]
+        L.or_f16_rne_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_radius_f32_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_performance.argtypes = [ctypes.c_double]
         L.or_performance.restype = ctypes.c_double
@@ -196,6 +198,14 @@ def bf16_rne_n(bits) -> np.ndarray:
     x = np.ascontiguousarray(bits, dtype=np.uint32)
     y = np.empty(x.size, np.uint16)
     lib().or_bf16_rne_n(_ptr(x), _ptr(y), x.size)
+    return y
+
+
+def f16_rne_n(bits) -> np.ndarray:
+    """fp32 bit patterns -> IEEE binary16 bit patterns (round to nearest even)."""
+    x = np.ascontiguousarray(bits, dtype=np.uint32)
+    y = np.empty(x.size, np.uint16)
+    lib().or_f16_rne_n(_ptr(x), _ptr(y), x.size)
     return y
 
 

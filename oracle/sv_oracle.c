@@ -218,6 +218,79 @@ uint16_t or_bf16_rne(uint32_t x) {
 static float bf16_to_f32(uint16_t h) { return u2f((uint32_t)h << 16); }
 
 /* ------------------------------------------------------------------------- */
+/* fp32 -> IEEE binary16 (1 sign, 5 exponent, 10 fraction bits), round to     */
+/* nearest even, subnormals kept, beyond the largest finite value -> Inf.      */
+/* A NaN keeps its sign and the top 10 bits of its fraction (bit 0 set if      */
+/* those are all zero, so that it stays a NaN).                                */
+/* ------------------------------------------------------------------------- */
+uint16_t or_f16_rne(uint32_t x) {
+  uint16_t sign = (uint16_t)((x >> 16) & 0x8000u);
+  uint32_t ax = x & 0x7FFFFFFFu;
+  if (ax > 0x7F800000u) {                          /* NaN */
+    uint16_t frac = (uint16_t)((ax & 0x7FFFFFu) >> 13);
+    return (uint16_t)(sign | 0x7C00u | (frac ? frac : 1u));
+  }
+  /* the halfway point between 65504 (the largest half) and 65536 is 65520; a
+   * tie there goes to the even neighbour 65536, which overflows */
+  if (ax >= 0x477FF000u) return (uint16_t)(sign | 0x7C00u);
+  if (ax <= 0x33000000u) return sign;              /* |v| <= 2^-25: to zero (2^-25 ties to even 0) */
+  uint32_t e = ax >> 23;                           /* biased fp32 exponent, 102 .. 142 */
+  uint32_t m = (ax & 0x7FFFFFu) | 0x800000u;       /* 24-bit significand */
+  /* keep 11 significant bits for a normal half (e >= 113, i.e. |v| >= 2^-14);
+   * for a subnormal half the quantum is 2^-24, so drop (126 - e) bits */
+  uint32_t drop = e >= 113u ? 13u : 126u - e;
+  uint32_t q = m >> drop, rest = m & ((1u << drop) - 1u), half = 1u << (drop - 1u);
+  if (rest > half || (rest == half && (q & 1u))) q++;
+  if (e >= 113u)                                   /* a carry into bit 11 moves to the next binade */
+    return (uint16_t)(sign | (((e - 112u) << 10) + (q - 0x400u)));
+  return (uint16_t)(sign | q);                     /* may round up to the smallest normal, 0x0400 */
+}
+
+/* binary16 -> fp32, exact */
+static float f16_to_f32(uint16_t h) {
+  uint32_t sign = ((uint32_t)h & 0x8000u) << 16;
+  uint32_t e = (h >> 10) & 0x1Fu, f = h & 0x3FFu;
+  if (e == 31u) return u2f(sign | 0x7F800000u | (f << 13));   /* Inf, NaN (fraction kept) */
+  float mag = e == 0u ? ldexpf((float)f, -24) : ldexpf((float)(f | 0x400u), (int)e - 25);
+  return u2f(sign | f2u(mag));
+}
+
+uint16_t or_next_f16(uint16_t x, int up) {
+  uint16_t mag = x & 0x7FFFu;
+  if (mag > 0x7C00u) return x;
+  if (mag == 0) return up ? (uint16_t)0x0001u : (uint16_t)0x8001u;
+  if (x == 0x7C00u && up) return x;
+  if (x == 0xFC00u && !up) return x;
+  int neg = (int)(x >> 15);
+  return (uint16_t)((up != neg) ? x + 1u : x - 1u);
+}
+
+uint64_t or_next_f64(uint64_t x, int up) {
+  uint64_t mag = x & 0x7FFFFFFFFFFFFFFFull;
+  if (mag > 0x7FF0000000000000ull) return x;
+  if (mag == 0) return up ? 1ull : 0x8000000000000001ull;
+  if (x == 0x7FF0000000000000ull && up) return x;
+  if (x == 0xFFF0000000000000ull && !up) return x;
+  int neg = (int)(x >> 63);
+  return (up != neg) ? x + 1u : x - 1u;
+}
+
+/* fp32 bits -> fp64 bits: exact for numbers; Inf stays Inf; a NaN keeps its
+ * sign and its fraction, moved to the top of the fp64 fraction */
+static uint64_t widen_f32_bits(uint32_t b) {
+  uint64_t sign = (uint64_t)(b >> 31) << 63;
+  if ((b & 0x7F800000u) == 0x7F800000u)
+    return sign | 0x7FF0000000000000ull | ((uint64_t)(b & 0x7FFFFFu) << 29);
+  double d = (double)u2f(b);
+  uint64_t u;
+  memcpy(&u, &d, 8);
+  return u;
+}
+
+static double u2d(uint64_t u) { double d; memcpy(&d, &u, 8); return d; }
+static uint64_t d2u(double d) { uint64_t u; memcpy(&u, &d, 8); return u; }
+
+/* ------------------------------------------------------------------------- */
 /* One step to the next representable value up (up != 0) or down.            */
 /* ------------------------------------------------------------------------- */
 uint32_t or_next_f32(uint32_t x, int up) {
@@ -261,26 +334,44 @@ void or_bf16_rne_n(const uint32_t *x, uint16_t *y, uint64_t n) {
   for (uint64_t k = 0; k < n; k++) y[k] = or_bf16_rne(x[k]);
 }
 
+void or_f16_rne_n(const uint32_t *x, uint16_t *y, uint64_t n) {
+  for (uint64_t k = 0; k < n; k++) y[k] = or_f16_rne(x[k]);
+}
+
 /* ------------------------------------------------------------------------- */
 /* Synthesis                                                                  */
 /* ------------------------------------------------------------------------- */
 typedef struct {
   float a, span;           /* uniform: a + span * U                      */
+  double a64, span64;      /* uniform into fp64: the same in fp64        */
   float mean, std;         /* normal                                     */
   int64_t lo;              /* integer range                              */
-  uint64_t range;          /* hi - lo + 1                                */
+  uint64_t range;          /* hi - lo + 1 (0 stands for 2^64)            */
   uint64_t t_nan, t_inf, t_den, t_zero;   /* cumulative class thresholds */
 } prepared;
 
 static uint64_t width32(double p) { return (uint64_t)floor(p * 4294967296.0); }
 
+static int is_float(int32_t dtype) {
+  return dtype == OR_F32 || dtype == OR_BF16 || dtype == OR_F16 || dtype == OR_F64;
+}
+static int is_int(int32_t dtype) { return dtype == OR_I32 || dtype == OR_U8 || dtype == OR_I64; }
+static int valid_dtype(int32_t dtype) { return is_float(dtype) || is_int(dtype); }
+
 static int prepare(int32_t dtype, int32_t dist, const or_dist_params *p, prepared *q) {
   memset(q, 0, sizeof(*q));
-  if (dtype != OR_F32 && dtype != OR_BF16 && dtype != OR_I32) return -2;
+  if (!valid_dtype(dtype)) return -2;
   if (!p) return -1;
   switch (dist) {
   case OR_UNIFORM: {
-    if (dtype == OR_I32) return -2;
+    if (!is_float(dtype)) return -2;
+    if (dtype == OR_F64) {
+      double a = p->a, b = p->b, span = b - a;
+      if (!(a < b) || !isfinite(a) || !isfinite(b) || !isfinite(span)) return -1;
+      q->a64 = a;
+      q->span64 = span;
+      return 0;
+    }
     float a = (float)p->a, b = (float)p->b;
     float span = b - a;
     if (!(a < b) || isinf(a) || isinf(b) || isinf(span)) return -1;
@@ -290,7 +381,7 @@ static int prepare(int32_t dtype, int32_t dist, const or_dist_params *p, prepare
   }
   case OR_NORMAL:
   case OR_SPECIAL: {
-    if (dtype == OR_I32) return -2;
+    if (!is_float(dtype)) return -2;
     q->mean = (float)p->mean;
     q->std = (float)p->std;
     if (!isfinite(q->mean) || !isfinite(q->std) || !(q->std >= 0.0f)) return -1;
@@ -310,20 +401,33 @@ static int prepare(int32_t dtype, int32_t dist, const or_dist_params *p, prepare
     return 0;
   }
   case OR_INT_RANGE:
-    if (dtype != OR_I32) return -2;
-    if (p->lo > p->hi || p->lo < INT32_MIN || p->hi > INT32_MAX) return -1;
+    if (!is_int(dtype)) return -2;
+    if (p->lo > p->hi) return -1;
+    if (dtype == OR_I32 && (p->lo < INT32_MIN || p->hi > INT32_MAX)) return -1;
+    if (dtype == OR_U8 && (p->lo < 0 || p->hi > 255)) return -1;
     q->lo = p->lo;
-    q->range = (uint64_t)(p->hi - p->lo) + 1u;
+    q->range = (uint64_t)p->hi - (uint64_t)p->lo + 1u;   /* wraps to 0 for the full int64 range */
     return 0;
   default:
     return -2;
   }
 }
 
-/* Value of element i as fp32 bits (UNIFORM, NORMAL, SPECIAL) or int32 bits. */
-static uint32_t element_bits(uint64_t seed, uint64_t stream, int32_t dist,
-                             const prepared *q, uint64_t i) {
+/* Value of element i: fp32 bits (UNIFORM, NORMAL, SPECIAL; fp64 uniform gives
+ * fp64 bits) or the integer (INT_RANGE), in the low bits of a 64-bit word. */
+static uint64_t element_value(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
+                              const prepared *q, uint64_t i) {
   uint32_t w[4];
+  if (dist == OR_UNIFORM && dtype == OR_F64) {
+    /* two elements per block, R = (w1:w0) for even i and (w3:w2) for odd i;
+     * U = (R >> 11) 2^-53 in [0, 1); a + span U in fp64, two roundings */
+    or_philox_block(seed, stream, i / 2u, w);
+    unsigned h = (unsigned)(i % 2u);
+    uint64_t R = ((uint64_t)w[2 * h + 1] << 32) | (uint64_t)w[2 * h];
+    double U = (double)(R >> 11) * 0x1p-53;
+    double t = q->span64 * U;
+    return d2u(q->a64 + t);
+  }
   if (dist == OR_UNIFORM) {
     /* four elements per block: element i takes word i mod 4 of block i / 4 */
     or_philox_block(seed, stream, i / 4u, w);
@@ -343,13 +447,13 @@ static uint32_t element_bits(uint64_t seed, uint64_t stream, int32_t dist,
   }
   if (dist == OR_INT_RANGE) {
     /* two elements per block: R = (w1:w0) for even i, (w3:w2) for odd i;
-     * value = lo + floor(R * range / 2^64) (Lemire's multiply-shift) */
+     * value = lo + floor(R * range / 2^64) (Lemire's multiply-shift); a range
+     * of 2^64 (the whole int64 line) takes R itself */
     or_philox_block(seed, stream, i / 2u, w);
     unsigned h = (unsigned)(i % 2u);
     uint64_t R = ((uint64_t)w[2 * h + 1] << 32) | (uint64_t)w[2 * h];
-    unsigned __int128 prod = (unsigned __int128)R * (unsigned __int128)q->range;
-    int64_t v = q->lo + (int64_t)(uint64_t)(prod >> 64);
-    return (uint32_t)(int32_t)v;
+    uint64_t off = q->range ? (uint64_t)(((unsigned __int128)R * (unsigned __int128)q->range) >> 64) : R;
+    return (uint64_t)q->lo + off;                   /* two's complement wrap-around: exact */
   }
   /* SPECIAL: one element per block.  w0 picks the class against cumulative
    * thresholds in the order NaN, Inf, denormal, zero, normal; w1 supplies the
@@ -369,11 +473,18 @@ static uint32_t element_bits(uint64_t seed, uint64_t stream, int32_t dist,
   return f2u(fmaf(q->std, zc, q->mean));
 }
 
-static void store(int32_t dtype, void *out, uint64_t k, uint32_t bits) {
-  if (dtype == OR_BF16)
-    ((uint16_t *)out)[k] = or_bf16_rne(bits);
-  else
-    ((uint32_t *)out)[k] = bits;
+/* Stores an element value in the tensor's format: bf16 and fp16 round the
+ * fp32 value to nearest even, fp64 widens it exactly (an fp64 uniform value
+ * is already fp64), integers keep their low bits. */
+static void store(int32_t dtype, int32_t dist, void *out, uint64_t k, uint64_t v) {
+  switch (dtype) {
+  case OR_BF16: ((uint16_t *)out)[k] = or_bf16_rne((uint32_t)v); break;
+  case OR_F16: ((uint16_t *)out)[k] = or_f16_rne((uint32_t)v); break;
+  case OR_F64: ((uint64_t *)out)[k] = dist == OR_UNIFORM ? v : widen_f32_bits((uint32_t)v); break;
+  case OR_I64: ((uint64_t *)out)[k] = v; break;
+  case OR_U8: ((uint8_t *)out)[k] = (uint8_t)v; break;
+  default: ((uint32_t *)out)[k] = (uint32_t)v; break;
+  }
 }
 
 int or_synth(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
@@ -383,7 +494,7 @@ int or_synth(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
   if (rc) return rc;
   if (n && !out) return -1;
   for (uint64_t k = 0; k < n; k++)
-    store(dtype, out, k, element_bits(seed, stream, dist, &q, offset + k));
+    store(dtype, dist, out, k, element_value(seed, stream, dtype, dist, &q, offset + k));
   return 0;
 }
 
@@ -394,7 +505,7 @@ int or_synth_at(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
   if (rc) return rc;
   if (n && (!out || !idx)) return -1;
   for (uint64_t k = 0; k < n; k++)
-    store(dtype, out, k, element_bits(seed, stream, dist, &q, idx[k]));
+    store(dtype, dist, out, k, element_value(seed, stream, dtype, dist, &q, idx[k]));
   return 0;
 }
 
@@ -417,29 +528,49 @@ int or_special_class_counts(uint64_t seed, uint64_t stream, const or_dist_params
 /* ------------------------------------------------------------------------- */
 /* Candidate derivation                                                       */
 /* ------------------------------------------------------------------------- */
-static uint32_t load_bits(int32_t dtype, const void *a, uint64_t k) {
-  return dtype == OR_BF16 ? (uint32_t)((const uint16_t *)a)[k] : ((const uint32_t *)a)[k];
+static size_t elem_bytes(int32_t dtype) {
+  switch (dtype) {
+  case OR_BF16: case OR_F16: return 2;
+  case OR_F64: case OR_I64: return 8;
+  case OR_U8: return 1;
+  default: return 4;
+  }
 }
 
-static void store_bits(int32_t dtype, void *a, uint64_t k, uint32_t bits) {
-  if (dtype == OR_BF16)
-    ((uint16_t *)a)[k] = (uint16_t)bits;
-  else
-    ((uint32_t *)a)[k] = bits;
+static uint64_t load_bits(int32_t dtype, const void *a, uint64_t k) {
+  switch (elem_bytes(dtype)) {
+  case 1: return ((const uint8_t *)a)[k];
+  case 2: return ((const uint16_t *)a)[k];
+  case 8: return ((const uint64_t *)a)[k];
+  default: return ((const uint32_t *)a)[k];
+  }
 }
 
-/* value of a float-typed element as fp32 (bf16 widens exactly) */
-static float as_f32(int32_t dtype, uint32_t bits) {
-  return dtype == OR_BF16 ? bf16_to_f32((uint16_t)bits) : u2f(bits);
+static void store_bits(int32_t dtype, void *a, uint64_t k, uint64_t bits) {
+  switch (elem_bytes(dtype)) {
+  case 1: ((uint8_t *)a)[k] = (uint8_t)bits; break;
+  case 2: ((uint16_t *)a)[k] = (uint16_t)bits; break;
+  case 8: ((uint64_t *)a)[k] = bits; break;
+  default: ((uint32_t *)a)[k] = (uint32_t)bits; break;
+  }
+}
+
+/* value of a 16- or 32-bit float element as fp32 (bf16 and fp16 widen exactly) */
+static float as_f32(int32_t dtype, uint64_t bits) {
+  if (dtype == OR_BF16) return bf16_to_f32((uint16_t)bits);
+  if (dtype == OR_F16) return f16_to_f32((uint16_t)bits);
+  return u2f((uint32_t)bits);
 }
 
 /* fp32 result back to the element format */
-static uint32_t from_f32(int32_t dtype, float v) {
-  return dtype == OR_BF16 ? (uint32_t)or_bf16_rne(f2u(v)) : f2u(v);
+static uint64_t from_f32(int32_t dtype, float v) {
+  if (dtype == OR_BF16) return or_bf16_rne(f2u(v));
+  if (dtype == OR_F16) return or_f16_rne(f2u(v));
+  return f2u(v);
 }
 
-static uint32_t perturb_element(uint64_t seed, uint64_t stream, int32_t dtype,
-                                const or_perturb_plan *plan, uint64_t i, uint32_t b) {
+static uint64_t perturb_element(uint64_t seed, uint64_t stream, int32_t dtype,
+                                const or_perturb_plan *plan, uint64_t i, uint64_t b) {
   if (plan->op == OR_OP_COPY) return b;
   /* one Philox block per element: w0 selects (w0 < floor(p 2^32)), the top
    * bit of w1 chooses the direction, w1 gives the NaN payload mask, the top
@@ -448,8 +579,12 @@ static uint32_t perturb_element(uint64_t seed, uint64_t stream, int32_t dtype,
   or_philox_block(seed, stream, i, w);
   if (!((uint64_t)w[0] < width32(plan->p))) return b;
   int up = (int)(w[1] >> 31);
-  if (plan->op == OR_OP_ULP)
-    return dtype == OR_BF16 ? (uint32_t)or_next_bf16((uint16_t)b, up) : or_next_f32(b, up);
+  if (plan->op == OR_OP_ULP) {
+    if (dtype == OR_BF16) return or_next_bf16((uint16_t)b, up);
+    if (dtype == OR_F16) return or_next_f16((uint16_t)b, up);
+    if (dtype == OR_F64) return or_next_f64(b, up);
+    return or_next_f32((uint32_t)b, up);
+  }
   if (plan->op == OR_OP_SCALE) {
     float U = (float)(w[2] >> 8) * 0x1p-24f;
     float amp = (float)plan->value;
@@ -462,7 +597,7 @@ static uint32_t perturb_element(uint64_t seed, uint64_t stream, int32_t dtype,
   /* SPECIAL_FLIP: zeros change sign, NaNs get their payload XOR-ed with a
    * nonzero mask below the quiet bit; everything else is left alone */
   if (dtype == OR_BF16) {
-    uint32_t mag = b & 0x7FFFu;
+    uint32_t mag = (uint32_t)b & 0x7FFFu;
     if (mag == 0) return b ^ 0x8000u;
     if (mag > 0x7F80u) {
       uint32_t m = w[1] & 0x003Fu;
@@ -470,7 +605,7 @@ static uint32_t perturb_element(uint64_t seed, uint64_t stream, int32_t dtype,
     }
     return b;
   }
-  uint32_t mag = b & 0x7FFFFFFFu;
+  uint32_t mag = (uint32_t)b & 0x7FFFFFFFu;
   if (mag == 0) return b ^ 0x80000000u;
   if (mag > 0x7F800000u) {
     uint32_t m = w[1] & 0x003FFFFFu;
@@ -479,29 +614,49 @@ static uint32_t perturb_element(uint64_t seed, uint64_t stream, int32_t dtype,
   return b;
 }
 
-static uint32_t index_op(int32_t dtype, const or_perturb_plan *plan, uint32_t b) {
-  if (plan->op == OR_OP_SET_AT)
-    return dtype == OR_BF16 ? (plan->bits & 0xFFFFu) : plan->bits;
+static uint64_t index_op(int32_t dtype, const or_perturb_plan *plan, uint64_t b) {
+  if (plan->op == OR_OP_SET_AT) {
+    uint64_t mask = elem_bytes(dtype) == 1 ? 0xFFu : elem_bytes(dtype) == 2 ? 0xFFFFu : 0xFFFFFFFFu;
+    return plan->bits & mask;
+  }
   if (plan->op == OR_OP_ADD_AT) {
     float v = (float)plan->value;
     return from_f32(dtype, as_f32(dtype, b) + v);
   }
-  /* FAULT_AT */
-  if (dtype == OR_I32) return b + 1u;
+  /* FAULT_AT: integers + 1 (wrapping in their width), floats x + (1 + |x|) */
+  if (is_int(dtype)) return b + 1u;
+  if (dtype == OR_F64) {
+    double x = u2d(b);
+    double t = 1.0 + fabs(x);
+    return d2u(x + t);
+  }
   float x = as_f32(dtype, b);
   float t = 1.0f + fabsf(x);
   return from_f32(dtype, x + t);
+}
+
+/* Which candidate steps each element type supports. */
+static int op_supported(int32_t dtype, int op) {
+  if (op == OR_OP_COPY || op == OR_OP_FAULT_AT) return 1;
+  switch (dtype) {
+  case OR_F32: case OR_BF16: return 1;
+  case OR_I32: return op == OR_OP_SET_AT;
+  case OR_F16: return op == OR_OP_ULP || op == OR_OP_SET_AT;
+  case OR_F64: return op == OR_OP_ULP;
+  case OR_U8: return op == OR_OP_SET_AT;
+  default: return 0;
+  }
 }
 
 int or_perturb(uint64_t seed, uint64_t stream, int32_t dtype,
                const or_perturb_plan *plan, uint64_t offset, uint64_t n,
                const void *ref, void *cand) {
   if (!plan) return -1;
-  if (dtype != OR_F32 && dtype != OR_BF16 && dtype != OR_I32) return -2;
+  if (!valid_dtype(dtype)) return -2;
   if (n && (!ref || !cand)) return -1;
   int op = plan->op;
   if (op < OR_OP_COPY || op > OR_OP_FAULT_AT) return -2;
-  if (dtype == OR_I32 && op != OR_OP_COPY && op != OR_OP_SET_AT && op != OR_OP_FAULT_AT) return -2;
+  if (!op_supported(dtype, op)) return -2;
   if (op <= OR_OP_SPECIAL_FLIP) {
     if (op != OR_OP_COPY && !(plan->p >= 0.0 && plan->p <= 1.0)) return -1;
     for (uint64_t k = 0; k < n; k++)
@@ -522,16 +677,22 @@ int or_perturb(uint64_t seed, uint64_t stream, int32_t dtype,
 /* ------------------------------------------------------------------------- */
 /* Eq. (1) and the report                                                     */
 /* ------------------------------------------------------------------------- */
+/* exact value of a float element, or of an int32 / uint8 element, in fp64 */
 static double load_value(int32_t dtype, const void *a, uint64_t k) {
-  if (dtype == OR_F32) return (double)((const float *)a)[k];
-  if (dtype == OR_BF16) return (double)bf16_to_f32(((const uint16_t *)a)[k]);
-  return (double)((const int32_t *)a)[k];
+  switch (dtype) {
+  case OR_F32: return (double)((const float *)a)[k];
+  case OR_BF16: return (double)bf16_to_f32(((const uint16_t *)a)[k]);
+  case OR_F16: return (double)f16_to_f32(((const uint16_t *)a)[k]);
+  case OR_F64: return ((const double *)a)[k];
+  case OR_U8: return (double)((const uint8_t *)a)[k];
+  default: return (double)((const int32_t *)a)[k];
+  }
 }
 
 int or_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
                double rtol, double atol, int32_t equal_nan, or_report *r) {
   if (!r) return -1;
-  if (dtype != OR_F32 && dtype != OR_BF16 && dtype != OR_I32) return -2;
+  if (!valid_dtype(dtype)) return -2;
   if (n && (!ref || !cand)) return -1;
   if (!(rtol >= 0.0) || !(atol >= 0.0) || isinf(rtol) || isinf(atol)) return -1;
   memset(r, 0, sizeof(*r));
@@ -539,16 +700,28 @@ int or_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
   r->first_mismatch = -1;
   double sum = 0.0, comp = 0.0;   /* Neumaier (1974) compensated summation */
   for (uint64_t k = 0; k < n; k++) {
-    double y = load_value(dtype, ref, k);    /* reference output y     */
-    double a = load_value(dtype, cand, k);   /* kernel output K(x)     */
+    double y, a;                             /* reference output y, kernel output K(x) */
     int match, finite;
     double d = 0.0;
-    if (dtype == OR_I32) {
-      /* integers are checked exactly; the tolerances do not apply */
+    if (dtype == OR_I64) {
+      /* int64: exact comparison; d is the exact difference rounded once to fp64
+       * (fp64 cannot hold every int64, so the values are not compared as fp64) */
+      int64_t yi = ((const int64_t *)ref)[k], ai = ((const int64_t *)cand)[k];
+      uint64_t mag = ai >= yi ? (uint64_t)ai - (uint64_t)yi : (uint64_t)yi - (uint64_t)ai;
+      d = (double)mag;
+      y = (double)yi;
+      match = (ai == yi);
+      finite = 1;
+    } else if (is_int(dtype)) {
+      /* int32 and uint8 are exact in fp64; checked exactly, tolerances do not apply */
+      y = load_value(dtype, ref, k);
+      a = load_value(dtype, cand, k);
       d = fabs(a - y);
       match = (a == y);
       finite = 1;
     } else {
+      y = load_value(dtype, ref, k);
+      a = load_value(dtype, cand, k);
       /* isnan / isinf may return any nonzero value (glibc's isinf gives -1 for
        * -Inf), so normalise to 0 / 1 before counting */
       int nan_y = isnan(y) != 0, nan_a = isnan(a) != 0;

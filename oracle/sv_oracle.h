@@ -23,7 +23,7 @@
 extern "C" {
 #endif
 
-enum { OR_F32 = 0, OR_BF16 = 1, OR_I32 = 2 };
+enum { OR_F32 = 0, OR_BF16 = 1, OR_I32 = 2, OR_F16 = 3, OR_F64 = 4, OR_U8 = 5, OR_I64 = 6 };
 enum { OR_UNIFORM = 0, OR_NORMAL = 1, OR_INT_RANGE = 2, OR_SPECIAL = 3 };
 enum {
   OR_OP_COPY = 0,          /* cand = ref                                   */
@@ -89,6 +89,8 @@ void or_ln_f32_n(const float *x, float *y, uint64_t n);
 void or_sincos_2pi_f32_n(const uint32_t *j24, float *s, float *c, uint64_t n);
 void or_radius_f32_n(const uint32_t *k24, float *r, uint64_t n);
 void or_bf16_rne_n(const uint32_t *x, uint16_t *y, uint64_t n);
+uint16_t or_f16_rne(uint32_t x);                 /* fp32 bits -> IEEE half bits, round to nearest even */
+void or_f16_rne_n(const uint32_t *x, uint16_t *y, uint64_t n);
 
 /* Synthesis of elements [offset, offset + n) into out (host memory). */
 int or_synth(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
