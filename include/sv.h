@@ -45,21 +45,22 @@ enum {
   SV_ERR_IO = -5           /* a file could not be opened, read or written (sv_*_file)           */
 };
 
-/* Element types.  Storage is contiguous, little-endian, 1-D. */
-enum { SV_F32 = 0, SV_BF16 = 1, SV_I32 = 2 };
+/* Element types.  Storage is contiguous, little-endian, 1-D.  fp16 is IEEE
+ * binary16, bf16 the upper half of an fp32. */
+enum { SV_F32 = 0, SV_BF16 = 1, SV_I32 = 2, SV_F16 = 3, SV_F64 = 4, SV_U8 = 5, SV_I64 = 6 };
 
 /* Distributions of sv_synth. */
 enum {
-  SV_UNIFORM = 0,   /* [a, b): fp32, bf16                                       */
-  SV_NORMAL = 1,    /* N(mean, std^2) by Box-Muller: fp32, bf16                 */
-  SV_INT_RANGE = 2, /* integers uniform on [lo, hi] inclusive: int32            */
-  SV_SPECIAL = 3    /* NaN / +-Inf / denormal / +-0 mix, else N(mean, std^2): fp32, bf16 */
+  SV_UNIFORM = 0,   /* [a, b): fp32, bf16, fp16, fp64                                */
+  SV_NORMAL = 1,    /* N(mean, std^2) by Box-Muller: fp32, bf16, fp16, fp64          */
+  SV_INT_RANGE = 2, /* integers uniform on [lo, hi] inclusive: int32, uint8, int64   */
+  SV_SPECIAL = 3    /* NaN / +-Inf / denormal / +-0 mix, else N(mean, std^2): fp32, bf16, fp16, fp64 */
 };
 
 typedef struct {
   double a, b;                            /* SV_UNIFORM                             */
   double mean, std;                       /* SV_NORMAL and the normal part of SPECIAL */
-  int64_t lo, hi;                         /* SV_INT_RANGE, within int32              */
+  int64_t lo, hi;                         /* SV_INT_RANGE, within the output type    */
   double p_nan, p_inf, p_denorm, p_zero;  /* SV_SPECIAL class probabilities, sum <= 1 */
 } sv_dist_params;
 
@@ -79,8 +80,8 @@ typedef struct {
   const void *ref;    /* device: reference output y                    */
   const void *cand;   /* device: candidate output K(x), same dtype and n */
   uint64_t n;         /* elements; 0 allowed                           */
-  int32_t dtype;      /* SV_F32 / SV_BF16 / SV_I32                      */
-  double rtol, atol;  /* finite, >= 0; ignored for SV_I32              */
+  int32_t dtype;      /* any SV_ element type                           */
+  double rtol, atol;  /* finite, >= 0; ignored for the integer types    */
   int32_t equal_nan;  /* nonzero: NaN vs NaN agrees                     */
 } sv_segment;
 
@@ -96,8 +97,14 @@ typedef struct {
  * Integer range: lo + floor(R * (hi - lo + 1) / 2^64), R a 64-bit word.
  * Special: class by thresholds floor(p * 2^32) on the first word; bit
  * patterns for NaN (quiet, random payload), Inf, denormals and zeros.  bf16
- * outputs are the round-to-nearest-even of the fp32 value.  Any slice of a
- * tensor can be regenerated alone.
+ * and fp16 outputs are the round-to-nearest-even of the fp32 value (an fp16
+ * NaN keeps its sign and the top 10 fraction bits, bit 0 set if they are all
+ * 0).  fp64 outputs: uniform from 53 random bits, U = (R >> 11) 2^-53 with R
+ * a 64-bit word (E = 2), a + (b - a) U in fp64; normal and special are the
+ * fp32 values widened exactly (a NaN's fraction moved to the top).  uint8 and
+ * int64 ranges use the integer-range rule; for the whole int64 range
+ * (hi - lo + 1 = 2^64) the value is lo + R.  Any slice of a tensor can be
+ * regenerated alone.
  *
  * seed, stream_id : generator key and substream (stream_id is not a HIP stream).
  * dtype, dist     : see the enums; other pairs return SV_ERR_UNSUPPORTED.
@@ -229,9 +236,10 @@ int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_pertur
  *   which = SV_EVAL_RADIUS : out[i] = bits of sqrt(-2 ln u1)  (the Box-Muller radius)
  *   which = SV_EVAL_SIN    : out[i] = bits of sin(2 pi (in[i] & 0xFFFFFF) 2^-24)
  *   which = SV_EVAL_COS    : out[i] = bits of cos(2 pi (in[i] & 0xFFFFFF) 2^-24)
+ *   which = SV_EVAL_F16    : out[i] = the fp16 bits sv_synth stores for the fp32 bits in[i]
  * in, out: device arrays of n uint32.  Asynchronous.
  */
-enum { SV_EVAL_LN = 0, SV_EVAL_RADIUS = 1, SV_EVAL_SIN = 2, SV_EVAL_COS = 3 };
+enum { SV_EVAL_LN = 0, SV_EVAL_RADIUS = 1, SV_EVAL_SIN = 2, SV_EVAL_COS = 3, SV_EVAL_F16 = 4 };
 int sv_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out);
 
 /*

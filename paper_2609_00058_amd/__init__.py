@@ -21,7 +21,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 SV_OK, SV_ERR_INVALID_ARG, SV_ERR_UNSUPPORTED, SV_ERR_HIP, SV_ERR_ALLOC, SV_ERR_IO = 0, -1, -2, -3, -4, -5
-DTYPE_CODES = {"f32": 0, "bf16": 1, "i32": 2}
+DTYPE_CODES = {"f32": 0, "bf16": 1, "i32": 2, "f16": 3, "f64": 4, "u8": 5, "i64": 6}
 DIST_CODES = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3}
 OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
             "add_at": 4, "set_at": 5, "fault_at": 6}
@@ -141,7 +141,8 @@ def _torch():
     if _torch_mod is None:
         import torch
         _torch_mod = torch
-        _tdtype_codes = {torch.float32: 0, torch.bfloat16: 1, torch.int32: 2}
+        _tdtype_codes = {torch.float32: 0, torch.bfloat16: 1, torch.int32: 2, torch.float16: 3,
+                         torch.float64: 4, torch.uint8: 5, torch.int64: 6}
     return _torch_mod
 
 
@@ -282,7 +283,7 @@ def perturb(ref, cand, seed: int, stream_id: int, op: str, p: float = 0.0, value
     return cand
 
 
-EVAL = {"ln": 0, "radius": 1, "sin": 2, "cos": 3}
+EVAL = {"ln": 0, "radius": 1, "sin": 2, "cos": 3, "f16": 4}
 
 
 def eval_transform(which: str, inp, out):

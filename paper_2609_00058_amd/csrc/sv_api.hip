@@ -243,8 +243,21 @@ void push_record(int kind, hipEvent_t a, hipEvent_t b) {
 }
 
 // ------------------------------------------------------------ validation helpers
-bool valid_dtype(int32_t d) { return d == SV_F32 || d == SV_BF16 || d == SV_I32; }
-size_t elem_size(int32_t d) { return d == SV_BF16 ? 2 : 4; }
+bool valid_dtype(int32_t d) { return d >= SV_F32 && d <= SV_I64; }
+bool int_dtype(int32_t d) { return d == SV_I32 || d == SV_U8 || d == SV_I64; }
+size_t elem_size(int32_t d) { return item_bytes(d); }
+
+// The candidate steps each element type supports.
+bool op_supported(int32_t dtype, int32_t op) {
+  if (op == SV_OP_COPY || op == SV_OP_FAULT_AT) return true;
+  switch (dtype) {
+    case SV_F32: case SV_BF16: return true;
+    case SV_I32: case SV_U8: return op == SV_OP_SET_AT;
+    case SV_F16: return op == SV_OP_ULP || op == SV_OP_SET_AT;
+    case SV_F64: return op == SV_OP_ULP;
+    default: return false;
+  }
+}
 constexpr uint64_t kMaxElems = 1ull << 60;
 
 int check_tensor(const void *p, uint64_t n, int32_t dtype, const char *name) {
@@ -267,7 +280,7 @@ int check_seg(const sv_segment &g, uint32_t k) {
   if (!valid_dtype(g.dtype)) return fail(SV_ERR_UNSUPPORTED, "segment %u: unknown dtype %d", k, g.dtype);
   int rc = check_tensor(g.ref, g.n, g.dtype, "segment ref");
   if (!rc) rc = check_tensor(g.cand, g.n, g.dtype, "segment cand");
-  if (!rc && g.dtype != SV_I32) rc = check_tolerances(g.rtol, g.atol);
+  if (!rc && !int_dtype(g.dtype)) rc = check_tolerances(g.rtol, g.atol);
   if (rc) t_error = "segment " + std::to_string(k) + ": " + t_error;
   return rc;
 }
@@ -278,8 +291,8 @@ SegDesc make_desc(const sv_segment &g, uint64_t unit_begin) {
   d.cand = g.cand;
   d.n = g.n;
   d.unit_begin = unit_begin;
-  d.rtol = g.dtype == SV_I32 ? 0.0 : g.rtol;
-  d.atol = g.dtype == SV_I32 ? 0.0 : g.atol;
+  d.rtol = int_dtype(g.dtype) ? 0.0 : g.rtol;
+  d.atol = int_dtype(g.dtype) ? 0.0 : g.atol;
   d.dtype = g.dtype;
   d.equal_nan = g.equal_nan ? 1 : 0;
   d.vec_ok = (((uintptr_t)g.ref | (uintptr_t)g.cand) & 15u) == 0 ? 1 : 0;
@@ -369,7 +382,7 @@ int prepare_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist
                   uint64_t n, void *out, SynthParams *pp) {
   if (!valid_dtype(dtype)) return fail(SV_ERR_UNSUPPORTED, "sv_synth: unknown dtype %d", dtype);
   if (dist < SV_UNIFORM || dist > SV_SPECIAL) return fail(SV_ERR_UNSUPPORTED, "sv_synth: unknown dist %d", dist);
-  if ((dist == SV_INT_RANGE) != (dtype == SV_I32))
+  if ((dist == SV_INT_RANGE) != int_dtype(dtype))
     return fail(SV_ERR_UNSUPPORTED, "sv_synth: dist %d cannot produce dtype %d", dist, dtype);
   if (!params) return fail(SV_ERR_INVALID_ARG, "sv_synth: params is NULL");
   int rc = check_tensor(out, n, dtype, "sv_synth out");
@@ -380,7 +393,14 @@ int prepare_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist
   p.k1 = (uint32_t)(seed >> 32);
   p.s0 = (uint32_t)stream_id;
   p.s1 = (uint32_t)(stream_id >> 32);
-  if (dist == SV_UNIFORM) {
+  if (dist == SV_UNIFORM && dtype == SV_F64) {
+    const double a = params->a, b = params->b, span = b - a;
+    if (!(a < b) || !std::isfinite(a) || !std::isfinite(b) || !std::isfinite(span))
+      return fail(SV_ERR_INVALID_ARG, "sv_synth: uniform needs finite a < b with finite b - a (a=%g b=%g)",
+                  params->a, params->b);
+    p.a64 = a;
+    p.span64 = span;
+  } else if (dist == SV_UNIFORM) {
     const float a = (float)params->a, b = (float)params->b;
     const float span = b - a;
     if (!(a < b) || !std::isfinite(a) || !std::isfinite(b) || !std::isfinite(span))
@@ -408,11 +428,15 @@ int prepare_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist
       p.t_zero = p.t_den + width32(params->p_zero);
     }
   } else {
-    if (params->lo > params->hi || params->lo < INT32_MIN || params->hi > INT32_MAX)
-      return fail(SV_ERR_INVALID_ARG, "sv_synth: integer range [%lld, %lld] must be non-empty and within int32",
-                  (long long)params->lo, (long long)params->hi);
-    p.lo = params->lo;
-    p.range = (uint64_t)(params->hi - params->lo) + 1u;
+    const int64_t lo = params->lo, hi = params->hi;
+    const bool inside = dtype == SV_I64 ? true
+                        : dtype == SV_U8 ? (lo >= 0 && hi <= 255)
+                                         : (lo >= INT32_MIN && hi <= INT32_MAX);
+    if (lo > hi || !inside)
+      return fail(SV_ERR_INVALID_ARG, "sv_synth: integer range [%lld, %lld] must be non-empty and within %s",
+                  (long long)lo, (long long)hi, dtype == SV_U8 ? "uint8" : dtype == SV_I64 ? "int64" : "int32");
+    p.lo = lo;
+    p.range = (uint64_t)hi - (uint64_t)lo + 1u;   // 0 for the whole int64 range
   }
   return SV_OK;
 }
@@ -451,7 +475,8 @@ int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t di
   if (rc) return rc;
   if (offset > kMaxElems || n > kMaxElems - offset)
     return fail(SV_ERR_INVALID_ARG, "sv_synth_window: offset + n exceeds 2^60");
-  const uint64_t per_block = dist == SV_SPECIAL ? 1 : dist == SV_INT_RANGE ? 2 : 4;
+  const uint64_t per_block =
+      dist == SV_SPECIAL ? 1 : (dist == SV_INT_RANGE || (dist == SV_UNIFORM && dtype == SV_F64)) ? 2 : 4;
   p.e0 = offset;
   p.c0 = offset / per_block;
   if (!n) return SV_OK;
@@ -472,11 +497,18 @@ int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t di
   return SV_OK;
 }
 
+// Jobs of the fp32 / bf16 / int32 kinds share one launch through a job table;
+// jobs of the other element types (fp16, fp64, uint8, int64) are launched one
+// by one after it (keeping the batched kernel's register budget to the kinds
+// the batched workloads use).
+static bool table_kind(int32_t dtype) { return dtype == SV_F32 || dtype == SV_BF16 || dtype == SV_I32; }
+
 int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
   t_error.clear();
   if (njobs == 0) return SV_OK;
   if (!jobs) return fail(SV_ERR_INVALID_ARG, "sv_synth_batched: jobs is NULL");
   std::vector<SynthParams> params(njobs);
+  std::vector<uint32_t> table_jobs, direct_jobs;
   uint64_t tiles = 0;
   for (uint32_t k = 0; k < njobs; ++k) {
     const sv_synth_job &j = jobs[k];
@@ -485,58 +517,70 @@ int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
       t_error = "job " + std::to_string(k) + ": " + t_error;
       return rc;
     }
-    const uint64_t per = j.dtype == SV_BF16 ? 8 : 4;
-    tiles += ((j.n + per - 1) / per + kBlock - 1) / kBlock;
+    if (!j.n) continue;
+    if (!table_kind(j.dtype)) {
+      direct_jobs.push_back(k);
+      continue;
+    }
+    table_jobs.push_back(k);
+    tiles += (units_of(j.dtype, j.n) + kBlock - 1) / kBlock;
   }
-  if (tiles == 0) return SV_OK;
+  if (table_jobs.empty() && direct_jobs.empty()) return SV_OK;
   DeviceState *ds;
   int rc = current_device(&ds);
   if (rc) return rc;
   std::lock_guard<std::mutex> lock(ds->mu);
   hipStream_t st = t_stream;
-  if (!ds->synth_copied) {
-    SV_HIP(hipEventCreateWithFlags(&ds->synth_copied, hipEventDisableTiming), "hipEventCreate");
-    SV_HIP(hipEventCreateWithFlags(&ds->synth_done, hipEventDisableTiming), "hipEventCreate");
-  }
-  if (ds->synth_pending) {
-    // the staging buffer is rewritten below: its last copy must have left it;
-    // the device table is rewritten on this stream after the last batch read it
-    SV_HIP(hipEventSynchronize(ds->synth_copied), "wait for the previous job-table copy");
-    SV_HIP(hipStreamWaitEvent(st, ds->synth_done, 0), "order after the previous batch");
-  }
-  rc = ensure_pinned(ds->h_synth, ds->h_synth_cap, njobs, "job table staging");
-  if (!rc) rc = ensure_device(ds->synth_table, ds->synth_table_cap, njobs, "job table");
-  if (rc) return rc;
-  uint64_t begin = 0;
-  for (uint32_t k = 0; k < njobs; ++k) {
-    const sv_synth_job &j = jobs[k];
-    const uint64_t per = j.dtype == SV_BF16 ? 8 : 4;
-    SynthJob &d = ds->h_synth[k];
-    d.p = params[k];
-    d.out = j.out;
-    d.n = j.n;
-    d.nvec = (j.n + per - 1) / per;
-    d.tile_begin = begin;
-    d.kind = j.dist * 4 + j.dtype;
-    d.vec_ok = ((uintptr_t)j.out & 15u) == 0 ? 1 : 0;
-    begin += (d.nvec + kBlock - 1) / kBlock;
-  }
-  SV_HIP(hipMemcpyAsync(ds->synth_table, ds->h_synth, njobs * sizeof(SynthJob), hipMemcpyHostToDevice, st),
-         "job table copy to device");
-  SV_HIP(hipEventRecord(ds->synth_copied, st), "hipEventRecord");
   hipEvent_t e0 = nullptr, e1 = nullptr;
   if (g_prof_on.load()) {
     e0 = take_event();
     e1 = take_event();
-    if (e0) (void)hipEventRecord(e0, st);
   }
-  SV_HIP(launch_synth_batched(ds->synth_table, njobs, tiles, ds->cus, st), "batched synthesis kernel launch");
+  const uint32_t nt = (uint32_t)table_jobs.size();
+  if (nt) {
+    if (!ds->synth_copied) {
+      SV_HIP(hipEventCreateWithFlags(&ds->synth_copied, hipEventDisableTiming), "hipEventCreate");
+      SV_HIP(hipEventCreateWithFlags(&ds->synth_done, hipEventDisableTiming), "hipEventCreate");
+    }
+    if (ds->synth_pending) {
+      // the staging buffer is rewritten below: its last copy must have left it;
+      // the device table is rewritten on this stream after the last batch read it
+      SV_HIP(hipEventSynchronize(ds->synth_copied), "wait for the previous job-table copy");
+      SV_HIP(hipStreamWaitEvent(st, ds->synth_done, 0), "order after the previous batch");
+    }
+    rc = ensure_pinned(ds->h_synth, ds->h_synth_cap, nt, "job table staging");
+    if (!rc) rc = ensure_device(ds->synth_table, ds->synth_table_cap, nt, "job table");
+    if (rc) return rc;
+    uint64_t begin = 0;
+    for (uint32_t t = 0; t < nt; ++t) {
+      const sv_synth_job &j = jobs[table_jobs[t]];
+      SynthJob &d = ds->h_synth[t];
+      d.p = params[table_jobs[t]];
+      d.out = j.out;
+      d.n = j.n;
+      d.nvec = units_of(j.dtype, j.n);
+      d.tile_begin = begin;
+      d.kind = j.dist * 4 + j.dtype;
+      d.vec_ok = ((uintptr_t)j.out & 15u) == 0 ? 1 : 0;
+      begin += (d.nvec + kBlock - 1) / kBlock;
+    }
+    SV_HIP(hipMemcpyAsync(ds->synth_table, ds->h_synth, nt * sizeof(SynthJob), hipMemcpyHostToDevice, st),
+           "job table copy to device");
+    SV_HIP(hipEventRecord(ds->synth_copied, st), "hipEventRecord");
+  }
+  if (e0) (void)hipEventRecord(e0, st);
+  if (nt) SV_HIP(launch_synth_batched(ds->synth_table, nt, tiles, ds->cus, st), "batched synthesis kernel launch");
+  for (uint32_t k : direct_jobs)
+    SV_HIP(launch_synth(jobs[k].dtype, jobs[k].dist, params[k], jobs[k].n, jobs[k].out, ds->cus, st),
+           "synthesis kernel launch");
   if (e0 && e1) {
     (void)hipEventRecord(e1, st);
     push_record(SV_PROF_SYNTH, e0, e1);
   }
-  SV_HIP(hipEventRecord(ds->synth_done, st), "hipEventRecord");
-  ds->synth_pending = true;
+  if (nt) {
+    SV_HIP(hipEventRecord(ds->synth_done, st), "hipEventRecord");
+    ds->synth_pending = true;
+  }
   return SV_OK;
 }
 
@@ -617,8 +661,8 @@ int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_pertur
   if (!valid_dtype(dtype)) return fail(SV_ERR_UNSUPPORTED, "sv_perturb: unknown dtype %d", dtype);
   const int32_t op = plan->op;
   if (op < SV_OP_COPY || op > SV_OP_FAULT_AT) return fail(SV_ERR_UNSUPPORTED, "sv_perturb: unknown op %d", op);
-  if (dtype == SV_I32 && op != SV_OP_COPY && op != SV_OP_SET_AT && op != SV_OP_FAULT_AT)
-    return fail(SV_ERR_UNSUPPORTED, "sv_perturb: op %d needs a floating-point dtype", op);
+  if (!op_supported(dtype, op))
+    return fail(SV_ERR_UNSUPPORTED, "sv_perturb: op %d is not available for dtype %d", op, dtype);
   int rc = check_tensor(ref, n, dtype, "sv_perturb ref");
   if (!rc) rc = check_tensor(cand, n, dtype, "sv_perturb cand");
   if (rc) return rc;
@@ -676,7 +720,7 @@ int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_pertur
 
 int sv_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out) {
   t_error.clear();
-  if (which < SV_EVAL_LN || which > SV_EVAL_COS)
+  if (which < SV_EVAL_LN || which > SV_EVAL_F16)
     return fail(SV_ERR_UNSUPPORTED, "sv_eval_transform: unknown transform %d", which);
   int rc = check_tensor(in, n, SV_F32, "sv_eval_transform in");
   if (!rc) rc = check_tensor(out, n, SV_F32, "sv_eval_transform out");

@@ -50,34 +50,73 @@ namespace sv {
 constexpr int kUnroll = SV_CMP_UNROLL;   // units per thread in flight
 constexpr int kWavesPerBlock = kBlock / kWave;
 
+// V elements per 16-byte unit, checked in groups of G.
 template <int DT> struct Elem;
-template <> struct Elem<SV_F32> { static constexpr int V = 4; };
-template <> struct Elem<SV_BF16> { static constexpr int V = 8; };
-template <> struct Elem<SV_I32> { static constexpr int V = 4; };
+template <> struct Elem<SV_F32> { static constexpr int V = 4, G = 4; };
+template <> struct Elem<SV_BF16> { static constexpr int V = 8, G = 4; };
+template <> struct Elem<SV_I32> { static constexpr int V = 4, G = 4; };
+template <> struct Elem<SV_F16> { static constexpr int V = 8, G = 4; };
+template <> struct Elem<SV_U8> { static constexpr int V = 16, G = 4; };
+template <> struct Elem<SV_F64> { static constexpr int V = 2, G = 2; };
+template <> struct Elem<SV_I64> { static constexpr int V = 2, G = 2; };
 
-// Element j of a 16-byte unit: fp32 bits (bf16 widened exactly) or int32 bits.
+template <int DT> constexpr bool kIntType = DT == SV_I32 || DT == SV_U8 || DT == SV_I64;
+template <int DT> constexpr bool kWideType = DT == SV_F64 || DT == SV_I64;   // 64-bit elements
+
+// Element j of a 16-byte unit, for the types up to 32 bits: fp32 bits (bf16
+// and fp16 widened exactly) or the integer.
 template <int DT>
 __device__ __forceinline__ uint32_t elem_bits(const u32x4 &v, int j) {
   if constexpr (DT == SV_BF16)
     return (j & 1) ? (v[j >> 1] & 0xFFFF0000u) : (v[j >> 1] << 16);
+  else if constexpr (DT == SV_F16)
+    return as_u32(f16_widen((j & 1) ? (v[j >> 1] >> 16) : (v[j >> 1] & 0xFFFFu)));
+  else if constexpr (DT == SV_U8)
+    return (v[j >> 2] >> (8 * (j & 3))) & 0xFFu;
   else
     return v[j];
+}
+
+// Element j of a unit of 64-bit elements.
+__device__ __forceinline__ uint64_t elem_bits64(const u32x4 &v, int j) {
+  return ((uint64_t)v[2 * j + 1] << 32) | v[2 * j];
 }
 
 template <int DT>
 __device__ __forceinline__ double widen(uint32_t bits) {
   if constexpr (DT == SV_I32)
     return (double)(int32_t)bits;
+  else if constexpr (DT == SV_U8)
+    return (double)bits;
   else
     return (double)as_f32(bits);
 }
 
 template <int DT>
-__device__ __forceinline__ uint32_t load_elem(const void *p, uint64_t i) {
-  if constexpr (DT == SV_BF16)
+__device__ __forceinline__ uint64_t load_elem(const void *p, uint64_t i) {
+  if constexpr (DT == SV_BF16 || DT == SV_F16)
     return ((const uint16_t *)p)[i];
+  else if constexpr (DT == SV_U8)
+    return ((const uint8_t *)p)[i];
+  else if constexpr (kWideType<DT>)
+    return ((const uint64_t *)p)[i];
   else
     return ((const uint32_t *)p)[i];
+}
+
+// Places element j's raw bits into a unit (the tail of a segment).
+template <int DT>
+__device__ __forceinline__ void put_elem(u32x4 &v, int j, uint64_t b) {
+  if constexpr (DT == SV_BF16 || DT == SV_F16) {
+    v[j >> 1] |= (j & 1) ? ((uint32_t)b << 16) : (uint32_t)b;
+  } else if constexpr (DT == SV_U8) {
+    v[j >> 2] |= (uint32_t)b << (8 * (j & 3));
+  } else if constexpr (kWideType<DT>) {
+    v[2 * j] = (uint32_t)b;
+    v[2 * j + 1] = (uint32_t)(b >> 32);
+  } else {
+    v[j] = (uint32_t)b;
+  }
 }
 
 struct LaneAcc {
@@ -96,27 +135,45 @@ __device__ __forceinline__ void update_rel(LaneAcc &L, double d, double y) {
   }
 }
 
-// Folds elements 4g .. 4g + 3 of one unit (lane l holds the unit whose first
-// element is wave_e0 + l V) into the lane accumulators and the wave counts;
-// bad[j] receives the ballot of the mismatches of element 4g + j.  Reached by
-// every lane of the wave (ballots).
+// Folds elements G g .. G g + G - 1 of one unit (lane l holds the unit whose
+// first element is wave_e0 + l V) into the lane accumulators and the wave
+// counts; bad[j] receives the ballot of the mismatches of element G g + j.
+// Reached by every lane of the wave (ballots).  int64 differences are formed
+// exactly and rounded once (fp64 cannot hold every int64); with the zero
+// tolerances of integer types the test d <= 0 is then exact equality.
 template <int DT>
 __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, int g, double rtol, double atol,
                                             bool eqn, LaneAcc &L, WaveAcc &W, uint64_t *bad) {
-  double Y[4], D[4];
+  constexpr int G = Elem<DT>::G;
+  double Y[G], D[G], A[G];
   bool nonfin = false;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    Y[j] = widen<DT>(elem_bits<DT>(yv, 4 * g + j));
-    D[j] = fabs(widen<DT>(elem_bits<DT>(av, 4 * g + j)) - Y[j]);
-    if constexpr (DT != SV_I32) nonfin |= !__builtin_isfinite(D[j]);
+  for (int j = 0; j < G; ++j) {
+    const int e = G * g + j;
+    if constexpr (DT == SV_I64) {
+      const int64_t yi = (int64_t)elem_bits64(yv, e), ai = (int64_t)elem_bits64(av, e);
+      const uint64_t mag = ai >= yi ? (uint64_t)ai - (uint64_t)yi : (uint64_t)yi - (uint64_t)ai;
+      Y[j] = (double)yi;
+      D[j] = (double)mag;
+      A[j] = 0.0;
+    } else if constexpr (DT == SV_F64) {
+      Y[j] = bits_f64(elem_bits64(yv, e));
+      A[j] = bits_f64(elem_bits64(av, e));
+      D[j] = fabs(A[j] - Y[j]);
+      nonfin |= !__builtin_isfinite(D[j]);
+    } else {
+      Y[j] = widen<DT>(elem_bits<DT>(yv, e));
+      A[j] = 0.0;
+      D[j] = fabs(widen<DT>(elem_bits<DT>(av, e)) - Y[j]);
+      if constexpr (!kIntType<DT>) nonfin |= !__builtin_isfinite(D[j]);
+    }
   }
-  bool f[4];
+  bool f[G];
   bool anyf = false;
-  if (DT == SV_I32 || __ballot(nonfin) == 0) {
+  if (kIntType<DT> || __ballot(nonfin) == 0) {
     // every pair of this group is finite across the wave
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < G; ++j) {
       const double ay = fabs(Y[j]);
       bad[j] = __ballot(!(D[j] <= atol + rtol * ay));
       L.sum += D[j];
@@ -126,17 +183,30 @@ __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, in
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float yf = as_f32(elem_bits<DT>(yv, 4 * g + j)), af = as_f32(elem_bits<DT>(av, 4 * g + j));
-      const bool ny = __builtin_isnan(yf), na = __builtin_isnan(af);
-      const bool iy = __builtin_isinf(yf), ia = __builtin_isinf(af);
+    for (int j = 0; j < G; ++j) {
+      bool ny, na, iy, ia;
+      double aval;
+      if constexpr (DT == SV_F64) {
+        ny = __builtin_isnan(Y[j]);
+        na = __builtin_isnan(A[j]);
+        iy = __builtin_isinf(Y[j]);
+        ia = __builtin_isinf(A[j]);
+        aval = A[j];
+      } else {
+        const float yf = as_f32(elem_bits<DT>(yv, G * g + j)), af = as_f32(elem_bits<DT>(av, G * g + j));
+        ny = __builtin_isnan(yf);
+        na = __builtin_isnan(af);
+        iy = __builtin_isinf(yf);
+        ia = __builtin_isinf(af);
+        aval = (double)af;
+      }
       W.nan_r += __popcll(__ballot(ny));
       W.nan_c += __popcll(__ballot(na));
       W.inf_r += __popcll(__ballot(iy));
       W.inf_c += __popcll(__ballot(ia));
       const bool fin = !(ny | na | iy | ia);
       const double ay = fabs(Y[j]);
-      const bool match = fin ? (D[j] <= atol + rtol * ay) : (((double)af == Y[j]) || (eqn && ny && na));
+      const bool match = fin ? (D[j] <= atol + rtol * ay) : ((aval == Y[j]) || (eqn && ny && na));
       bad[j] = __ballot(!match);
       const double dj = fin ? D[j] : 0.0;
       L.sum += dj;
@@ -147,7 +217,7 @@ __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, in
   }
   if (__ballot(anyf)) {              // a lane may have a new relative maximum
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < G; ++j)
       if (f[j]) update_rel(L, D[j], Y[j]);
   }
 }
@@ -158,9 +228,10 @@ template <int DT>
 __device__ __forceinline__ void check_unit(const u32x4 &yv, const u32x4 &av, uint64_t wave_e0, double rtol,
                                            double atol, bool eqn, LaneAcc &L, WaveAcc &W) {
   constexpr int V = Elem<DT>::V;
+  constexpr int G = Elem<DT>::G;
   uint64_t bad[V];                   // wave masks, kept in scalar registers
 #pragma unroll
-  for (int g = 0; g < V / 4; ++g) check_group<DT>(yv, av, g, rtol, atol, eqn, L, W, bad + 4 * g);
+  for (int g = 0; g < V / G; ++g) check_group<DT>(yv, av, g, rtol, atol, eqn, L, W, bad + G * g);
   uint64_t any = 0;
 #pragma unroll
   for (int j = 0; j < V; ++j) any |= bad[j];
@@ -345,14 +416,8 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
 #pragma unroll
       for (int j = 0; j < V; ++j) {
         if (e0 + j < n) {
-          const uint32_t yb = load_elem<DT>(sd.ref, e0 + j), ab = load_elem<DT>(sd.cand, e0 + j);
-          if constexpr (DT == SV_BF16) {
-            yv[j >> 1] |= (j & 1) ? (yb << 16) : yb;
-            av[j >> 1] |= (j & 1) ? (ab << 16) : ab;
-          } else {
-            yv[j] = yb;
-            av[j] = ab;
-          }
+          put_elem<DT>(yv, j, load_elem<DT>(sd.ref, e0 + j));
+          put_elem<DT>(av, j, load_elem<DT>(sd.cand, e0 + j));
         }
       }
     }
@@ -441,6 +506,22 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
 // kMask: the set of dtypes (bit 1 << dtype) the segments of this launch use;
 // only their code paths are compiled in, which keeps register pressure at
 // what the widest of them needs.
+// The check of one piece for the element types in kMask (bit 1 << dtype):
+// with one type the code of that type only, else a branch on the segment's.
+template <int kMask, bool kStop, int DT = 0>
+__device__ __forceinline__ Partial check_any(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Partial *lds) {
+  if constexpr (DT > SV_I64) {
+    return empty_partial();                         // not reached: the host passes types in kMask only
+  } else if constexpr ((kMask & (1 << DT)) == 0) {
+    return check_any<kMask, kStop, DT + 1>(sd, ulo, uhi, lds);
+  } else if constexpr ((kMask >> (DT + 1)) == 0) {
+    return check_piece<DT, kStop>(sd, ulo, uhi, lds);   // the last type in the mask
+  } else {
+    if (sd.dtype == DT) return check_piece<DT, kStop>(sd, ulo, uhi, lds);
+    return check_any<kMask, kStop, DT + 1>(sd, ulo, uhi, lds);
+  }
+}
+
 template <bool kSingle, int kMask, bool kStop = false>
 __global__ __launch_bounds__(kBlock) void compare_kernel(CompareArgs args) {
   __shared__ Partial lds[kWavesPerBlock];
@@ -453,21 +534,7 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(CompareArgs args) {
     const uint64_t seg_end = sd.unit_begin + units_of(sd.dtype, sd.n);
     const uint64_t piece_hi = hi < seg_end ? hi : seg_end;
     const uint64_t ulo = lo - sd.unit_begin, uhi = piece_hi - sd.unit_begin;
-    Partial p;
-    if constexpr (kMask == (1 << SV_F32)) {
-      p = check_piece<SV_F32, kStop>(sd, ulo, uhi, lds);
-    } else if constexpr (kMask == (1 << SV_BF16)) {
-      p = check_piece<SV_BF16, kStop>(sd, ulo, uhi, lds);
-    } else if constexpr (kMask == (1 << SV_I32)) {
-      p = check_piece<SV_I32, kStop>(sd, ulo, uhi, lds);
-    } else {
-      if ((kMask & (1 << SV_F32)) && sd.dtype == SV_F32)
-        p = check_piece<SV_F32, kStop>(sd, ulo, uhi, lds);
-      else if ((kMask & (1 << SV_BF16)) && sd.dtype == SV_BF16)
-        p = check_piece<SV_BF16, kStop>(sd, ulo, uhi, lds);
-      else
-        p = check_piece<SV_I32, kStop>(sd, ulo, uhi, lds);
-    }
+    const Partial p = check_any<kMask, kStop>(sd, ulo, uhi, lds);
     if (threadIdx.x == 0) args.partials[b + s] = p;
     if constexpr (kSingle) return;   // one segment: the chunk is a single piece
     lo = piece_hi;
@@ -494,16 +561,23 @@ static void launch_masked(const CompareArgs &args, uint32_t nblocks, hipStream_t
     hipLaunchKernelGGL(finalize_kernel<false>, dim3(args.nseg), dim3(kFinBlock), 0, stream, args);
 }
 
+// Kernels exist for each type alone, for the mixes of fp32 / bf16 / int32 the
+// batched workloads use, and one for any other mix.
 hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream,
                           hipEvent_t ev_mid) {
   switch (dtype_mask) {
-    case 1: launch_masked<1>(args, nblocks, stream, ev_mid); break;
-    case 2: launch_masked<2>(args, nblocks, stream, ev_mid); break;
+    case 1 << SV_F32: launch_masked<1 << SV_F32>(args, nblocks, stream, ev_mid); break;
+    case 1 << SV_BF16: launch_masked<1 << SV_BF16>(args, nblocks, stream, ev_mid); break;
+    case 1 << SV_I32: launch_masked<1 << SV_I32>(args, nblocks, stream, ev_mid); break;
+    case 1 << SV_F16: launch_masked<1 << SV_F16>(args, nblocks, stream, ev_mid); break;
+    case 1 << SV_F64: launch_masked<1 << SV_F64>(args, nblocks, stream, ev_mid); break;
+    case 1 << SV_U8: launch_masked<1 << SV_U8>(args, nblocks, stream, ev_mid); break;
+    case 1 << SV_I64: launch_masked<1 << SV_I64>(args, nblocks, stream, ev_mid); break;
     case 3: launch_masked<3>(args, nblocks, stream, ev_mid); break;
-    case 4: launch_masked<4>(args, nblocks, stream, ev_mid); break;
     case 5: launch_masked<5>(args, nblocks, stream, ev_mid); break;
     case 6: launch_masked<6>(args, nblocks, stream, ev_mid); break;
-    default: launch_masked<7>(args, nblocks, stream, ev_mid); break;
+    case 7: launch_masked<7>(args, nblocks, stream, ev_mid); break;
+    default: launch_masked<0x7F>(args, nblocks, stream, ev_mid); break;
   }
   return hipGetLastError();
 }

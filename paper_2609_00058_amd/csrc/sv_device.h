@@ -207,4 +207,50 @@ __device__ __forceinline__ uint32_t next_bf16(uint32_t x, bool up) {
   return ((up != neg) ? x + 1u : x - 1u) & 0xFFFFu;
 }
 
+__device__ __forceinline__ uint32_t next_f16(uint32_t x, bool up) {
+  const uint32_t mag = x & 0x7FFFu;
+  if (mag > 0x7C00u) return x;
+  if (mag == 0u) return up ? 0x0001u : 0x8001u;
+  if ((x == 0x7C00u && up) || (x == 0xFC00u && !up)) return x;
+  const bool neg = (x >> 15) != 0u;
+  return ((up != neg) ? x + 1u : x - 1u) & 0xFFFFu;
+}
+
+__device__ __forceinline__ uint64_t next_f64(uint64_t x, bool up) {
+  const uint64_t mag = x & 0x7FFFFFFFFFFFFFFFull;
+  if (mag > 0x7FF0000000000000ull) return x;
+  if (mag == 0u) return up ? 1ull : 0x8000000000000001ull;
+  if ((x == 0x7FF0000000000000ull && up) || (x == 0xFFF0000000000000ull && !up)) return x;
+  const bool neg = (x >> 63) != 0u;
+  return (up != neg) ? x + 1u : x - 1u;
+}
+
+// ---------------------------------------------------------------------------
+// fp16 and fp64 outputs of fp32 values.  fp16: round to nearest even through
+// the hardware conversion (IEEE, subnormals kept, overflow to Inf); a NaN
+// keeps its sign and the top 10 fraction bits, bit 0 set if those are zero.
+// fp64: exact widening; Inf stays Inf and a NaN keeps its sign and fraction,
+// moved to the top of the fp64 fraction.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint32_t f16_rne(uint32_t x) {
+  if ((x & 0x7FFFFFFFu) > 0x7F800000u) {
+    const uint32_t frac = (x & 0x7FFFFFu) >> 13;
+    return ((x >> 16) & 0x8000u) | 0x7C00u | (frac ? frac : 1u);
+  }
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)as_f32(x));
+}
+
+__device__ __forceinline__ float f16_widen(uint32_t h) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+__device__ __forceinline__ uint64_t widen_f32_bits(uint32_t b) {
+  if ((b & 0x7F800000u) == 0x7F800000u)
+    return ((uint64_t)(b >> 31) << 63) | 0x7FF0000000000000ull | ((uint64_t)(b & 0x7FFFFFu) << 29);
+  return (uint64_t)__double_as_longlong((double)as_f32(b));
+}
+
+__device__ __forceinline__ uint64_t f64_bits(double d) { return (uint64_t)__double_as_longlong(d); }
+__device__ __forceinline__ double bits_f64(uint64_t u) { return __longlong_as_double((long long)u); }
+
 }  // namespace sv

@@ -29,10 +29,10 @@
 namespace sv {
 namespace {
 
-constexpr uint64_t kChunkBytes = 64ull << 20;
+constexpr uint64_t kChunkBytes = 64ull << 20;   // a multiple of 16 bytes and of every Philox block's span
 constexpr int kRing = 3;                       // pinned buffers per file in the check's read-ahead ring
 
-size_t item_size(int32_t dtype) { return dtype == SV_BF16 ? 2 : 4; }
+size_t item_size(int32_t dtype) { return item_bytes(dtype); }
 
 int io_fail(const char *what, const char *path) {
   const std::string msg = std::string(what) + " '" + path + "': " + std::strerror(errno);

@@ -36,8 +36,9 @@ struct SynthParams {
   float a, span;                // uniform: a + span * U
   float mean, std;              // normal and the normal part of SPECIAL
   int64_t lo;                   // integer range
-  uint64_t range;               // hi - lo + 1 (<= 2^32)
+  uint64_t range;               // hi - lo + 1 (0 stands for 2^64: the whole int64 range)
   uint64_t t_nan, t_inf, t_den, t_zero;   // cumulative class thresholds on w0
+  double a64, span64;           // fp64 uniform: a + span U53
   uint64_t e0;                  // tensor index of out[0] (a window of the tensor; 0 for a whole tensor)
   uint64_t c0;                  // e0 / E, the first Philox block (used when E divides e0)
 };
@@ -126,8 +127,17 @@ int api_hip_fail(hipError_t e, const char *what);
 void perf_shutdown();                             // sv_perf.hip: frees its per-device state
 void files_shutdown();                            // sv_files.hip: frees its staging buffers
 
+__host__ __device__ inline uint32_t item_bytes(int32_t dtype) {
+  switch (dtype) {
+    case SV_BF16: case SV_F16: return 2;
+    case SV_F64: case SV_I64: return 8;
+    case SV_U8: return 1;
+    default: return 4;
+  }
+}
+
 __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
-  const uint64_t per = dtype == SV_BF16 ? 8 : 4;
+  const uint64_t per = 16 / item_bytes(dtype);
   return (n + per - 1) / per;
 }
 

@@ -11,63 +11,75 @@
 namespace sv {
 
 template <int DT>
-__device__ __forceinline__ uint32_t load_bits(const void *a, uint64_t i) {
-  if constexpr (DT == SV_BF16)
-    return ((const uint16_t *)a)[i];
-  else
-    return ((const uint32_t *)a)[i];
+__device__ __forceinline__ uint64_t load_bits(const void *a, uint64_t i) {
+  if constexpr (DT == SV_BF16 || DT == SV_F16) return ((const uint16_t *)a)[i];
+  else if constexpr (DT == SV_U8) return ((const uint8_t *)a)[i];
+  else if constexpr (DT == SV_F64 || DT == SV_I64) return ((const uint64_t *)a)[i];
+  else return ((const uint32_t *)a)[i];
 }
 
 template <int DT>
-__device__ __forceinline__ void store_bits(void *a, uint64_t i, uint32_t v) {
-  if constexpr (DT == SV_BF16)
-    ((uint16_t *)a)[i] = (uint16_t)v;
-  else
-    ((uint32_t *)a)[i] = v;
+__device__ __forceinline__ void store_bits(void *a, uint64_t i, uint64_t v) {
+  if constexpr (DT == SV_BF16 || DT == SV_F16) ((uint16_t *)a)[i] = (uint16_t)v;
+  else if constexpr (DT == SV_U8) ((uint8_t *)a)[i] = (uint8_t)v;
+  else if constexpr (DT == SV_F64 || DT == SV_I64) ((uint64_t *)a)[i] = v;
+  else ((uint32_t *)a)[i] = (uint32_t)v;
 }
 
-// float-typed element <-> fp32 (bf16 widens exactly; narrowing rounds to nearest even)
+// float-typed element <-> fp32 (bf16 and fp16 widen exactly; narrowing rounds to nearest even)
 template <int DT>
-__device__ __forceinline__ float widen(uint32_t b) {
-  return DT == SV_BF16 ? as_f32(b << 16) : as_f32(b);
+__device__ __forceinline__ float widen(uint64_t b) {
+  if constexpr (DT == SV_BF16) return as_f32((uint32_t)b << 16);
+  else if constexpr (DT == SV_F16) return f16_widen((uint32_t)b);
+  else return as_f32((uint32_t)b);
 }
 template <int DT>
-__device__ __forceinline__ uint32_t narrow(float x) {
-  return DT == SV_BF16 ? bf16_rne(as_u32(x)) : as_u32(x);
+__device__ __forceinline__ uint64_t narrow(float x) {
+  if constexpr (DT == SV_BF16) return bf16_rne(as_u32(x));
+  else if constexpr (DT == SV_F16) return f16_rne(as_u32(x));
+  else return as_u32(x);
 }
 
 template <int DT>
-__device__ __forceinline__ uint32_t derive(const PerturbParams &p, uint64_t i, uint32_t y) {
+__device__ __forceinline__ uint64_t derive(const PerturbParams &p, uint64_t i, uint64_t y) {
   if (p.op == SV_OP_COPY) return y;
   const u32x4 w = philox_block(Key{p.k0, p.k1, p.s0, p.s1}, i);
   if (!((uint64_t)w.x < p.threshold)) return y;
   const bool up = (w.y >> 31) != 0u;
-  if (p.op == SV_OP_ULP) return DT == SV_BF16 ? next_bf16(y, up) : next_f32(y, up);
-  if (p.op == SV_OP_SCALE) {
-    const float U = unit24(w.z);
-    const float two = 2.0f * p.value;
-    const float u = two * U - p.value;
-    const float s = 1.0f + u;
-    return narrow<DT>(widen<DT>(y) * s);
+  if (p.op == SV_OP_ULP) {
+    if constexpr (DT == SV_BF16) return next_bf16((uint32_t)y, up);
+    else if constexpr (DT == SV_F16) return next_f16((uint32_t)y, up);
+    else if constexpr (DT == SV_F64) return next_f64(y, up);
+    else return next_f32((uint32_t)y, up);
   }
-  // SPECIAL_FLIP
-  if constexpr (DT == SV_BF16) {
-    const uint32_t mag = y & 0x7FFFu;
-    if (mag == 0u) return y ^ 0x8000u;
-    if (mag > 0x7F80u) {
-      const uint32_t m = w.y & 0x3Fu;
-      return y ^ (m ? m : 1u);
+  if constexpr (DT == SV_F32 || DT == SV_BF16) {
+    if (p.op == SV_OP_SCALE) {
+      const float U = unit24(w.z);
+      const float two = 2.0f * p.value;
+      const float u = two * U - p.value;
+      const float s = 1.0f + u;
+      return narrow<DT>(widen<DT>(y) * s);
     }
-    return y;
-  } else {
-    const uint32_t mag = y & 0x7FFFFFFFu;
-    if (mag == 0u) return y ^ 0x80000000u;
-    if (mag > 0x7F800000u) {
-      const uint32_t m = w.y & 0x003FFFFFu;
-      return y ^ (m ? m : 1u);
+    // SPECIAL_FLIP
+    if constexpr (DT == SV_BF16) {
+      const uint32_t mag = (uint32_t)y & 0x7FFFu;
+      if (mag == 0u) return y ^ 0x8000u;
+      if (mag > 0x7F80u) {
+        const uint32_t m = w.y & 0x3Fu;
+        return y ^ (m ? m : 1u);
+      }
+      return y;
+    } else {
+      const uint32_t mag = (uint32_t)y & 0x7FFFFFFFu;
+      if (mag == 0u) return y ^ 0x80000000u;
+      if (mag > 0x7F800000u) {
+        const uint32_t m = w.y & 0x003FFFFFu;
+        return y ^ (m ? m : 1u);
+      }
+      return y;
     }
-    return y;
   }
+  return y;                                     // not reached: the host admits these steps only for fp32 / bf16
 }
 
 template <int DT>
@@ -84,14 +96,18 @@ __global__ __launch_bounds__(kBlock) void perturb_index_kernel(PerturbParams p, 
   const uint64_t k = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
   if (k >= nidx) return;
   const uint64_t i = idx[k];
-  const uint32_t y = load_bits<DT>(ref, i);
-  uint32_t out;
+  const uint64_t y = load_bits<DT>(ref, i);
+  uint64_t out;
   if (p.op == SV_OP_SET_AT) {
-    out = DT == SV_BF16 ? (p.bits & 0xFFFFu) : p.bits;
+    out = DT == SV_BF16 || DT == SV_F16 ? (p.bits & 0xFFFFu) : DT == SV_U8 ? (p.bits & 0xFFu) : p.bits;
+  } else if constexpr (DT == SV_I32 || DT == SV_U8 || DT == SV_I64) {
+    out = y + 1u;                                   // FAULT_AT on integers, wrapping in their width
+  } else if constexpr (DT == SV_F64) {
+    const double x = bits_f64(y);
+    const double t = 1.0 + fabs(x);
+    out = f64_bits(x + t);                          // FAULT_AT in fp64
   } else if (p.op == SV_OP_ADD_AT) {
     out = narrow<DT>(widen<DT>(y) + p.value);
-  } else if constexpr (DT == SV_I32) {
-    out = y + 1u;                                   // FAULT_AT on integers, wrapping
   } else {
     const float x = widen<DT>(y);
     out = narrow<DT>(x + (1.0f + fabsf(x)));        // FAULT_AT: always outside any sane tolerance
@@ -99,19 +115,27 @@ __global__ __launch_bounds__(kBlock) void perturb_index_kernel(PerturbParams p, 
   store_bits<DT>(cand, i, out);
 }
 
+template <template <int> class K, class... A>
+static void dispatch_dtype(int32_t dtype, dim3 grid, hipStream_t stream, A... args) {
+  switch (dtype) {
+    case SV_F32: hipLaunchKernelGGL(K<SV_F32>::fn, grid, dim3(kBlock), 0, stream, args...); break;
+    case SV_BF16: hipLaunchKernelGGL(K<SV_BF16>::fn, grid, dim3(kBlock), 0, stream, args...); break;
+    case SV_I32: hipLaunchKernelGGL(K<SV_I32>::fn, grid, dim3(kBlock), 0, stream, args...); break;
+    case SV_F16: hipLaunchKernelGGL(K<SV_F16>::fn, grid, dim3(kBlock), 0, stream, args...); break;
+    case SV_F64: hipLaunchKernelGGL(K<SV_F64>::fn, grid, dim3(kBlock), 0, stream, args...); break;
+    case SV_U8: hipLaunchKernelGGL(K<SV_U8>::fn, grid, dim3(kBlock), 0, stream, args...); break;
+    default: hipLaunchKernelGGL(K<SV_I64>::fn, grid, dim3(kBlock), 0, stream, args...); break;
+  }
+}
+
+template <int DT> struct ElemK { static constexpr auto fn = perturb_elem_kernel<DT>; };
+template <int DT> struct IndexK { static constexpr auto fn = perturb_index_kernel<DT>; };
+
 hipError_t launch_perturb_elementwise(int32_t dtype, const PerturbParams &p, uint64_t n, const void *ref,
                                       void *cand, int cus, hipStream_t stream) {
   if (!n) return hipSuccess;
   const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, (uint64_t)cus * 8);
-  if (dtype == SV_BF16)
-    hipLaunchKernelGGL(perturb_elem_kernel<SV_BF16>, dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n, ref,
-                       cand);
-  else if (dtype == SV_F32)
-    hipLaunchKernelGGL(perturb_elem_kernel<SV_F32>, dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n, ref,
-                       cand);
-  else
-    hipLaunchKernelGGL(perturb_elem_kernel<SV_I32>, dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n, ref,
-                       cand);
+  dispatch_dtype<ElemK>(dtype, dim3((unsigned)blocks), stream, p, n, ref, cand);
   return hipGetLastError();
 }
 
@@ -119,15 +143,7 @@ hipError_t launch_perturb_indexed(int32_t dtype, const PerturbParams &p, const u
                                   const void *ref, void *cand, hipStream_t stream) {
   if (!nidx) return hipSuccess;
   const uint64_t blocks = (nidx + kBlock - 1) / kBlock;
-  if (dtype == SV_BF16)
-    hipLaunchKernelGGL(perturb_index_kernel<SV_BF16>, dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, idx_dev,
-                       nidx, ref, cand);
-  else if (dtype == SV_F32)
-    hipLaunchKernelGGL(perturb_index_kernel<SV_F32>, dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, idx_dev,
-                       nidx, ref, cand);
-  else
-    hipLaunchKernelGGL(perturb_index_kernel<SV_I32>, dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, idx_dev,
-                       nidx, ref, cand);
+  dispatch_dtype<IndexK>(dtype, dim3((unsigned)blocks), stream, p, idx_dev, nidx, ref, cand);
   return hipGetLastError();
 }
 

@@ -148,16 +148,149 @@ static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int 
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------ fp16, fp64, uint8, int64
+// The same elements stored in the other types: fp16 bits, fp64 bits, the low
+// byte, the int64.  E elements per Philox block as above, except fp64 uniform
+// (53 random bits from a 64-bit word: E = 2).  A 16-byte vector holds V =
+// 16 / itemsize elements; only fp64 normal has V < E (two of a block's four).
+template <int DIST, int DT> struct Wide {
+  static constexpr int E = (DIST == SV_UNIFORM && DT == SV_F64) ? 2 : DistTraits<DIST>::E;
+  static constexpr int V = DT == SV_F16 ? 8 : DT == SV_U8 ? 16 : 2;
+};
+
+template <int DT>
+__device__ __forceinline__ uint64_t from_value32(uint32_t v) {
+  if constexpr (DT == SV_F16) return f16_rne(v);
+  else if constexpr (DT == SV_F64) return widen_f32_bits(v);
+  else return v & 0xFFu;                       // SV_U8: the integer range value is in [0, 255]
+}
+
+// The E stored values of Philox block `block`.
+template <int DIST, int DT>
+__device__ __forceinline__ void wide_block(const SynthParams &p, uint64_t block, uint64_t *v) {
+  if constexpr ((DIST == SV_UNIFORM && DT == SV_F64) || (DIST == SV_INT_RANGE && DT == SV_I64)) {
+    const u32x4 w = philox_block(Key{p.k0, p.k1, p.s0, p.s1}, block);
+    const uint64_t r[2] = {((uint64_t)w.y << 32) | w.x, ((uint64_t)w.w << 32) | w.z};
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      if constexpr (DIST == SV_UNIFORM) {
+        const double t = p.span64 * ((double)(r[k] >> 11) * 0x1p-53);
+        v[k] = f64_bits(p.a64 + t);
+      } else {
+        v[k] = (uint64_t)p.lo + (p.range ? __umul64hi(r[k], p.range) : r[k]);
+      }
+    }
+  } else {
+    constexpr int E = DistTraits<DIST>::E;
+    uint32_t f[E];
+    block_values<DIST>(p, block, f);
+#pragma unroll
+    for (int k = 0; k < E; ++k) v[k] = from_value32<DT>(f[k]);
+  }
+}
+
+// The V stored values of output vector u (the window starts on a block).
+template <int DIST, int DT>
+__device__ __forceinline__ void wide_vector(const SynthParams &p, uint64_t u, uint64_t *v) {
+  constexpr int E = Wide<DIST, DT>::E, V = Wide<DIST, DT>::V;
+  if constexpr (V >= E) {
+#pragma unroll
+    for (int b = 0; b < V / E; ++b) wide_block<DIST, DT>(p, p.c0 + u * (V / E) + b, v + b * E);
+  } else {                                     // fp64 normal: one Box-Muller pair of the block
+    const u32x4 w = philox_block(Key{p.k0, p.k1, p.s0, p.s1}, p.c0 + u / 2);
+    const bool second = (u & 1u) != 0u;
+    float zc, zs;
+    box_muller(second ? w.z : w.x, second ? w.w : w.y, zc, zs);
+    v[0] = widen_f32_bits(as_u32(__builtin_fmaf(p.std, zc, p.mean)));
+    v[1] = widen_f32_bits(as_u32(__builtin_fmaf(p.std, zs, p.mean)));
+  }
+}
+
+template <int DT>
+__device__ __forceinline__ void store_wide(void *out, uint64_t i, uint64_t x) {
+  if constexpr (DT == SV_F16) ((uint16_t *)out)[i] = (uint16_t)x;
+  else if constexpr (DT == SV_U8) ((uint8_t *)out)[i] = (uint8_t)x;
+  else ((uint64_t *)out)[i] = x;
+}
+
+template <int DIST, int DT>
+__device__ __forceinline__ uint64_t wide_elem(const SynthParams &p, uint64_t g) {
+  constexpr int E = Wide<DIST, DT>::E;
+  uint64_t v[E];
+  wide_block<DIST, DT>(p, g / E, v);
+  return v[g % E];
+}
+
+template <int DIST, int DT>
+__global__ __launch_bounds__(kBlock) void synth_wide_vec_kernel(SynthParams p, uint64_t nvec, uint64_t n,
+                                                                u32x4 *__restrict__ out) {
+  constexpr int V = Wide<DIST, DT>::V;
+  const uint64_t gid = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t u = gid; u < nvec; u += stride) {
+    uint64_t v[V];
+    wide_vector<DIST, DT>(p, u, v);
+    u32x4 o;
+    if constexpr (DT == SV_F16) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = (uint32_t)v[2 * k] | ((uint32_t)v[2 * k + 1] << 16);
+    } else if constexpr (DT == SV_U8) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        o[k] = (uint32_t)v[4 * k] | ((uint32_t)v[4 * k + 1] << 8) | ((uint32_t)v[4 * k + 2] << 16) |
+               ((uint32_t)v[4 * k + 3] << 24);
+    } else {
+      o = u32x4{(uint32_t)v[0], (uint32_t)(v[0] >> 32), (uint32_t)v[1], (uint32_t)(v[1] >> 32)};
+    }
+    out[u] = o;
+  }
+  const uint64_t i = nvec * V + gid;
+  if (i < n) store_wide<DT>(out, i, wide_elem<DIST, DT>(p, p.e0 + i));
+}
+
+template <int DIST, int DT>
+__global__ __launch_bounds__(kBlock) void synth_wide_elem_kernel(SynthParams p, uint64_t n, void *__restrict__ out) {
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride)
+    store_wide<DT>(out, i, wide_elem<DIST, DT>(p, p.e0 + i));
+}
+
+template <int DIST, int DT>
+static hipError_t launch_wide(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
+  constexpr uint64_t V = Wide<DIST, DT>::V;
+  const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
+  if (((uintptr_t)out & 15u) == 0 && p.e0 % Wide<DIST, DT>::E == 0) {
+    const uint64_t nvec = n / V;
+    const uint64_t threads = std::max<uint64_t>(nvec, n - nvec * V);
+    const uint64_t blocks = std::min<uint64_t>((threads + kBlock - 1) / kBlock, max_blocks);
+    hipLaunchKernelGGL((synth_wide_vec_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, nvec,
+                       n, (u32x4 *)out);
+  } else {
+    const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, max_blocks);
+    hipLaunchKernelGGL((synth_wide_elem_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n,
+                       out);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint64_t n, void *out, int cus,
                         hipStream_t stream) {
-  switch (dist * 4 + dtype) {
-    case SV_UNIFORM * 4 + SV_F32: return launch_typed<SV_UNIFORM, SV_F32>(p, n, out, cus, stream);
-    case SV_UNIFORM * 4 + SV_BF16: return launch_typed<SV_UNIFORM, SV_BF16>(p, n, out, cus, stream);
-    case SV_NORMAL * 4 + SV_F32: return launch_typed<SV_NORMAL, SV_F32>(p, n, out, cus, stream);
-    case SV_NORMAL * 4 + SV_BF16: return launch_typed<SV_NORMAL, SV_BF16>(p, n, out, cus, stream);
-    case SV_INT_RANGE * 4 + SV_I32: return launch_typed<SV_INT_RANGE, SV_I32>(p, n, out, cus, stream);
-    case SV_SPECIAL * 4 + SV_F32: return launch_typed<SV_SPECIAL, SV_F32>(p, n, out, cus, stream);
-    case SV_SPECIAL * 4 + SV_BF16: return launch_typed<SV_SPECIAL, SV_BF16>(p, n, out, cus, stream);
+  switch (dist * 8 + dtype) {
+    case SV_UNIFORM * 8 + SV_F32: return launch_typed<SV_UNIFORM, SV_F32>(p, n, out, cus, stream);
+    case SV_UNIFORM * 8 + SV_BF16: return launch_typed<SV_UNIFORM, SV_BF16>(p, n, out, cus, stream);
+    case SV_NORMAL * 8 + SV_F32: return launch_typed<SV_NORMAL, SV_F32>(p, n, out, cus, stream);
+    case SV_NORMAL * 8 + SV_BF16: return launch_typed<SV_NORMAL, SV_BF16>(p, n, out, cus, stream);
+    case SV_INT_RANGE * 8 + SV_I32: return launch_typed<SV_INT_RANGE, SV_I32>(p, n, out, cus, stream);
+    case SV_SPECIAL * 8 + SV_F32: return launch_typed<SV_SPECIAL, SV_F32>(p, n, out, cus, stream);
+    case SV_SPECIAL * 8 + SV_BF16: return launch_typed<SV_SPECIAL, SV_BF16>(p, n, out, cus, stream);
+    case SV_UNIFORM * 8 + SV_F16: return launch_wide<SV_UNIFORM, SV_F16>(p, n, out, cus, stream);
+    case SV_UNIFORM * 8 + SV_F64: return launch_wide<SV_UNIFORM, SV_F64>(p, n, out, cus, stream);
+    case SV_NORMAL * 8 + SV_F16: return launch_wide<SV_NORMAL, SV_F16>(p, n, out, cus, stream);
+    case SV_NORMAL * 8 + SV_F64: return launch_wide<SV_NORMAL, SV_F64>(p, n, out, cus, stream);
+    case SV_SPECIAL * 8 + SV_F16: return launch_wide<SV_SPECIAL, SV_F16>(p, n, out, cus, stream);
+    case SV_SPECIAL * 8 + SV_F64: return launch_wide<SV_SPECIAL, SV_F64>(p, n, out, cus, stream);
+    case SV_INT_RANGE * 8 + SV_U8: return launch_wide<SV_INT_RANGE, SV_U8>(p, n, out, cus, stream);
+    case SV_INT_RANGE * 8 + SV_I64: return launch_wide<SV_INT_RANGE, SV_I64>(p, n, out, cus, stream);
     default: return hipErrorInvalidValue;
   }
 }
@@ -167,6 +300,10 @@ __global__ __launch_bounds__(kBlock) void eval_transform_kernel(int32_t which, c
                                                                 uint64_t n, uint32_t *__restrict__ out) {
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
+    if (which == SV_EVAL_F16) {
+      out[i] = f16_rne(in[i]);
+      continue;
+    }
     const uint32_t k = in[i] & 0x00FFFFFFu;
     float v;
     if (which == SV_EVAL_LN) {

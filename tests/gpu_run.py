@@ -4,8 +4,10 @@ import torch
 
 import paper_2609_00058_amd as sv
 
-TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16, "i32": torch.int32}
-STORAGE = {"f32": np.uint32, "bf16": np.uint16, "i32": np.uint32}
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16, "i32": torch.int32, "f16": torch.float16,
+               "f64": torch.float64, "u8": torch.uint8, "i64": torch.int64}
+STORAGE = {"f32": np.uint32, "bf16": np.uint16, "i32": np.uint32, "f16": np.uint16, "f64": np.uint64,
+           "u8": np.uint8, "i64": np.uint64}
 
 
 def empty(n, dtype, device="cuda"):
@@ -30,9 +32,21 @@ def gpu_cand(case, ref, cand=None):
 
 def bits(t):
     """Raw storage of a device tensor as a host numpy array."""
-    if t.dtype == torch.bfloat16:
+    if t.dtype in (torch.bfloat16, torch.float16):
         return t.view(torch.int16).cpu().numpy().view(np.uint16)
+    if t.dtype == torch.uint8:
+        return t.cpu().numpy()
+    if t.dtype in (torch.float64, torch.int64):
+        return t.view(torch.int64).cpu().numpy().view(np.uint64)
     return t.view(torch.int32).cpu().numpy().view(np.uint32)
+
+
+def dev_bits(arr, dtype):
+    """A device tensor of `dtype` holding the raw storage array `arr`."""
+    view = {np.uint16: np.int16, np.uint32: np.int32, np.uint64: np.int64, np.uint8: np.uint8}
+    a = np.ascontiguousarray(arr)
+    t = torch.from_numpy(a.view(view[a.dtype.type])).to("cuda")
+    return t.view(TORCH_DTYPE[dtype])
 
 
 def bits_at(t, idx):

@@ -45,7 +45,11 @@ def test_abi_version_and_enums_match_header(svlib):
     for name, code in [("SV_F32", 0), ("SV_BF16", 1), ("SV_I32", 2), ("SV_UNIFORM", 0), ("SV_NORMAL", 1),
                        ("SV_INT_RANGE", 2), ("SV_SPECIAL", 3), ("SV_OP_FAULT_AT", 6)]:
         assert re.search(r"\b%s = %d\b" % (name, code), src), name
-    assert svlib.DTYPE_CODES == {"f32": 0, "bf16": 1, "i32": 2}
+    assert svlib.DTYPE_CODES == {"f32": 0, "bf16": 1, "i32": 2, "f16": 3, "f64": 4, "u8": 5, "i64": 6}
+    for name, code in [("SV_F16", 3), ("SV_F64", 4), ("SV_U8", 5), ("SV_I64", 6)]:
+        assert re.search(r"\b%s = %d\b" % (name, code), src), name
+    import oracle
+    assert oracle.DTYPES == svlib.DTYPE_CODES
 
 
 def test_struct_layouts_match_the_c_compiler(svlib, tmp_path):
@@ -80,6 +84,11 @@ def test_synth_argument_errors_before_any_device_work(svlib):
     L = svlib.lib()
     INV, UNS = svlib.SV_ERR_INVALID_ARG, svlib.SV_ERR_UNSUPPORTED
     assert _synth(L, svlib, 7, 0, a=0.0, b=1.0) == UNS                      # unknown dtype
+    assert _synth(L, svlib, 5, 0, a=0.0, b=1.0) == UNS                      # uniform into uint8
+    assert _synth(L, svlib, 3, 2, lo=0, hi=3) == UNS                        # int range into fp16
+    assert _synth(L, svlib, 5, 2, lo=0, hi=256) == INV                      # beyond uint8
+    assert _synth(L, svlib, 6, 2, lo=3, hi=2) == INV
+    assert _synth(L, svlib, 4, 0, out=0x1004, a=0.0, b=1.0) == INV          # misaligned fp64
     assert _synth(L, svlib, 0, 9, a=0.0, b=1.0) == UNS                      # unknown dist
     assert _synth(L, svlib, 0, 2, lo=0, hi=3) == UNS                        # int range into fp32
     assert _synth(L, svlib, 2, 0, a=0.0, b=1.0) == UNS                      # uniform into int32
@@ -125,7 +134,7 @@ def test_compare_argument_errors_and_empty(svlib):
     assert L.sv_compare(0x1000, 0x2000, 4, 0, math.inf, 0.0, 0, ctypes.byref(rep)) == INV
     assert L.sv_compare(0x1000, 0x2000, 4, 0, 0.0, math.nan, 0, ctypes.byref(rep)) == INV
     assert L.sv_compare(0x1001, 0x2000, 4, 1, 0.0, 0.0, 0, ctypes.byref(rep)) == INV   # misaligned bf16
-    assert L.sv_compare(0x1000, 0x2000, 4, 5, 0.0, 0.0, 0, ctypes.byref(rep)) == svlib.SV_ERR_UNSUPPORTED
+    assert L.sv_compare(0x1000, 0x2000, 4, 7, 0.0, 0.0, 0, ctypes.byref(rep)) == svlib.SV_ERR_UNSUPPORTED
     assert "rtol" in L.sv_last_error().decode() or "dtype" in L.sv_last_error().decode()
     assert L.sv_compare(0, 0, 0, 0, 1e-5, 1e-8, 0, ctypes.byref(rep)) == svlib.SV_OK
     assert rep.n == 0 and rep.mismatches == 0 and rep.first_mismatch == -1 and rep.err_sum == 0.0
@@ -170,7 +179,7 @@ def test_profile_read_with_nothing_recorded(svlib):
 
 def test_eval_transform_argument_errors(svlib):
     L = svlib._lib
-    assert L.sv_eval_transform(4, 0x1000, 4, 0x2000) == svlib.SV_ERR_UNSUPPORTED
+    assert L.sv_eval_transform(5, 0x1000, 4, 0x2000) == svlib.SV_ERR_UNSUPPORTED
     assert L.sv_eval_transform(-1, 0x1000, 4, 0x2000) == svlib.SV_ERR_UNSUPPORTED
     assert L.sv_eval_transform(0, None, 4, 0x2000) == svlib.SV_ERR_INVALID_ARG
     assert L.sv_eval_transform(0, 0x1002, 4, 0x2000) == svlib.SV_ERR_INVALID_ARG   # misaligned

@@ -1,0 +1,168 @@
+"""GPU parity of the fp16, fp64, uint8 and int64 paths against the oracle:
+synthesis bit for bit (aligned, unaligned, windows), the fp16 rounding over
+every fp32 pattern, the check (alone, batched with all seven types, early
+exit), candidate steps and files."""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_00058_amd as sv
+from gpu_run import STORAGE, bits, dev_bits, empty, same_report
+
+pytestmark = pytest.mark.gpu
+
+SPECIAL = dict(mean=0.0, std=1e3, p_nan=0.05, p_inf=0.02, p_denorm=0.05, p_zero=0.05)
+SYNTH = [("uniform", "f16", dict(a=-4.0, b=4.0)), ("uniform", "f64", dict(a=-0.3, b=0.7)),
+         ("normal", "f16", dict(mean=5.0, std=10.0)), ("normal", "f64", dict(mean=5.0, std=10.0)),
+         ("special", "f16", SPECIAL), ("special", "f64", SPECIAL),
+         ("int_range", "u8", dict(lo=0, hi=255)), ("int_range", "u8", dict(lo=3, hi=9)),
+         ("int_range", "i64", dict(lo=-2 ** 63, hi=2 ** 63 - 1)), ("int_range", "i64", dict(lo=-7, hi=10 ** 15))]
+
+
+@pytest.mark.parametrize("dist,dtype,params", SYNTH)
+def test_synth_new_types_bit_exact(oracle, dist, dtype, params):
+    p = oracle.dist_params(**params)
+    for n in (1, 3, 17, 1000, 65543, (1 << 20) + 3):
+        print("synth", dist, dtype, n, flush=True)
+        g = empty(n, dtype)
+        sv.synth(g, 21, 4, dist, **params)
+        assert np.array_equal(bits(g), oracle.synth(21, 4, dtype, dist, p, n))
+    big = empty(5000 + 16, dtype)                     # unaligned output, and windows on and off a block
+    isz = big.element_size()
+    for shift in (1, 16 // isz - 1):
+        w = big[shift:shift + 5000]
+        sv.synth(w, 21, 4, dist, **params)
+        assert np.array_equal(bits(w), oracle.synth(21, 4, dtype, dist, p, 5000))
+    for off in (2, 4, 5, 999_999):
+        w = empty(3001, dtype)
+        sv.synth_window(w, 21, 4, dist, off, **params)
+        assert np.array_equal(bits(w), oracle.synth(21, 4, dtype, dist, p, 3001, off))
+
+
+def test_f16_rounding_every_fp32_pattern(oracle):
+    chunk = 1 << 28
+    out = torch.empty(chunk, dtype=torch.int32, device="cuda")
+    pool = ThreadPoolExecutor(16)
+    for c in range(1 << 4):
+        print("f16 patterns, chunk", c, flush=True)
+        base = c * chunk
+        x = (torch.arange(chunk, dtype=torch.int64, device="cuda") + base).to(torch.int32)  # wraps to the bits
+        sv.eval_transform("f16", x, out)
+        got = out.cpu().numpy().view(np.uint32)
+        pats = (np.arange(chunk, dtype=np.uint64) + base).astype(np.uint32)
+        parts = np.array_split(np.arange(chunk), 16)
+        want = np.concatenate(list(pool.map(lambda ix: oracle.f16_rne_n(pats[ix]), parts))).astype(np.uint32)
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, "pattern %#x: got %#x want %#x" % (pats[bad[0]], got[bad[0]], want[bad[0]])
+
+
+def _pair(rng, n, dtype):
+    if dtype == "u8":
+        y = rng.integers(0, 256, n).astype(np.uint8)
+        a = y.copy()
+        k = rng.random(n) < 0.01
+        a[k] = rng.integers(0, 256, k.sum()).astype(np.uint8)
+        return y, a
+    if dtype == "i64":
+        y = rng.integers(-2 ** 63, 2 ** 63 - 1, n, dtype=np.int64)
+        y[: n // 2] = rng.integers(-1000, 1000, n // 2)
+        a = y.copy()
+        k = rng.random(n) < 0.01
+        a[k] += rng.integers(-3, 4, k.sum())
+        a[min(5, n - 1)] = y[min(5, n - 1)] ^ 1 if n > 5 else a[0]
+        return y.view(np.uint64), a.view(np.uint64)
+    y = rng.normal(5.0, 10.0, n)
+    a = y * (1 + rng.normal(0, 1, n) * 10.0 ** rng.uniform(-9, -1, n))
+    sp = np.array([np.nan, np.inf, -np.inf, 0.0, -0.0, 1e-310, 6e-8])
+    for arr in (y, a):
+        k = rng.random(n) < 0.03
+        arr[k] = rng.choice(sp, k.sum())
+    t = np.float16 if dtype == "f16" else np.float64
+    return y.astype(t).view(STORAGE[dtype]), a.astype(t).view(STORAGE[dtype])
+
+
+TOLS = {"f16": (1e-3, 1e-4, True), "f64": (1e-7, 1e-12, False), "u8": (0.0, 0.0, False), "i64": (0.0, 0.0, False)}
+
+
+@pytest.mark.parametrize("dtype", ["f16", "f64", "u8", "i64"])
+def test_compare_new_types(oracle, dtype):
+    rng = np.random.default_rng(77)
+    for n in (1, 7, 4099, (1 << 20) + 5):
+        print("compare", dtype, n, flush=True)
+        y, a = _pair(rng, n, dtype)
+        Y, A = dev_bits(y, dtype), dev_bits(a, dtype)
+        rtol, atol, eqn = TOLS[dtype]
+        same_report(sv.compare(Y, A, rtol, atol, eqn), oracle.compare(y, a, dtype, rtol, atol, eqn))
+        if n > 8:   # unaligned views take the element path
+            same_report(sv.compare(Y[1:], A[1:], rtol, atol, eqn),
+                        oracle.compare(y[1:], a[1:], dtype, rtol, atol, eqn))
+
+
+def test_batched_all_types_and_early_exit(oracle):
+    rng = np.random.default_rng(78)
+    types = ["f32", "bf16", "i32", "f16", "f64", "u8", "i64"]
+    segs, want, keep = [], [], []
+    for k in range(21):
+        dtype = types[k % 7]
+        n = int(rng.choice([0, 1, 100, 70001, 300000]))
+        if dtype in ("f32", "bf16", "i32"):
+            from test_gpu_compare import random_pair
+            y, a = random_pair(rng, n, dtype)
+            tol = (1e-5, 1e-8, k % 2 == 0)
+        else:
+            y, a = _pair(rng, n, dtype) if n else (np.empty(0, STORAGE[dtype]), np.empty(0, STORAGE[dtype]))
+            tol = TOLS[dtype]
+        Y, A = dev_bits(y, dtype), dev_bits(a, dtype)
+        keep += [Y, A]
+        segs.append((Y, A, *tol))
+        want.append(oracle.compare(y, a, dtype, *tol))
+    print("batched all types", len(segs), flush=True)
+    for g, w in zip(sv.compare_batched(segs), want):
+        same_report(g, w)
+    for g, w in zip(sv.compare_batched(segs, stop_at_first=True), want):
+        if w["mismatches"] == 0:
+            same_report(g, w)
+        else:
+            assert g["mismatches"] == 1 and g["first_mismatch"] == w["first_mismatch"] and g["err_sum"] == 0.0
+
+
+@pytest.mark.parametrize("dtype,op,kw", [("f16", "ulp", dict(p=0.5)), ("f64", "ulp", dict(p=0.5)),
+                                         ("f16", "fault_at", {}), ("f64", "fault_at", {}), ("u8", "fault_at", {}),
+                                         ("i64", "fault_at", {}), ("f16", "set_at", dict(bits=0x7E00)),
+                                         ("u8", "set_at", dict(bits=0xAB))])
+def test_candidate_steps_new_types(oracle, dtype, op, kw):
+    dist, prm = {"f16": ("normal", dict(mean=0.0, std=100.0)), "f64": ("normal", dict(mean=0.0, std=1e6)),
+                 "u8": ("int_range", dict(lo=0, hi=255)), "i64": ("int_range", dict(lo=-2 ** 63, hi=2 ** 63 - 1))}[dtype]
+    n = 100_003
+    ref = empty(n, dtype)
+    sv.synth(ref, 5, 6, dist, **prm)
+    r = oracle.synth(5, 6, dtype, dist, oracle.dist_params(**prm), n)
+    cand = ref.clone()
+    if op == "ulp":
+        sv.perturb(ref, cand, 9, 10, op, **kw)
+        want = oracle.perturb(9, 10, dtype, op, r, np.empty_like(r), **kw)
+    else:
+        idx = np.array([0, 17, n - 1], np.uint64)
+        sv.perturb(ref, cand, 0, 0, op, idx=idx, **kw)
+        want = oracle.perturb(0, 0, dtype, op, r, r.copy(), idx=idx, **kw)
+    assert np.array_equal(bits(cand), want)
+    with pytest.raises(sv.SVError) as e:
+        sv.perturb(ref, cand, 0, 0, "special_flip", p=0.5)
+    assert e.value.code == sv.SV_ERR_UNSUPPORTED
+
+
+def test_uint8_files_are_read_as_bytes(oracle, tmp_path):
+    n = (1 << 26) + 7                                  # one full 64 MiB chunk and a tail
+    rp, cp = str(tmp_path / "r.u8"), str(tmp_path / "c.u8")
+    sv.synth_file(rp, n, 3, 3, "u8", "int_range", lo=0, hi=255)
+    y = np.fromfile(rp, dtype=np.uint8)
+    assert np.array_equal(y, oracle.synth(3, 3, "u8", "int_range", oracle.dist_params(lo=0, hi=255), n))
+    a = y.copy()
+    a[[10, n - 1]] ^= 1
+    a.tofile(cp)
+    rep = sv.compare_file(rp, cp, n, "u8", 0.0, 0.0)
+    same_report(rep, oracle.compare(y, a, "u8", 0.0, 0.0, False))
+    assert rep["mismatches"] == 2 and rep["first_mismatch"] == 10
