@@ -157,8 +157,10 @@ int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t di
  * only when equal_nan is set and both are NaN; otherwise if either is
  * infinite the pair agrees only when the values are equal; otherwise it
  * agrees when |K(x) - y| <= atol + rtol * |y|, each operation rounded to
- * nearest in fp64 (no fused multiply-add).  SV_I32 pairs agree only when
- * equal.  V(K, x, y) = 1 exactly when report->mismatches == 0.
+ * nearest in fp64 (no fused multiply-add).  Integer pairs (int32, uint8,
+ * int64) agree only when equal; tolerances do not apply to them, and an int64
+ * difference is formed exactly before it is rounded to fp64 for the report.
+ * V(K, x, y) = 1 exactly when report->mismatches == 0.
  *
  * ref, cand : device pointers to n elements of dtype (any element alignment).
  * report    : host pointer, written on success.
@@ -193,6 +195,40 @@ int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports
  */
 enum { SV_CHECK_FULL = 0, SV_CHECK_STOP_AT_FIRST = 1 };
 int sv_compare_batched_mode(const sv_segment *segs, uint32_t nseg, int32_t mode, sv_report *reports);
+
+/*
+ * sv_compare_submit, sv_compare_batched_submit, sv_compare_ready,
+ * sv_compare_wait -- the checks above without waiting for their reports, so
+ * that the next piece of work (the next candidate's launch, the next
+ * synthesis, the next check) is already queued while a report travels to the
+ * host.  The generation loop of Sec. 4.3 checks G candidates per round, round
+ * after round, and the GPU need not idle between them.
+ *
+ * A submit call validates its arguments exactly as its synchronous
+ * counterpart, queues the same kernels on the selected stream and returns at
+ * once with *ticket set.  The tensors must stay valid and unchanged until the
+ * check has run (work queued later on the same stream runs after it), and the
+ * stream must outlive the wait.  sv_compare_wait(ticket, reports, nreports)
+ * blocks until that check's reports are on the host and copies them into
+ * reports[0..nreports): nreports must be 1 for sv_compare_submit and nseg for
+ * a batch (otherwise INVALID_ARG, and the ticket stays pending).  On success,
+ * or on a HIP error, the ticket is used up; waiting twice is INVALID_ARG.
+ * sv_compare_ready sets *ready to 1 once a wait would not block, else 0.
+ *
+ * At most SV_MAX_PENDING_CHECKS submitted checks per device are pending (not
+ * yet waited for); one more submit returns INVALID_ARG.  A ticket names its
+ * device, so it may be waited for with any device current.  Checks of one
+ * device run one after another in submission order, also across streams: a
+ * check queued on another stream than the previous check first waits, on
+ * the host, until the pending checks have run.  The synchronous calls are a
+ * submit and a wait in one, in a slot of their own.
+ */
+#define SV_MAX_PENDING_CHECKS 16
+int sv_compare_submit(const void *ref, const void *cand, uint64_t n, int32_t dtype, double rtol, double atol,
+                      int32_t equal_nan, uint64_t *ticket);
+int sv_compare_batched_submit(const sv_segment *segs, uint32_t nseg, int32_t mode, uint64_t *ticket);
+int sv_compare_ready(uint64_t ticket, int32_t *ready);
+int sv_compare_wait(uint64_t ticket, sv_report *reports, uint32_t nreports);
 
 /* Candidate derivation steps of sv_perturb (workload support, not part of the check). */
 enum {

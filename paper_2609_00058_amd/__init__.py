@@ -21,6 +21,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 SV_OK, SV_ERR_INVALID_ARG, SV_ERR_UNSUPPORTED, SV_ERR_HIP, SV_ERR_ALLOC, SV_ERR_IO = 0, -1, -2, -3, -4, -5
+SV_MAX_PENDING_CHECKS = 16   # submitted checks per device not yet waited for
 DTYPE_CODES = {"f32": 0, "bf16": 1, "i32": 2, "f16": 3, "f64": 4, "u8": 5, "i64": 6}
 DIST_CODES = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3}
 OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
@@ -29,7 +30,7 @@ PROF_KINDS = {"synth": 0, "compare": 1, "perturb": 2, "finalize": 3}
 
 # every symbol include/sv.h declares
 SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_synth_window", "sv_compare", "sv_compare_batched", "sv_compare_batched_mode",
-           "sv_perturb",
+           "sv_compare_submit", "sv_compare_batched_submit", "sv_compare_ready", "sv_compare_wait", "sv_perturb",
            "sv_eval_transform", "sv_synth_file", "sv_compare_file", "sv_kernel_load", "sv_kernel_free", "sv_kernel_launch", "sv_kernel_time",
            "sv_reward", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
 
@@ -95,6 +96,10 @@ _lib.sv_synth_window.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistPara
 _lib.sv_compare.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(Report)]
 _lib.sv_compare_batched.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, ctypes.POINTER(Report)]
 _lib.sv_compare_batched_mode.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, _i32, ctypes.POINTER(Report)]
+_lib.sv_compare_submit.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(_u64)]
+_lib.sv_compare_batched_submit.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, _i32, ctypes.POINTER(_u64)]
+_lib.sv_compare_ready.argtypes = [_u64, ctypes.POINTER(_i32)]
+_lib.sv_compare_wait.argtypes = [_u64, ctypes.POINTER(Report), ctypes.c_uint32]
 _lib.sv_perturb.argtypes = [_u64, _u64, _i32, ctypes.POINTER(PerturbPlan), _u64, _vp, _vp]
 _lib.sv_eval_transform.argtypes = [_i32, _vp, _u64, _vp]
 _lib.sv_kernel_load.argtypes = [ctypes.c_char_p, _u64, ctypes.c_char_p, ctypes.POINTER(_vp)]
@@ -250,13 +255,7 @@ def compare(ref, cand, rtol: float, atol: float, equal_nan: bool = False) -> dic
     return rep.as_dict()
 
 
-def compare_batched(segments, stop_at_first: bool = False) -> list:
-    """segments: list of (ref, cand, rtol, atol, equal_nan); one launch, one report each.
-    stop_at_first: a failing segment is checked only as far as needed to know
-    its first mismatch exactly; its report then holds n, mismatches = 1 and
-    first_mismatch, everything else 0."""
-    if not segments:
-        return []
+def _segment_array(segments):
     arr = (Segment * len(segments))()
     for k, (ref, cand, rtol, atol, eqn) in enumerate(segments):
         if ref.dtype != cand.dtype or ref.numel() != cand.numel():
@@ -264,9 +263,67 @@ def compare_batched(segments, stop_at_first: bool = False) -> list:
         arr[k] = Segment(_dev_ptr(ref, "ref") if ref.numel() else None,
                          _dev_ptr(cand, "cand") if cand.numel() else None,
                          ref.numel(), dtype_code(ref), rtol, atol, int(bool(eqn)))
+    return arr
+
+
+def compare_batched(segments, stop_at_first: bool = False) -> list:
+    """segments: list of (ref, cand, rtol, atol, equal_nan); one launch, one report each.
+    stop_at_first: a failing segment is checked only as far as needed to know
+    its first mismatch exactly; its report then holds n, mismatches = 1 and
+    first_mismatch, everything else 0."""
+    if not segments:
+        return []
+    arr = _segment_array(segments)
     reps = (Report * len(segments))()
     _run(segments[0][0], _lib.sv_compare_batched_mode, arr, len(segments), 1 if stop_at_first else 0, reps)
     return [reps[k].as_dict() for k in range(len(segments))]
+
+
+class CheckTicket:
+    """A submitted check (compare_submit, compare_batched_submit).  It keeps its
+    tensors alive until waited for; wait() returns what compare() or
+    compare_batched() would have returned."""
+
+    def __init__(self, ticket: int, nreports: int, batched: bool, keep):
+        self.ticket, self.nreports, self.batched, self._keep = ticket, nreports, batched, keep
+        self._result = None
+
+    def ready(self) -> bool:
+        if self._result is not None:
+            return True
+        flag = ctypes.c_int32(0)
+        _check(_lib.sv_compare_ready(self.ticket, ctypes.byref(flag)))
+        return bool(flag.value)
+
+    def wait(self):
+        if self._result is None:
+            reps = (Report * max(self.nreports, 1))()
+            _check(_lib.sv_compare_wait(self.ticket, reps, self.nreports))
+            out = [reps[k].as_dict() for k in range(self.nreports)]
+            self._result = out if self.batched else out[0]
+            self._keep = None
+        return self._result
+
+
+def compare_submit(ref, cand, rtol: float, atol: float, equal_nan: bool = False) -> CheckTicket:
+    """compare() queued on the current stream without waiting; .wait() gives the report."""
+    if ref.dtype != cand.dtype or ref.numel() != cand.numel():
+        raise SVError(SV_ERR_INVALID_ARG, "ref and cand must have the same dtype and size")
+    t = ctypes.c_uint64(0)
+    _run(ref, _lib.sv_compare_submit, _dev_ptr(ref, "ref"), _dev_ptr(cand, "cand"), ref.numel(),
+         dtype_code(ref), rtol, atol, int(bool(equal_nan)), ctypes.byref(t))
+    return CheckTicket(t.value, 1, False, (ref, cand))
+
+
+def compare_batched_submit(segments, stop_at_first: bool = False) -> CheckTicket:
+    """compare_batched() queued on the current stream without waiting; .wait() gives the reports."""
+    if not segments:
+        raise SVError(SV_ERR_INVALID_ARG, "compare_batched_submit: no segments")
+    arr = _segment_array(segments)
+    t = ctypes.c_uint64(0)
+    _run(segments[0][0], _lib.sv_compare_batched_submit, arr, len(segments), 1 if stop_at_first else 0,
+         ctypes.byref(t))
+    return CheckTicket(t.value, len(segments), True, [s[:2] for s in segments])
 
 
 def perturb(ref, cand, seed: int, stream_id: int, op: str, p: float = 0.0, value: float = 0.0,

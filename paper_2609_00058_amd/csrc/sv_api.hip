@@ -48,8 +48,34 @@ int hip_fail(hipError_t e, const char *what) {
   } while (0)
 
 // ------------------------------------------------------------ per-device scratch
+// Every check in flight owns a slot: its reports and its completion word in
+// host-mapped memory, the pinned staging of its segment table, and what the
+// wait needs to finish its reports.  Slots 0 .. SV_MAX_PENDING_CHECKS - 1 hold
+// submitted checks; the synchronous calls use the last one.
+constexpr int kAsyncSlots = SV_MAX_PENDING_CHECKS;
+constexpr int kSyncSlot = kAsyncSlots;
+constexpr int kSlots = kAsyncSlots + 1;
+constexpr int kDoneStride = 8;        // completion words 64 bytes apart
+constexpr int kTicketSeqBits = 56;    // ticket = (device + 1) << 56 | sequence number
+
+struct CheckSlot {
+  bool pending = false;          // holds a check not yet waited for
+  bool waiting = false;          // a thread waits for it, outside the device lock
+  bool launched = false;         // kernels were queued (not when every segment is empty)
+  bool stop_at_first = false;
+  uint64_t seq = 0;              // the check's sequence number
+  hipStream_t stream = nullptr;  // where its kernels were queued
+  std::vector<uint64_t> lengths; // n of each segment
+  sv_report *h_reports = nullptr;  // pinned, host-mapped, coherent: the finalize writes here
+  sv_report *d_reports = nullptr;  // the device address of h_reports
+  size_t reports_cap = 0;
+  SegDesc *h_table = nullptr;    // pinned staging of the segment table
+  size_t h_table_cap = 0;
+};
+
 struct DeviceState {
   std::mutex mu;                 // serialises calls that use the scratch below
+  int device = 0;
   int cus = 0;
   Partial *partials = nullptr;   // one per (workgroup, segment piece)
   size_t partials_cap = 0;
@@ -57,11 +83,6 @@ struct DeviceState {
   size_t table_cap = 0;
   uint64_t *idx = nullptr;
   size_t idx_cap = 0;
-  SegDesc *h_table = nullptr;    // pinned staging
-  size_t h_table_cap = 0;
-  sv_report *h_reports = nullptr;  // pinned, host-mapped, coherent: the kernel writes reports here
-  sv_report *d_reports = nullptr;  // the device address of h_reports
-  size_t h_reports_cap = 0;
   uint64_t *h_idx = nullptr;
   size_t h_idx_cap = 0;
   SynthJob *synth_table = nullptr;   // batched synthesis job table
@@ -73,9 +94,13 @@ struct DeviceState {
   bool synth_pending = false;        // the two events above have been recorded
   uint32_t *counters = nullptr;      // arrival counters of the check (zero between launches)
   size_t counters_cap = 0;
-  uint64_t *h_done = nullptr;        // pinned, host-mapped, coherent: a check's last word written
+  uint64_t *h_done = nullptr;        // pinned, host-mapped, coherent: one completion word per slot
   uint64_t *d_done = nullptr;        // its device address
-  uint64_t seq = 0;                  // sequence number of the last check launched
+  uint64_t seq = 0;                  // sequence number of the last check submitted
+  CheckSlot slots[kSlots];
+  int npending = 0;                  // submitted checks not yet waited for
+  bool has_last = false;             // a check has been queued on last_stream
+  hipStream_t last_stream = nullptr; // stream of the last check queued
 };
 
 std::mutex g_devices_mu;
@@ -91,6 +116,7 @@ int current_device(DeviceState **out) {
     SV_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev),
            "hipDeviceGetAttribute(multiProcessorCount)");
     auto *s = new DeviceState;
+    s->device = dev;
     s->cus = cus > 0 ? cus : 1;
     g_devices[dev] = s;
   }
@@ -122,27 +148,26 @@ int ensure_device(T *&ptr, size_t &cap, size_t need, const char *what) {
   return SV_OK;
 }
 
-int ensure_reports(DeviceState *ds, size_t need) {
-  if (need <= ds->h_reports_cap) return SV_OK;
-  const size_t want = std::max(need, ds->h_reports_cap + ds->h_reports_cap / 2);
-  if (ds->h_reports) (void)hipHostFree(ds->h_reports);
-  ds->h_reports = nullptr;
-  ds->d_reports = nullptr;
-  ds->h_reports_cap = 0;
-  hipError_t e = hipHostMalloc((void **)&ds->h_reports, want * sizeof(sv_report),
+int ensure_reports(CheckSlot &sl, size_t need) {
+  if (need <= sl.reports_cap) return SV_OK;
+  const size_t want = std::max(need, sl.reports_cap + sl.reports_cap / 2);
+  if (sl.h_reports) (void)hipHostFree(sl.h_reports);
+  sl.h_reports = nullptr;
+  sl.d_reports = nullptr;
+  sl.reports_cap = 0;
+  hipError_t e = hipHostMalloc((void **)&sl.h_reports, want * sizeof(sv_report),
                                hipHostMallocMapped | hipHostMallocCoherent);
   if (e != hipSuccess) {
-    ds->h_reports = nullptr;
-    return fail(SV_ERR_ALLOC, "hipHostMalloc of %zu bytes for reports: %s", want * sizeof(sv_report),
-                hipGetErrorString(e));
+    sl.h_reports = nullptr;
+    return fail(SV_ERR_ALLOC, "hipHostMalloc of %zu reports: %s", want, hipGetErrorString(e));
   }
-  e = hipHostGetDevicePointer((void **)&ds->d_reports, ds->h_reports, 0);
+  e = hipHostGetDevicePointer((void **)&sl.d_reports, sl.h_reports, 0);
   if (e != hipSuccess) {
-    (void)hipHostFree(ds->h_reports);
-    ds->h_reports = nullptr;
+    (void)hipHostFree(sl.h_reports);
+    sl.h_reports = nullptr;
     return hip_fail(e, "hipHostGetDevicePointer(reports)");
   }
-  ds->h_reports_cap = want;
+  sl.reports_cap = want;
   return SV_OK;
 }
 
@@ -156,28 +181,28 @@ int ensure_counters(DeviceState *ds, size_t need) {
 
 int ensure_done(DeviceState *ds) {
   if (ds->h_done) return SV_OK;
-  hipError_t e = hipHostMalloc((void **)&ds->h_done, 64, hipHostMallocMapped | hipHostMallocCoherent);
+  const size_t bytes = (size_t)kSlots * kDoneStride * sizeof(uint64_t);
+  hipError_t e = hipHostMalloc((void **)&ds->h_done, bytes, hipHostMallocMapped | hipHostMallocCoherent);
   if (e != hipSuccess) {
     ds->h_done = nullptr;
-    return fail(SV_ERR_ALLOC, "hipHostMalloc of the completion word: %s", hipGetErrorString(e));
+    return fail(SV_ERR_ALLOC, "hipHostMalloc of the completion words: %s", hipGetErrorString(e));
   }
   e = hipHostGetDevicePointer((void **)&ds->d_done, ds->h_done, 0);
   if (e != hipSuccess) {
     (void)hipHostFree(ds->h_done);
     ds->h_done = nullptr;
-    return hip_fail(e, "hipHostGetDevicePointer(completion word)");
+    return hip_fail(e, "hipHostGetDevicePointer(completion words)");
   }
-  *(volatile uint64_t *)ds->h_done = ds->seq;
+  for (int k = 0; k < kSlots * kDoneStride; ++k) ((volatile uint64_t *)ds->h_done)[k] = 0;   // sequence numbers start at 1
   return SV_OK;
 }
 
-// Waits until the check launched with sequence number `seq` has written its
-// reports: spins on the host-mapped completion word (a few hundred ns after
-// the kernel's last store, well before a stream synchronisation would
-// return), asking the stream now and then whether it failed instead.
-int wait_done(DeviceState *ds, uint64_t seq, hipStream_t st) {
+// Waits until the check with sequence number `seq` has written its reports:
+// spins on its host-mapped completion word (a few hundred ns after the
+// kernel's last store, well before a stream synchronisation would return),
+// asking the stream now and then whether it failed instead.
+int wait_done(const volatile uint64_t *flag, uint64_t seq, hipStream_t st) {
   using clock = std::chrono::steady_clock;
-  const volatile uint64_t *flag = ds->h_done;
   std::chrono::microseconds interval(50);
   auto next = clock::now() + interval;
   while (*flag != seq) {
@@ -319,23 +344,100 @@ void compare_grid(uint64_t units, int cus, bool batched, uint32_t *nblocks, uint
   *nblocks = (uint32_t)((units + c - 1) / c);
 }
 
-// The check kernel (and, for a batch, its finalize kernel), which write the
-// reports into host-mapped memory and then the launch's sequence number; the
-// host waits for that number.  Segments with no elements get their (empty)
-// report here.
-int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_segment *segs, uint32_t nseg,
-                sv_report *out, bool stop_at_first = false) {
+// Waits on the host for every submitted check still pending (they stay
+// pending for their waiters).  Called before a check is queued on another
+// stream than the previous one and before shared scratch is reallocated, so
+// that no queued check can still read what is about to change: a check whose
+// completion word has been written has read all of it.
+int drain_pending(DeviceState *ds) {
+  if (ds->npending == 0) return SV_OK;
+  for (int k = 0; k < kAsyncSlots; ++k) {
+    const CheckSlot &sl = ds->slots[k];
+    if (!sl.pending || !sl.launched) continue;
+    const int rc = wait_done(ds->h_done + (size_t)k * kDoneStride, sl.seq, sl.stream);
+    if (rc) return rc;
+  }
+  return SV_OK;
+}
+
+// A validated check: kernel arguments (segment table aside), grid, segments.
+struct CheckPlan {
+  CompareArgs args;
+  uint32_t nblocks = 0;
+  const sv_segment *segs = nullptr;   // nullptr: the one segment in args.single
+  uint32_t nseg = 0;
+  bool stop_at_first = false;
+  uint64_t total_units = 0;
+};
+
+void plan_single(const sv_segment &g, int cus, CheckPlan &plan) {
+  std::memset(&plan.args, 0, sizeof plan.args);
+  plan.segs = nullptr;
+  plan.nseg = 1;
+  plan.stop_at_first = false;
+  plan.args.single = make_desc(g, 0);
+  plan.args.nseg = 1;
+  plan.total_units = plan.args.total_units = units_of(g.dtype, g.n);
+  if (plan.total_units) compare_grid(plan.total_units, cus, false, &plan.nblocks, &plan.args.chunk);
+}
+
+void plan_batched(const sv_segment *segs, uint32_t nseg, int32_t mode, int cus, CheckPlan &plan) {
+  std::memset(&plan.args, 0, sizeof plan.args);
+  plan.segs = segs;
+  plan.nseg = nseg;
+  plan.stop_at_first = mode == SV_CHECK_STOP_AT_FIRST;
+  uint64_t total = 0;
+  for (uint32_t k = 0; k < nseg; ++k) total += units_of(segs[k].dtype, segs[k].n);
+  plan.args.nseg = nseg;
+  plan.total_units = plan.args.total_units = total;
+  if (total) compare_grid(total, cus, true, &plan.nblocks, &plan.args.chunk);
+}
+
+// Queues the kernels of `plan` into slot k on the selected stream and marks
+// the slot pending under a new sequence number.  The check kernel and its
+// finalize kernel write the reports into the slot's host-mapped memory, then
+// the sequence number into the slot's completion word.
+int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   hipStream_t st = t_stream;
-  int rc = ensure_device(ds->partials, ds->partials_cap, (size_t)nblocks + nseg, "partials");
-  if (!rc) rc = ensure_reports(ds, nseg);
+  CheckSlot &sl = ds->slots[k];
+  const uint32_t nseg = plan.nseg;
+  const bool batched = plan.segs != nullptr;
+  sl.lengths.resize(nseg);
+  for (uint32_t j = 0; j < nseg; ++j) sl.lengths[j] = batched ? plan.segs[j].n : plan.args.single.n;
+  sl.stop_at_first = plan.stop_at_first;
+  sl.launched = false;
+  sl.waiting = false;
+  if (plan.total_units == 0) {                   // nothing to launch: every report is empty
+    sl.seq = ++ds->seq;
+    sl.pending = true;
+    return SV_OK;
+  }
+  const bool grow = (size_t)plan.nblocks + nseg > ds->partials_cap || (batched && nseg > ds->table_cap);
+  int rc = SV_OK;
+  if (grow || (ds->has_last && ds->last_stream != st)) rc = drain_pending(ds);
+  if (!rc) rc = ensure_device(ds->partials, ds->partials_cap, (size_t)plan.nblocks + nseg, "partials");
+  if (!rc && batched) rc = ensure_device(ds->table, ds->table_cap, nseg, "segment table");
+  if (!rc && batched) rc = ensure_pinned(sl.h_table, sl.h_table_cap, nseg, "segment table staging");
+  if (!rc) rc = ensure_reports(sl, nseg);
   if (!rc) rc = ensure_counters(ds, 1);
   if (!rc) rc = ensure_done(ds);
   if (rc) return rc;
-  args.stop_at_first = stop_at_first ? 1 : 0;
+  CompareArgs &args = plan.args;
+  if (batched) {
+    uint64_t begin = 0;
+    for (uint32_t j = 0; j < nseg; ++j) {
+      sl.h_table[j] = make_desc(plan.segs[j], begin);
+      begin += units_of(plan.segs[j].dtype, plan.segs[j].n);
+    }
+    SV_HIP(hipMemcpyAsync(ds->table, sl.h_table, nseg * sizeof(SegDesc), hipMemcpyHostToDevice, st),
+           "segment table copy to device");
+    args.segs = ds->table;
+  }
+  args.stop_at_first = plan.stop_at_first ? 1 : 0;
   args.partials = ds->partials;
   args.counter = ds->counters;
-  args.reports = ds->d_reports;
-  args.done = ds->d_done;
+  args.reports = sl.d_reports;
+  args.done = ds->d_done + (size_t)k * kDoneStride;
   args.seq = ds->seq + 1;
   hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
   if (g_prof_on.load()) {
@@ -345,35 +447,84 @@ int run_compare(DeviceState *ds, CompareArgs &args, uint32_t nblocks, const sv_s
     if (e0) (void)hipEventRecord(e0, st);
   }
   uint32_t mask = 0;
-  for (uint32_t k = 0; k < nseg; ++k) {
-    const sv_segment *g = segs ? &segs[k] : nullptr;
-    const uint64_t n = g ? g->n : args.single.n;
-    if (n) mask |= 1u << (g ? g->dtype : args.single.dtype);
+  for (uint32_t j = 0; j < nseg; ++j) {
+    const uint64_t n = batched ? plan.segs[j].n : args.single.n;
+    if (n) mask |= 1u << (batched ? plan.segs[j].dtype : args.single.dtype);
   }
-  hipError_t e = launch_compare(args, nblocks, mask, st, e0 ? e1 : nullptr);
+  hipError_t e = launch_compare(args, plan.nblocks, mask, st, e0 ? e1 : nullptr);
   if (e != hipSuccess) return hip_fail(e, "check kernel launch");
   ds->seq = args.seq;
+  ds->has_last = true;
+  ds->last_stream = st;
+  sl.seq = args.seq;
+  sl.stream = st;
+  sl.launched = true;
+  sl.pending = true;
   if (e0 && e1 && e2) {
     (void)hipEventRecord(e2, st);
     push_record(SV_PROF_COMPARE, e0, e1);
     push_record(SV_PROF_FINALIZE, e1, e2);
   }
-  rc = wait_done(ds, args.seq, st);
-  if (rc) return rc;
-  for (uint32_t k = 0; k < nseg; ++k) {
-    const uint64_t n = segs ? segs[k].n : args.single.n;
+  return SV_OK;
+}
+
+// The reports of a completed check, out of its slot.  Segments with no
+// elements get their empty report here; in stop-at-first mode a failing
+// segment keeps only its verdict and its first index.
+void finish_check(const CheckSlot &sl, sv_report *out) {
+  for (size_t j = 0; j < sl.lengths.size(); ++j) {
+    const uint64_t n = sl.lengths[j];
     if (n)
-      out[k] = ds->h_reports[k];
+      out[j] = sl.h_reports[j];
     else
-      zero_report(&out[k], 0);
-    if (stop_at_first && out[k].mismatches) {   // only the verdict and the first index are defined
-      const int64_t first = out[k].first_mismatch;
-      zero_report(&out[k], n);
-      out[k].mismatches = 1;
-      out[k].first_mismatch = first;
+      zero_report(&out[j], 0);
+    if (sl.stop_at_first && out[j].mismatches) {
+      const int64_t first = out[j].first_mismatch;
+      zero_report(&out[j], n);
+      out[j].mismatches = 1;
+      out[j].first_mismatch = first;
     }
   }
-  return SV_OK;
+}
+
+// A synchronous check: submit into the synchronous slot and wait (the
+// caller holds the device lock throughout).
+int run_sync(DeviceState *ds, CheckPlan &plan, sv_report *out) {
+  CheckSlot &sl = ds->slots[kSyncSlot];
+  int rc = submit_check(ds, kSyncSlot, plan);
+  if (!rc && sl.launched) rc = wait_done(ds->h_done + (size_t)kSyncSlot * kDoneStride, sl.seq, sl.stream);
+  if (!rc) finish_check(sl, out);
+  sl.pending = false;
+  return rc;
+}
+
+uint64_t make_ticket(int device, uint64_t seq) { return ((uint64_t)(device + 1) << kTicketSeqBits) | seq; }
+
+// The device state a ticket names, or nullptr.
+DeviceState *ticket_device(uint64_t ticket) {
+  const uint64_t d = ticket >> kTicketSeqBits;
+  std::lock_guard<std::mutex> g(g_devices_mu);
+  if (d == 0 || d > g_devices.size()) return nullptr;
+  return g_devices[d - 1];
+}
+
+// The async slot holding `ticket`, or -1 (caller holds the device lock).
+int ticket_slot(const DeviceState *ds, uint64_t ticket) {
+  const uint64_t seq = ticket & ((1ull << kTicketSeqBits) - 1);
+  for (int k = 0; k < kAsyncSlots; ++k)
+    if (ds->slots[k].pending && ds->slots[k].seq == seq) return k;
+  return -1;
+}
+
+// A free async slot for a submission, or an error (caller holds the lock).
+int take_slot(DeviceState *ds, int *k) {
+  for (int j = 0; j < kAsyncSlots; ++j)
+    if (!ds->slots[j].pending) {
+      *k = j;
+      return SV_OK;
+    }
+  return fail(SV_ERR_INVALID_ARG, "%d checks are already pending on device %d: wait for one first",
+              kAsyncSlots, ds->device);
 }
 
 // Validates the arguments of one synthesis and prepares its kernel
@@ -599,19 +750,25 @@ int sv_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype, dou
   rc = current_device(&ds);
   if (rc) return rc;
   std::lock_guard<std::mutex> lock(ds->mu);
-  CompareArgs args;
-  std::memset(&args, 0, sizeof args);
-  args.segs = nullptr;
-  args.single = make_desc(g, 0);
-  args.nseg = 1;
-  args.total_units = units_of(dtype, n);
-  uint32_t nblocks;
-  compare_grid(args.total_units, ds->cus, false, &nblocks, &args.chunk);
-  return run_compare(ds, args, nblocks, nullptr, 1, report);
+  CheckPlan plan;
+  plan_single(g, ds->cus, plan);
+  return run_sync(ds, plan, report);
 }
 
 int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports) {
   return sv_compare_batched_mode(segs, nseg, SV_CHECK_FULL, reports);
+}
+
+// Arguments of a batched check; no HIP call.
+static int check_batch(const sv_segment *segs, uint32_t nseg, int32_t mode, const char *who) {
+  if (mode != SV_CHECK_FULL && mode != SV_CHECK_STOP_AT_FIRST)
+    return fail(SV_ERR_UNSUPPORTED, "%s: unknown mode %d", who, mode);
+  if (nseg && !segs) return fail(SV_ERR_INVALID_ARG, "%s: segs is NULL", who);
+  for (uint32_t k = 0; k < nseg; ++k) {
+    int rc = check_seg(segs[k], k);
+    if (rc) return rc;
+  }
+  return SV_OK;
 }
 
 int sv_compare_batched_mode(const sv_segment *segs, uint32_t nseg, int32_t mode, sv_report *reports) {
@@ -620,38 +777,130 @@ int sv_compare_batched_mode(const sv_segment *segs, uint32_t nseg, int32_t mode,
     return fail(SV_ERR_UNSUPPORTED, "sv_compare_batched_mode: unknown mode %d", mode);
   if (nseg == 0) return SV_OK;
   if (!segs || !reports) return fail(SV_ERR_INVALID_ARG, "sv_compare_batched: segs or reports is NULL");
+  int rc = check_batch(segs, nseg, mode, "sv_compare_batched");
+  if (rc) return rc;
   uint64_t total = 0;
-  for (uint32_t k = 0; k < nseg; ++k) {
-    int rc = check_seg(segs[k], k);
-    if (rc) return rc;
-    total += units_of(segs[k].dtype, segs[k].n);
-  }
+  for (uint32_t k = 0; k < nseg; ++k) total += units_of(segs[k].dtype, segs[k].n);
   if (total == 0) {
     for (uint32_t k = 0; k < nseg; ++k) zero_report(&reports[k], 0);
     return SV_OK;
   }
   DeviceState *ds;
-  int rc = current_device(&ds);
+  rc = current_device(&ds);
   if (rc) return rc;
   std::lock_guard<std::mutex> lock(ds->mu);
-  rc = ensure_pinned(ds->h_table, ds->h_table_cap, nseg, "segment table staging");
-  if (!rc) rc = ensure_device(ds->table, ds->table_cap, nseg, "segment table");
+  CheckPlan plan;
+  plan_batched(segs, nseg, mode, ds->cus, plan);
+  return run_sync(ds, plan, reports);
+}
+
+int sv_compare_submit(const void *ref, const void *cand, uint64_t n, int32_t dtype, double rtol, double atol,
+                      int32_t equal_nan, uint64_t *ticket) {
+  t_error.clear();
+  if (!ticket) return fail(SV_ERR_INVALID_ARG, "sv_compare_submit: ticket is NULL");
+  const sv_segment g{ref, cand, n, dtype, rtol, atol, equal_nan};
+  int rc = check_seg(g, 0);
   if (rc) return rc;
-  uint64_t begin = 0;
-  for (uint32_t k = 0; k < nseg; ++k) {
-    ds->h_table[k] = make_desc(segs[k], begin);
-    begin += units_of(segs[k].dtype, segs[k].n);
+  DeviceState *ds;
+  rc = current_device(&ds);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lock(ds->mu);
+  int k;
+  rc = take_slot(ds, &k);
+  if (rc) return rc;
+  CheckPlan plan;
+  plan_single(g, ds->cus, plan);
+  rc = submit_check(ds, k, plan);
+  if (rc) {
+    ds->slots[k].pending = false;
+    return rc;
   }
-  SV_HIP(hipMemcpyAsync(ds->table, ds->h_table, nseg * sizeof(SegDesc), hipMemcpyHostToDevice, t_stream),
-         "segment table copy to device");
-  CompareArgs args;
-  std::memset(&args, 0, sizeof args);
-  args.segs = ds->table;
-  args.nseg = nseg;
-  args.total_units = total;
-  uint32_t nblocks;
-  compare_grid(total, ds->cus, true, &nblocks, &args.chunk);
-  return run_compare(ds, args, nblocks, segs, nseg, reports, mode == SV_CHECK_STOP_AT_FIRST);
+  ++ds->npending;
+  *ticket = make_ticket(ds->device, ds->slots[k].seq);
+  return SV_OK;
+}
+
+int sv_compare_batched_submit(const sv_segment *segs, uint32_t nseg, int32_t mode, uint64_t *ticket) {
+  t_error.clear();
+  if (!ticket) return fail(SV_ERR_INVALID_ARG, "sv_compare_batched_submit: ticket is NULL");
+  int rc = check_batch(segs, nseg, mode, "sv_compare_batched_submit");
+  if (rc) return rc;
+  DeviceState *ds;
+  rc = current_device(&ds);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lock(ds->mu);
+  int k;
+  rc = take_slot(ds, &k);
+  if (rc) return rc;
+  CheckPlan plan;
+  plan_batched(segs, nseg, mode, ds->cus, plan);
+  rc = submit_check(ds, k, plan);
+  if (rc) {
+    ds->slots[k].pending = false;
+    return rc;
+  }
+  ++ds->npending;
+  *ticket = make_ticket(ds->device, ds->slots[k].seq);
+  return SV_OK;
+}
+
+int sv_compare_ready(uint64_t ticket, int32_t *ready) {
+  t_error.clear();
+  if (!ready) return fail(SV_ERR_INVALID_ARG, "sv_compare_ready: ready is NULL");
+  DeviceState *ds = ticket_device(ticket);
+  if (!ds) return fail(SV_ERR_INVALID_ARG, "sv_compare_ready: ticket %#llx names no device in use",
+                       (unsigned long long)ticket);
+  std::lock_guard<std::mutex> lock(ds->mu);
+  const int k = ticket_slot(ds, ticket);
+  if (k < 0) return fail(SV_ERR_INVALID_ARG, "sv_compare_ready: ticket %#llx is not pending", (unsigned long long)ticket);
+  const CheckSlot &sl = ds->slots[k];
+  const volatile uint64_t *flag = ds->h_done + (size_t)k * kDoneStride;
+  if (!sl.launched || *flag == sl.seq) {
+    *ready = 1;
+    return SV_OK;
+  }
+  const hipError_t e = hipStreamQuery(sl.stream);
+  if (e != hipSuccess && e != hipErrorNotReady) return hip_fail(e, "sv_compare_ready");
+  if (e == hipSuccess && *flag != sl.seq)
+    return fail(SV_ERR_HIP, "the check kernel finished without writing its reports");
+  *ready = *flag == sl.seq ? 1 : 0;
+  return SV_OK;
+}
+
+int sv_compare_wait(uint64_t ticket, sv_report *reports, uint32_t nreports) {
+  t_error.clear();
+  DeviceState *ds = ticket_device(ticket);
+  if (!ds) return fail(SV_ERR_INVALID_ARG, "sv_compare_wait: ticket %#llx names no device in use",
+                       (unsigned long long)ticket);
+  int k;
+  uint64_t seq;
+  bool launched;
+  hipStream_t st;
+  {
+    std::lock_guard<std::mutex> lock(ds->mu);
+    k = ticket_slot(ds, ticket);
+    if (k < 0 || ds->slots[k].waiting)
+      return fail(SV_ERR_INVALID_ARG, "sv_compare_wait: ticket %#llx is not pending (already waited for?)",
+                  (unsigned long long)ticket);
+    CheckSlot &sl = ds->slots[k];
+    if (nreports != sl.lengths.size())
+      return fail(SV_ERR_INVALID_ARG, "sv_compare_wait: the check has %zu reports, nreports = %u",
+                  sl.lengths.size(), nreports);
+    if (nreports && !reports) return fail(SV_ERR_INVALID_ARG, "sv_compare_wait: reports is NULL");
+    sl.waiting = true;
+    seq = sl.seq;
+    launched = sl.launched;
+    st = sl.stream;
+  }
+  // the slot stays pending (not reusable) while this thread spins unlocked
+  const int rc = launched ? wait_done(ds->h_done + (size_t)k * kDoneStride, seq, st) : SV_OK;
+  std::lock_guard<std::mutex> lock(ds->mu);
+  CheckSlot &sl = ds->slots[k];
+  if (!rc) finish_check(sl, reports);
+  sl.pending = false;
+  sl.waiting = false;
+  --ds->npending;
+  return rc;
 }
 
 int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_perturb_plan *plan, uint64_t n,
@@ -779,8 +1028,14 @@ int sv_shutdown(void) {
     if (s->partials) (void)hipFree(s->partials);
     if (s->table) (void)hipFree(s->table);
     if (s->idx) (void)hipFree(s->idx);
-    if (s->h_table) (void)hipHostFree(s->h_table);
-    if (s->h_reports) (void)hipHostFree(s->h_reports);
+    for (CheckSlot &sl : s->slots) {
+      if (sl.h_reports) (void)hipHostFree(sl.h_reports);
+      if (sl.h_table) (void)hipHostFree(sl.h_table);
+      sl = CheckSlot();
+    }
+    s->npending = 0;
+    s->has_last = false;
+    s->last_stream = nullptr;
     if (s->h_idx) (void)hipHostFree(s->h_idx);
     if (s->synth_table) (void)hipFree(s->synth_table);
     if (s->h_synth) (void)hipHostFree(s->h_synth);
@@ -794,9 +1049,9 @@ int sv_shutdown(void) {
     s->synth_table_cap = s->h_synth_cap = 0;
     s->synth_pending = false;
     s->partials = nullptr; s->table = nullptr; s->idx = nullptr;
-    s->h_table = nullptr; s->h_reports = nullptr; s->d_reports = nullptr; s->h_idx = nullptr;
+    s->h_idx = nullptr;
     s->partials_cap = s->table_cap = s->idx_cap = 0;
-    s->h_table_cap = s->h_reports_cap = s->h_idx_cap = 0;
+    s->h_idx_cap = 0;
   }
   perf_shutdown();
   files_shutdown();

@@ -50,6 +50,7 @@ def test_abi_version_and_enums_match_header(svlib):
         assert re.search(r"\b%s = %d\b" % (name, code), src), name
     import oracle
     assert oracle.DTYPES == svlib.DTYPE_CODES
+    assert re.search(r"#define SV_MAX_PENDING_CHECKS %d\b" % svlib.SV_MAX_PENDING_CHECKS, src)
 
 
 def test_struct_layouts_match_the_c_compiler(svlib, tmp_path):
@@ -155,6 +156,32 @@ def test_batched_argument_errors_and_empty(svlib):
     segs[1] = svlib.Segment(0x1000, None, 8, 0, 1e-5, 1e-8, 0)
     assert L.sv_compare_batched(segs, 3, reps) == svlib.SV_ERR_INVALID_ARG
     assert "segment 1" in L.sv_last_error().decode()
+
+
+def test_async_check_argument_errors_without_a_device(svlib):
+    L = svlib.lib()
+    INV, UNS = svlib.SV_ERR_INVALID_ARG, svlib.SV_ERR_UNSUPPORTED
+    t = ctypes.c_uint64(0)
+    r = ctypes.c_int32(0)
+    reps = (svlib.Report * 2)()
+    assert L.sv_compare_submit(0x1000, 0x2000, 4, 0, 1e-5, 1e-8, 0, None) == INV
+    assert L.sv_compare_submit(0, 0x2000, 4, 0, 1e-5, 1e-8, 0, ctypes.byref(t)) == INV
+    assert L.sv_compare_submit(0x1000, 0x2000, 4, 0, -1.0, 0.0, 0, ctypes.byref(t)) == INV
+    assert L.sv_compare_submit(0x1000, 0x2000, 4, 7, 0.0, 0.0, 0, ctypes.byref(t)) == UNS
+    segs = (svlib.Segment * 2)()
+    segs[0] = svlib.Segment(None, None, 0, 0, 1e-5, 1e-8, 0)
+    segs[1] = svlib.Segment(0x1000, None, 8, 0, 1e-5, 1e-8, 0)
+    assert L.sv_compare_batched_submit(segs, 2, 0, None) == INV
+    assert L.sv_compare_batched_submit(None, 2, 0, ctypes.byref(t)) == INV
+    assert L.sv_compare_batched_submit(segs, 2, 5, ctypes.byref(t)) == UNS
+    assert L.sv_compare_batched_submit(segs, 2, 0, ctypes.byref(t)) == INV
+    assert "segment 1" in L.sv_last_error().decode()
+    # tickets that name no device in use, or no device at all
+    for bad in (0, 5, (200 << 56) | 3):
+        assert L.sv_compare_ready(bad, ctypes.byref(r)) == INV
+        assert L.sv_compare_wait(bad, reps, 1) == INV
+        assert "ticket" in L.sv_last_error().decode()
+    assert L.sv_compare_ready(1 << 56, None) == INV
 
 
 def test_perturb_argument_errors(svlib):

@@ -1,0 +1,145 @@
+"""Submitted checks (sv_compare_submit / sv_compare_batched_submit / sv_compare_wait):
+the reports equal those of the synchronous calls, whatever the order of the
+waits, the number pending, the streams used, and reallocations of the shared
+scratch while checks are pending.  One case is also held against the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_00058_amd as sv
+from gpu_run import bits, empty
+
+pytestmark = pytest.mark.gpu
+
+NORMAL = dict(mean=0.0, std=1.0)
+
+
+def _pair(n, seed, p=1e-3, dtype="f32"):
+    ref = empty(n, dtype)
+    sv.synth(ref, seed, 1, "normal", **NORMAL)
+    cand = empty(n, dtype)
+    sv.perturb(ref, cand, seed, 2, "ulp", p=p)
+    return ref, cand
+
+
+def test_submit_and_wait_in_any_order_match_sync():
+    pairs = [_pair(n, k) for k, n in enumerate([1, 5, 4099, 65543, (1 << 20) + 3, 1 << 22])]
+    want = [sv.compare(r, c, 1e-8, 0.0) for r, c in pairs]
+    print("async submit order", flush=True)
+    tickets = [sv.compare_submit(r, c, 1e-8, 0.0) for r, c in pairs]
+    for k in (3, 0, 5, 1, 4, 2):             # waits out of submission order
+        assert tickets[k].wait() == want[k]
+    assert all(t.ready() for t in tickets)
+    assert any(w["mismatches"] > 0 for w in want)
+
+
+def test_async_report_matches_the_oracle(oracle):
+    n = 70001
+    ref, cand = _pair(n, 9, p=0.01)
+    print("async vs oracle", flush=True)
+    got = sv.compare_submit(ref, cand, 1e-8, 1e-9).wait()
+    want = oracle.compare(bits(ref), bits(cand), "f32", 1e-8, 1e-9, False)
+    assert got["mismatches"] == want["mismatches"] and got["first_mismatch"] == want["first_mismatch"]
+    assert got["max_abs_err"] == want["max_abs_err"] and got["max_rel_err"] == want["max_rel_err"]
+    assert abs(got["err_sum"] - want["err_sum"]) <= 1e-12 * want["err_sum"]
+
+
+def test_pipelined_synthesis_and_checks_reuse_one_reference_buffer():
+    # step k: synthesize reference k into the same buffer, submit its check,
+    # then wait for step k - 1 (the buffer is overwritten behind a pending check)
+    n = 1 << 22
+    cand = empty(n, "f32")
+    sv.synth(cand, 0, 1, "normal", **NORMAL)
+    want = []
+    for k in range(12):
+        r = empty(n, "f32")
+        sv.synth(r, k % 3, 1, "normal", **NORMAL)    # seed 0 matches cand exactly
+        want.append(sv.compare(r, cand, 1e-3, 0.0))
+    ref = empty(n, "f32")
+    got, prev = [], None
+    print("pipelined steps", flush=True)
+    for k in range(12):
+        sv.synth(ref, k % 3, 1, "normal", **NORMAL)
+        t = sv.compare_submit(ref, cand, 1e-3, 0.0)
+        if prev is not None:
+            got.append(prev.wait())
+        prev = t
+    got.append(prev.wait())
+    assert got == want
+    assert want[0]["mismatches"] == 0 and want[1]["mismatches"] > 0
+
+
+def test_batched_submit_both_modes():
+    segs = []
+    for k, n in enumerate([0, 17, 4099, 1 << 20, 3, 65536]):
+        r, c = _pair(n, 20 + k, p=0.01 if k % 2 else 0.0)
+        segs.append((r, c, 1e-8, 0.0, False))
+    for stop in (False, True):
+        want = sv.compare_batched(segs, stop_at_first=stop)
+        print("batched submit stop=%s" % stop, flush=True)
+        t = sv.compare_batched_submit(segs, stop_at_first=stop)
+        assert t.wait() == want
+
+
+def test_pending_limit_double_wait_and_wrong_count():
+    ref, cand = _pair(4096, 3)
+    want = sv.compare(ref, cand, 1e-8, 0.0)
+    print("pending limit", flush=True)
+    tickets = [sv.compare_submit(ref, cand, 1e-8, 0.0) for _ in range(sv.SV_MAX_PENDING_CHECKS)]
+    with pytest.raises(sv.SVError) as e:
+        sv.compare_submit(ref, cand, 1e-8, 0.0)
+    assert e.value.code == sv.SV_ERR_INVALID_ARG and "pending" in str(e.value)
+    # a synchronous call still works with every submission slot taken
+    assert sv.compare(ref, cand, 1e-8, 0.0) == want
+    L = sv.lib()
+    reps = (sv.Report * 2)()
+    assert L.sv_compare_wait(tickets[0].ticket, reps, 2) == sv.SV_ERR_INVALID_ARG   # wrong count: stays pending
+    assert tickets[0].wait() == want
+    assert L.sv_compare_wait(tickets[0].ticket, reps, 1) == sv.SV_ERR_INVALID_ARG   # already waited for
+    extra = sv.compare_submit(ref, cand, 1e-8, 0.0)                               # one slot free again
+    for t in tickets[1:] + [extra]:
+        assert t.wait() == want
+
+
+def test_empty_submissions_are_ready_at_once():
+    z = empty(0, "f32")
+    print("empty submit", flush=True)
+    t = sv.compare_submit(z, z, 1e-8, 0.0)
+    assert t.ready()
+    assert t.wait() == {**sv.compare(z, z, 1e-8, 0.0)}
+    t = sv.compare_batched_submit([(z, z, 1e-8, 0.0, False)] * 3)
+    assert t.ready() and len(t.wait()) == 3
+
+
+def test_checks_on_two_streams_and_sync_calls_between():
+    a = _pair(1 << 21, 40, p=0.02)
+    b = _pair(1 << 20, 41, p=0.0)
+    want_a, want_b = sv.compare(*a, 1e-8, 0.0), sv.compare(*b, 1e-8, 0.0)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    print("two streams", flush=True)
+    with torch.cuda.stream(s1):
+        t1 = sv.compare_submit(*a, 1e-8, 0.0)
+    with torch.cuda.stream(s2):
+        t2 = sv.compare_submit(*b, 1e-8, 0.0)
+        assert sv.compare(*a, 1e-8, 0.0) == want_a
+        t3 = sv.compare_submit(*a, 1e-8, 0.0)
+    assert sv.compare(*b, 1e-8, 0.0) == want_b    # current (default) stream
+    assert t3.wait() == want_a and t2.wait() == want_b and t1.wait() == want_a
+    torch.cuda.synchronize()
+
+
+def test_scratch_grows_while_checks_are_pending():
+    small = [(*_pair(1000 + k, 50 + k), 1e-8, 0.0, False) for k in range(2)]
+    want_small = sv.compare_batched(small)
+    r, c = _pair(4096, 60)
+    print("growth while pending", flush=True)
+    t1 = sv.compare_batched_submit(small)
+    many = [(r, c, 1e-8, 0.0, False)] * 20000     # more segments (and partials) than held so far
+    t2 = sv.compare_batched_submit(many)
+    t3 = sv.compare_batched_submit(small)
+    want_one = sv.compare(r, c, 1e-8, 0.0)
+    assert t1.wait() == want_small
+    assert all(x == want_one for x in t2.wait())
+    assert t3.wait() == want_small
