@@ -61,6 +61,7 @@ template <> struct Elem<SV_F64> { static constexpr int V = 2, G = 2; };
 template <> struct Elem<SV_I64> { static constexpr int V = 2, G = 2; };
 
 template <int DT> constexpr bool kIntType = DT == SV_I32 || DT == SV_U8 || DT == SV_I64;
+template <int DT> constexpr bool kSmallInt = DT == SV_I32 || DT == SV_U8;   // |a - y| fits 32 bits
 template <int DT> constexpr bool kWideType = DT == SV_F64 || DT == SV_I64;   // 64-bit elements
 
 // Element j of a 16-byte unit, for the types up to 32 bits: fp32 bits (bf16
@@ -121,6 +122,9 @@ __device__ __forceinline__ void put_elem(u32x4 &v, int j, uint64_t b) {
 
 struct LaneAcc {
   double maxabs, maxrel, mrc, sum;   // mrc = maxrel (1 - 2^-50): the division filter
+  uint64_t isum;                     // int32 / uint8: exact sum of |a - y| since the last fold into sum
+  uint32_t imax;                     // int32 / uint8: max |a - y|
+  uint32_t rd, ry;                   // int32 / uint8: max d / |y| as the exact ratio rd / ry (ry = 0: +Inf)
 };
 
 struct WaveAcc {                      // wave-uniform
@@ -222,6 +226,52 @@ __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, in
   }
 }
 
+// Elements G g .. G g + G - 1 of a unit of int32 or uint8 elements.  Eq. (1)
+// is plain equality for integers, and d = |a - y| < 2^32 is exact in 32
+// bits, so the decision, the sum (exact, folded into the fp64 sum once per
+// tile), the maximum and the largest d / |y| need no floating point: the
+// ratio is kept exactly as rd / ry and compared by cross-multiplication
+// (d ry > rd |y|, products below 2^63); starting from 0 / 1, a d > 0 at y = 0
+// makes it +Inf (ry = 0), which nothing then beats.  Rounding being
+// monotone, the one fp64 division at the end gives the largest of the
+// rounded quotients.
+template <int DT>
+__device__ __forceinline__ void check_group_int(const u32x4 &yv, const u32x4 &av, int g, LaneAcc &L,
+                                                uint64_t *bad) {
+  constexpr int G = Elem<DT>::G;
+  uint32_t gsum = 0;                 // uint8: the group's sum, at most 4 * 255
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    const int e = G * g + j;
+    uint32_t d, ay;
+    bool beats;
+    if constexpr (DT == SV_I32) {
+      const int32_t yi = (int32_t)yv[e], ai = (int32_t)av[e];
+      d = ai >= yi ? (uint32_t)ai - (uint32_t)yi : (uint32_t)yi - (uint32_t)ai;
+      ay = yi < 0 ? 0u - (uint32_t)yi : (uint32_t)yi;
+      L.isum += d;
+      beats = (uint64_t)d * L.ry > (uint64_t)L.rd * ay;
+    } else {
+      const uint32_t yb = elem_bits<DT>(yv, e), ab = elem_bits<DT>(av, e);
+      d = ab >= yb ? ab - yb : yb - ab;
+      ay = yb;
+      gsum += d;
+      beats = d * L.ry > L.rd * ay;  // products below 2^16
+    }
+    bad[j] = __ballot(d != 0);
+    L.imax = d > L.imax ? d : L.imax;
+    L.rd = beats ? d : L.rd;
+    L.ry = beats ? ay : L.ry;
+  }
+  if constexpr (DT == SV_U8) L.isum += gsum;
+}
+
+// Folds the exact integer sum into the fp64 sum.
+__device__ __forceinline__ void fold_int_sum(LaneAcc &L) {
+  L.sum += (double)L.isum;
+  L.isum = 0;
+}
+
 // One unit: its groups, then the mismatch count and, for the first
 // mismatching unit a wave sees, the smallest mismatching index.
 template <int DT>
@@ -229,9 +279,19 @@ __device__ __forceinline__ void check_unit(const u32x4 &yv, const u32x4 &av, uin
                                            double atol, bool eqn, LaneAcc &L, WaveAcc &W) {
   constexpr int V = Elem<DT>::V;
   constexpr int G = Elem<DT>::G;
+  if constexpr (kIntType<DT>) {
+    // every lane's unit bitwise equal: every d is 0 and nothing is counted
+    const bool same = yv[0] == av[0] && yv[1] == av[1] && yv[2] == av[2] && yv[3] == av[3];
+    if (__ballot(!same) == 0) return;
+  }
   uint64_t bad[V];                   // wave masks, kept in scalar registers
 #pragma unroll
-  for (int g = 0; g < V / G; ++g) check_group<DT>(yv, av, g, rtol, atol, eqn, L, W, bad + G * g);
+  for (int g = 0; g < V / G; ++g) {
+    if constexpr (kSmallInt<DT>)
+      check_group_int<DT>(yv, av, g, L, bad + G * g);
+    else
+      check_group<DT>(yv, av, g, rtol, atol, eqn, L, W, bad + G * g);
+  }
   uint64_t any = 0;
 #pragma unroll
   for (int j = 0; j < V; ++j) any |= bad[j];
@@ -386,7 +446,7 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
   const uint64_t n = sd.n;
   // units below full_end are whole and 16-byte loadable
   const uint64_t full_end = sd.vec_ok ? (uhi < n / V ? uhi : n / V) : 0;
-  LaneAcc L{0.0, 0.0, 0.0, 0.0};
+  LaneAcc L{0.0, 0.0, 0.0, 0.0, 0, 0, 0, 1};
   WaveAcc W{0, kNone, 0, 0, 0, 0};
   uint64_t base = ulo + wave * kWave;
   // whole tiles: kUnroll sub-iterations of kBlock units, every unit full
@@ -402,6 +462,7 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k)
       check_unit<DT>(yv[k], av[k], (base + (uint64_t)k * kBlock) * V, rtol, atol, eqn, L, W);
+    if constexpr (kSmallInt<DT>) fold_int_sum(L);
   }
   // the rest, one sub-iteration at a time, guarded (same unit order)
   for (; base < uhi; base += kBlock) {
@@ -422,6 +483,11 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
       }
     }
     check_unit<DT>(yv, av, base * V, rtol, atol, eqn, L, W);
+    if constexpr (kSmallInt<DT>) fold_int_sum(L);
+  }
+  if constexpr (kSmallInt<DT>) {
+    L.maxabs = (double)L.imax;
+    L.maxrel = L.rd == 0 ? 0.0 : (L.ry == 0 ? __builtin_inf() : (double)L.rd / (double)L.ry);
   }
   // lanes -> wave -> workgroup
   lane_step<0>(L);

@@ -166,3 +166,49 @@ def test_uint8_files_are_read_as_bytes(oracle, tmp_path):
     rep = sv.compare_file(rp, cp, n, "u8", 0.0, 0.0)
     same_report(rep, oracle.compare(y, a, "u8", 0.0, 0.0, False))
     assert rep["mismatches"] == 2 and rep["first_mismatch"] == 10
+
+
+def _int_cases(rng, n):
+    """(name, dtype, y, a): integer pairs that differ almost everywhere, with and
+    without zeros in y, and int32 values at the ends of the range."""
+    yu = rng.integers(1, 256, n).astype(np.uint8)
+    au = rng.integers(0, 256, n).astype(np.uint8)
+    yz = yu.copy()
+    yz[rng.random(n) < 0.02] = 0
+    ext = np.array([-2 ** 31, 2 ** 31 - 1, -1, 1, 2, -2, 2 ** 30, -2 ** 30 - 7], np.int64)
+    yi = rng.choice(ext, n).astype(np.int32)
+    yi[yi == 0] = 3
+    ai = rng.choice(ext, n).astype(np.int32)
+    yi0 = yi.copy()
+    yi0[rng.random(n) < 0.01] = 0
+    one = yi.copy()
+    one[-1] ^= 1
+    return [("u8 no zeros", "u8", yu, au), ("u8 zeros", "u8", yz, au),
+            ("i32 extremes", "i32", yi.view(np.uint32), ai.view(np.uint32)),
+            ("i32 extremes zeros", "i32", yi0.view(np.uint32), ai.view(np.uint32)),
+            ("i32 one mismatch", "i32", yi.view(np.uint32), one.view(np.uint32))]
+
+
+def test_integer_checks_every_field_against_the_oracle(oracle):
+    rng = np.random.default_rng(91)
+    segs, want, keep = [], [], []
+    for n in (1, 17, 70001, (1 << 20) + 3):
+        for name, dtype, y, a in _int_cases(rng, n):
+            print("integer check", name, n, flush=True)
+            Y, A = dev_bits(y, dtype), dev_bits(a, dtype)
+            w = oracle.compare(y, a, dtype, 0.0, 0.0, False)
+            same_report(sv.compare(Y, A, 0.0, 0.0), w)
+            if n > 17:
+                same_report(sv.compare(Y[3:], A[3:], 0.0, 0.0), oracle.compare(y[3:], a[3:], dtype, 0.0, 0.0, False))
+                keep += [Y, A]
+                segs.append((Y, A, 0.0, 0.0, False))
+                want.append(w)
+            if name == "u8 no zeros" and n > 17:
+                assert 0 < w["max_rel_err"] < np.inf
+            if name == "u8 zeros" and n > 17:
+                assert w["max_rel_err"] == np.inf
+            if name == "i32 extremes" and n > 17:
+                assert w["max_abs_err"] == 2.0 ** 32 - 1 and 0 < w["max_rel_err"] < np.inf
+    print("integer check batched", len(segs), flush=True)
+    for got, w in zip(sv.compare_batched(segs), want):
+        same_report(got, w)
