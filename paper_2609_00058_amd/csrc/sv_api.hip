@@ -451,8 +451,11 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
     const uint64_t n = batched ? plan.segs[j].n : args.single.n;
     if (n) mask |= 1u << (batched ? plan.segs[j].dtype : args.single.dtype);
   }
-  hipError_t e = launch_compare(args, plan.nblocks, mask, st, e0 ? e1 : nullptr);
+  hipError_t e = launch_compare(args, plan.nblocks, mask, st);
   if (e != hipSuccess) return hip_fail(e, "check kernel launch");
+  if (e1) (void)hipEventRecord(e1, st);
+  e = launch_finalize(args, st);
+  if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
   ds->seq = args.seq;
   ds->has_last = true;
   ds->last_stream = st;

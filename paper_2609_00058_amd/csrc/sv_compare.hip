@@ -409,14 +409,18 @@ __device__ __forceinline__ void report_words(const Partial &r, uint64_t n, uint6
 constexpr int kReportWords = 10;
 
 // Called by one thread of every finalize workgroup once its report (if any)
-// is written: the last to arrive clears the counter and, after every store
-// before it has landed, hands the sequence number to the host.
+// is written and has landed (each workgroup waits for its own stores before
+// it arrives): the last to arrive clears the counter and hands the sequence
+// number to the host.  A lone workgroup needs no counter.  The counter's
+// reset need not land before the sequence number: the next launch that uses
+// it starts after this kernel has ended.
 __device__ __forceinline__ void arrive_and_signal(const CompareArgs &args) {
   wait_memory();
-  if (__hip_atomic_fetch_add(args.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != gridDim.x - 1)
-    return;
-  __hip_atomic_store(args.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  wait_memory();
+  if (gridDim.x > 1) {
+    if (__hip_atomic_fetch_add(args.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != gridDim.x - 1)
+      return;
+    __hip_atomic_store(args.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   __hip_atomic_store(args.done, args.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
@@ -612,39 +616,40 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(CompareArgs args) {
 }
 
 template <int kMask>
-static void launch_masked(const CompareArgs &args, uint32_t nblocks, hipStream_t stream, hipEvent_t ev_mid) {
-  const bool single = args.segs == nullptr;
-  if (single)
+static void launch_masked(const CompareArgs &args, uint32_t nblocks, hipStream_t stream) {
+  if (args.segs == nullptr)
     hipLaunchKernelGGL((compare_kernel<true, kMask>), dim3(nblocks), dim3(kBlock), 0, stream, args);
   else if (args.stop_at_first)
     hipLaunchKernelGGL((compare_kernel<false, kMask, true>), dim3(nblocks), dim3(kBlock), 0, stream, args);
   else
     hipLaunchKernelGGL((compare_kernel<false, kMask>), dim3(nblocks), dim3(kBlock), 0, stream, args);
-  if (ev_mid) (void)hipEventRecord(ev_mid, stream);
-  if (single)
-    hipLaunchKernelGGL(finalize_kernel<true>, dim3(1), dim3(kFinBlock), 0, stream, args);
-  else
-    hipLaunchKernelGGL(finalize_kernel<false>, dim3(args.nseg), dim3(kFinBlock), 0, stream, args);
 }
 
 // Kernels exist for each type alone, for the mixes of fp32 / bf16 / int32 the
 // batched workloads use, and one for any other mix.
-hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream,
-                          hipEvent_t ev_mid) {
+hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream) {
   switch (dtype_mask) {
-    case 1 << SV_F32: launch_masked<1 << SV_F32>(args, nblocks, stream, ev_mid); break;
-    case 1 << SV_BF16: launch_masked<1 << SV_BF16>(args, nblocks, stream, ev_mid); break;
-    case 1 << SV_I32: launch_masked<1 << SV_I32>(args, nblocks, stream, ev_mid); break;
-    case 1 << SV_F16: launch_masked<1 << SV_F16>(args, nblocks, stream, ev_mid); break;
-    case 1 << SV_F64: launch_masked<1 << SV_F64>(args, nblocks, stream, ev_mid); break;
-    case 1 << SV_U8: launch_masked<1 << SV_U8>(args, nblocks, stream, ev_mid); break;
-    case 1 << SV_I64: launch_masked<1 << SV_I64>(args, nblocks, stream, ev_mid); break;
-    case 3: launch_masked<3>(args, nblocks, stream, ev_mid); break;
-    case 5: launch_masked<5>(args, nblocks, stream, ev_mid); break;
-    case 6: launch_masked<6>(args, nblocks, stream, ev_mid); break;
-    case 7: launch_masked<7>(args, nblocks, stream, ev_mid); break;
-    default: launch_masked<0x7F>(args, nblocks, stream, ev_mid); break;
+    case 1 << SV_F32: launch_masked<1 << SV_F32>(args, nblocks, stream); break;
+    case 1 << SV_BF16: launch_masked<1 << SV_BF16>(args, nblocks, stream); break;
+    case 1 << SV_I32: launch_masked<1 << SV_I32>(args, nblocks, stream); break;
+    case 1 << SV_F16: launch_masked<1 << SV_F16>(args, nblocks, stream); break;
+    case 1 << SV_F64: launch_masked<1 << SV_F64>(args, nblocks, stream); break;
+    case 1 << SV_U8: launch_masked<1 << SV_U8>(args, nblocks, stream); break;
+    case 1 << SV_I64: launch_masked<1 << SV_I64>(args, nblocks, stream); break;
+    case 3: launch_masked<3>(args, nblocks, stream); break;
+    case 5: launch_masked<5>(args, nblocks, stream); break;
+    case 6: launch_masked<6>(args, nblocks, stream); break;
+    case 7: launch_masked<7>(args, nblocks, stream); break;
+    default: launch_masked<0x7F>(args, nblocks, stream); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize(const CompareArgs &args, hipStream_t stream) {
+  if (args.segs == nullptr)
+    hipLaunchKernelGGL(finalize_kernel<true>, dim3(1), dim3(kFinBlock), 0, stream, args);
+  else
+    hipLaunchKernelGGL(finalize_kernel<false>, dim3(args.nseg), dim3(kFinBlock), 0, stream, args);
   return hipGetLastError();
 }
 

@@ -141,9 +141,9 @@ __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
   return (n + per - 1) / per;
 }
 
-// dtype_mask: OR of (1 << dtype) over the segments with elements
-// ev_mid (optional) is recorded between the check kernel and its finalize kernel.
-hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream,
-                          hipEvent_t ev_mid);
+// The check kernel (dtype_mask: OR of (1 << dtype) over the segments with
+// elements), and the finalize kernel that turns its partials into reports.
+hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream);
+hipError_t launch_finalize(const CompareArgs &args, hipStream_t stream);
 
 }  // namespace sv
