@@ -334,7 +334,7 @@ void zero_report(sv_report *r, uint64_t n) {
 // grid for a check over `units` 16-byte units: at most SV_CMP_BLOCKS_PER_CU
 // workgroups per CU, each owning whole waves of units
 void compare_grid(uint64_t units, int cus, bool batched, uint32_t *nblocks, uint64_t *chunk) {
-  const uint64_t per_iter = (uint64_t)kBlock;
+  const uint64_t per_iter = (uint64_t)kCmpBlock;
   const uint64_t per_cu = batched ? SV_CMP_BATCH_BLOCKS_PER_CU : SV_CMP_BLOCKS_PER_CU;
   uint64_t nb = std::min<uint64_t>((units + per_iter - 1) / per_iter, (uint64_t)cus * per_cu);
   if (nb == 0) nb = 1;

@@ -48,7 +48,7 @@
 namespace sv {
 
 constexpr int kUnroll = SV_CMP_UNROLL;   // units per thread in flight
-constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kWavesPerBlock = kCmpBlock / kWave;
 
 // V elements per 16-byte unit, checked in groups of G.
 template <int DT> struct Elem;
@@ -453,23 +453,23 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
   LaneAcc L{0.0, 0.0, 0.0, 0.0, 0, 0, 0, 1};
   WaveAcc W{0, kNone, 0, 0, 0, 0};
   uint64_t base = ulo + wave * kWave;
-  // whole tiles: kUnroll sub-iterations of kBlock units, every unit full
-  for (; base + (uint64_t)(kUnroll - 1) * kBlock + kWave <= full_end; base += (uint64_t)kBlock * kUnroll) {
+  // whole tiles: kUnroll sub-iterations of kCmpBlock units, every unit full
+  for (; base + (uint64_t)(kUnroll - 1) * kCmpBlock + kWave <= full_end; base += (uint64_t)kCmpBlock * kUnroll) {
     if (kStop && base * V > W.first) break;
     u32x4 yv[kUnroll], av[kUnroll];
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k) {
-      const uint64_t u = base + (uint64_t)k * kBlock + lane;
+      const uint64_t u = base + (uint64_t)k * kCmpBlock + lane;
       yv[k] = __builtin_nontemporal_load(yv4 + u);
       av[k] = __builtin_nontemporal_load(av4 + u);
     }
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k)
-      check_unit<DT>(yv[k], av[k], (base + (uint64_t)k * kBlock) * V, rtol, atol, eqn, L, W);
+      check_unit<DT>(yv[k], av[k], (base + (uint64_t)k * kCmpBlock) * V, rtol, atol, eqn, L, W);
     if constexpr (kSmallInt<DT>) fold_int_sum(L);
   }
   // the rest, one sub-iteration at a time, guarded (same unit order)
-  for (; base < uhi; base += kBlock) {
+  for (; base < uhi; base += kCmpBlock) {
     if (kStop && base * V > W.first) break;
     const uint64_t u = base + lane;
     u32x4 yv = u32x4{0, 0, 0, 0}, av = u32x4{0, 0, 0, 0};
@@ -593,7 +593,7 @@ __device__ __forceinline__ Partial check_any(const SegDesc &sd, uint64_t ulo, ui
 }
 
 template <bool kSingle, int kMask, bool kStop = false>
-__global__ __launch_bounds__(kBlock) void compare_kernel(CompareArgs args) {
+__global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
   __shared__ Partial lds[kWavesPerBlock];
   const uint64_t b = blockIdx.x;
   uint64_t lo = b * args.chunk;
@@ -618,11 +618,11 @@ __global__ __launch_bounds__(kBlock) void compare_kernel(CompareArgs args) {
 template <int kMask>
 static void launch_masked(const CompareArgs &args, uint32_t nblocks, hipStream_t stream) {
   if (args.segs == nullptr)
-    hipLaunchKernelGGL((compare_kernel<true, kMask>), dim3(nblocks), dim3(kBlock), 0, stream, args);
+    hipLaunchKernelGGL((compare_kernel<true, kMask>), dim3(nblocks), dim3(kCmpBlock), 0, stream, args);
   else if (args.stop_at_first)
-    hipLaunchKernelGGL((compare_kernel<false, kMask, true>), dim3(nblocks), dim3(kBlock), 0, stream, args);
+    hipLaunchKernelGGL((compare_kernel<false, kMask, true>), dim3(nblocks), dim3(kCmpBlock), 0, stream, args);
   else
-    hipLaunchKernelGGL((compare_kernel<false, kMask>), dim3(nblocks), dim3(kBlock), 0, stream, args);
+    hipLaunchKernelGGL((compare_kernel<false, kMask>), dim3(nblocks), dim3(kCmpBlock), 0, stream, args);
 }
 
 // Kernels exist for each type alone, for the mixes of fp32 / bf16 / int32 the

@@ -13,8 +13,11 @@ namespace sv {
 #ifndef SV_CMP_UNROLL
 #define SV_CMP_UNROLL 4              // 16-byte units per thread in flight in the check
 #endif
+#ifndef SV_CMP_BLOCK
+#define SV_CMP_BLOCK 512             // threads per check workgroup
+#endif
 #ifndef SV_CMP_BLOCKS_PER_CU
-#define SV_CMP_BLOCKS_PER_CU 16      // check workgroups per CU, single tensor
+#define SV_CMP_BLOCKS_PER_CU 8       // check workgroups per CU, single tensor
 #endif
 #ifndef SV_CMP_BATCH_BLOCKS_PER_CU
 #define SV_CMP_BATCH_BLOCKS_PER_CU 12   // check workgroups per CU, batched
@@ -27,6 +30,7 @@ namespace sv {
 #endif
 
 constexpr int kBlock = 256;          // threads per workgroup of every streaming kernel
+constexpr int kCmpBlock = SV_CMP_BLOCK;   // threads per workgroup of the check kernel
 constexpr int kWave = 64;            // CDNA wavefront
 constexpr uint64_t kNone = ~0ull;    // "no mismatch yet"
 
