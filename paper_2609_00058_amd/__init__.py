@@ -234,15 +234,30 @@ def compare_file(ref_path: str, cand_path: str, n: int, dtype: str, rtol: float,
     return r.as_dict()
 
 
+class SynthBatch:
+    """The jobs of synth_batched() marshalled once, for a batch synthesized
+    again and again: pass it to synth_batched() in place of the list.  It
+    keeps its output tensors alive."""
+
+    def __init__(self, jobs):
+        if not jobs:
+            raise SVError(SV_ERR_INVALID_ARG, "SynthBatch: no jobs")
+        self.arr = (SynthJob * len(jobs))()
+        for k, (out, seed, stream_id, dist, params) in enumerate(jobs):
+            self.arr[k] = SynthJob(seed, stream_id, dtype_code(out), DIST_CODES[dist], dist_params(**params),
+                                   out.numel(), _dev_ptr(out, "out") if out.numel() else None)
+        self.n = len(jobs)
+        self.outs = [j[0] for j in jobs]
+
+
 def synth_batched(jobs):
-    """jobs: list of (out, seed, stream_id, dist, params dict); one launch (asynchronous)."""
-    if not jobs:
-        return
-    arr = (SynthJob * len(jobs))()
-    for k, (out, seed, stream_id, dist, params) in enumerate(jobs):
-        arr[k] = SynthJob(seed, stream_id, dtype_code(out), DIST_CODES[dist], dist_params(**params),
-                          out.numel(), _dev_ptr(out, "out") if out.numel() else None)
-    _run(jobs[0][0], _lib.sv_synth_batched, arr, len(jobs))
+    """jobs: list of (out, seed, stream_id, dist, params dict), or a SynthBatch;
+    one launch (asynchronous)."""
+    if not isinstance(jobs, SynthBatch):
+        if not jobs:
+            return
+        jobs = SynthBatch(jobs)
+    _run(jobs.outs[0], _lib.sv_synth_batched, jobs.arr, jobs.n)
 
 
 def compare(ref, cand, rtol: float, atol: float, equal_nan: bool = False) -> dict:
@@ -266,17 +281,35 @@ def _segment_array(segments):
     return arr
 
 
+class SegmentBatch:
+    """The segments of compare_batched() marshalled once, for a batch checked
+    again and again: pass it in place of the list to compare_batched() or
+    compare_batched_submit().  It keeps its tensors alive."""
+
+    def __init__(self, segments):
+        if not segments:
+            raise SVError(SV_ERR_INVALID_ARG, "SegmentBatch: no segments")
+        self.arr = _segment_array(segments)
+        self.n = len(segments)
+        self.tensors = [s[:2] for s in segments]
+
+
+def _as_batch(segments):
+    return segments if isinstance(segments, SegmentBatch) else SegmentBatch(segments)
+
+
 def compare_batched(segments, stop_at_first: bool = False) -> list:
-    """segments: list of (ref, cand, rtol, atol, equal_nan); one launch, one report each.
+    """segments: list of (ref, cand, rtol, atol, equal_nan), or a SegmentBatch;
+    one launch, one report each.
     stop_at_first: a failing segment is checked only as far as needed to know
     its first mismatch exactly; its report then holds n, mismatches = 1 and
     first_mismatch, everything else 0."""
-    if not segments:
+    if not isinstance(segments, SegmentBatch) and not segments:
         return []
-    arr = _segment_array(segments)
-    reps = (Report * len(segments))()
-    _run(segments[0][0], _lib.sv_compare_batched_mode, arr, len(segments), 1 if stop_at_first else 0, reps)
-    return [reps[k].as_dict() for k in range(len(segments))]
+    b = _as_batch(segments)
+    reps = (Report * b.n)()
+    _run(b.tensors[0][0], _lib.sv_compare_batched_mode, b.arr, b.n, 1 if stop_at_first else 0, reps)
+    return [reps[k].as_dict() for k in range(b.n)]
 
 
 class CheckTicket:
@@ -317,13 +350,12 @@ def compare_submit(ref, cand, rtol: float, atol: float, equal_nan: bool = False)
 
 def compare_batched_submit(segments, stop_at_first: bool = False) -> CheckTicket:
     """compare_batched() queued on the current stream without waiting; .wait() gives the reports."""
-    if not segments:
+    if not isinstance(segments, SegmentBatch) and not segments:
         raise SVError(SV_ERR_INVALID_ARG, "compare_batched_submit: no segments")
-    arr = _segment_array(segments)
+    b = _as_batch(segments)
     t = ctypes.c_uint64(0)
-    _run(segments[0][0], _lib.sv_compare_batched_submit, arr, len(segments), 1 if stop_at_first else 0,
-         ctypes.byref(t))
-    return CheckTicket(t.value, len(segments), True, [s[:2] for s in segments])
+    _run(b.tensors[0][0], _lib.sv_compare_batched_submit, b.arr, b.n, 1 if stop_at_first else 0, ctypes.byref(t))
+    return CheckTicket(t.value, b.n, True, b)
 
 
 def perturb(ref, cand, seed: int, stream_id: int, op: str, p: float = 0.0, value: float = 0.0,

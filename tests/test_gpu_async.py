@@ -143,3 +143,24 @@ def test_scratch_grows_while_checks_are_pending():
     assert t1.wait() == want_small
     assert all(x == want_one for x in t2.wait())
     assert t3.wait() == want_small
+
+
+def test_prepared_batches_match_lists():
+    outs = [empty(n, "f32") for n in (1000, 70001, 3)]
+    jobs = [(o, 7, k, "normal", NORMAL) for k, o in enumerate(outs)]
+    want = [empty(o.numel(), "f32") for o in outs]
+    sv.synth_batched([(w, 7, k, "normal", NORMAL) for k, w in enumerate(want)])
+    prepared = sv.SynthBatch(jobs)
+    print("prepared batches", flush=True)
+    for _ in range(2):
+        for o in outs:
+            o.zero_()
+        sv.synth_batched(prepared)
+        assert all(torch.equal(o, w) for o, w in zip(outs, want))
+    cands = [_pair(o.numel(), 30 + k, p=0.01)[1] for k, o in enumerate(outs)]
+    segs = [(o, c, 1e-8, 0.0, False) for o, c in zip(outs, cands)]
+    batch = sv.SegmentBatch(segs)
+    ref = sv.compare_batched(segs)
+    assert sv.compare_batched(batch) == ref
+    assert sv.compare_batched_submit(batch).wait() == ref
+    assert sv.compare_batched(batch, stop_at_first=True) == sv.compare_batched(segs, stop_at_first=True)
