@@ -337,6 +337,7 @@ void compare_grid(uint64_t units, int cus, bool batched, uint32_t *nblocks, uint
   const uint64_t per_iter = (uint64_t)kCmpBlock;
   const uint64_t per_cu = batched ? SV_CMP_BATCH_BLOCKS_PER_CU : SV_CMP_BLOCKS_PER_CU;
   uint64_t nb = std::min<uint64_t>((units + per_iter - 1) / per_iter, (uint64_t)cus * per_cu);
+  if (!batched && units <= SV_CMP_FUSE_UNITS) nb = 1;   // small: one workgroup reports by itself
   if (nb == 0) nb = 1;
   uint64_t c = (units + nb - 1) / nb;
   c = (c + kWave - 1) / kWave * kWave;       // whole waves of units per workgroup
@@ -434,6 +435,7 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
     args.segs = ds->table;
   }
   args.stop_at_first = plan.stop_at_first ? 1 : 0;
+  args.fused = batched ? 0 : plan.nblocks == 1 ? 1 : plan.nblocks <= SV_CMP_LAST_BLOCK_MAX ? 2 : 0;
   args.partials = ds->partials;
   args.counter = ds->counters;
   args.reports = sl.d_reports;
@@ -443,7 +445,7 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   if (g_prof_on.load()) {
     e0 = take_event();
     e1 = take_event();
-    e2 = take_event();
+    if (!args.fused) e2 = take_event();
     if (e0) (void)hipEventRecord(e0, st);
   }
   uint32_t mask = 0;
@@ -454,8 +456,10 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   hipError_t e = launch_compare(args, plan.nblocks, mask, st);
   if (e != hipSuccess) return hip_fail(e, "check kernel launch");
   if (e1) (void)hipEventRecord(e1, st);
-  e = launch_finalize(args, st);
-  if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
+  if (!args.fused) {
+    e = launch_finalize(args, st);
+    if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
+  }
   ds->seq = args.seq;
   ds->has_last = true;
   ds->last_stream = st;
@@ -463,10 +467,12 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   sl.stream = st;
   sl.launched = true;
   sl.pending = true;
-  if (e0 && e1 && e2) {
-    (void)hipEventRecord(e2, st);
+  if (e0 && e1) {
     push_record(SV_PROF_COMPARE, e0, e1);
-    push_record(SV_PROF_FINALIZE, e1, e2);
+    if (e2) {
+      (void)hipEventRecord(e2, st);
+      push_record(SV_PROF_FINALIZE, e1, e2);
+    }
   }
   return SV_OK;
 }

@@ -408,6 +408,18 @@ __device__ __forceinline__ void report_words(const Partial &r, uint64_t n, uint6
 }
 constexpr int kReportWords = 10;
 
+// Thread 0's merged result r becomes the report *dst: ten lanes of wave 0
+// write its words together, with system-scope stores.  Reached by every
+// thread of the workgroup.
+__device__ __forceinline__ void publish_report(const Partial &r, uint64_t n, sv_report *dst) {
+  __shared__ uint64_t words[kReportWords];
+  if (threadIdx.x == 0) report_words(r, n, words);
+  __syncthreads();
+  if (threadIdx.x < kReportWords)
+    __hip_atomic_store((uint64_t *)dst + threadIdx.x, words[threadIdx.x], __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // Called by one thread of every finalize workgroup once its report (if any)
 // is written and has landed (each workgroup waits for its own stores before
 // it arrives): the last to arrive clears the counter and hands the sequence
@@ -557,18 +569,12 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
     wave_merge(acc);
     if (lane == 0) lds[wave] = acc;
     __syncthreads();
-    __shared__ uint64_t words[kReportWords];
+    Partial r = lds[0];
     if (tid == 0) {
-      Partial r = lds[0];
 #pragma unroll
       for (int w = 1; w < kFinWaves; ++w) merge(r, lds[w]);
-      report_words(r, sd.n, words);
     }
-    __syncthreads();
-    // ten lanes of wave 0 write the report together, with system-scope stores
-    if (tid < kReportWords)
-      __hip_atomic_store((uint64_t *)(args.reports + s) + tid, words[tid], __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_SYSTEM);
+    publish_report(r, sd.n, args.reports + s);
   }
   if (tid == 0) arrive_and_signal(args);
 }
@@ -592,6 +598,42 @@ __device__ __forceinline__ Partial check_any(const SegDesc &sd, uint64_t ulo, ui
   }
 }
 
+// A small single-tensor grid (at most one wave's worth of workgroups): the
+// last workgroup to finish merges every partial and writes the report, so no
+// finalize kernel is launched.  Each workgroup makes its partial visible with
+// a device-scope fence before it arrives on the counter; the last one fences
+// again before it reads.  (Such a fence writes back the issuing XCD's L2: a
+// few dozen of them cost little, thousands are what rule this scheme out for
+// large grids.)  Lane t of wave 0 takes partial t and the wave reduces them
+// by the finalize kernel's tree, the other lanes and waves holding empty
+// partials there, so the report is bit-identical to the finalize's.
+static_assert(SV_CMP_LAST_BLOCK_MAX <= kWave, "the last workgroup merges the partials in one wave");
+
+__device__ __forceinline__ void last_block_report(const CompareArgs &args, const Partial &p, uint64_t n) {
+  __shared__ uint32_t is_last;
+  const uint32_t tid = threadIdx.x;
+  if (tid == 0) {
+    args.partials[blockIdx.x] = p;
+    __threadfence();
+    is_last = __hip_atomic_fetch_add(args.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+              gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();
+  Partial acc = empty_partial();
+  if (tid < kWave) {
+    if (tid < gridDim.x) merge(acc, args.partials[tid]);
+    wave_merge(acc);
+  }
+  publish_report(acc, n, args.reports);
+  if (tid == 0) {
+    __hip_atomic_store(args.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    wait_memory();
+    __hip_atomic_store(args.done, args.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+}
+
 template <bool kSingle, int kMask, bool kStop = false>
 __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
   __shared__ Partial lds[kWavesPerBlock];
@@ -605,6 +647,17 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
     const uint64_t piece_hi = hi < seg_end ? hi : seg_end;
     const uint64_t ulo = lo - sd.unit_begin, uhi = piece_hi - sd.unit_begin;
     const Partial p = check_any<kMask, kStop>(sd, ulo, uhi, lds);
+    if constexpr (kSingle) {
+      if (args.fused == 1) {         // the only workgroup: its partial is the whole result
+        publish_report(p, sd.n, args.reports);
+        if (threadIdx.x == 0) arrive_and_signal(args);
+        return;
+      }
+      if (args.fused == 2) {
+        last_block_report(args, p, sd.n);
+        return;
+      }
+    }
     if (threadIdx.x == 0) args.partials[b + s] = p;
     if constexpr (kSingle) return;   // one segment: the chunk is a single piece
     lo = piece_hi;

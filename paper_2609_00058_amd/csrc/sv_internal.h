@@ -19,6 +19,12 @@ namespace sv {
 #ifndef SV_CMP_BLOCKS_PER_CU
 #define SV_CMP_BLOCKS_PER_CU 8       // check workgroups per CU, single tensor
 #endif
+#ifndef SV_CMP_FUSE_UNITS
+#define SV_CMP_FUSE_UNITS 4096       // a single tensor of at most this many 16-byte units: one workgroup, no finalize
+#endif
+#ifndef SV_CMP_LAST_BLOCK_MAX
+#define SV_CMP_LAST_BLOCK_MAX 64     // single-tensor grids up to this size: the last workgroup reports, no finalize
+#endif
 #ifndef SV_CMP_BATCH_BLOCKS_PER_CU
 #define SV_CMP_BATCH_BLOCKS_PER_CU 12   // check workgroups per CU, batched
 #endif
@@ -117,6 +123,7 @@ struct CompareArgs {
   Partial *partials;            // nblocks + nseg slots
   uint32_t *counter;            // finalize arrivals, zero between launches
   int32_t stop_at_first;        // batched: each wave stops at its first mismatch
+  int32_t fused;                // one tensor, no finalize: 1 = the only workgroup reports, 2 = the last one does
   sv_report *reports;           // nseg reports, in host-mapped pinned memory
   uint64_t *done;               // host-mapped word that receives `seq` once every report is written
   uint64_t seq;

@@ -110,6 +110,25 @@ def test_empty_and_determinism(oracle):
     assert sv.compare_batched([(R, C, 1e-5, 1e-8, False)])[0] == r1
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_single_equals_batched_across_grid_sizes(oracle, dtype):
+    # a single tensor is reported by its only workgroup (small), by the last
+    # workgroup to finish (up to one wave of workgroups) or by the finalize
+    # kernel (larger); a one-segment batch always by the finalize kernel: the
+    # reports must be bit-identical, and match the oracle
+    rng = np.random.default_rng(9)
+    per = 4 if dtype == "f32" else 8
+    for units in (1, 4095, 4096, 4097, 16384, 32767, 32768, 32769, 40000, 300000):
+        n = units * per - (1 if units > 1 else 0)
+        print("single vs batched", dtype, n, flush=True)
+        ref, cand = random_pair(rng, n, dtype)
+        R, C = dev(ref, dtype), dev(cand, dtype)
+        single = sv.compare(R, C, 1e-5, 1e-8, True)
+        assert sv.compare_batched([(R, C, 1e-5, 1e-8, True)])[0] == single
+        assert sv.compare_submit(R, C, 1e-5, 1e-8, True).wait() == single
+        same_report(single, oracle.compare(ref, cand, dtype, 1e-5, 1e-8, True))
+
+
 def test_bad_arguments_raise():
     x = empty(8, "f32")
     for rtol, atol in [(-1.0, 0.0), (0.0, math.nan), (math.inf, 0.0)]:

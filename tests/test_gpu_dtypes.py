@@ -212,3 +212,22 @@ def test_integer_checks_every_field_against_the_oracle(oracle):
     print("integer check batched", len(segs), flush=True)
     for got, w in zip(sv.compare_batched(segs), want):
         same_report(got, w)
+
+
+def test_synth_batched_mixes_all_types(oracle):
+    # the table kernel takes fp32 / bf16 / int32 jobs; the other types are launched one by one in the same call
+    jobs, want = [], []
+    specs = [("f32", "normal", dict(mean=0.0, std=1.0)), ("bf16", "uniform", dict(a=-4.0, b=4.0)),
+             ("i32", "int_range", dict(lo=-5, hi=9)), ("f16", "normal", dict(mean=5.0, std=10.0)),
+             ("f64", "uniform", dict(a=-1.0, b=3.0)), ("u8", "int_range", dict(lo=0, hi=255)),
+             ("i64", "int_range", dict(lo=-(1 << 62), hi=1 << 62)), ("f64", "special", SPECIAL)]
+    for k, (dtype, dist, params) in enumerate(specs * 2):
+        n = [0, 1, 4099, 70001][k % 4]
+        out = empty(n, dtype)
+        jobs.append((out, 40 + k, k, dist, params))
+        want.append((dtype, dist, params, 40 + k, k, n))
+    print("synth batched all types", len(jobs), flush=True)
+    sv.synth_batched(jobs)
+    for (out, *_), (dtype, dist, params, seed, stream, n) in zip(jobs, want):
+        assert np.array_equal(bits(out), oracle.synth(seed, stream, dtype, dist, oracle.dist_params(**params), n)), \
+            (dtype, dist, n)
