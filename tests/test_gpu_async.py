@@ -164,3 +164,26 @@ def test_prepared_batches_match_lists():
     assert sv.compare_batched(batch) == ref
     assert sv.compare_batched_submit(batch).wait() == ref
     assert sv.compare_batched(batch, stop_at_first=True) == sv.compare_batched(segs, stop_at_first=True)
+
+
+def test_threads_submit_and_wait_concurrently():
+    from concurrent.futures import ThreadPoolExecutor
+    pairs = [_pair(n, 70 + k, p=0.01) for k, n in enumerate([5000, 70001, 1 << 18, 1 << 20])]
+    want = [sv.compare(r, c, 1e-8, 0.0) for r, c in pairs]
+    batch = sv.SegmentBatch([(r, c, 1e-8, 0.0, False) for r, c in pairs])
+    want_b = sv.compare_batched(batch)
+    torch.cuda.synchronize()
+
+    def worker(k):
+        got = []
+        for i in range(25):
+            if (i + k) % 3 == 0:
+                got.append(sv.compare_batched_submit(batch).wait() == want_b)
+            else:
+                t = sv.compare_submit(*pairs[k], 1e-8, 0.0)
+                got.append(t.wait() == want[k])
+        return all(got)
+
+    print("threads", flush=True)
+    with ThreadPoolExecutor(4) as ex:
+        assert all(ex.map(worker, range(4)))
