@@ -445,8 +445,15 @@ static uint64_t element_value(uint64_t seed, uint64_t stream, int32_t dtype, int
     float z = (i % 2u == 0u) ? zc : zs;
     return f2u(fmaf(q->std, z, q->mean));           /* mean + std z, one rounding */
   }
+  if (dist == OR_INT_RANGE && dtype == OR_U8) {
+    /* uint8: four elements per block, element i takes word i mod 4 of block
+     * i / 4; value = lo + floor(w * range / 2^32) (range <= 256, so the
+     * multiply-shift is biased by less than 2^-24) */
+    or_philox_block(seed, stream, i / 4u, w);
+    return (uint64_t)q->lo + (((uint64_t)w[i % 4u] * q->range) >> 32);
+  }
   if (dist == OR_INT_RANGE) {
-    /* two elements per block: R = (w1:w0) for even i, (w3:w2) for odd i;
+    /* int32, int64: two elements per block: R = (w1:w0) for even i, (w3:w2) for odd i;
      * value = lo + floor(R * range / 2^64) (Lemire's multiply-shift); a range
      * of 2^64 (the whole int64 line) takes R itself */
     or_philox_block(seed, stream, i / 2u, w);

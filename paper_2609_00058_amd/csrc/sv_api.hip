@@ -636,7 +636,9 @@ int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t di
   if (offset > kMaxElems || n > kMaxElems - offset)
     return fail(SV_ERR_INVALID_ARG, "sv_synth_window: offset + n exceeds 2^60");
   const uint64_t per_block =
-      dist == SV_SPECIAL ? 1 : (dist == SV_INT_RANGE || (dist == SV_UNIFORM && dtype == SV_F64)) ? 2 : 4;
+      dist == SV_SPECIAL ? 1
+      : ((dist == SV_INT_RANGE && dtype != SV_U8) || (dist == SV_UNIFORM && dtype == SV_F64)) ? 2
+                                                                                            : 4;
   p.e0 = offset;
   p.c0 = offset / per_block;
   if (!n) return SV_OK;

@@ -149,12 +149,16 @@ static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int 
 }
 
 // ------------------------------------------------------------ fp16, fp64, uint8, int64
-// The same elements stored in the other types: fp16 bits, fp64 bits, the low
-// byte, the int64.  E elements per Philox block as above, except fp64 uniform
-// (53 random bits from a 64-bit word: E = 2).  A 16-byte vector holds V =
-// 16 / itemsize elements; only fp64 normal has V < E (two of a block's four).
+// The same elements stored in the other types: fp16 bits, fp64 bits, the
+// int64.  E elements per Philox block as above, except fp64 uniform (53
+// random bits from a 64-bit word: E = 2) and uint8, whose range of at most
+// 256 values takes one 32-bit word per element (E = 4; the multiply-shift is
+// then biased by less than 2^-24).  A 16-byte vector holds V = 16 / itemsize
+// elements; only fp64 normal has V < E (two of a block's four).
 template <int DIST, int DT> struct Wide {
-  static constexpr int E = (DIST == SV_UNIFORM && DT == SV_F64) ? 2 : DistTraits<DIST>::E;
+  static constexpr int E = (DIST == SV_UNIFORM && DT == SV_F64) ? 2
+                           : (DIST == SV_INT_RANGE && DT == SV_U8) ? 4
+                                                                   : DistTraits<DIST>::E;
   static constexpr int V = DT == SV_F16 ? 8 : DT == SV_U8 ? 16 : 2;
 };
 
@@ -162,7 +166,7 @@ template <int DT>
 __device__ __forceinline__ uint64_t from_value32(uint32_t v) {
   if constexpr (DT == SV_F16) return f16_rne(v);
   else if constexpr (DT == SV_F64) return widen_f32_bits(v);
-  else return v & 0xFFu;                       // SV_U8: the integer range value is in [0, 255]
+  else return v & 0xFFu;                       // (not reached for uint8: wide_block forms its values)
 }
 
 // The E stored values of Philox block `block`.
@@ -180,6 +184,11 @@ __device__ __forceinline__ void wide_block(const SynthParams &p, uint64_t block,
         v[k] = (uint64_t)p.lo + (p.range ? __umul64hi(r[k], p.range) : r[k]);
       }
     }
+  } else if constexpr (DIST == SV_INT_RANGE && DT == SV_U8) {
+    const u32x4 w = philox_block(Key{p.k0, p.k1, p.s0, p.s1}, block);
+    const uint32_t lo = (uint32_t)p.lo, range = (uint32_t)p.range;   // range <= 256
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = lo + __umulhi(w[k], range);
   } else {
     constexpr int E = DistTraits<DIST>::E;
     uint32_t f[E];

@@ -81,8 +81,14 @@ def test_integer_ranges_closed_forms(oracle):
     n = 20000
     w = oracle.philox_blocks(6, 2, 0, n // 2).reshape(-1, 4).astype(np.uint64)
     R = np.stack([(w[:, 1] << 32) | w[:, 0], (w[:, 3] << 32) | w[:, 2]], axis=1).reshape(-1)
+    # uint8: one 32-bit word per element, word i mod 4 of block i / 4
+    w32 = oracle.philox_blocks(6, 2, 0, n // 4).reshape(-1).astype(np.uint64)
     u8 = oracle.synth(6, 2, "u8", "int_range", oracle.dist_params(lo=0, hi=255), n)
-    assert np.array_equal(u8, (R >> 56).astype(np.uint8))                  # range 2^8: the top 8 bits
+    assert np.array_equal(u8, (w32 >> 24).astype(np.uint8))                # range 2^8: the top 8 bits
+    u8_16 = oracle.synth(6, 2, "u8", "int_range", oracle.dist_params(lo=100, hi=115), n)
+    assert np.array_equal(u8_16, (100 + (w32 >> 28)).astype(np.uint8))     # range 2^4: the top 4 bits
+    u8_odd = oracle.synth(6, 2, "u8", "int_range", oracle.dist_params(lo=3, hi=203), n)
+    assert u8_odd.tolist() == [3 + ((int(x) * 201) >> 32) for x in w32]   # floor(w * 201 / 2^32)
     full = oracle.synth(6, 2, "i64", "int_range", oracle.dist_params(lo=-2 ** 63, hi=2 ** 63 - 1), n)
     assert np.array_equal(full, R ^ np.uint64(1 << 63))                    # range 2^64: lo + R
     p40 = oracle.synth(6, 2, "i64", "int_range", oracle.dist_params(lo=-(2 ** 39), hi=2 ** 39 - 1), n)
