@@ -29,7 +29,7 @@ LIB_PATH = os.path.join(HERE, "libsvoracle.so")
 DTYPES = {"f32": 0, "bf16": 1, "i32": 2, "f16": 3, "f64": 4, "u8": 5, "i64": 6}
 NP_STORAGE = {"f32": np.uint32, "bf16": np.uint16, "i32": np.uint32, "f16": np.uint16, "f64": np.uint64,
               "u8": np.uint8, "i64": np.uint64}
-DISTS = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3}
+DISTS = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3, "permutation": 4}
 OPS = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
        "add_at": 4, "set_at": 5, "fault_at": 6}
 

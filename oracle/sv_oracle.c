@@ -345,8 +345,9 @@ typedef struct {
   float a, span;           /* uniform: a + span * U                      */
   double a64, span64;      /* uniform into fp64: the same in fp64        */
   float mean, std;         /* normal                                     */
-  int64_t lo;              /* integer range                              */
+  int64_t lo;              /* integer range, permutation                 */
   uint64_t range;          /* hi - lo + 1 (0 stands for 2^64)            */
+  unsigned half;           /* permutation: bits of each Feistel half     */
   uint64_t t_nan, t_inf, t_den, t_zero;   /* cumulative class thresholds */
 } prepared;
 
@@ -400,6 +401,21 @@ static int prepare(int32_t dtype, int32_t dist, const or_dist_params *p, prepare
     }
     return 0;
   }
+  case OR_PERMUTATION:
+    /* the N = hi - lo + 1 values lo .. hi in a seeded order, N <= 2^60 */
+    if (!is_int(dtype)) return -2;
+    if (p->lo > p->hi) return -1;
+    if (dtype == OR_I32 && (p->lo < INT32_MIN || p->hi > INT32_MAX)) return -1;
+    if (dtype == OR_U8 && (p->lo < 0 || p->hi > 255)) return -1;
+    q->lo = p->lo;
+    q->range = (uint64_t)p->hi - (uint64_t)p->lo + 1u;
+    if (q->range == 0 || q->range > (1ull << 60)) return -1;
+    {
+      unsigned bits = 0;                      /* smallest b with 2^b >= N */
+      while (bits < 64 && (1ull << bits) < q->range) bits++;
+      q->half = bits < 2 ? 1u : (bits + 1u) / 2u;
+    }
+    return 0;
   case OR_INT_RANGE:
     if (!is_int(dtype)) return -2;
     if (p->lo > p->hi) return -1;
@@ -413,11 +429,59 @@ static int prepare(int32_t dtype, int32_t dist, const or_dist_params *p, prepare
   }
 }
 
+/* Permutation.  pi is a bijection of [0, N): a permutation G of the 2h-bit
+ * words (2^2h the smallest even power of two >= N, h >= 1), followed from i
+ * until it lands below N (cycle walking: the walk returns to [0, N) because
+ * i's own cycle does, after fewer than 4 steps on average as 2^2h < 4N).
+ * G(x) = (Feistel(x) + K_10) mod 2^2h.  The Feistel network has ten rounds
+ * (six left the orders of 5 and 6 values measurably uneven); round r maps the
+ * halves (L, R) to (R, L xor (F(R xor K_r) mod 2^h)), F the lowbias32 integer
+ * hash (C. Wellons, hash-prospector, 2018).  Feistel rounds are even
+ * permutations of the words, and the walk from even permutations does not
+ * reach every order of [0, N) equally often; the added constant rotates the
+ * words, an odd permutation for odd K_10, which evens this out.  The keys
+ * K_0 .. K_10 are the words of Philox blocks 0, 1 and 2 of the tensor's
+ * (seed, stream) sequence, in order. */
+static uint32_t lowbias32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+static uint64_t word_permutation(uint64_t x, unsigned h, const uint32_t key[11]) {
+  const uint64_t mask = (1ull << h) - 1u;
+  uint64_t l = x >> h, r = x & mask;
+  for (int k = 0; k < 10; k++) {
+    uint64_t f = (uint64_t)lowbias32((uint32_t)r ^ key[k]) & mask;
+    uint64_t t = l ^ f;
+    l = r;
+    r = t;
+  }
+  const uint64_t words = (1ull << (2u * h)) - 1u;   /* mask of the 2h-bit word */
+  return (((l << h) | r) + key[10]) & words;
+}
+
+static uint64_t permute(uint64_t seed, uint64_t stream, const prepared *q, uint64_t i) {
+  uint32_t key[12];
+  or_philox_block(seed, stream, 0, key);
+  or_philox_block(seed, stream, 1, key + 4);
+  or_philox_block(seed, stream, 2, key + 8);
+  uint64_t x = i;
+  do {
+    x = word_permutation(x, q->half, key);
+  } while (x >= q->range);
+  return x;
+}
+
 /* Value of element i: fp32 bits (UNIFORM, NORMAL, SPECIAL; fp64 uniform gives
  * fp64 bits) or the integer (INT_RANGE), in the low bits of a 64-bit word. */
 static uint64_t element_value(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
                               const prepared *q, uint64_t i) {
   uint32_t w[4];
+  if (dist == OR_PERMUTATION) return (uint64_t)q->lo + permute(seed, stream, q, i);
   if (dist == OR_UNIFORM && dtype == OR_F64) {
     /* two elements per block, R = (w1:w0) for even i and (w3:w2) for odd i;
      * U = (R >> 11) 2^-53 in [0, 1); a + span U in fp64, two roundings */
@@ -500,6 +564,7 @@ int or_synth(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
   int rc = prepare(dtype, dist, p, &q);
   if (rc) return rc;
   if (n && !out) return -1;
+  if (dist == OR_PERMUTATION && (offset > q.range || n > q.range - offset)) return -1;   /* past the N values */
   for (uint64_t k = 0; k < n; k++)
     store(dtype, dist, out, k, element_value(seed, stream, dtype, dist, &q, offset + k));
   return 0;
@@ -511,6 +576,9 @@ int or_synth_at(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
   int rc = prepare(dtype, dist, p, &q);
   if (rc) return rc;
   if (n && (!out || !idx)) return -1;
+  if (dist == OR_PERMUTATION)
+    for (uint64_t k = 0; k < n; k++)
+      if (idx[k] >= q.range) return -1;
   for (uint64_t k = 0; k < n; k++)
     store(dtype, dist, out, k, element_value(seed, stream, dtype, dist, &q, idx[k]));
   return 0;

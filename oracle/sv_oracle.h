@@ -24,7 +24,7 @@ extern "C" {
 #endif
 
 enum { OR_F32 = 0, OR_BF16 = 1, OR_I32 = 2, OR_F16 = 3, OR_F64 = 4, OR_U8 = 5, OR_I64 = 6 };
-enum { OR_UNIFORM = 0, OR_NORMAL = 1, OR_INT_RANGE = 2, OR_SPECIAL = 3 };
+enum { OR_UNIFORM = 0, OR_NORMAL = 1, OR_INT_RANGE = 2, OR_SPECIAL = 3, OR_PERMUTATION = 4 };
 enum {
   OR_OP_COPY = 0,          /* cand = ref                                   */
   OR_OP_ULP = 1,           /* Bernoulli(p): one ulp up or down             */
