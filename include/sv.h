@@ -54,13 +54,14 @@ enum {
   SV_UNIFORM = 0,   /* [a, b): fp32, bf16, fp16, fp64                                */
   SV_NORMAL = 1,    /* N(mean, std^2) by Box-Muller: fp32, bf16, fp16, fp64          */
   SV_INT_RANGE = 2, /* integers uniform on [lo, hi] inclusive: int32, uint8, int64   */
-  SV_SPECIAL = 3    /* NaN / +-Inf / denormal / +-0 mix, else N(mean, std^2): fp32, bf16, fp16, fp64 */
+  SV_SPECIAL = 3,   /* NaN / +-Inf / denormal / +-0 mix, else N(mean, std^2): fp32, bf16, fp16, fp64 */
+  SV_PERMUTATION = 4 /* the values lo .. hi, each once, in a seeded order: int32, uint8, int64 */
 };
 
 typedef struct {
   double a, b;                            /* SV_UNIFORM                             */
   double mean, std;                       /* SV_NORMAL and the normal part of SPECIAL */
-  int64_t lo, hi;                         /* SV_INT_RANGE, within the output type    */
+  int64_t lo, hi;                         /* SV_INT_RANGE, SV_PERMUTATION; within the output type */
   double p_nan, p_inf, p_denorm, p_zero;  /* SV_SPECIAL class probabilities, sum <= 1 */
 } sv_dist_params;
 
@@ -101,10 +102,16 @@ typedef struct {
  * NaN keeps its sign and the top 10 fraction bits, bit 0 set if they are all
  * 0).  fp64 outputs: uniform from 53 random bits, U = (R >> 11) 2^-53 with R
  * a 64-bit word (E = 2), a + (b - a) U in fp64; normal and special are the
- * fp32 values widened exactly (a NaN's fraction moved to the top).  uint8 and
- * int64 ranges use the integer-range rule; for the whole int64 range
- * (hi - lo + 1 = 2^64) the value is lo + R.  Any slice of a tensor can be
- * regenerated alone.
+ * fp32 values widened exactly (a NaN's fraction moved to the top).  int64
+ * ranges use the integer-range rule; for the whole int64 range (hi - lo + 1
+ * = 2^64) the value is lo + R.  uint8 ranges take one 32-bit word w per
+ * element (E = 4): lo + floor(w * (hi - lo + 1) / 2^32).  Permutation:
+ * element i = lo + pi(i), pi a bijection of [0, N), N = hi - lo + 1 <= 2^60:
+ * a ten-round Feistel network plus a keyed rotation on the smallest
+ * even-bit word domain >= N, repeated until the word falls below N, its keys
+ * the words of Philox blocks 0 .. 2; n <= N (n < N: a sample without
+ * replacement), and a window must lie inside [0, N).  Any slice of a tensor
+ * can be regenerated alone.
  *
  * seed, stream_id : generator key and substream (stream_id is not a HIP stream).
  * dtype, dist     : see the enums; other pairs return SV_ERR_UNSUPPORTED.

@@ -23,7 +23,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 SV_OK, SV_ERR_INVALID_ARG, SV_ERR_UNSUPPORTED, SV_ERR_HIP, SV_ERR_ALLOC, SV_ERR_IO = 0, -1, -2, -3, -4, -5
 SV_MAX_PENDING_CHECKS = 16   # submitted checks per device not yet waited for
 DTYPE_CODES = {"f32": 0, "bf16": 1, "i32": 2, "f16": 3, "f64": 4, "u8": 5, "i64": 6}
-DIST_CODES = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3}
+DIST_CODES = {"uniform": 0, "normal": 1, "int_range": 2, "special": 3, "permutation": 4}
 OP_CODES = {"copy": 0, "ulp": 1, "scale": 2, "special_flip": 3,
             "add_at": 4, "set_at": 5, "fault_at": 6}
 PROF_KINDS = {"synth": 0, "compare": 1, "perturb": 2, "finalize": 3}

@@ -541,8 +541,8 @@ int take_slot(DeviceState *ds, int *k) {
 int prepare_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist, const sv_dist_params *params,
                   uint64_t n, void *out, SynthParams *pp) {
   if (!valid_dtype(dtype)) return fail(SV_ERR_UNSUPPORTED, "sv_synth: unknown dtype %d", dtype);
-  if (dist < SV_UNIFORM || dist > SV_SPECIAL) return fail(SV_ERR_UNSUPPORTED, "sv_synth: unknown dist %d", dist);
-  if ((dist == SV_INT_RANGE) != int_dtype(dtype))
+  if (dist < SV_UNIFORM || dist > SV_PERMUTATION) return fail(SV_ERR_UNSUPPORTED, "sv_synth: unknown dist %d", dist);
+  if ((dist == SV_INT_RANGE || dist == SV_PERMUTATION) != int_dtype(dtype))
     return fail(SV_ERR_UNSUPPORTED, "sv_synth: dist %d cannot produce dtype %d", dist, dtype);
   if (!params) return fail(SV_ERR_INVALID_ARG, "sv_synth: params is NULL");
   int rc = check_tensor(out, n, dtype, "sv_synth out");
@@ -597,6 +597,16 @@ int prepare_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist
                   (long long)lo, (long long)hi, dtype == SV_U8 ? "uint8" : dtype == SV_I64 ? "int64" : "int32");
     p.lo = lo;
     p.range = (uint64_t)hi - (uint64_t)lo + 1u;   // 0 for the whole int64 range
+    if (dist == SV_PERMUTATION) {
+      if (p.range == 0 || p.range > (1ull << 60))
+        return fail(SV_ERR_INVALID_ARG, "sv_synth: a permutation takes at most 2^60 values");
+      if (n > p.range)
+        return fail(SV_ERR_INVALID_ARG, "sv_synth: %llu elements exceed the %llu values of the permutation",
+                    (unsigned long long)n, (unsigned long long)p.range);
+      uint32_t bits = 0;                          // smallest b with 2^b >= N
+      while ((1ull << bits) < p.range) ++bits;
+      p.half = bits < 2 ? 1u : (bits + 1u) / 2u;
+    }
   }
   return SV_OK;
 }
@@ -635,8 +645,11 @@ int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t di
   if (rc) return rc;
   if (offset > kMaxElems || n > kMaxElems - offset)
     return fail(SV_ERR_INVALID_ARG, "sv_synth_window: offset + n exceeds 2^60");
+  if (dist == SV_PERMUTATION && (offset > p.range || n > p.range - offset))
+    return fail(SV_ERR_INVALID_ARG, "sv_synth_window: elements [%llu, %llu) lie past the %llu values of the permutation",
+                (unsigned long long)offset, (unsigned long long)(offset + n), (unsigned long long)p.range);
   const uint64_t per_block =
-      dist == SV_SPECIAL ? 1
+      dist == SV_SPECIAL || dist == SV_PERMUTATION ? 1
       : ((dist == SV_INT_RANGE && dtype != SV_U8) || (dist == SV_UNIFORM && dtype == SV_F64)) ? 2
                                                                                             : 4;
   p.e0 = offset;
@@ -680,7 +693,7 @@ int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
       return rc;
     }
     if (!j.n) continue;
-    if (!table_kind(j.dtype)) {
+    if (!table_kind(j.dtype) || j.dist == SV_PERMUTATION) {
       direct_jobs.push_back(k);
       continue;
     }

@@ -47,6 +47,7 @@ struct SynthParams {
   float mean, std;              // normal and the normal part of SPECIAL
   int64_t lo;                   // integer range
   uint64_t range;               // hi - lo + 1 (0 stands for 2^64: the whole int64 range)
+  uint32_t half;                // permutation: bits of each Feistel half
   uint64_t t_nan, t_inf, t_den, t_zero;   // cumulative class thresholds on w0
   double a64, span64;           // fp64 uniform: a + span U53
   uint64_t e0;                  // tensor index of out[0] (a window of the tensor; 0 for a whole tensor)

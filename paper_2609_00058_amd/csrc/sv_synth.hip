@@ -282,6 +282,74 @@ static hipError_t launch_wide(const SynthParams &p, uint64_t n, void *out, int c
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------ permutation
+// Element i = lo + pi(i), pi a bijection of [0, N): the word permutation
+// G(x) = (Feistel(x) + K_10) mod 2^2h on the smallest even-bit domain 2^2h >=
+// N, applied again until the word falls below N (cycle walking: i's own cycle
+// returns to [0, N), after fewer than 4 steps on average as 2^2h < 4N).  Ten
+// Feistel rounds map the h-bit halves (L, R) to (R, L xor (F(R xor K_r) mod
+// 2^h)), F the lowbias32 integer hash (C. Wellons, hash-prospector, 2018).
+// Feistel rounds alone are even permutations of the words, from which the
+// walk does not reach every order of [0, N) equally often; the keyed
+// rotation, odd for odd K_10, evens this out.  K_0 .. K_10 are the words of
+// Philox blocks 0, 1 and 2 of the tensor's (seed, stream) sequence, which
+// every thread forms once.  The walk lengths differ from element to element
+// (geometric, mean below 4): a lane whose element has landed stores it and
+// takes its next element at once, so that a wave does not wait on its
+// slowest lane for each element (the longest of 64 walks averages ~16 steps).
+__device__ __forceinline__ uint32_t lowbias32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x7feb352du;
+  x ^= x >> 15;
+  x *= 0x846ca68bu;
+  x ^= x >> 16;
+  return x;
+}
+
+template <int DT>
+__global__ __launch_bounds__(kBlock) void synth_perm_kernel(SynthParams p, uint64_t n, void *__restrict__ out) {
+  const Key key{p.k0, p.k1, p.s0, p.s1};
+  const u32x4 b0 = philox_block(key, 0), b1 = philox_block(key, 1), b2 = philox_block(key, 2);
+  const uint32_t k[11] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w, b2.x, b2.y, b2.z};
+  const uint32_t h = p.half;
+  const uint32_t mask = (1u << h) - 1u;
+  const uint64_t words = (1ull << (2u * h)) - 1u;
+  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+  uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;   // this lane's element
+  uint64_t x = p.e0 + i;                                     // its word so far
+  bool live = i < n;
+  // every walk returns below N (its element's own cycle does), and each lane
+  // then moves on by `stride` until it passes n: every wave leaves the loop
+  while (__any(live)) {
+    if (live) {
+      uint32_t l = (uint32_t)(x >> h), r = (uint32_t)x & mask;
+#pragma unroll
+      for (int rd = 0; rd < 10; ++rd) {
+        const uint32_t t = l ^ (lowbias32(r ^ k[rd]) & mask);
+        l = r;
+        r = t;
+      }
+      x = ((((uint64_t)l << h) | r) + k[10]) & words;
+      if (x < p.range) {
+        const uint64_t v = (uint64_t)p.lo + x;
+        if constexpr (DT == SV_U8) ((uint8_t *)out)[i] = (uint8_t)v;
+        else if constexpr (DT == SV_I32) ((uint32_t *)out)[i] = (uint32_t)v;
+        else ((uint64_t *)out)[i] = v;
+        i += stride;
+        live = i < n;
+        x = p.e0 + i;
+      }
+    }
+  }
+}
+
+template <int DT>
+static hipError_t launch_perm(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
+  const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU);
+  hipLaunchKernelGGL((synth_perm_kernel<DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n, out);
+  return hipGetLastError();
+}
+
 hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint64_t n, void *out, int cus,
                         hipStream_t stream) {
   switch (dist * 8 + dtype) {
@@ -300,6 +368,9 @@ hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint6
     case SV_SPECIAL * 8 + SV_F64: return launch_wide<SV_SPECIAL, SV_F64>(p, n, out, cus, stream);
     case SV_INT_RANGE * 8 + SV_U8: return launch_wide<SV_INT_RANGE, SV_U8>(p, n, out, cus, stream);
     case SV_INT_RANGE * 8 + SV_I64: return launch_wide<SV_INT_RANGE, SV_I64>(p, n, out, cus, stream);
+    case SV_PERMUTATION * 8 + SV_I32: return launch_perm<SV_I32>(p, n, out, cus, stream);
+    case SV_PERMUTATION * 8 + SV_U8: return launch_perm<SV_U8>(p, n, out, cus, stream);
+    case SV_PERMUTATION * 8 + SV_I64: return launch_perm<SV_I64>(p, n, out, cus, stream);
     default: return hipErrorInvalidValue;
   }
 }

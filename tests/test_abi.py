@@ -46,6 +46,9 @@ def test_abi_version_and_enums_match_header(svlib):
                        ("SV_INT_RANGE", 2), ("SV_SPECIAL", 3), ("SV_OP_FAULT_AT", 6)]:
         assert re.search(r"\b%s = %d\b" % (name, code), src), name
     assert svlib.DTYPE_CODES == {"f32": 0, "bf16": 1, "i32": 2, "f16": 3, "f64": 4, "u8": 5, "i64": 6}
+    assert re.search(r"\bSV_PERMUTATION = 4\b", src)
+    import oracle as _o
+    assert _o.DISTS == svlib.DIST_CODES
     for name, code in [("SV_F16", 3), ("SV_F64", 4), ("SV_U8", 5), ("SV_I64", 6)]:
         assert re.search(r"\b%s = %d\b" % (name, code), src), name
     import oracle
@@ -91,6 +94,14 @@ def test_synth_argument_errors_before_any_device_work(svlib):
     assert _synth(L, svlib, 6, 2, lo=3, hi=2) == INV
     assert _synth(L, svlib, 4, 0, out=0x1004, a=0.0, b=1.0) == INV          # misaligned fp64
     assert _synth(L, svlib, 0, 9, a=0.0, b=1.0) == UNS                      # unknown dist
+    # permutation: integer types only, at most 2^60 values, no more elements than values
+    assert _synth(L, svlib, 0, 4, lo=0, hi=9) == UNS                        # fp32
+    assert _synth(L, svlib, 2, 4, lo=0, hi=9, n=11) == INV                  # 11 elements of 10 values
+    assert _synth(L, svlib, 6, 4, lo=0, hi=2 ** 61, n=4, out=0x1000) == INV
+    assert _synth(L, svlib, 5, 4, lo=0, hi=256, n=4) == INV                 # beyond uint8
+    assert _synth(L, svlib, 2, 4, lo=5, hi=4, n=0) == INV                   # empty domain
+    p = svlib.dist_params(lo=0, hi=99)
+    assert L.sv_synth_window(0, 0, 2, 4, ctypes.byref(p), 95, 6, 0x1000) == INV   # past the 100 values
     assert _synth(L, svlib, 0, 2, lo=0, hi=3) == UNS                        # int range into fp32
     assert _synth(L, svlib, 2, 0, a=0.0, b=1.0) == UNS                      # uniform into int32
     assert _synth(L, svlib, 0, 0, params=False) == INV
