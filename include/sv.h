@@ -91,8 +91,8 @@ typedef struct {
  *
  * Element i is a function of (seed, stream_id, i) only: Philox4x32-10
  * (Salmon et al., SC'11) keyed by the seed, with counter (block index,
- * stream_id), where block = i / E and E = 4 (uniform, normal), 2 (integer
- * range) or 1 (special).  Uniform: a + (b - a) * (top 24 bits) * 2^-24 in
+ * stream_id), where block = i / E and E = 4 (uniform, normal, uint8 range),
+ * 2 (int32 / int64 range) or 1 (special).  Uniform: a + (b - a) * (top 24 bits) * 2^-24 in
  * fp32.  Normal: Box-Muller with ln, sin, cos evaluated as fixed fp32
  * operation sequences, so the bits are reproducible on any IEEE-754 machine.
  * Integer range: lo + floor(R * (hi - lo + 1) / 2^64), R a 64-bit word.

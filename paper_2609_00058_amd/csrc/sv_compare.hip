@@ -3,20 +3,23 @@
 //
 // Memory plan.  The check reads every reference and candidate byte once and
 // writes a few hundred bytes, so it is bound by HBM bandwidth.  Segments are
-// laid end to end in 16-byte units (4 fp32 / int32 or 8 bf16 elements);
+// laid end to end in 16-byte units (16 uint8, 8 bf16 / fp16, 4 fp32 / int32
+// or 2 fp64 / int64 elements);
 // workgroup b owns a contiguous chunk of that unit space, so work is balanced
 // by bytes across ragged batches.  Inside a chunk each wave reads 64
 // consecutive units per operand per dwordx4 load (1 KiB, fully coalesced),
 // several units per thread in flight; loads are non-temporal because the data
 // is used once.
 //
-// Per element: both values are widened exactly to fp64, d = |a - y|,
-// t = atol + rtol |y| (no fma), and the pair agrees when d <= t if both are
-// finite, otherwise when the values are equal (identical infinities) or both
-// are NaN under equal_nan.  A wave first checks whether every d of its unit is
-// finite (true for all but special-value data); then it needs one comparison
-// per element and no NaN / Inf classification.  Elements past the end of a
-// segment are loaded as zero on both sides, which agrees and adds nothing.
+// Per element of a floating-point type: both values are widened exactly to
+// fp64, d = |a - y|, t = atol + rtol |y| (no fma), and the pair agrees when
+// d <= t if both are finite, otherwise when the values are equal (identical
+// infinities) or both are NaN under equal_nan.  A wave first checks whether
+// every d of its group is finite (true for all but special-value data); then
+// it needs one comparison per element and no NaN / Inf classification.
+// Integer types agree only when equal and are checked in integer arithmetic
+// (check_group_int).  Elements past the end of a segment are loaded as zero
+// on both sides, which agrees and adds nothing.
 //
 // Counts (mismatches, NaN, Inf) and the first mismatching index are
 // wave-uniform: predicate ballots popcounted on the scalar unit; the first
@@ -26,22 +29,24 @@
 // lane's running maximum m (the test d > fp64(m (1 - 2^-50)) |y| never
 // rejects a quotient that rounds above m).
 //
-// Reduction.  Lanes -> wave by xor shuffles, waves -> workgroup through LDS,
-// one 72-byte partial per (workgroup, segment piece) in scratch slot b + s.
-// The finalize kernel -- one workgroup per segment, launched behind the check
-// -- combines a segment's partials in a fixed order and writes the report
-// straight into host-mapped pinned memory, then the last finalize workgroup
-// writes the launch's sequence number, which the host spins on.  No
-// floating-point atomics: reports are bit-reproducible run to run for a given
-// device.
+// Reduction.  Lanes -> wave by DPP moves and xor shuffles, waves ->
+// workgroup through LDS, one 72-byte partial per (workgroup, segment piece)
+// in scratch slot b + s.  The finalize kernel -- one workgroup per segment,
+// launched behind the check -- combines a segment's partials in a fixed order
+// and writes the report straight into host-mapped pinned memory, then the
+// last finalize workgroup writes the launch's sequence number, which the host
+// spins on.  No floating-point atomics: reports are bit-reproducible run to
+// run for a given device.  A small single tensor needs no finalize: one
+// workgroup, or the last of a few dozen, writes the report itself
+// (last_block_report), by the same reduction tree.
 //
-// The partials need no device-scope fence inside the check: the finalize runs
-// after it.  (On gfx950 such a fence writes back the whole L2 of the issuing
-// XCD, which cuts the check to a third of its bandwidth when thousands of
-// workgroups each issue one; an in-kernel "last workgroup finishes" scheme
-// built from device-scope atomic stores instead of fences measured slower than
-// the separate finalize, its chain of round trips to the coherence point being
-// longer than a kernel launch.)
+// The partials of a large grid need no device-scope fence inside the check:
+// the finalize runs after it.  (On gfx950 such a fence writes back the whole
+// L2 of the issuing XCD, which cuts the check to a third of its bandwidth
+// when thousands of workgroups each issue one; an in-kernel "last workgroup
+// finishes" scheme built from device-scope atomic stores instead of fences
+// measured slower than the separate finalize, its chain of round trips to the
+// coherence point being longer than a kernel launch.)
 #include "sv_device.h"
 #include "sv_internal.h"
 
