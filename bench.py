@@ -38,14 +38,18 @@ KERNEL_NAMES = {"synth": "void sv::synth_vec_kernel<1, 0>", "compare": "void sv:
 
 
 def kernel_source_hash():
-    """Hash of the library sources and build flags: the HBM-traffic counters in
-    profiles/ are reported only while the kernels they were taken on are unchanged."""
+    """Hash of the library sources (comments and blank lines removed) and build
+    flags: the HBM-traffic counters in profiles/ are reported only while the
+    code they were taken on is unchanged."""
     import hashlib
+    import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2609_00058_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(name.encode() + f.read())
+        with open(os.path.join(csrc, name)) as f:
+            code = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+        code = "\n".join(l for l in (re.sub(r"//.*", "", x).rstrip() for x in code.split("\n")) if l)
+        h.update(name.encode() + code.encode())
     with open(os.path.join(ROOT, "paper_2609_00058_amd", "build.py"), "rb") as f:
         h.update(f.read())
     return h.hexdigest()[:16]
@@ -85,6 +89,24 @@ def parse():
     if args.steps < 1 or args.warmup < 0:
         ap.error("--steps must be at least 1 and --warmup at least 0")
     return args
+
+
+def stream_copy_GBps(torch):
+    """A STREAM-like reference on the same GPU: a 512 MiB device-to-device copy
+    (torch's copy kernel), bytes read + written per second, best of 20."""
+    src = torch.ones(1 << 27, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    best = None
+    for _ in range(23):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        b.synchronize()
+        ms = a.elapsed_time(b)
+        best = ms if best is None or ms < best else best
+    del src, dst
+    return round(2 * (1 << 29) / (best * 1e-3) / 1e9, 1)
 
 
 def cpu_baseline(wl):
@@ -356,6 +378,9 @@ def main():
     kt_ms = (kt["synth"][1] + kt["compare"][1]) / args.steps
     kernels["synth_and_check_GBps"] = round((sbytes + cbytes) / (kt_ms / 1e3) / 1e9, 1)
     kernels["synth_and_check_frac"] = round(kernels["synth_and_check_GBps"] / HBM_PEAK_GBS, 4)
+    kernel_ms = sum(kt[k][1] for k in kinds) / args.steps
+    kernels["tensors_per_s"] = round(len(wl.cases) / (kernel_ms / 1e3), 1)   # kernel time only
+    copy = stream_copy_GBps(torch)
     dom = max(("synth", "compare"), key=lambda k: kernels[k]["ms_per_step"])
     achieved = kernels[dom]["GBps"]
     out = {
@@ -369,6 +394,7 @@ def main():
         "config": {"workload": wl.name, "description": wl.description, "tensors": len(wl.cases),
                    "elements": wl.total_elems, "synth_bytes": sbytes, "check_bytes": cbytes,
                    "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
+                   "stream_copy_GBps": copy, "frac_of_stream_copy": round(value / copy, 4),
                    "tensors_per_s": round(len(wl.cases) / (ms / 1e3), 1)},
         "kernels": kernels,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
