@@ -7,12 +7,23 @@
  * in "CUDA-Harness" (arXiv 2609.00058), Sec. 4.2:
  *   - sv_synth produces isolated, reproducible test data (Sec. 4.2.1: test
  *     inputs are synthesized apart from kernel generation, from a broad numeric
- *     range);
+ *     range); sv_synth_window any slice of such a tensor, sv_synth_batched
+ *     many tensors in one launch;
  *   - sv_compare evaluates the functional validation rule, Eq. (1),
  *       V(K, x, y) = I[ |K(x) - y| <= atol + rtol * |y| ],
  *     element by element, y being the reference output and K(x) the candidate;
  *   - sv_compare_batched checks many outputs in one launch, one report each,
- *     for the progressive, fail-fast validation of Sec. 4.2.2.
+ *     for the progressive, fail-fast validation of Sec. 4.2.2
+ *     (sv_compare_batched_mode: each failing output only up to its first
+ *     mismatch); sv_compare_submit / sv_compare_batched_submit and
+ *     sv_compare_wait run the same checks without waiting for the reports;
+ *   - sv_kernel_load / sv_kernel_launch / sv_kernel_time / sv_kernel_free and
+ *     sv_reward: the performance stage and the reward (Eq. 3 and 4);
+ *   - sv_synth_file and sv_compare_file: test data as raw binary files, the
+ *     way the generated programs of Sec. 4.1 exchange it.
+ * sv_perturb derives candidates from a reference (test workloads),
+ * sv_eval_transform evaluates the building blocks of the normal transform
+ * (diagnostics), sv_profile_* times the library's own kernels.
  *
  * Conventions.  All functions return an sv_status (0 on success).  On error
  * nothing is launched and sv_last_error() returns a message for the calling
@@ -23,7 +34,8 @@
  * (the null stream by default).  The library owns a per-device scratch area
  * (partial reductions, segment table, report staging) that it allocates on
  * first use, grows when needed and releases in sv_shutdown(); calls that use
- * it on the same device are serialised by a lock.
+ * it on the same device are serialised by a lock, and checks of one device
+ * run in submission order.
  */
 #ifndef SV_H
 #define SV_H
