@@ -292,9 +292,11 @@ int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_pertur
  *   which = SV_EVAL_SIN    : out[i] = bits of sin(2 pi (in[i] & 0xFFFFFF) 2^-24)
  *   which = SV_EVAL_COS    : out[i] = bits of cos(2 pi (in[i] & 0xFFFFFF) 2^-24)
  *   which = SV_EVAL_F16    : out[i] = the fp16 bits sv_synth stores for the fp32 bits in[i]
+ *   which = SV_EVAL_BF16   : out[i] = the bf16 bits of the hardware conversion sv_synth
+ *                            uses for uniform and normal bf16 values (for in[i] not a NaN)
  * in, out: device arrays of n uint32.  Asynchronous.
  */
-enum { SV_EVAL_LN = 0, SV_EVAL_RADIUS = 1, SV_EVAL_SIN = 2, SV_EVAL_COS = 3, SV_EVAL_F16 = 4 };
+enum { SV_EVAL_LN = 0, SV_EVAL_RADIUS = 1, SV_EVAL_SIN = 2, SV_EVAL_COS = 3, SV_EVAL_F16 = 4, SV_EVAL_BF16 = 5 };
 int sv_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out);
 
 /*

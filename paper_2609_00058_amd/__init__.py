@@ -372,7 +372,7 @@ def perturb(ref, cand, seed: int, stream_id: int, op: str, p: float = 0.0, value
     return cand
 
 
-EVAL = {"ln": 0, "radius": 1, "sin": 2, "cos": 3, "f16": 4}
+EVAL = {"ln": 0, "radius": 1, "sin": 2, "cos": 3, "f16": 4, "bf16": 5}
 
 
 def eval_transform(which: str, inp, out):

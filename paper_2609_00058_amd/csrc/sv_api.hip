@@ -993,7 +993,7 @@ int sv_perturb(uint64_t seed, uint64_t stream_id, int32_t dtype, const sv_pertur
 
 int sv_eval_transform(int32_t which, const uint32_t *in, uint64_t n, uint32_t *out) {
   t_error.clear();
-  if (which < SV_EVAL_LN || which > SV_EVAL_F16)
+  if (which < SV_EVAL_LN || which > SV_EVAL_BF16)
     return fail(SV_ERR_UNSUPPORTED, "sv_eval_transform: unknown transform %d", which);
   int rc = check_tensor(in, n, SV_F32, "sv_eval_transform in");
   if (!rc) rc = check_tensor(out, n, SV_F32, "sv_eval_transform out");

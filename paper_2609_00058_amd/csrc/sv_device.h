@@ -83,6 +83,18 @@ __device__ __forceinline__ uint32_t bf16_rne(uint32_t x) {
   return nan ? ((x >> 16) | 0x40u) : r;
 }
 
+// Two fp32 values, neither a NaN, to two bf16 in one word (the first in the
+// low half) by the hardware conversion (v_cvt_pk_bf16_f32): round to nearest
+// even, Inf stays Inf, denormals are kept -- bf16_rne's result for every fp32
+// bit pattern that is not a NaN (checked on all of them).  For values that
+// cannot be NaN: uniform and normal synthesis.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_rne_not_nan(uint32_t lo, uint32_t hi) {
+  const bf16x2_t h = __builtin_convertvector((f32x2_t{as_f32(lo), as_f32(hi)}), bf16x2_t);
+  return __builtin_bit_cast(uint32_t, h);
+}
+
 // 24-bit uniform: top 24 bits of a word scaled by 2^-24 (exact).
 __device__ __forceinline__ float unit24(uint32_t w) { return (float)(w >> 8) * 0x1p-24f; }
 

@@ -73,6 +73,17 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
   }
 }
 
+// Two elements as bf16 in one word.  Uniform and normal values are never
+// NaN, so the hardware conversion applies; special values go through
+// bf16_rne and its NaN rule.
+template <int DIST>
+__device__ __forceinline__ uint32_t bf16_pair(uint32_t lo, uint32_t hi) {
+  if constexpr (DIST == SV_UNIFORM || DIST == SV_NORMAL)
+    return bf16x2_rne_not_nan(lo, hi);
+  else
+    return bf16_rne(lo) | (bf16_rne(hi) << 16);
+}
+
 template <int DIST, int DT>
 __device__ __forceinline__ void store_elem(void *out, uint64_t i, uint32_t x) {
   if constexpr (DT == SV_BF16)
@@ -97,10 +108,10 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
     for (int b = 0; b < B; ++b) block_values<DIST>(p, p.c0 + u * B + b, v + b * E);
     u32x4 o;
     if constexpr (DT == SV_BF16) {
-      o.x = bf16_rne(v[0]) | (bf16_rne(v[1]) << 16);
-      o.y = bf16_rne(v[2]) | (bf16_rne(v[3]) << 16);
-      o.z = bf16_rne(v[4]) | (bf16_rne(v[5]) << 16);
-      o.w = bf16_rne(v[6]) | (bf16_rne(v[7]) << 16);
+      o.x = bf16_pair<DIST>(v[0], v[1]);
+      o.y = bf16_pair<DIST>(v[2], v[3]);
+      o.z = bf16_pair<DIST>(v[4], v[5]);
+      o.w = bf16_pair<DIST>(v[6], v[7]);
     } else {
       o = u32x4{v[0], v[1], v[2], v[3]};
     }
@@ -384,6 +395,10 @@ __global__ __launch_bounds__(kBlock) void eval_transform_kernel(int32_t which, c
       out[i] = f16_rne(in[i]);
       continue;
     }
+    if (which == SV_EVAL_BF16) {
+      out[i] = bf16x2_rne_not_nan(in[i], 0u) & 0xFFFFu;
+      continue;
+    }
     const uint32_t k = in[i] & 0x00FFFFFFu;
     float v;
     if (which == SV_EVAL_LN) {
@@ -422,10 +437,10 @@ __device__ __forceinline__ void synth_vector(const SynthParams &p, void *out, ui
   if (vec_ok && (u + 1) * V <= n) {
     u32x4 o;
     if constexpr (DT == SV_BF16) {
-      o.x = bf16_rne(v[0]) | (bf16_rne(v[1]) << 16);
-      o.y = bf16_rne(v[2]) | (bf16_rne(v[3]) << 16);
-      o.z = bf16_rne(v[4]) | (bf16_rne(v[5]) << 16);
-      o.w = bf16_rne(v[6]) | (bf16_rne(v[7]) << 16);
+      o.x = bf16_pair<DIST>(v[0], v[1]);
+      o.y = bf16_pair<DIST>(v[2], v[3]);
+      o.z = bf16_pair<DIST>(v[4], v[5]);
+      o.w = bf16_pair<DIST>(v[6], v[7]);
     } else {
       o = u32x4{v[0], v[1], v[2], v[3]};
     }

@@ -217,7 +217,7 @@ def test_profile_read_with_nothing_recorded(svlib):
 
 def test_eval_transform_argument_errors(svlib):
     L = svlib._lib
-    assert L.sv_eval_transform(5, 0x1000, 4, 0x2000) == svlib.SV_ERR_UNSUPPORTED
+    assert L.sv_eval_transform(6, 0x1000, 4, 0x2000) == svlib.SV_ERR_UNSUPPORTED
     assert L.sv_eval_transform(-1, 0x1000, 4, 0x2000) == svlib.SV_ERR_UNSUPPORTED
     assert L.sv_eval_transform(0, None, 4, 0x2000) == svlib.SV_ERR_INVALID_ARG
     assert L.sv_eval_transform(0, 0x1002, 4, 0x2000) == svlib.SV_ERR_INVALID_ARG   # misaligned

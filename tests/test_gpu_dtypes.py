@@ -59,6 +59,27 @@ def test_f16_rounding_every_fp32_pattern(oracle):
         assert bad.size == 0, "pattern %#x: got %#x want %#x" % (pats[bad[0]], got[bad[0]], want[bad[0]])
 
 
+def test_bf16_hardware_conversion_every_non_nan_fp32_pattern(oracle):
+    # uniform and normal bf16 synthesis round with the hardware conversion (their
+    # values are never NaN): it must equal the oracle's round-to-nearest-even on
+    # every fp32 bit pattern that is not a NaN
+    chunk = 1 << 28
+    out = torch.empty(chunk, dtype=torch.int32, device="cuda")
+    pool = ThreadPoolExecutor(16)
+    for c in range(1 << 4):
+        print("bf16 patterns, chunk", c, flush=True)
+        base = c * chunk
+        x = (torch.arange(chunk, dtype=torch.int64, device="cuda") + base).to(torch.int32)
+        sv.eval_transform("bf16", x, out)
+        got = out.cpu().numpy().view(np.uint32)
+        pats = (np.arange(chunk, dtype=np.uint64) + base).astype(np.uint32)
+        parts = np.array_split(np.arange(chunk), 16)
+        want = np.concatenate(list(pool.map(lambda ix: oracle.bf16_rne_n(pats[ix]), parts))).astype(np.uint32)
+        ok = (pats & 0x7FFFFFFF) <= 0x7F800000                        # not a NaN
+        bad = np.nonzero((got != want) & ok)[0]
+        assert bad.size == 0, "pattern %#x: got %#x want %#x" % (pats[bad[0]], got[bad[0]], want[bad[0]])
+
+
 def _pair(rng, n, dtype):
     if dtype == "u8":
         y = rng.integers(0, 256, n).astype(np.uint8)
