@@ -91,6 +91,9 @@ __device__ __forceinline__ uint32_t bf16_rne(uint32_t x) {
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t bf16x2_rne_not_nan(uint32_t lo, uint32_t hi) {
+  // the empty asm keeps the fp32 rounding of the values: no fusion of the
+  // arithmetic that produced them with this conversion
+  asm("" : "+v"(lo), "+v"(hi));
   const bf16x2_t h = __builtin_convertvector((f32x2_t{as_f32(lo), as_f32(hi)}), bf16x2_t);
   return __builtin_bit_cast(uint32_t, h);
 }

@@ -173,9 +173,17 @@ template <int DIST, int DT> struct Wide {
   static constexpr int V = DT == SV_F16 ? 8 : DT == SV_U8 ? 16 : 2;
 };
 
-template <int DT>
+template <int DIST, int DT>
 __device__ __forceinline__ uint64_t from_value32(uint32_t v) {
-  if constexpr (DT == SV_F16) return f16_rne(v);
+  if constexpr (DT == SV_F16 && (DIST == SV_UNIFORM || DIST == SV_NORMAL)) {   // never NaN: no NaN rule
+    // The fp16 value is the rounding of the fp32 value: the empty asm keeps
+    // the compiler from fusing the fp32 multiply-add before it and this
+    // conversion into one mixed-precision fma that rounds once, to fp16.
+    uint32_t b = v;
+    asm("" : "+v"(b));
+    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)as_f32(b));
+  }
+  else if constexpr (DT == SV_F16) return f16_rne(v);
   else if constexpr (DT == SV_F64) return widen_f32_bits(v);
   else return v & 0xFFu;                       // (not reached for uint8: wide_block forms its values)
 }
@@ -205,7 +213,7 @@ __device__ __forceinline__ void wide_block(const SynthParams &p, uint64_t block,
     uint32_t f[E];
     block_values<DIST>(p, block, f);
 #pragma unroll
-    for (int k = 0; k < E; ++k) v[k] = from_value32<DT>(f[k]);
+    for (int k = 0; k < E; ++k) v[k] = from_value32<DIST, DT>(f[k]);
   }
 }
 
