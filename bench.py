@@ -312,13 +312,17 @@ def main():
     jobs = sv.SynthBatch([(r, spec.seed, spec.stream, spec.dist, spec.params) for spec, r in zip(uniq, refs)])
     batch = sv.SegmentBatch(segs)
 
+    if not wl.batched:   # one tensor: both calls marshalled once as well
+        c0 = wl.cases[0]
+        synth_call = sv.PreparedSynth(refs[0], c0.ref.seed, c0.ref.stream, c0.ref.dist, **c0.ref.params)
+        check_call = sv.PreparedCheck(*segs[0])
+
     def submit():
         if wl.batched:
             sv.synth_batched(jobs)
             return sv.compare_batched_submit(batch, stop_at_first=wl.stop_at_first)
-        c = wl.cases[0]
-        sv.synth(refs[0], c.ref.seed, c.ref.stream, c.ref.dist, **c.ref.params)
-        return sv.compare_submit(*segs[0])
+        synth_call()
+        return check_call.submit()
 
     def reports(ticket):
         r = ticket.wait()

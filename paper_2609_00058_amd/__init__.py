@@ -358,6 +358,68 @@ def compare_batched_submit(segments, stop_at_first: bool = False) -> CheckTicket
     return CheckTicket(t.value, b.n, True, b)
 
 
+class _Prepared:
+    """A library call with its arguments marshalled once, for calls repeated on
+    the same tensors: each call hands torch's current stream of the device to
+    the library (when it changed) and calls it.  Keeps its tensors alive."""
+
+    def __init__(self, dev, keep):
+        self._dev = dev
+        self._keep = keep
+
+    def _call(self, fn, *args):
+        torch = _torch()
+        dev = self._dev
+        if torch._C._cuda_getDevice() != dev:
+            return _run_on(dev, fn, *args)
+        stream = torch._C._cuda_getCurrentRawStream(dev)
+        if getattr(_tls, "stream", None) != (dev, stream):
+            _check(_lib.sv_set_stream(stream))
+            _tls.stream = (dev, stream)
+        rc = fn(*args)
+        if rc:
+            _check(rc)
+
+
+class PreparedSynth(_Prepared):
+    """synth(out, seed, stream_id, dist, **params) marshalled once; call it to launch."""
+
+    def __init__(self, out, seed: int, stream_id: int, dist: str, **params):
+        super().__init__(out.get_device(), out)
+        self._params = dist_params(**params)
+        self._args = (ctypes.c_uint64(seed), ctypes.c_uint64(stream_id), ctypes.c_int32(dtype_code(out)),
+                      ctypes.c_int32(DIST_CODES[dist]), ctypes.byref(self._params), ctypes.c_uint64(out.numel()),
+                      ctypes.c_void_p(_dev_ptr(out, "out") if out.numel() else None))
+
+    def __call__(self):
+        self._call(_lib.sv_synth, *self._args)
+
+
+class PreparedCheck(_Prepared):
+    """compare(ref, cand, rtol, atol, equal_nan) marshalled once: run() checks and
+    returns the report, submit() queues the check and returns its ticket."""
+
+    def __init__(self, ref, cand, rtol: float, atol: float, equal_nan: bool = False):
+        if ref.dtype != cand.dtype or ref.numel() != cand.numel():
+            raise SVError(SV_ERR_INVALID_ARG, "ref and cand must have the same dtype and size")
+        super().__init__(ref.get_device(), (ref, cand))
+        n = ref.numel()
+        self._args = (ctypes.c_void_p(_dev_ptr(ref, "ref") if n else None),
+                      ctypes.c_void_p(_dev_ptr(cand, "cand") if n else None), ctypes.c_uint64(n),
+                      ctypes.c_int32(dtype_code(ref)), ctypes.c_double(rtol), ctypes.c_double(atol),
+                      ctypes.c_int32(int(bool(equal_nan))))
+        self._rep = Report()
+        self._ticket = ctypes.c_uint64(0)
+
+    def run(self) -> dict:
+        self._call(_lib.sv_compare, *self._args, ctypes.byref(self._rep))
+        return self._rep.as_dict()
+
+    def submit(self) -> CheckTicket:
+        self._call(_lib.sv_compare_submit, *self._args, ctypes.byref(self._ticket))
+        return CheckTicket(self._ticket.value, 1, False, self)
+
+
 def perturb(ref, cand, seed: int, stream_id: int, op: str, p: float = 0.0, value: float = 0.0,
             bits: int = 0, idx=None):
     """One candidate-derivation step from ref into cand (workload support)."""

@@ -187,3 +187,17 @@ def test_threads_submit_and_wait_concurrently():
     print("threads", flush=True)
     with ThreadPoolExecutor(4) as ex:
         assert all(ex.map(worker, range(4)))
+
+
+def test_prepared_calls_match_plain_calls(oracle):
+    for n in (0, 1, 70001, 1 << 20):
+        ref, cand = empty(n, "f32"), empty(n, "f32")
+        print("prepared calls", n, flush=True)
+        sv.PreparedSynth(ref, 3, 9, "normal", mean=1.0, std=2.0)()
+        assert np.array_equal(bits(ref), oracle.synth(3, 9, "f32", "normal", oracle.dist_params(mean=1.0, std=2.0), n))
+        sv.perturb(ref, cand, 3, 10, "ulp", p=0.01)
+        check = sv.PreparedCheck(ref, cand, 1e-8, 0.0)
+        want = sv.compare(ref, cand, 1e-8, 0.0)
+        assert check.run() == want and check.submit().wait() == want
+        tickets = [check.submit() for _ in range(3)]
+        assert [t.wait() for t in tickets] == [want] * 3
