@@ -14,6 +14,8 @@
 // slice of the whole tensor: only the counter base moves.  The path is ALU-bound (Philox is
 // 20 64-bit multiply-adds and 20 three-input XORs per block; Box-Muller adds a
 // logarithm, a square root and a sine / cosine pair per two elements).
+#include <type_traits>
+
 #include "sv_device.h"
 #include "sv_internal.h"
 
@@ -93,19 +95,24 @@ __device__ __forceinline__ void store_elem(void *out, uint64_t i, uint32_t x) {
 }
 
 // Vectors [0, nvec) of a 16-byte aligned output, then the n - nvec V ragged
-// tail elements, one per thread of the first threads of the grid.
-template <int DIST, int DT>
+// tail elements, one per thread of the first threads of the grid.  kNarrow:
+// every block index and byte offset of the launch fits 32 bits (the launch
+// checks), so the loop counts, the Philox counter and the addresses are
+// 32-bit (the counter's high word is 0).
+template <int DIST, int DT, bool kNarrow>
 __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                            u32x4 *__restrict__ out) {
   constexpr int E = DistTraits<DIST>::E;
   constexpr int V = DT == SV_BF16 ? 8 : 4;   // elements per 16-byte vector
   constexpr int B = V / E;                   // Philox blocks per vector
-  const uint64_t gid = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-  const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t u = gid; u < nvec; u += stride) {
+  using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
+  const Idx gid = (Idx)blockIdx.x * kBlock + threadIdx.x;
+  const Idx stride = (Idx)gridDim.x * kBlock;
+  const Idx c0 = (Idx)p.c0;
+  for (Idx u = gid; u < (Idx)nvec; u += stride) {
     uint32_t v[V];
 #pragma unroll
-    for (int b = 0; b < B; ++b) block_values<DIST>(p, p.c0 + u * B + b, v + b * E);
+    for (int b = 0; b < B; ++b) block_values<DIST>(p, (uint64_t)(c0 + u * B + b), v + b * E);
     u32x4 o;
     if constexpr (DT == SV_BF16) {
       o.x = bf16_pair<DIST>(v[0], v[1]);
@@ -120,7 +127,7 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
     else
       out[u] = o;
   }
-  const uint64_t i = nvec * V + gid;
+  const uint64_t i = nvec * V + (uint64_t)gid;
   if (i < n) {
     const uint64_t g = p.e0 + i;
     uint32_t v[E];
@@ -150,8 +157,14 @@ static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int 
     const uint64_t nvec = n / V;
     const uint64_t threads = std::max<uint64_t>(nvec, n - nvec * V);   // the tail needs n - nvec V < V threads
     const uint64_t blocks = std::min<uint64_t>((threads + kBlock - 1) / kBlock, max_blocks);
-    hipLaunchKernelGGL((synth_vec_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, nvec, n,
-                       (u32x4 *)out);
+    constexpr uint64_t B = V / DistTraits<DIST>::E;
+    const bool narrow = p.c0 + (nvec + 1) * B < (1ull << 32) && blocks * kBlock + nvec < (1ull << 32);
+    if (narrow)
+      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, true>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
+                         nvec, n, (u32x4 *)out);
+    else
+      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, false>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
+                         nvec, n, (u32x4 *)out);
   } else {
     const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, max_blocks);
     hipLaunchKernelGGL((synth_elem_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n, out);
