@@ -476,6 +476,9 @@ static uint64_t permute(uint64_t seed, uint64_t stream, const prepared *q, uint6
   return x;
 }
 
+#define SPECIAL_CLASS_BLOCKS (1ull << 62)
+#define SPECIAL_PAYLOAD_BLOCKS ((1ull << 62) + (1ull << 61))
+
 /* Value of element i: fp32 bits (UNIFORM, NORMAL, SPECIAL; fp64 uniform gives
  * fp64 bits) or the integer (INT_RANGE), in the low bits of a 64-bit word. */
 static uint64_t element_value(uint64_t seed, uint64_t stream, int32_t dtype, int32_t dist,
@@ -526,22 +529,26 @@ static uint64_t element_value(uint64_t seed, uint64_t stream, int32_t dtype, int
     uint64_t off = q->range ? (uint64_t)(((unsigned __int128)R * (unsigned __int128)q->range) >> 64) : R;
     return (uint64_t)q->lo + off;                   /* two's complement wrap-around: exact */
   }
-  /* SPECIAL: one element per block.  w0 picks the class against cumulative
-   * thresholds in the order NaN, Inf, denormal, zero, normal; w1 supplies the
-   * sign and the payload / mantissa; (w2, w3) feed Box-Muller, cos branch. */
-  or_philox_block(seed, stream, i, w);
-  uint32_t sign = w[1] & 0x80000000u;
-  uint64_t x = w[0];
-  if (x < q->t_nan) return sign | 0x7FC00000u | (w[1] & 0x003FFFFFu);
+  /* SPECIAL: the normal sequence above with some elements replaced.  Element
+   * i = 4c + k takes its class from word k of Philox block 2^62 + c, against
+   * cumulative thresholds in the order NaN, Inf, denormal, zero, normal, and
+   * its sign and payload / mantissa from word k of block 2^62 + 2^61 + c
+   * (block indices that the sequence of normal values, below 2^58, never
+   * reaches); an element of the normal class keeps the normal value. */
+  uint32_t cls[4], pay[4];
+  or_philox_block(seed, stream, SPECIAL_CLASS_BLOCKS + i / 4u, cls);
+  const uint64_t x = cls[i % 4u];
+  if (x >= q->t_zero) return element_value(seed, stream, dtype, OR_NORMAL, q, i);
+  or_philox_block(seed, stream, SPECIAL_PAYLOAD_BLOCKS + i / 4u, pay);
+  const uint32_t r = pay[i % 4u];
+  const uint32_t sign = r & 0x80000000u;
+  if (x < q->t_nan) return sign | 0x7FC00000u | (r & 0x003FFFFFu);
   if (x < q->t_inf) return sign | 0x7F800000u;
   if (x < q->t_den) {
-    uint32_t m = w[1] & 0x007FFFFFu;
+    const uint32_t m = r & 0x007FFFFFu;
     return sign | (m ? m : 1u);
   }
-  if (x < q->t_zero) return sign;
-  float zc, zs;
-  or_box_muller_f32(w[2], w[3], &zc, &zs);
-  return f2u(fmaf(q->std, zc, q->mean));
+  return sign;
 }
 
 /* Stores an element value in the tensor's format: bf16 and fp16 round the
@@ -592,8 +599,8 @@ int or_special_class_counts(uint64_t seed, uint64_t stream, const or_dist_params
   for (int k = 0; k < 5; k++) counts[k] = 0;
   for (uint64_t i = offset; i < offset + n; i++) {
     uint32_t w[4];
-    or_philox_block(seed, stream, i, w);
-    uint64_t x = w[0];
+    or_philox_block(seed, stream, SPECIAL_CLASS_BLOCKS + i / 4u, w);
+    uint64_t x = w[i % 4u];
     int cls = x < q.t_nan ? 0 : x < q.t_inf ? 1 : x < q.t_den ? 2 : x < q.t_zero ? 3 : 4;
     counts[cls]++;
   }

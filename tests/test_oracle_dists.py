@@ -243,29 +243,38 @@ SPECIAL = dict(mean=0.0, std=1e3, p_nan=0.01, p_inf=0.005, p_denorm=0.01, p_zero
 
 
 def test_special_classes_follow_thresholds_and_bit_rules(oracle):
+    # element i = 4c + k: class from word k of block 2^62 + c, sign and payload
+    # from word k of block 2^62 + 2^61 + c; the normal class keeps element i of
+    # the normal distribution with the same (seed, stream, mean, std)
     n = 1 << 16
     bits = oracle.synth(0, 0, "f32", "special", oracle.dist_params(**SPECIAL), n)
-    w = oracle.philox_blocks(0, 0, 0, n)
+    q = oracle.philox_blocks(0, 0, 1 << 62, n // 4).reshape(-1)
+    r = oracle.philox_blocks(0, 0, (1 << 62) + (1 << 61), n // 4).reshape(-1)
     widths = [math.floor(p * 2 ** 32) for p in (0.01, 0.005, 0.01, 0.01)]
     assert widths == [42949672, 21474836, 42949672, 42949672]
     t = np.cumsum(widths)
-    sign = w[:, 1] & 0x80000000
-    cls = np.searchsorted(t, w[:, 0].astype(np.int64), side="right")   # 0 nan 1 inf 2 den 3 zero 4 normal
+    sign = r & 0x80000000
+    cls = np.searchsorted(t, q.astype(np.int64), side="right")   # 0 nan 1 inf 2 den 3 zero 4 normal
     mag = bits & 0x7FFFFFFF
     spec = cls < 4
     assert np.all((bits[spec] & 0x80000000) == sign[spec])
     nan = cls == 0
-    assert np.all(bits[nan] == (sign[nan] | 0x7FC00000 | (w[nan, 1] & 0x3FFFFF)))
+    assert np.all(bits[nan] == (sign[nan] | 0x7FC00000 | (r[nan] & 0x3FFFFF)))
     inf = cls == 1
     assert np.all(mag[inf] == 0x7F800000)
     den = cls == 2
-    m = w[den, 1] & 0x7FFFFF
+    m = r[den] & 0x7FFFFF
     assert np.all(mag[den] == np.where(m == 0, 1, m))
     assert np.all(mag[cls == 3] == 0)
-    nor = np.nonzero(cls == 4)[0]
-    for i in nor[:2000]:
-        zc, _ = oracle.box_muller_f32(int(w[i, 2]), int(w[i, 3]))
-        assert float(f32(bits[i])) == rne32_exact(Fraction(float(np.float32(1e3))) * Fraction(float(zc)))
+    nor = cls == 4
+    normal = oracle.synth(0, 0, "f32", "normal", oracle.dist_params(mean=0.0, std=1e3), n)
+    assert np.array_equal(bits[nor], normal[nor])
+    w = oracle.philox_blocks(0, 0, 0, n // 4)
+    for i in np.nonzero(nor)[0][:2000]:
+        c, k = divmod(int(i), 4)
+        zc, zs = oracle.box_muller_f32(int(w[c, 2 * (k // 2)]), int(w[c, 2 * (k // 2) + 1]))
+        z = zc if k % 2 == 0 else zs
+        assert float(f32(bits[i])) == rne32_exact(Fraction(float(np.float32(1e3))) * Fraction(float(z)))
     x = f32(bits)
     assert np.all(np.isnan(x[nan])) and np.all(np.isinf(x[inf]))
     assert np.all(np.isfinite(x[cls >= 2]))
