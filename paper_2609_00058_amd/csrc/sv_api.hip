@@ -649,7 +649,7 @@ int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t di
     return fail(SV_ERR_INVALID_ARG, "sv_synth_window: elements [%llu, %llu) lie past the %llu values of the permutation",
                 (unsigned long long)offset, (unsigned long long)(offset + n), (unsigned long long)p.range);
   const uint64_t per_block =
-      dist == SV_SPECIAL || dist == SV_PERMUTATION ? 1
+      dist == SV_PERMUTATION ? 1
       : ((dist == SV_INT_RANGE && dtype != SV_U8) || (dist == SV_UNIFORM && dtype == SV_F64)) ? 2
                                                                                             : 4;
   p.e0 = offset;

@@ -25,7 +25,24 @@ template <int DIST> struct DistTraits;
 template <> struct DistTraits<SV_UNIFORM> { static constexpr int E = 4; };
 template <> struct DistTraits<SV_NORMAL> { static constexpr int E = 4; };
 template <> struct DistTraits<SV_INT_RANGE> { static constexpr int E = 2; };
-template <> struct DistTraits<SV_SPECIAL> { static constexpr int E = 1; };
+template <> struct DistTraits<SV_SPECIAL> { static constexpr int E = 4; };
+
+// Special values: the normal sequence with some elements replaced, their
+// class and payload words from Philox blocks that the normal values (block
+// indices below 2^58) never reach.
+constexpr uint64_t kSpecialClassBlocks = 1ull << 62;
+constexpr uint64_t kSpecialPayloadBlocks = (1ull << 62) + (1ull << 61);
+
+__device__ __forceinline__ void special_overlay(const SynthParams &p, uint32_t x, uint32_t r, uint32_t &v) {
+  if (x < p.t_zero) {
+    const uint32_t sign = r & 0x80000000u;
+    const uint32_t m = r & 0x007FFFFFu;
+    v = x < p.t_nan   ? sign | 0x7FC00000u | (r & 0x003FFFFFu)
+        : x < p.t_inf ? sign | 0x7F800000u
+        : x < p.t_den ? sign | (m ? m : 1u)
+                      : sign;
+  }
+}
 
 // The E element values (fp32 bits or int32 bits) of Philox block `block`.
 template <int DIST>
@@ -52,26 +69,23 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
     v[0] = (uint32_t)(int32_t)(p.lo + (int64_t)__umul64hi(r0, p.range));
     v[1] = (uint32_t)(int32_t)(p.lo + (int64_t)__umul64hi(r1, p.range));
   } else {
-    // class by cumulative thresholds on w0 (NaN, Inf, denormal, zero, normal);
-    // w1 carries the sign and the payload / mantissa; (w2, w3) feed Box-Muller
-    const uint32_t sign = w.y & 0x80000000u;
-    const uint64_t x = w.x;
-    uint32_t out;
-    if (x < p.t_nan) {
-      out = sign | 0x7FC00000u | (w.y & 0x003FFFFFu);
-    } else if (x < p.t_inf) {
-      out = sign | 0x7F800000u;
-    } else if (x < p.t_den) {
-      const uint32_t m = w.y & 0x007FFFFFu;
-      out = sign | (m ? m : 1u);
-    } else if (x < p.t_zero) {
-      out = sign;
-    } else {
-      float zc, zs;
-      box_muller(w.z, w.w, zc, zs);
-      out = as_u32(__builtin_fmaf(p.std, zc, p.mean));
-    }
-    v[0] = out;
+    // the normal values of the block, then the overlay: element k of the
+    // block takes its class from word k of block 2^62 + block (cumulative
+    // thresholds: NaN, Inf, denormal, zero, normal) and its sign and payload
+    // / mantissa from word k of block 2^62 + 2^61 + block
+    float c0, s0, c1, s1;
+    box_muller(w.x, w.y, c0, s0);
+    box_muller(w.z, w.w, c1, s1);
+    v[0] = as_u32(__builtin_fmaf(p.std, c0, p.mean));
+    v[1] = as_u32(__builtin_fmaf(p.std, s0, p.mean));
+    v[2] = as_u32(__builtin_fmaf(p.std, c1, p.mean));
+    v[3] = as_u32(__builtin_fmaf(p.std, s1, p.mean));
+    const u32x4 q = philox_block(key, kSpecialClassBlocks + block);
+    const u32x4 r = philox_block(key, kSpecialPayloadBlocks + block);
+    special_overlay(p, q.x, r.x, v[0]);
+    special_overlay(p, q.y, r.y, v[1]);
+    special_overlay(p, q.z, r.z, v[2]);
+    special_overlay(p, q.w, r.w, v[3]);
   }
 }
 
@@ -230,23 +244,6 @@ __device__ __forceinline__ void wide_block(const SynthParams &p, uint64_t block,
   }
 }
 
-// The V stored values of output vector u (the window starts on a block).
-template <int DIST, int DT>
-__device__ __forceinline__ void wide_vector(const SynthParams &p, uint64_t u, uint64_t *v) {
-  constexpr int E = Wide<DIST, DT>::E, V = Wide<DIST, DT>::V;
-  if constexpr (V >= E) {
-#pragma unroll
-    for (int b = 0; b < V / E; ++b) wide_block<DIST, DT>(p, p.c0 + u * (V / E) + b, v + b * E);
-  } else {                                     // fp64 normal: one Box-Muller pair of the block
-    const u32x4 w = philox_block(Key{p.k0, p.k1, p.s0, p.s1}, p.c0 + u / 2);
-    const bool second = (u & 1u) != 0u;
-    float zc, zs;
-    box_muller(second ? w.z : w.x, second ? w.w : w.y, zc, zs);
-    v[0] = widen_f32_bits(as_u32(__builtin_fmaf(p.std, zc, p.mean)));
-    v[1] = widen_f32_bits(as_u32(__builtin_fmaf(p.std, zs, p.mean)));
-  }
-}
-
 template <int DT>
 __device__ __forceinline__ void store_wide(void *out, uint64_t i, uint64_t x) {
   if constexpr (DT == SV_F16) ((uint16_t *)out)[i] = (uint16_t)x;
@@ -262,30 +259,47 @@ __device__ __forceinline__ uint64_t wide_elem(const SynthParams &p, uint64_t g) 
   return v[g % E];
 }
 
+// Groups of G 16-byte vectors, W = G V elements: one vector (G = 1) made of
+// V / E whole blocks, or, where a vector holds fewer elements than a block
+// (fp64 normal and special: V = 2, E = 4), the G = E / V vectors of one
+// block, so that no Philox word is wasted.  Then the n - groups W ragged tail
+// elements, one per thread of the first threads of the grid (the window
+// starts on a block).
 template <int DIST, int DT>
-__global__ __launch_bounds__(kBlock) void synth_wide_vec_kernel(SynthParams p, uint64_t nvec, uint64_t n,
+__global__ __launch_bounds__(kBlock) void synth_wide_vec_kernel(SynthParams p, uint64_t ngroups, uint64_t n,
                                                                 u32x4 *__restrict__ out) {
-  constexpr int V = Wide<DIST, DT>::V;
+  constexpr int E = Wide<DIST, DT>::E, V = Wide<DIST, DT>::V;
+  constexpr int G = V >= E ? 1 : E / V;
+  constexpr int W = G * V;
   const uint64_t gid = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
-  for (uint64_t u = gid; u < nvec; u += stride) {
-    uint64_t v[V];
-    wide_vector<DIST, DT>(p, u, v);
-    u32x4 o;
-    if constexpr (DT == SV_F16) {
+  for (uint64_t g = gid; g < ngroups; g += stride) {
+    uint64_t v[W];
+    if constexpr (G == 1) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) o[k] = (uint32_t)v[2 * k] | ((uint32_t)v[2 * k + 1] << 16);
-    } else if constexpr (DT == SV_U8) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-        o[k] = (uint32_t)v[4 * k] | ((uint32_t)v[4 * k + 1] << 8) | ((uint32_t)v[4 * k + 2] << 16) |
-               ((uint32_t)v[4 * k + 3] << 24);
+      for (int b = 0; b < V / E; ++b) wide_block<DIST, DT>(p, p.c0 + g * (V / E) + b, v + b * E);
     } else {
-      o = u32x4{(uint32_t)v[0], (uint32_t)(v[0] >> 32), (uint32_t)v[1], (uint32_t)(v[1] >> 32)};
+      wide_block<DIST, DT>(p, p.c0 + g, v);
     }
-    out[u] = o;
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      const uint64_t *x = v + j * V;
+      u32x4 o;
+      if constexpr (DT == SV_F16) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) o[k] = (uint32_t)x[2 * k] | ((uint32_t)x[2 * k + 1] << 16);
+      } else if constexpr (DT == SV_U8) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          o[k] = (uint32_t)x[4 * k] | ((uint32_t)x[4 * k + 1] << 8) | ((uint32_t)x[4 * k + 2] << 16) |
+                 ((uint32_t)x[4 * k + 3] << 24);
+      } else {
+        o = u32x4{(uint32_t)x[0], (uint32_t)(x[0] >> 32), (uint32_t)x[1], (uint32_t)(x[1] >> 32)};
+      }
+      out[g * G + j] = o;
+    }
   }
-  const uint64_t i = nvec * V + gid;
+  const uint64_t i = ngroups * W + gid;
   if (i < n) store_wide<DT>(out, i, wide_elem<DIST, DT>(p, p.e0 + i));
 }
 
@@ -298,14 +312,15 @@ __global__ __launch_bounds__(kBlock) void synth_wide_elem_kernel(SynthParams p, 
 
 template <int DIST, int DT>
 static hipError_t launch_wide(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
-  constexpr uint64_t V = Wide<DIST, DT>::V;
+  constexpr uint64_t E = Wide<DIST, DT>::E, V = Wide<DIST, DT>::V;
+  constexpr uint64_t W = V >= E ? V : E;          // elements per group of vectors
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
-  if (((uintptr_t)out & 15u) == 0 && p.e0 % Wide<DIST, DT>::E == 0) {
-    const uint64_t nvec = n / V;
-    const uint64_t threads = std::max<uint64_t>(nvec, n - nvec * V);
+  if (((uintptr_t)out & 15u) == 0 && p.e0 % E == 0) {
+    const uint64_t ngroups = n / W;
+    const uint64_t threads = std::max<uint64_t>(ngroups, n - ngroups * W);   // the tail needs < W threads
     const uint64_t blocks = std::min<uint64_t>((threads + kBlock - 1) / kBlock, max_blocks);
-    hipLaunchKernelGGL((synth_wide_vec_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, nvec,
-                       n, (u32x4 *)out);
+    hipLaunchKernelGGL((synth_wide_vec_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
+                       ngroups, n, (u32x4 *)out);
   } else {
     const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, max_blocks);
     hipLaunchKernelGGL((synth_wide_elem_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n,
