@@ -684,7 +684,7 @@ int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
   if (!jobs) return fail(SV_ERR_INVALID_ARG, "sv_synth_batched: jobs is NULL");
   std::vector<SynthParams> params(njobs);
   std::vector<uint32_t> table_jobs, direct_jobs;
-  uint64_t tiles = 0;
+  uint64_t total_vecs = 0;
   for (uint32_t k = 0; k < njobs; ++k) {
     const sv_synth_job &j = jobs[k];
     int rc = prepare_synth(j.seed, j.stream_id, j.dtype, j.dist, &j.params, j.n, j.out, &params[k]);
@@ -698,12 +698,15 @@ int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
       continue;
     }
     table_jobs.push_back(k);
-    tiles += (units_of(j.dtype, j.n) + kBlock - 1) / kBlock;
+    total_vecs += units_of(j.dtype, j.n);
   }
   if (table_jobs.empty() && direct_jobs.empty()) return SV_OK;
   DeviceState *ds;
   int rc = current_device(&ds);
   if (rc) return rc;
+  const uint32_t rounds = synth_tile_rounds(total_vecs, ds->cus);   // vectors per thread in a tile
+  const uint64_t tile_vecs = (uint64_t)rounds * kBlock;
+  uint64_t tiles = 0;
   std::lock_guard<std::mutex> lock(ds->mu);
   hipStream_t st = t_stream;
   hipEvent_t e0 = nullptr, e1 = nullptr;
@@ -737,14 +740,16 @@ int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
       d.tile_begin = begin;
       d.kind = j.dist * 4 + j.dtype;
       d.vec_ok = ((uintptr_t)j.out & 15u) == 0 ? 1 : 0;
-      begin += (d.nvec + kBlock - 1) / kBlock;
+      begin += (d.nvec + tile_vecs - 1) / tile_vecs;
     }
+    tiles = begin;
     SV_HIP(hipMemcpyAsync(ds->synth_table, ds->h_synth, nt * sizeof(SynthJob), hipMemcpyHostToDevice, st),
            "job table copy to device");
     SV_HIP(hipEventRecord(ds->synth_copied, st), "hipEventRecord");
   }
   if (e0) (void)hipEventRecord(e0, st);
-  if (nt) SV_HIP(launch_synth_batched(ds->synth_table, nt, tiles, ds->cus, st), "batched synthesis kernel launch");
+  if (nt)
+    SV_HIP(launch_synth_batched(ds->synth_table, nt, tiles, rounds, ds->cus, st), "batched synthesis kernel launch");
   for (uint32_t k : direct_jobs)
     SV_HIP(launch_synth(jobs[k].dtype, jobs[k].dist, params[k], jobs[k].n, jobs[k].out, ds->cus, st),
            "synthesis kernel launch");

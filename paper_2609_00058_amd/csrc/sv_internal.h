@@ -37,6 +37,12 @@ namespace sv {
 
 constexpr int kBlock = 256;          // threads per workgroup of every streaming kernel
 constexpr int kCmpBlock = SV_CMP_BLOCK;   // threads per workgroup of the check kernel
+#ifndef SV_SYNTH_TILE_ROUNDS
+#define SV_SYNTH_TILE_ROUNDS 32      // at most this many vectors per thread in a tile of the batched synthesis
+#endif
+#ifndef SV_SYNTH_TILES_PER_CU
+#define SV_SYNTH_TILES_PER_CU 32     // ... as long as a batch still has this many tiles per CU
+#endif
 constexpr int kWave = 64;            // CDNA wavefront
 constexpr uint64_t kNone = ~0ull;    // "no mismatch yet"
 
@@ -73,8 +79,13 @@ struct SynthJob {
   int32_t vec_ok;               // out is 16-byte aligned
 };
 
-hipError_t launch_synth_batched(const SynthJob *jobs, uint32_t njobs, uint64_t total_tiles, int cus,
-                                hipStream_t stream);
+// Vectors per thread in a tile of a batch of total_vecs 16-byte vectors.
+inline uint32_t synth_tile_rounds(uint64_t total_vecs, int cus) {
+  const uint64_t r = total_vecs / ((uint64_t)cus * SV_SYNTH_TILES_PER_CU * kBlock);
+  return (uint32_t)(r < 1 ? 1 : r > SV_SYNTH_TILE_ROUNDS ? SV_SYNTH_TILE_ROUNDS : r);
+}
+hipError_t launch_synth_batched(const SynthJob *jobs, uint32_t njobs, uint64_t total_tiles, uint32_t rounds,
+                                int cus, hipStream_t stream);
 
 // ----------------------------------------------------------------- candidates
 struct PerturbParams {
