@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, AMD public figure
 ELEMENTWISE = ("copy", "ulp", "scale", "special_flip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
-KERNEL_NAMES = {"synth": "void sv::synth_vec_kernel<1, 0>", "compare": "void sv::compare_kernel<true, 1, false>"}
+KERNEL_NAMES = {"synth": "void sv::synth_vec_kernel<1, 0, true>", "compare": "void sv::compare_kernel<true, 1, false>"}
 
 
 def kernel_source_hash():

@@ -152,7 +152,8 @@ typedef struct {
  *
  * Job k writes exactly what sv_synth(jobs[k].seed, jobs[k].stream_id,
  * jobs[k].dtype, jobs[k].dist, &jobs[k].params, jobs[k].n, jobs[k].out)
- * writes.  The work is cut into tiles of 1,024 16-byte output vectors spread
+ * writes.  The work is cut into tiles of 256 to 8,192 16-byte output vectors
+ * (larger tiles for larger batches, so that every CU still gets dozens) spread
  * over the whole grid, so many small tensors cost one launch.  jobs is a host
  * array read during the call; its device copy goes through the library's
  * scratch on the calling thread's stream.  Asynchronous: returns after the
