@@ -208,12 +208,14 @@ int sv_compare_batched(const sv_segment *segs, uint32_t nseg, sv_report *reports
  * failing output ends its candidate's validation, e.g. G candidates x their
  * outputs of one round in one call).
  *   mode = SV_CHECK_FULL (0): exactly sv_compare_batched.
- *   mode = SV_CHECK_STOP_AT_FIRST (1): the check of a segment stops where
- *     it first meets a mismatch (each part of the segment checked in parallel
- *     stops at its own first one), but every element before the segment's
- *     first mismatch is still checked.  A passing segment gets its full
- *     report.  A failing one gets n, mismatches = 1 (meaning "at least one")
- *     and the exact first_mismatch; its other fields are 0.
+ *   mode = SV_CHECK_STOP_AT_FIRST (1): the check of a segment stops near
+ *     where it first meets a mismatch (the segment is swept from the front by
+ *     workgroups of its own, which tell each other of the mismatches they
+ *     find), but every element before the segment's first mismatch is still
+ *     checked.  A passing segment gets its full report (its fp64 error sum
+ *     may differ from mode 0's in the last bits: another summation order).
+ *     A failing one gets n, mismatches = 1 (meaning "at least one") and the
+ *     exact first_mismatch; its other fields are 0.
  * Errors as sv_compare_batched; UNSUPPORTED for another mode.
  */
 enum { SV_CHECK_FULL = 0, SV_CHECK_STOP_AT_FIRST = 1 };

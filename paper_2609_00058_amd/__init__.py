@@ -11,6 +11,8 @@ import ctypes
 import os
 import threading
 
+import numpy as np
+
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsynthverify.so")
 
@@ -59,6 +61,19 @@ class Report(ctypes.Structure):
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+# the same layout as a numpy structured type: reports as one array, without a
+# Python object per report (as_array=True below)
+REPORT_DTYPE = np.dtype([(name, {ctypes.c_uint64: "<u8", ctypes.c_int64: "<i8", ctypes.c_double: "<f8"}[t])
+                         for name, t in Report._fields_])
+assert REPORT_DTYPE.itemsize == ctypes.sizeof(Report)
+
+
+def _reports(reps, n: int, as_array: bool):
+    if as_array:
+        return np.frombuffer(reps, dtype=REPORT_DTYPE, count=n)   # a view of the filled array
+    return [reps[k].as_dict() for k in range(n)]
 
 
 class Segment(ctypes.Structure):
@@ -298,43 +313,48 @@ def _as_batch(segments):
     return segments if isinstance(segments, SegmentBatch) else SegmentBatch(segments)
 
 
-def compare_batched(segments, stop_at_first: bool = False) -> list:
+def compare_batched(segments, stop_at_first: bool = False, as_array: bool = False):
     """segments: list of (ref, cand, rtol, atol, equal_nan), or a SegmentBatch;
-    one launch, one report each.
+    one launch, one report each (a list of dicts, or with as_array a numpy array
+    of REPORT_DTYPE, one record per segment).
     stop_at_first: a failing segment is checked only as far as needed to know
     its first mismatch exactly; its report then holds n, mismatches = 1 and
     first_mismatch, everything else 0."""
     if not isinstance(segments, SegmentBatch) and not segments:
-        return []
+        return np.zeros(0, REPORT_DTYPE) if as_array else []
     b = _as_batch(segments)
     reps = (Report * b.n)()
     _run(b.tensors[0][0], _lib.sv_compare_batched_mode, b.arr, b.n, 1 if stop_at_first else 0, reps)
-    return [reps[k].as_dict() for k in range(b.n)]
+    return _reports(reps, b.n, as_array)
 
 
 class CheckTicket:
     """A submitted check (compare_submit, compare_batched_submit).  It keeps its
     tensors alive until waited for; wait() returns what compare() or
-    compare_batched() would have returned."""
+    compare_batched() would have returned (with as_array, the reports as a numpy
+    array of REPORT_DTYPE, one record per segment, also for a single tensor)."""
 
     def __init__(self, ticket: int, nreports: int, batched: bool, keep):
         self.ticket, self.nreports, self.batched, self._keep = ticket, nreports, batched, keep
-        self._result = None
+        self._reps, self._result = None, None
 
     def ready(self) -> bool:
-        if self._result is not None:
+        if self._reps is not None:
             return True
         flag = ctypes.c_int32(0)
         _check(_lib.sv_compare_ready(self.ticket, ctypes.byref(flag)))
         return bool(flag.value)
 
-    def wait(self):
-        if self._result is None:
+    def wait(self, as_array: bool = False):
+        if self._reps is None:
             reps = (Report * max(self.nreports, 1))()
             _check(_lib.sv_compare_wait(self.ticket, reps, self.nreports))
-            out = [reps[k].as_dict() for k in range(self.nreports)]
+            self._reps, self._keep = reps, None
+        if as_array:
+            return _reports(self._reps, self.nreports, True)
+        if self._result is None:
+            out = _reports(self._reps, self.nreports, False)
             self._result = out if self.batched else out[0]
-            self._keep = None
         return self._result
 
 

@@ -94,6 +94,8 @@ struct DeviceState {
   bool synth_pending = false;        // the two events above have been recorded
   uint32_t *counters = nullptr;      // arrival counters of the check (zero between launches)
   size_t counters_cap = 0;
+  uint64_t *firsts = nullptr;        // stop-at-first: a tagged first-mismatch word per segment
+  size_t firsts_cap = 0;
   uint64_t *h_done = nullptr;        // pinned, host-mapped, coherent: one completion word per slot
   uint64_t *d_done = nullptr;        // its device address
   uint64_t seq = 0;                  // sequence number of the last check submitted
@@ -176,6 +178,23 @@ int ensure_counters(DeviceState *ds, size_t need) {
   int rc = ensure_device(ds->counters, ds->counters_cap, need, "arrival counters");
   if (rc) return rc;
   SV_HIP(hipMemset(ds->counters, 0, ds->counters_cap * sizeof(uint32_t)), "hipMemset(arrival counters)");
+  return SV_OK;
+}
+
+// The stop-at-first words; a fresh allocation is cleared on the calling
+// thread's stream, ahead of the check that needs it (a zero word carries tag 0
+// and the tile 2^32 - 1, past every tile: it stops nothing).
+int ensure_firsts(DeviceState *ds, size_t need) {
+  if (need <= ds->firsts_cap) return SV_OK;
+  int rc = ensure_device(ds->firsts, ds->firsts_cap, need, "first-mismatch words");
+  if (rc) return rc;
+  const hipError_t e = launch_fill_u64(ds->firsts, ds->firsts_cap, 0, t_stream);
+  if (e != hipSuccess) {
+    (void)hipFree(ds->firsts);
+    ds->firsts = nullptr;
+    ds->firsts_cap = 0;
+    return hip_fail(e, "clearing the first-mismatch words");
+  }
   return SV_OK;
 }
 
@@ -321,7 +340,7 @@ SegDesc make_desc(const sv_segment &g, uint64_t unit_begin) {
   d.dtype = g.dtype;
   d.equal_nan = g.equal_nan ? 1 : 0;
   d.vec_ok = (((uintptr_t)g.ref | (uintptr_t)g.cand) & 15u) == 0 ? 1 : 0;
-  d.pad = 0;
+  d.blk = 0;
   return d;
 }
 
@@ -392,6 +411,11 @@ void plan_batched(const sv_segment *segs, uint32_t nseg, int32_t mode, int cus, 
   plan.args.nseg = nseg;
   plan.total_units = plan.args.total_units = total;
   if (total) compare_grid(total, cus, true, &plan.nblocks, &plan.args.chunk);
+  if (total && plan.stop_at_first) {   // workgroups of their own per segment
+    uint64_t blocks = 0;
+    for (uint32_t k = 0; k < nseg; ++k) blocks += stop_blocks(units_of(segs[k].dtype, segs[k].n), plan.args.chunk);
+    plan.nblocks = blocks <= kMaxStopBlocks ? (uint32_t)blocks : 0;   // 0: too many, refused at submission
+  }
 }
 
 // Queues the kernels of `plan` into slot k on the selected stream and marks
@@ -413,10 +437,16 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
     sl.pending = true;
     return SV_OK;
   }
-  const bool grow = (size_t)plan.nblocks + nseg > ds->partials_cap || (batched && nseg > ds->table_cap);
+  if (plan.nblocks == 0)
+    return fail(SV_ERR_INVALID_ARG, "stop-at-first check of %u segments: more than %u workgroups", nseg,
+                (unsigned)kMaxStopBlocks);
+  const size_t nfirsts = plan.stop_at_first ? (size_t)nseg * kFirstStride : 0;
+  const bool grow = (size_t)plan.nblocks + nseg > ds->partials_cap || (batched && nseg > ds->table_cap) ||
+                    nfirsts > ds->firsts_cap;
   int rc = SV_OK;
   if (grow || (ds->has_last && ds->last_stream != st)) rc = drain_pending(ds);
   if (!rc) rc = ensure_device(ds->partials, ds->partials_cap, (size_t)plan.nblocks + nseg, "partials");
+  if (!rc && nfirsts) rc = ensure_firsts(ds, nfirsts);
   if (!rc && batched) rc = ensure_device(ds->table, ds->table_cap, nseg, "segment table");
   if (!rc && batched) rc = ensure_pinned(sl.h_table, sl.h_table_cap, nseg, "segment table staging");
   if (!rc) rc = ensure_reports(sl, nseg);
@@ -425,22 +455,33 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   if (rc) return rc;
   CompareArgs &args = plan.args;
   if (batched) {
-    uint64_t begin = 0;
+    uint64_t begin = 0, blk = 0;
     for (uint32_t j = 0; j < nseg; ++j) {
       sl.h_table[j] = make_desc(plan.segs[j], begin);
-      begin += units_of(plan.segs[j].dtype, plan.segs[j].n);
+      const uint64_t units = units_of(plan.segs[j].dtype, plan.segs[j].n);
+      if (plan.stop_at_first) {
+        sl.h_table[j].blk = (uint32_t)blk;
+        blk += stop_blocks(units, plan.args.chunk);
+      }
+      begin += units;
     }
     SV_HIP(hipMemcpyAsync(ds->table, sl.h_table, nseg * sizeof(SegDesc), hipMemcpyHostToDevice, st),
            "segment table copy to device");
     args.segs = ds->table;
   }
   args.stop_at_first = plan.stop_at_first ? 1 : 0;
+  args.firsts = ds->firsts;
   args.fused = batched ? 0 : plan.nblocks == 1 ? 1 : plan.nblocks <= SV_CMP_LAST_BLOCK_MAX ? 2 : 0;
   args.partials = ds->partials;
   args.counter = ds->counters;
   args.reports = sl.d_reports;
   args.done = ds->d_done + (size_t)k * kDoneStride;
   args.seq = ds->seq + 1;
+  if (plan.stop_at_first && (uint32_t)args.seq == 0) {
+    // the words' 32-bit launch tags start over: clear the tags of 2^32 launches ago
+    const hipError_t e = launch_fill_u64(ds->firsts, ds->firsts_cap, 0, st);
+    if (e != hipSuccess) return hip_fail(e, "clearing the first-mismatch words");
+  }
   hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
   if (g_prof_on.load()) {
     e0 = take_event();
@@ -1071,6 +1112,8 @@ int sv_shutdown(void) {
     if (s->synth_copied) (void)hipEventDestroy(s->synth_copied);
     if (s->synth_done) (void)hipEventDestroy(s->synth_done);
     if (s->counters) (void)hipFree(s->counters);
+    if (s->firsts) (void)hipFree(s->firsts);
+    s->firsts = nullptr; s->firsts_cap = 0;
     if (s->h_done) (void)hipHostFree(s->h_done);
     s->counters = nullptr; s->counters_cap = 0;
     s->h_done = nullptr; s->d_done = nullptr;

@@ -448,16 +448,60 @@ __device__ __forceinline__ void lane_step(LaneAcc &L) {
   L.maxrel = fmax(L.maxrel, lane_pair<kStep>(L.maxrel));
 }
 
-// Early exit (kStop): a wave leaves its piece once its next tile starts past
-// its own first mismatch.  Every unit below a wave's first mismatch is still
-// checked, so the segment's first mismatch (the smallest over its waves) stays
-// exact; the other statistics cover a timing-independent but partial set.  A
-// shared "first mismatch so far" word that every wave could poll was measured
-// slower: thousands of device-scope atomics and uncached reads on a few words
-// queue up at their memory channels.
-// Units [ulo, uhi) of one segment -> a workgroup partial, valid on thread 0.
+// What a stop-at-first workgroup shares: the segment's word in `firsts` and
+// an LDS copy of the smallest tile known to the workgroup to hold a mismatch.
+struct StopCtx {
+  uint64_t *word;
+  uint32_t epoch;               // the launch's tag in the word's high half
+  uint32_t *lim;                // LDS
+};
+
+// Early exit (kStop): a wave leaves the segment once its next tile t starts
+// past its own first mismatch, or lies past a tile that holds one.  Only
+// units past a known mismatch are skipped, so the segment's first mismatch
+// (the smallest over its waves) stays exact; every other statistic of a
+// failing segment is dropped from its report.  A wave posts its own first
+// mismatch once: to the workgroup's LDS minimum and, when that improves it,
+// to the segment's word (an atomic max of the tagged, inverted tile index; a
+// word left by an earlier launch carries another tag and counts as nothing).
+// Each iteration a wave reads the LDS minimum; one wave per iteration (each
+// wave on its first) also reads the segment's word, which costs one uncached
+// 8-byte load per workgroup per tile instead of one per wave.
+template <int V>
+__device__ __forceinline__ bool leave_segment(const StopCtx &sc, uint64_t t, uint64_t wbase, const WaveAcc &W,
+                                              bool &told, uint32_t it, uint32_t wave, uint32_t lane) {
+  if (W.first != kNone && !told) {
+    told = true;
+    const uint32_t f = (uint32_t)(W.first / V / kCmpTile);
+    if (lane == 0) {
+      const uint32_t old = __hip_atomic_fetch_min(sc.lim, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (f < old)
+        __hip_atomic_fetch_max(sc.word, ((uint64_t)sc.epoch << 32) | (0xFFFFFFFFu - f), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+  if (wbase * V > W.first) return true;
+  uint32_t lim = __hip_atomic_load(sc.lim, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  if (it == 0 || it % kWavesPerBlock == wave) {
+    const uint64_t w = __hip_atomic_load(sc.word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((uint32_t)(w >> 32) == sc.epoch) {
+      const uint32_t g = 0xFFFFFFFFu - (uint32_t)w;
+      if (g < lim) {
+        lim = g;
+        if (lane == 0) __hip_atomic_fetch_min(sc.lim, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+    }
+  }
+  return t / kCmpTile > __builtin_amdgcn_readfirstlane(lim);
+}
+
+// The tiles ulo, ulo + step, ... below uhi of one segment (units, relative to
+// the segment; ulo and step multiples of kCmpTile) -> a workgroup partial,
+// valid on thread 0.  A plain launch passes its contiguous piece with step =
+// kCmpTile; a stop-at-first launch its share of the segment's tiles.
 template <int DT, bool kStop = false>
-__device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Partial *lds) {
+__device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, uint64_t step, const StopCtx *sc,
+                               Partial *lds) {
   constexpr int V = Elem<DT>::V;
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const u32x4 *yv4 = (const u32x4 *)sd.ref;
@@ -469,10 +513,16 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
   const uint64_t full_end = sd.vec_ok ? (uhi < n / V ? uhi : n / V) : 0;
   LaneAcc L{0.0, 0.0, 0.0, 0.0, 0, 0, 0, 1};
   WaveAcc W{0, kNone, 0, 0, 0, 0};
-  uint64_t base = ulo + wave * kWave;
+  const uint64_t wofs = (uint64_t)wave * kWave;   // this wave's units in a tile: wofs + k * kCmpBlock + lane
+  bool told = false;
+  uint32_t it = 0;
+  uint64_t t = ulo;
   // whole tiles: kUnroll sub-iterations of kCmpBlock units, every unit full
-  for (; base + (uint64_t)(kUnroll - 1) * kCmpBlock + kWave <= full_end; base += (uint64_t)kCmpBlock * kUnroll) {
-    if (kStop && base * V > W.first) break;
+  for (; t + wofs + (uint64_t)(kUnroll - 1) * kCmpBlock + kWave <= full_end; t += step, ++it) {
+    if constexpr (kStop) {
+      if (leave_segment<V>(*sc, t, t + wofs, W, told, it, wave, lane)) break;
+    }
+    const uint64_t base = t + wofs;
     u32x4 yv[kUnroll], av[kUnroll];
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k) {
@@ -485,9 +535,14 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
       check_unit<DT>(yv[k], av[k], (base + (uint64_t)k * kCmpBlock) * V, rtol, atol, eqn, L, W);
     if constexpr (kSmallInt<DT>) fold_int_sum(L);
   }
-  // the rest, one sub-iteration at a time, guarded (same unit order)
-  for (; base < uhi; base += kCmpBlock) {
-    if (kStop && base * V > W.first) break;
+  // the rest, one sub-iteration at a time, guarded (same unit order); a plain
+  // launch's tiles are contiguous, a stop-at-first share jumps by `step`
+  // after each tile's last sub-iteration
+  for (uint64_t base = t + wofs, k = 0; base < uhi; ++k) {
+    if constexpr (kStop) {
+      if (k % kUnroll == 0 && leave_segment<V>(*sc, base - wofs, base, W, told, it++, wave, lane)) break;
+      if (base * V > W.first) break;
+    }
     const uint64_t u = base + lane;
     u32x4 yv = u32x4{0, 0, 0, 0}, av = u32x4{0, 0, 0, 0};
     if (u < full_end) {
@@ -505,6 +560,18 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Pa
     }
     check_unit<DT>(yv, av, base * V, rtol, atol, eqn, L, W);
     if constexpr (kSmallInt<DT>) fold_int_sum(L);
+    if constexpr (kStop)
+      base += (k % kUnroll == kUnroll - 1) ? step - (uint64_t)(kUnroll - 1) * kCmpBlock : (uint64_t)kCmpBlock;
+    else
+      base += kCmpBlock;
+  }
+  if constexpr (kStop) {
+    // a mismatch in the wave's last tile: post it for the segment's other workgroups
+    if (W.first != kNone && !told && lane == 0) {
+      const uint32_t f = (uint32_t)(W.first / V / kCmpTile);
+      __hip_atomic_fetch_max(sc->word, ((uint64_t)sc->epoch << 32) | (0xFFFFFFFFu - f), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
   if constexpr (kSmallInt<DT>) {
     L.maxabs = (double)L.imax;
@@ -558,9 +625,12 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
   const SegDesc sd = kSingle ? args.single : args.segs[s];
   const uint64_t units = units_of(sd.dtype, sd.n);
   if (units != 0) {                  // empty segments are reported by the host
-    const uint64_t b0 = sd.unit_begin / args.chunk;
-    const uint64_t b1 = (sd.unit_begin + units - 1) / args.chunk;
-    const Partial *P = args.partials + s;
+    // the segment's workgroups and their slots: a piece of workgroups b0..b1 in
+    // slots b + s, or (stop at first) workgroups of its own in slots b
+    const bool own = !kSingle && args.stop_at_first;
+    const uint64_t b0 = own ? sd.blk : sd.unit_begin / args.chunk;
+    const uint64_t b1 = own ? sd.blk + stop_blocks(units, args.chunk) - 1 : (sd.unit_begin + units - 1) / args.chunk;
+    const Partial *P = args.partials + (own ? 0 : s);
     Partial acc = empty_partial();
     uint64_t b = b0 + tid;
     for (; b + 3 * kFinBlock <= b1; b += 4 * kFinBlock) {
@@ -590,16 +660,17 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
 // The check of one piece for the element types in kMask (bit 1 << dtype):
 // with one type the code of that type only, else a branch on the segment's.
 template <int kMask, bool kStop, int DT = 0>
-__device__ __forceinline__ Partial check_any(const SegDesc &sd, uint64_t ulo, uint64_t uhi, Partial *lds) {
+__device__ __forceinline__ Partial check_any(const SegDesc &sd, uint64_t ulo, uint64_t uhi, uint64_t step,
+                                             const StopCtx *sc, Partial *lds) {
   if constexpr (DT > SV_I64) {
     return empty_partial();                         // not reached: the host passes types in kMask only
   } else if constexpr ((kMask & (1 << DT)) == 0) {
-    return check_any<kMask, kStop, DT + 1>(sd, ulo, uhi, lds);
+    return check_any<kMask, kStop, DT + 1>(sd, ulo, uhi, step, sc, lds);
   } else if constexpr ((kMask >> (DT + 1)) == 0) {
-    return check_piece<DT, kStop>(sd, ulo, uhi, lds);   // the last type in the mask
+    return check_piece<DT, kStop>(sd, ulo, uhi, step, sc, lds);   // the last type in the mask
   } else {
-    if (sd.dtype == DT) return check_piece<DT, kStop>(sd, ulo, uhi, lds);
-    return check_any<kMask, kStop, DT + 1>(sd, ulo, uhi, lds);
+    if (sd.dtype == DT) return check_piece<DT, kStop>(sd, ulo, uhi, step, sc, lds);
+    return check_any<kMask, kStop, DT + 1>(sd, ulo, uhi, step, sc, lds);
   }
 }
 
@@ -639,10 +710,35 @@ __device__ __forceinline__ void last_block_report(const CompareArgs &args, const
   }
 }
 
+// Segment owning workgroup b of a stop-at-first launch: the last one whose
+// first workgroup is <= b (segments without units own none and are skipped).
+__device__ __forceinline__ uint32_t find_block_segment(const SegDesc *segs, uint32_t nseg, uint32_t b) {
+  uint32_t lo = 0, hi = nseg;
+  while (hi - lo > 1) {
+    const uint32_t mid = (lo + hi) / 2;
+    if (segs[mid].blk <= b) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
 template <bool kSingle, int kMask, bool kStop = false>
 __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
   __shared__ Partial lds[kWavesPerBlock];
   const uint64_t b = blockIdx.x;
+  if constexpr (kStop) {
+    // one segment per workgroup: its tiles i, i + g, ... (i = b - blk)
+    __shared__ uint32_t lim;
+    const uint32_t s = find_block_segment(args.segs, args.nseg, (uint32_t)b);
+    const SegDesc sd = args.segs[s];
+    const uint64_t units = units_of(sd.dtype, sd.n);
+    const uint64_t g = stop_blocks(units, args.chunk);
+    if (threadIdx.x == 0) lim = 0xFFFFFFFFu;
+    __syncthreads();
+    const StopCtx sc{args.firsts + (size_t)s * kFirstStride, (uint32_t)args.seq, &lim};
+    const Partial p = check_any<kMask, true>(sd, (b - sd.blk) * kCmpTile, units, g * kCmpTile, &sc, lds);
+    if (threadIdx.x == 0) args.partials[b] = p;
+    return;
+  }
   uint64_t lo = b * args.chunk;
   const uint64_t hi = lo + args.chunk < args.total_units ? lo + args.chunk : args.total_units;
   uint32_t s = kSingle ? 0u : find_segment(args.segs, args.nseg, lo);
@@ -651,7 +747,7 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
     const uint64_t seg_end = sd.unit_begin + units_of(sd.dtype, sd.n);
     const uint64_t piece_hi = hi < seg_end ? hi : seg_end;
     const uint64_t ulo = lo - sd.unit_begin, uhi = piece_hi - sd.unit_begin;
-    const Partial p = check_any<kMask, kStop>(sd, ulo, uhi, lds);
+    const Partial p = check_any<kMask, false>(sd, ulo, uhi, kCmpTile, nullptr, lds);
     if constexpr (kSingle) {
       if (args.fused == 1) {         // the only workgroup: its partial is the whole result
         publish_report(p, sd.n, args.reports);
@@ -700,6 +796,18 @@ hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dt
     case 7: launch_masked<7>(args, nblocks, stream); break;
     default: launch_masked<0x7F>(args, nblocks, stream); break;
   }
+  return hipGetLastError();
+}
+
+__global__ void fill_u64_kernel(uint64_t *p, uint64_t n, uint64_t value) {
+  for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (uint64_t)gridDim.x * blockDim.x)
+    p[i] = value;
+}
+
+hipError_t launch_fill_u64(uint64_t *p, uint64_t n, uint64_t value, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  const uint64_t want = (n + kBlock - 1) / kBlock, blocks = want < 1024 ? want : 1024;
+  hipLaunchKernelGGL(fill_u64_kernel, dim3((uint32_t)blocks), dim3(kBlock), 0, stream, p, n, value);
   return hipGetLastError();
 }
 

@@ -107,6 +107,14 @@ hipError_t launch_perturb_indexed(int32_t dtype, const PerturbParams &p, const u
 // [b * chunk, (b + 1) * chunk) of that space and writes one partial per
 // segment piece it touches, into slot b + s (distinct for every (b, s) pair
 // that occurs, because both b and s grow along the unit space).
+//
+// Stop-at-first launches lay the workgroups out by segment instead: segment s
+// gets stop_blocks(units, chunk) workgroups of its own, from workgroup blk on,
+// which sweep it together from the front, workgroup i taking tiles i, i + g,
+// i + 2g, ... (a tile is kCmpBlock * SV_CMP_UNROLL units, one iteration of a
+// workgroup); each writes one partial, into slot b.  A mismatch found in a tile
+// is posted to the segment's word in `firsts`, so that the segment's other
+// workgroups, which are all near that tile, stop there too.
 struct SegDesc {
   const void *ref;
   const void *cand;
@@ -116,8 +124,19 @@ struct SegDesc {
   int32_t dtype;
   int32_t equal_nan;
   int32_t vec_ok;               // both pointers 16-byte aligned
-  int32_t pad;
+  uint32_t blk;                 // stop-at-first launches: the segment's first workgroup
 };
+
+constexpr uint64_t kCmpTile = (uint64_t)kCmpBlock * SV_CMP_UNROLL;   // units per workgroup iteration
+constexpr uint64_t kMaxStopBlocks = 0xFFFFFFFFull / kCmpBlock;   // a grid's work-items fit in 32 bits
+constexpr size_t kFirstStride = 16;   // uint64 words between the segments' words in `firsts` (128 bytes)
+
+// Workgroups of one segment in a stop-at-first launch: a share of about
+// `chunk` units each, and no more workgroups than tiles.
+__host__ __device__ inline uint64_t stop_blocks(uint64_t units, uint64_t chunk) {
+  const uint64_t by_chunk = (units + chunk - 1) / chunk, tiles = (units + kCmpTile - 1) / kCmpTile;
+  return by_chunk < tiles ? by_chunk : tiles;
+}
 
 struct Partial {
   uint64_t mism;
@@ -134,7 +153,10 @@ struct CompareArgs {
   uint64_t chunk;               // units per workgroup
   Partial *partials;            // nblocks + nseg slots
   uint32_t *counter;            // finalize arrivals, zero between launches
-  int32_t stop_at_first;        // batched: each wave stops at its first mismatch
+  int32_t stop_at_first;        // batched: each failing segment checked only up to its first mismatch
+  uint64_t *firsts;             // stop-at-first: word s * kFirstStride of segment s holds
+                                // (uint32 seq) << 32 | (2^32 - 1 - t), t the first tile found
+                                // with a mismatch in this launch (larger is earlier)
   int32_t fused;                // one tensor, no finalize: 1 = the only workgroup reports, 2 = the last one does
   sv_report *reports;           // nseg reports, in host-mapped pinned memory
   uint64_t *done;               // host-mapped word that receives `seq` once every report is written
@@ -168,5 +190,6 @@ __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
 // elements), and the finalize kernel that turns its partials into reports.
 hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream);
 hipError_t launch_finalize(const CompareArgs &args, hipStream_t stream);
+hipError_t launch_fill_u64(uint64_t *p, uint64_t n, uint64_t value, hipStream_t stream);
 
 }  // namespace sv

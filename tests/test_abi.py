@@ -77,6 +77,10 @@ def test_struct_layouts_match_the_c_compiler(svlib, tmp_path):
         assert int(got[cname]) == ctypes.sizeof(mirror), cname
         for field, _ in mirror._fields_:
             assert int(got["%s.%s" % (cname, field)]) == getattr(mirror, field).offset, (cname, field)
+    # the numpy form of the report (as_array=True) has the same layout
+    assert svlib.REPORT_DTYPE.itemsize == int(got["sv_report"])
+    for field, _ in svlib.Report._fields_:
+        assert svlib.REPORT_DTYPE.fields[field][1] == int(got["sv_report.%s" % field]), field
 
 
 def _synth(L, svlib, dtype, dist, n=16, out=0x1000, params=True, **kw):

@@ -201,3 +201,18 @@ def test_prepared_calls_match_plain_calls(oracle):
         assert check.run() == want and check.submit().wait() == want
         tickets = [check.submit() for _ in range(3)]
         assert [t.wait() for t in tickets] == [want] * 3
+
+
+def test_reports_as_arrays_equal_the_dicts():
+    segs = [(*_pair(n, 80 + k, p=0.01 if k % 2 else 0.0), 1e-8, 0.0, False) for k, n in enumerate([17, 4099, 1 << 20])]
+    print("reports as arrays", flush=True)
+    for stop in (False, True):
+        want = sv.compare_batched(segs, stop_at_first=stop)
+        for got in (sv.compare_batched(segs, stop_at_first=stop, as_array=True),
+                    sv.compare_batched_submit(segs, stop_at_first=stop).wait(as_array=True)):
+            assert got.dtype == sv.REPORT_DTYPE and got.shape == (3,)
+            assert [{f: got[k][f].item() for f in got.dtype.names} for k in range(3)] == want
+    t = sv.compare_submit(*segs[1][:4])
+    arr = t.wait(as_array=True)
+    assert arr.shape == (1,) and {f: arr[0][f].item() for f in arr.dtype.names} == t.wait()
+    assert sv.compare_batched([], as_array=True).shape == (0,)

@@ -232,7 +232,7 @@ def test_batched_stop_at_first(oracle):
             segs.append((R, C, *tol))
             want.append(oracle.compare(ref, c, dtype, *tol))
     print("stop-at-first batch", len(segs), flush=True)
-    for rep in range(2):                                         # the early-exit words reset between calls
+    for rep in range(2):                                         # the first call's posted mismatches do not stop the second
         got = sv.compare_batched(segs, stop_at_first=True)
         for g, w in zip(got, want):
             same_report(g, _stop_expect(w))
@@ -244,3 +244,68 @@ def test_batched_stop_at_first(oracle):
         reps = (sv.Report * 1)()
         sv._check(sv.lib().sv_compare_batched_mode(arr, 1, 2, reps))
     assert e.value.code == sv.SV_ERR_UNSUPPORTED
+
+
+TILE = 512 * 4          # units per workgroup iteration of the check (threads x units in flight)
+
+
+def test_stop_at_first_shared_between_workgroups(oracle):
+    # In stop-at-first mode a segment's workgroups sweep it together and post the
+    # first mismatch they find for the others.  Faults at tile edges, several per
+    # segment (a later one may be posted first), segments of one and of thousands
+    # of workgroups, unaligned operands (guarded loads only), empty segments
+    # between; then the same segments without faults, which must not be stopped by
+    # what the first launch posted.
+    rng = np.random.default_rng(35)
+    E = TILE * 4                                                 # fp32 elements per tile
+    cases = [((1 << 24) + 37, [3 * E + 5, 9 * E - 1, 2000 * E]),    # thousands of workgroups
+             ((1 << 24) + 37, [(1 << 24) + 36]),                   # the last element
+             ((1 << 24) + 37, [0, 12345678]),
+             ((1 << 22) + 3, [E - 1, E]),                          # both sides of a tile edge
+             ((1 << 22) + 3, [377 * E + 1000, 50 * E + 17, 500 * E + 2, 100 * E]),
+             (0, []),
+             (5 * E + 3, [4 * E + 1]),                             # one workgroup
+             (70_001, [69_999]), (70_001, [40_000, 20_001])]       # unaligned below
+    rows, segs, want, keep = [], [], [], []
+    for k, (n, faults) in enumerate(cases):
+        unaligned = n == 70_001
+        ref = rng.normal(0.0, 1.0, n + 1).astype(np.float32).view(np.uint32)
+        cand = ref.copy()
+        for f in faults:
+            cand[f + 1 if unaligned else f] ^= 0x00400000            # far outside rtol
+        near = ref ^ np.uint32(1)                                # 1 ulp off everywhere: passes, err_sum > 0
+        R, C, N = dev(ref, "f32"), dev(cand, "f32"), dev(near, "f32")
+        keep += [R, C, N]
+        if unaligned:                                            # views 4 bytes into the storage
+            R, C, N, r, c, m = R[1:], C[1:], N[1:], ref[1:], cand[1:], near[1:]
+        else:
+            R, C, N, r, c, m = R[:n], C[:n], N[:n], ref[:n], cand[:n], near[:n]
+        segs.append((R, C, 1e-6, 0.0, False))
+        rows.append((r, m, (R, N, 1e-6, 0.0, False)))
+        w = oracle.compare(r, c, "f32", 1e-6, 0.0, False)
+        assert w["mismatches"] == len(faults) and (not faults or w["first_mismatch"] == min(faults))
+        want.append(w)
+    print("stop-at-first shared", len(segs), flush=True)
+    for rep in range(3):
+        got = sv.compare_batched(segs, stop_at_first=True)
+        for g, w in zip(got, want):
+            same_report(g, _stop_expect(w))
+        clean = sv.compare_batched([row[2] for row in rows], stop_at_first=True)
+        for g, (r, m, _) in zip(clean, rows):
+            w = oracle.compare(r, m, "f32", 1e-6, 0.0, False)
+            assert w["mismatches"] == 0 and (w["err_sum"] > 0 or r.size == 0)
+            same_report(g, w)
+    # many small segments, one failing in four, empty ones between
+    segs, want = [], []
+    for k in range(3000):
+        n = 0 if k % 7 == 3 else int(rng.integers(1, 3 * E))
+        r = rng.normal(0.0, 1.0, n).astype(np.float32).view(np.uint32)
+        c = r.copy()
+        if n and k % 4 == 0:
+            c[rng.integers(0, n, 3)] ^= 0x00400000
+        R, C = dev(r, "f32"), dev(c, "f32")
+        segs.append((R, C, 1e-6, 0.0, False))
+        want.append(_stop_expect(oracle.compare(r, c, "f32", 1e-6, 0.0, False)))
+    print("stop-at-first many", len(segs), flush=True)
+    for g, w in zip(sv.compare_batched(segs, stop_at_first=True), want):
+        same_report(g, w)
