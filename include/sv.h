@@ -423,6 +423,17 @@ int sv_profile_read(int32_t kind, uint64_t *count, double *total_ms);
 /* Frees the scratch areas of every device.  Later calls allocate again. */
 int sv_shutdown(void);
 
+/*
+ * For tests: sets the sequence number of the last check on the calling
+ * thread's current device, so that the next check gets last + 1.  Checks
+ * number themselves per device; the stop-at-first mode tags words in device
+ * memory with the low 32 bits of that number and clears them when the high
+ * bits change, and this lets a test cross that boundary without 2^32 checks.
+ * INVALID_ARG while submitted checks of the device are not yet waited for, or
+ * for last >= 2^56 - 2^32 (tickets hold 56 bits of it).
+ */
+int sv_testing_set_sequence(uint64_t last);
+
 int sv_abi_version(void);
 
 #ifdef __cplusplus

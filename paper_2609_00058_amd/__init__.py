@@ -34,7 +34,8 @@ PROF_KINDS = {"synth": 0, "compare": 1, "perturb": 2, "finalize": 3}
 SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_synth_window", "sv_compare", "sv_compare_batched", "sv_compare_batched_mode",
            "sv_compare_submit", "sv_compare_batched_submit", "sv_compare_ready", "sv_compare_wait", "sv_perturb",
            "sv_eval_transform", "sv_synth_file", "sv_compare_file", "sv_kernel_load", "sv_kernel_free", "sv_kernel_launch", "sv_kernel_time",
-           "sv_reward", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown", "sv_abi_version")
+           "sv_reward", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown",
+           "sv_testing_set_sequence", "sv_abi_version")
 
 
 class DistParams(ctypes.Structure):
@@ -126,6 +127,7 @@ _lib.sv_synth_file.argtypes = [ctypes.c_char_p, _u64, _u64, _i32, _i32, ctypes.P
 _lib.sv_compare_file.argtypes = [ctypes.c_char_p, ctypes.c_char_p, _u64, _i32, _dbl, _dbl, _i32,
                                  ctypes.POINTER(Report)]
 _lib.sv_set_stream.argtypes = [_vp]
+_lib.sv_testing_set_sequence.argtypes = [_u64]
 _lib.sv_last_error.restype = ctypes.c_char_p
 _lib.sv_profile_enable.argtypes = [_i32]
 _lib.sv_profile_read.argtypes = [_i32, ctypes.POINTER(_u64), ctypes.POINTER(_dbl)]

@@ -96,6 +96,7 @@ struct DeviceState {
   size_t counters_cap = 0;
   uint64_t *firsts = nullptr;        // stop-at-first: a tagged first-mismatch word per segment
   size_t firsts_cap = 0;
+  uint64_t firsts_hi = ~0ull;        // seq >> 32 of the launches whose tags the words may hold
   uint64_t *h_done = nullptr;        // pinned, host-mapped, coherent: one completion word per slot
   uint64_t *d_done = nullptr;        // its device address
   uint64_t seq = 0;                  // sequence number of the last check submitted
@@ -181,20 +182,23 @@ int ensure_counters(DeviceState *ds, size_t need) {
   return SV_OK;
 }
 
-// The stop-at-first words; a fresh allocation is cleared on the calling
-// thread's stream, ahead of the check that needs it (a zero word carries tag 0
-// and the tile 2^32 - 1, past every tile: it stops nothing).
-int ensure_firsts(DeviceState *ds, size_t need) {
-  if (need <= ds->firsts_cap) return SV_OK;
-  int rc = ensure_device(ds->firsts, ds->firsts_cap, need, "first-mismatch words");
-  if (rc) return rc;
-  const hipError_t e = launch_fill_u64(ds->firsts, ds->firsts_cap, 0, t_stream);
-  if (e != hipSuccess) {
-    (void)hipFree(ds->firsts);
-    ds->firsts = nullptr;
-    ds->firsts_cap = 0;
-    return hip_fail(e, "clearing the first-mismatch words");
+// The stop-at-first words for a check with sequence number seq.  A word's tag
+// is the low 32 bits of its launch's sequence number, so a word counts as
+// nothing once the tags have moved on -- until they come round again 2^32
+// checks later.  The words are therefore cleared (on the calling thread's
+// stream, ahead of the check) when they are allocated and whenever the high
+// bits of the sequence number differ from those of the last clear.  A zero
+// word carries tag 0 and the tile 2^32 - 1, past every tile: it stops nothing.
+int ensure_firsts(DeviceState *ds, size_t need, uint64_t seq) {
+  if (need > ds->firsts_cap) {
+    const int rc = ensure_device(ds->firsts, ds->firsts_cap, need, "first-mismatch words");
+    if (rc) return rc;
+    ds->firsts_hi = ~0ull;
   }
+  if ((seq >> 32) == ds->firsts_hi) return SV_OK;
+  const hipError_t e = launch_fill_u64(ds->firsts, ds->firsts_cap, 0, t_stream);
+  if (e != hipSuccess) return hip_fail(e, "clearing the first-mismatch words");
+  ds->firsts_hi = seq >> 32;
   return SV_OK;
 }
 
@@ -446,7 +450,7 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   int rc = SV_OK;
   if (grow || (ds->has_last && ds->last_stream != st)) rc = drain_pending(ds);
   if (!rc) rc = ensure_device(ds->partials, ds->partials_cap, (size_t)plan.nblocks + nseg, "partials");
-  if (!rc && nfirsts) rc = ensure_firsts(ds, nfirsts);
+  if (!rc && nfirsts) rc = ensure_firsts(ds, nfirsts, ds->seq + 1);
   if (!rc && batched) rc = ensure_device(ds->table, ds->table_cap, nseg, "segment table");
   if (!rc && batched) rc = ensure_pinned(sl.h_table, sl.h_table_cap, nseg, "segment table staging");
   if (!rc) rc = ensure_reports(sl, nseg);
@@ -477,11 +481,6 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   args.reports = sl.d_reports;
   args.done = ds->d_done + (size_t)k * kDoneStride;
   args.seq = ds->seq + 1;
-  if (plan.stop_at_first && (uint32_t)args.seq == 0) {
-    // the words' 32-bit launch tags start over: clear the tags of 2^32 launches ago
-    const hipError_t e = launch_fill_u64(ds->firsts, ds->firsts_cap, 0, st);
-    if (e != hipSuccess) return hip_fail(e, "clearing the first-mismatch words");
-  }
   hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
   if (g_prof_on.load()) {
     e0 = take_event();
@@ -1084,6 +1083,20 @@ int sv_profile_read(int32_t kind, uint64_t *count, double *total_ms) {
   return rc;
 }
 
+int sv_testing_set_sequence(uint64_t last) {
+  t_error.clear();
+  if (last >= (1ull << kTicketSeqBits) - (1ull << 32))
+    return fail(SV_ERR_INVALID_ARG, "sv_testing_set_sequence: %llu is too large", (unsigned long long)last);
+  DeviceState *ds;
+  int rc = current_device(&ds);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lock(ds->mu);
+  if (ds->npending)
+    return fail(SV_ERR_INVALID_ARG, "sv_testing_set_sequence: %d submitted checks not yet waited for", ds->npending);
+  ds->seq = last;
+  return SV_OK;
+}
+
 int sv_shutdown(void) {
   t_error.clear();
   int prev = 0;
@@ -1113,7 +1126,7 @@ int sv_shutdown(void) {
     if (s->synth_done) (void)hipEventDestroy(s->synth_done);
     if (s->counters) (void)hipFree(s->counters);
     if (s->firsts) (void)hipFree(s->firsts);
-    s->firsts = nullptr; s->firsts_cap = 0;
+    s->firsts = nullptr; s->firsts_cap = 0; s->firsts_hi = ~0ull;
     if (s->h_done) (void)hipHostFree(s->h_done);
     s->counters = nullptr; s->counters_cap = 0;
     s->h_done = nullptr; s->d_done = nullptr;

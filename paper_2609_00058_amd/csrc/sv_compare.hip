@@ -613,7 +613,7 @@ __device__ __forceinline__ uint32_t find_segment(const SegDesc *segs, uint32_t n
 }
 
 // One workgroup per segment, behind the check kernel: thread t merges slots
-// b0 + t, b0 + t + 1024, ... in order (four loaded at a time), then a fixed
+// b0 + t, b0 + t + 1024, ... in order (loaded four at a time), then a fixed
 // shuffle tree and the waves in order; the report goes into host-mapped memory.
 constexpr int kFinBlock = 1024;                  // finalize threads per segment
 constexpr int kFinWaves = kFinBlock / kWave;
@@ -640,7 +640,16 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
       merge(acc, p2);
       merge(acc, p3);
     }
-    for (; b <= b1; b += kFinBlock) merge(acc, P[b]);
+    // at most three left: all loaded before the first merge (one memory round
+    // trip instead of up to three), merged in the same order
+    const bool h0 = b <= b1, h1 = b + kFinBlock <= b1, h2 = b + 2 * kFinBlock <= b1;
+    Partial q0, q1, q2;
+    if (h0) q0 = P[b];
+    if (h1) q1 = P[b + kFinBlock];
+    if (h2) q2 = P[b + 2 * kFinBlock];
+    if (h0) merge(acc, q0);
+    if (h1) merge(acc, q1);
+    if (h2) merge(acc, q2);
     wave_merge(acc);
     if (lane == 0) lds[wave] = acc;
     __syncthreads();

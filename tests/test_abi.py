@@ -197,6 +197,9 @@ def test_async_check_argument_errors_without_a_device(svlib):
         assert L.sv_compare_wait(bad, reps, 1) == INV
         assert "ticket" in L.sv_last_error().decode()
     assert L.sv_compare_ready(1 << 56, None) == INV
+    # the testing hook refuses sequence numbers that tickets cannot hold
+    assert L.sv_testing_set_sequence((1 << 56) - (1 << 32)) == INV
+    assert "too large" in L.sv_last_error().decode()
 
 
 def test_perturb_argument_errors(svlib):

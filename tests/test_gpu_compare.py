@@ -309,3 +309,35 @@ def test_stop_at_first_shared_between_workgroups(oracle):
     print("stop-at-first many", len(segs), flush=True)
     for g, w in zip(sv.compare_batched(segs, stop_at_first=True), want):
         same_report(g, w)
+
+
+def test_stop_at_first_words_from_2_32_checks_ago_count_for_nothing(oracle):
+    # The words carry the low 32 bits of their check's sequence number.  A check
+    # 2^32 numbers after one that posted a mismatch at tile 0 has the same tag:
+    # the words must have been cleared in between, or its waves would stop at
+    # tile 0 of a segment that passes.  Also across a boundary taken by a plain
+    # check, and back to a smaller number.
+    L = sv.lib()
+    rng = np.random.default_rng(36)
+    n = 1 << 22
+    ref = rng.normal(0.0, 1.0, n).astype(np.float32).view(np.uint32)
+    bad, near = ref.copy(), ref ^ np.uint32(1)
+    bad[5] ^= 0x00400000                                         # a mismatch in tile 0
+    R, B, N = dev(ref, "f32"), dev(bad, "f32"), dev(near, "f32")
+    want_bad = _stop_expect(oracle.compare(ref, bad, "f32", 1e-6, 0.0, False))
+    want_near = oracle.compare(ref, near, "f32", 1e-6, 0.0, False)
+    assert want_bad["first_mismatch"] == 5 and want_near["mismatches"] == 0 and want_near["err_sum"] > 0
+    fail, clean = [(R, B, 1e-6, 0.0, False)], [(R, N, 1e-6, 0.0, False)]
+    print("stop-at-first tags", flush=True)
+    for before, after, plain_between in ((9, (1 << 32) + 9, False), ((1 << 32) - 3, (2 << 32) - 3, True),
+                                         ((3 << 32) + 100, 100, False)):
+        assert L.sv_testing_set_sequence(before) == 0
+        same_report(sv.compare_batched(fail, stop_at_first=True)[0], want_bad)       # posts tile 0
+        assert L.sv_testing_set_sequence(after) == 0
+        if plain_between:                                        # a plain check takes the next number
+            same_report(sv.compare(R, N, 1e-6, 0.0), want_near)
+            assert L.sv_testing_set_sequence(after) == 0
+        same_report(sv.compare_batched(clean, stop_at_first=True)[0], want_near)    # same tag, cleared
+    t = sv.compare_submit(R, N, 1e-6, 0.0)
+    assert L.sv_testing_set_sequence(7) == sv.SV_ERR_INVALID_ARG                 # a check is pending
+    same_report(t.wait(), want_near)
