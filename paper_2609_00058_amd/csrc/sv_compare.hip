@@ -98,16 +98,23 @@ __device__ __forceinline__ double widen(uint32_t bits) {
     return (double)as_f32(bits);
 }
 
+// Operands live in device (global) memory.  A segment's pointers are read
+// from the segment table, so the compiler cannot infer their address space
+// and would address them as generic (flat) pointers: flat loads also count
+// against the LDS / scalar-load counter the loop waits on.  Casting them to
+// the global address space gives global loads, as for kernel arguments.
+#define kGlobal __attribute__((address_space(1)))
+
 template <int DT>
 __device__ __forceinline__ uint64_t load_elem(const void *p, uint64_t i) {
   if constexpr (DT == SV_BF16 || DT == SV_F16)
-    return ((const uint16_t *)p)[i];
+    return ((const kGlobal uint16_t *)p)[i];
   else if constexpr (DT == SV_U8)
-    return ((const uint8_t *)p)[i];
+    return ((const kGlobal uint8_t *)p)[i];
   else if constexpr (kWideType<DT>)
-    return ((const uint64_t *)p)[i];
+    return ((const kGlobal uint64_t *)p)[i];
   else
-    return ((const uint32_t *)p)[i];
+    return ((const kGlobal uint32_t *)p)[i];
 }
 
 // Places element j's raw bits into a unit (the tail of a segment).
@@ -504,8 +511,8 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, ui
                                Partial *lds) {
   constexpr int V = Elem<DT>::V;
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
-  const u32x4 *yv4 = (const u32x4 *)sd.ref;
-  const u32x4 *av4 = (const u32x4 *)sd.cand;
+  const kGlobal u32x4 *yv4 = (const kGlobal u32x4 *)sd.ref;
+  const kGlobal u32x4 *av4 = (const kGlobal u32x4 *)sd.cand;
   const double rtol = sd.rtol, atol = sd.atol;
   const bool eqn = sd.equal_nan != 0;
   const uint64_t n = sd.n;
