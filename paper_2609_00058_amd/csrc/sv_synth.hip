@@ -507,9 +507,37 @@ __device__ __forceinline__ uint32_t find_job(const SynthJob *jobs, uint32_t njob
   return lo;
 }
 
-// One tile of a job: `rounds` vectors per thread, kBlock apart.
+// One tile of a job: `rounds` vectors per thread, kBlock apart.  A thread
+// whose vectors are all whole and 16-byte aligned, in a job whose Philox
+// counters fit 32 bits, takes the lean loop of the single-tensor kernel
+// (32-bit counters, no per-vector checks); the others, at a job's end or for
+// unaligned outputs, take the general one.
 template <int DIST, int DT>
 __device__ __forceinline__ void synth_tile(const SynthJob &job, uint64_t u0, uint32_t rounds, bool ok) {
+  constexpr int E = DistTraits<DIST>::E;
+  constexpr int V = DT == SV_BF16 ? 8 : 4;
+  constexpr uint32_t B = V / E;
+  const uint64_t whole = job.n / V;
+  if (ok && job.nvec * B < (1ull << 32) && u0 + (uint64_t)(rounds - 1) * kBlock < whole) {
+    u32x4 *out = (u32x4 *)job.out;
+    for (uint32_t r = 0; r < rounds; ++r) {
+      const uint32_t u = (uint32_t)u0 + r * (uint32_t)kBlock;
+      uint32_t v[V];
+#pragma unroll
+      for (uint32_t b = 0; b < B; ++b) block_values<DIST>(job.p, (uint64_t)(u * B + b), v + b * E);
+      u32x4 o;
+      if constexpr (DT == SV_BF16) {
+        o.x = bf16_pair<DIST>(v[0], v[1]);
+        o.y = bf16_pair<DIST>(v[2], v[3]);
+        o.z = bf16_pair<DIST>(v[4], v[5]);
+        o.w = bf16_pair<DIST>(v[6], v[7]);
+      } else {
+        o = u32x4{v[0], v[1], v[2], v[3]};
+      }
+      out[u] = o;
+    }
+    return;
+  }
   for (uint32_t r = 0; r < rounds; ++r) {
     const uint64_t u = u0 + (uint64_t)r * kBlock;
     if (u >= job.nvec) break;
