@@ -240,6 +240,15 @@ int sv_compare_batched_mode(const sv_segment *segs, uint32_t nseg, int32_t mode,
  * or on a HIP error, the ticket is used up; waiting twice is INVALID_ARG.
  * sv_compare_ready sets *ready to 1 once a wait would not block, else 0.
  *
+ * The last step of a submitted single-tensor check (reducing its workgroups'
+ * partial results into the report) is left to the next check queued on the
+ * same stream, which does it in one of its own workgroups: one kernel launch
+ * less per check when checks follow each other.  If no such check comes,
+ * sv_compare_wait and sv_compare_ready queue that step themselves (on the
+ * check's stream), as does any call that must drain the pending checks, so a
+ * report may not be ready after a mere stream synchronization: poll with
+ * sv_compare_ready or wait.  The reports are the same bits either way.
+ *
  * At most SV_MAX_PENDING_CHECKS submitted checks per device are pending (not
  * yet waited for); one more submit returns INVALID_ARG.  A ticket names its
  * device, so it may be waited for with any device current.  Checks of one

@@ -71,14 +71,19 @@ struct CheckSlot {
   size_t reports_cap = 0;
   SegDesc *h_table = nullptr;    // pinned staging of the segment table
   size_t h_table_cap = 0;
+  bool deferred = false;         // its finalize is left to the next check launched on its stream
+  CompareArgs fin{};             // ... and what that finalize needs
+  uint64_t nparts = 0;           // its partials (one per check workgroup)
 };
 
 struct DeviceState {
   std::mutex mu;                 // serialises calls that use the scratch below
   int device = 0;
   int cus = 0;
-  Partial *partials = nullptr;   // one per (workgroup, segment piece)
-  size_t partials_cap = 0;
+  Partial *partials[2] = {nullptr, nullptr};   // one per (workgroup, segment piece), in two halves that
+  size_t partials_cap[2] = {0, 0};              // launched checks take in turn, so that a check can
+  int half = 0;                                 // finish the one before it while writing its own
+  int deferred = -1;                 // the slot whose finalize waits for the next check on its stream
   SegDesc *table = nullptr;      // batched segment table
   size_t table_cap = 0;
   uint64_t *idx = nullptr;
@@ -368,12 +373,37 @@ void compare_grid(uint64_t units, int cus, bool batched, uint32_t *nblocks, uint
   *nblocks = (uint32_t)((units + c - 1) / c);
 }
 
+// Queues the finalize that a submitted single-tensor check left to the next
+// check on its stream, when that check is not coming: before a wait, a
+// readiness query, a check on another stream or a reallocation of scratch.
+int flush_deferred(DeviceState *ds) {
+  if (ds->deferred < 0) return SV_OK;
+  CheckSlot &sl = ds->slots[ds->deferred];
+  ds->deferred = -1;
+  sl.deferred = false;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (g_prof_on.load()) {
+    e0 = take_event();
+    e1 = take_event();
+    if (e0) (void)hipEventRecord(e0, sl.stream);
+  }
+  const hipError_t e = launch_finalize(sl.fin, sl.stream);
+  if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
+  if (e0 && e1) {
+    (void)hipEventRecord(e1, sl.stream);
+    push_record(SV_PROF_FINALIZE, e0, e1);
+  }
+  return SV_OK;
+}
+
 // Waits on the host for every submitted check still pending (they stay
 // pending for their waiters).  Called before a check is queued on another
 // stream than the previous one and before shared scratch is reallocated, so
 // that no queued check can still read what is about to change: a check whose
 // completion word has been written has read all of it.
 int drain_pending(DeviceState *ds) {
+  const int rc = flush_deferred(ds);
+  if (rc) return rc;
   if (ds->npending == 0) return SV_OK;
   for (int k = 0; k < kAsyncSlots; ++k) {
     const CheckSlot &sl = ds->slots[k];
@@ -445,11 +475,12 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
     return fail(SV_ERR_INVALID_ARG, "stop-at-first check of %u segments: more than %u workgroups", nseg,
                 (unsigned)kMaxStopBlocks);
   const size_t nfirsts = plan.stop_at_first ? (size_t)nseg * kFirstStride : 0;
-  const bool grow = (size_t)plan.nblocks + nseg > ds->partials_cap || (batched && nseg > ds->table_cap) ||
+  const int par = ds->half;                      // this check's half of the partials
+  const bool grow = (size_t)plan.nblocks + nseg > ds->partials_cap[par] || (batched && nseg > ds->table_cap) ||
                     nfirsts > ds->firsts_cap;
   int rc = SV_OK;
   if (grow || (ds->has_last && ds->last_stream != st)) rc = drain_pending(ds);
-  if (!rc) rc = ensure_device(ds->partials, ds->partials_cap, (size_t)plan.nblocks + nseg, "partials");
+  if (!rc) rc = ensure_device(ds->partials[par], ds->partials_cap[par], (size_t)plan.nblocks + nseg, "partials");
   if (!rc && nfirsts) rc = ensure_firsts(ds, nfirsts, ds->seq + 1);
   if (!rc && batched) rc = ensure_device(ds->table, ds->table_cap, nseg, "segment table");
   if (!rc && batched) rc = ensure_pinned(sl.h_table, sl.h_table_cap, nseg, "segment table staging");
@@ -476,16 +507,17 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   args.stop_at_first = plan.stop_at_first ? 1 : 0;
   args.firsts = ds->firsts;
   args.fused = batched ? 0 : plan.nblocks == 1 ? 1 : plan.nblocks <= SV_CMP_LAST_BLOCK_MAX ? 2 : 0;
-  args.partials = ds->partials;
+  args.partials = ds->partials[par];
   args.counter = ds->counters;
   args.reports = sl.d_reports;
   args.done = ds->d_done + (size_t)k * kDoneStride;
   args.seq = ds->seq + 1;
+  const bool defer = !args.fused && k != kSyncSlot && !batched;   // see below
   hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
   if (g_prof_on.load()) {
     e0 = take_event();
     e1 = take_event();
-    if (!args.fused) e2 = take_event();
+    if (!args.fused && !defer) e2 = take_event();
     if (e0) (void)hipEventRecord(e0, st);
   }
   uint32_t mask = 0;
@@ -493,14 +525,38 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
     const uint64_t n = batched ? plan.segs[j].n : args.single.n;
     if (n) mask |= 1u << (batched ? plan.segs[j].dtype : args.single.dtype);
   }
-  hipError_t e = launch_compare(args, plan.nblocks, mask, st);
+  // A submitted single-tensor check leaves its finalize to the next check on
+  // its stream, whose workgroup 0 runs it (one launch less per check when
+  // checks follow each other); a single-tensor check with a grid of its own
+  // takes it on, any other check has it queued first.
+  args.prev = DeferredFinalize{};
+  const bool host_prev = !batched && args.fused == 0;
+  if (ds->deferred >= 0) {
+    CheckSlot &pd = ds->slots[ds->deferred];
+    if (host_prev && pd.stream == st) {
+      args.prev = DeferredFinalize{pd.fin.partials, pd.nparts, pd.fin.single.n, pd.fin.reports, pd.fin.done,
+                                   pd.fin.seq};
+      ds->deferred = -1;
+      pd.deferred = false;
+    } else if ((rc = flush_deferred(ds)) != SV_OK) {
+      return rc;
+    }
+  }
+  hipError_t e = launch_compare(args, plan.nblocks + (args.prev.partials ? 1u : 0u), mask, st);
   if (e != hipSuccess) return hip_fail(e, "check kernel launch");
   if (e1) (void)hipEventRecord(e1, st);
-  if (!args.fused) {
+  if (defer) {
+    sl.fin = args;
+    sl.fin.prev = DeferredFinalize{};
+    sl.nparts = plan.nblocks;
+    sl.deferred = true;
+    ds->deferred = k;
+  } else if (!args.fused) {
     e = launch_finalize(args, st);
     if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
   }
   ds->seq = args.seq;
+  ds->half ^= 1;
   ds->has_last = true;
   ds->last_stream = st;
   sl.seq = args.seq;
@@ -924,6 +980,10 @@ int sv_compare_ready(uint64_t ticket, int32_t *ready) {
   if (k < 0) return fail(SV_ERR_INVALID_ARG, "sv_compare_ready: ticket %#llx is not pending", (unsigned long long)ticket);
   const CheckSlot &sl = ds->slots[k];
   const volatile uint64_t *flag = ds->h_done + (size_t)k * kDoneStride;
+  if (sl.deferred) {
+    const int rc = flush_deferred(ds);
+    if (rc) return rc;
+  }
   if (!sl.launched || *flag == sl.seq) {
     *ready = 1;
     return SV_OK;
@@ -956,6 +1016,10 @@ int sv_compare_wait(uint64_t ticket, sv_report *reports, uint32_t nreports) {
       return fail(SV_ERR_INVALID_ARG, "sv_compare_wait: the check has %zu reports, nreports = %u",
                   sl.lengths.size(), nreports);
     if (nreports && !reports) return fail(SV_ERR_INVALID_ARG, "sv_compare_wait: reports is NULL");
+    if (sl.deferred) {
+      const int rc = flush_deferred(ds);
+      if (rc) return rc;
+    }
     sl.waiting = true;
     seq = sl.seq;
     launched = sl.launched;
@@ -1108,7 +1172,13 @@ int sv_shutdown(void) {
     std::lock_guard<std::mutex> lock(s->mu);
     (void)hipSetDevice((int)d);
     (void)hipDeviceSynchronize();
-    if (s->partials) (void)hipFree(s->partials);
+    for (int h = 0; h < 2; ++h) {
+      if (s->partials[h]) (void)hipFree(s->partials[h]);
+      s->partials[h] = nullptr;
+      s->partials_cap[h] = 0;
+    }
+    s->deferred = -1;
+    s->half = 0;
     if (s->table) (void)hipFree(s->table);
     if (s->idx) (void)hipFree(s->idx);
     for (CheckSlot &sl : s->slots) {
@@ -1133,9 +1203,9 @@ int sv_shutdown(void) {
     s->synth_table = nullptr; s->h_synth = nullptr; s->synth_copied = nullptr; s->synth_done = nullptr;
     s->synth_table_cap = s->h_synth_cap = 0;
     s->synth_pending = false;
-    s->partials = nullptr; s->table = nullptr; s->idx = nullptr;
+    s->table = nullptr; s->idx = nullptr;
     s->h_idx = nullptr;
-    s->partials_cap = s->table_cap = s->idx_cap = 0;
+    s->table_cap = s->idx_cap = 0;
     s->h_idx_cap = 0;
   }
   perf_shutdown();

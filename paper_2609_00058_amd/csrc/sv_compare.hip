@@ -619,16 +619,55 @@ __device__ __forceinline__ uint32_t find_segment(const SegDesc *segs, uint32_t n
   return lo;
 }
 
-// One workgroup per segment, behind the check kernel: thread t merges slots
-// b0 + t, b0 + t + 1024, ... in order (loaded four at a time), then a fixed
-// shuffle tree and the waves in order; the report goes into host-mapped memory.
-constexpr int kFinBlock = 1024;                  // finalize threads per segment
+// The reduction of a segment's partials P[b0 .. b1] into its report, by a
+// workgroup of kFinBlock threads: thread t merges slots b0 + t, b0 + t +
+// kFinBlock, ... in order (loaded four at a time), then a fixed shuffle tree
+// and the waves in order.  The result is valid on thread 0.  The finalize
+// kernel runs it, and so does the first workgroup of a check kernel that
+// finishes an earlier check (the same threads, the same tree: the same bits).
+constexpr int kFinBlock = kCmpBlock;             // finalize threads per segment
 constexpr int kFinWaves = kFinBlock / kWave;
+static_assert(kFinWaves == kWavesPerBlock, "a check workgroup runs the finalize's tree");
 
+__device__ Partial reduce_partials(const Partial *P, uint64_t b0, uint64_t b1, Partial *lds) {
+  const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  Partial acc = empty_partial();
+  uint64_t b = b0 + tid;
+  for (; b + 3 * kFinBlock <= b1; b += 4 * kFinBlock) {
+    const Partial p0 = P[b], p1 = P[b + kFinBlock], p2 = P[b + 2 * kFinBlock], p3 = P[b + 3 * kFinBlock];
+    merge(acc, p0);
+    merge(acc, p1);
+    merge(acc, p2);
+    merge(acc, p3);
+  }
+  // at most three left: all loaded before the first merge (one memory round
+  // trip instead of up to three), merged in the same order
+  const bool h0 = b <= b1, h1 = b + kFinBlock <= b1, h2 = b + 2 * kFinBlock <= b1;
+  Partial q0, q1, q2;
+  if (h0) q0 = P[b];
+  if (h1) q1 = P[b + kFinBlock];
+  if (h2) q2 = P[b + 2 * kFinBlock];
+  if (h0) merge(acc, q0);
+  if (h1) merge(acc, q1);
+  if (h2) merge(acc, q2);
+  wave_merge(acc);
+  if (lane == 0) lds[wave] = acc;
+  __syncthreads();
+  Partial r = lds[0];
+  if (tid == 0) {
+#pragma unroll
+    for (int w = 1; w < kFinWaves; ++w) merge(r, lds[w]);
+  }
+  __syncthreads();   // lds is reused
+  return r;
+}
+
+// One workgroup per segment, behind the check kernel; the report goes into
+// host-mapped memory.
 template <bool kSingle>
 __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
   __shared__ Partial lds[kFinWaves];
-  const uint32_t s = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const uint32_t s = blockIdx.x, tid = threadIdx.x;
   const SegDesc sd = kSingle ? args.single : args.segs[s];
   const uint64_t units = units_of(sd.dtype, sd.n);
   if (units != 0) {                  // empty segments are reported by the host
@@ -637,34 +676,7 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
     const bool own = !kSingle && args.stop_at_first;
     const uint64_t b0 = own ? sd.blk : sd.unit_begin / args.chunk;
     const uint64_t b1 = own ? sd.blk + stop_blocks(units, args.chunk) - 1 : (sd.unit_begin + units - 1) / args.chunk;
-    const Partial *P = args.partials + (own ? 0 : s);
-    Partial acc = empty_partial();
-    uint64_t b = b0 + tid;
-    for (; b + 3 * kFinBlock <= b1; b += 4 * kFinBlock) {
-      const Partial p0 = P[b], p1 = P[b + kFinBlock], p2 = P[b + 2 * kFinBlock], p3 = P[b + 3 * kFinBlock];
-      merge(acc, p0);
-      merge(acc, p1);
-      merge(acc, p2);
-      merge(acc, p3);
-    }
-    // at most three left: all loaded before the first merge (one memory round
-    // trip instead of up to three), merged in the same order
-    const bool h0 = b <= b1, h1 = b + kFinBlock <= b1, h2 = b + 2 * kFinBlock <= b1;
-    Partial q0, q1, q2;
-    if (h0) q0 = P[b];
-    if (h1) q1 = P[b + kFinBlock];
-    if (h2) q2 = P[b + 2 * kFinBlock];
-    if (h0) merge(acc, q0);
-    if (h1) merge(acc, q1);
-    if (h2) merge(acc, q2);
-    wave_merge(acc);
-    if (lane == 0) lds[wave] = acc;
-    __syncthreads();
-    Partial r = lds[0];
-    if (tid == 0) {
-#pragma unroll
-      for (int w = 1; w < kFinWaves; ++w) merge(r, lds[w]);
-    }
+    const Partial r = reduce_partials(args.partials + (own ? 0 : s), b0, b1, lds);
     publish_report(r, sd.n, args.reports + s);
   }
   if (tid == 0) arrive_and_signal(args);
@@ -740,7 +752,23 @@ __device__ __forceinline__ uint32_t find_block_segment(const SegDesc *segs, uint
 template <bool kSingle, int kMask, bool kStop = false>
 __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
   __shared__ Partial lds[kWavesPerBlock];
-  const uint64_t b = blockIdx.x;
+  uint64_t b = blockIdx.x;
+  if constexpr (kSingle) {
+    if (args.prev.partials != nullptr) {
+      // workgroup 0 finishes the earlier check left to this launch (its
+      // partials are complete: that check kernel ended before this one began)
+      if (b == 0) {
+        const Partial r = reduce_partials(args.prev.partials, 0, args.prev.nparts - 1, lds);
+        publish_report(r, args.prev.n, args.prev.reports);
+        if (threadIdx.x == 0) {
+          wait_memory();
+          __hip_atomic_store(args.prev.done, args.prev.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+        return;
+      }
+      --b;
+    }
+  }
   if constexpr (kStop) {
     // one segment per workgroup: its tiles i, i + g, ... (i = b - blk)
     __shared__ uint32_t lim;

@@ -145,6 +145,18 @@ struct Partial {
   uint64_t nan_r, nan_c, inf_r, inf_c;
 };
 
+// A single-tensor check whose finalize was left to the next check launched
+// on its stream: that launch's workgroup 0 reduces these partials (the
+// finalize's tree), writes the report and hands `seq` to the host.
+struct DeferredFinalize {
+  const Partial *partials;      // nullptr: none
+  uint64_t nparts;
+  uint64_t n;
+  sv_report *reports;
+  uint64_t *done;
+  uint64_t seq;
+};
+
 struct CompareArgs {
   const SegDesc *segs;          // device table (batched) or nullptr (single)
   SegDesc single;               // the segment of a single-tensor check
@@ -161,6 +173,7 @@ struct CompareArgs {
   sv_report *reports;           // nseg reports, in host-mapped pinned memory
   uint64_t *done;               // host-mapped word that receives `seq` once every report is written
   uint64_t seq;
+  DeferredFinalize prev;        // single tensor, no fused report: an earlier check to finish first
 };
 
 // ----------------------------------------------------------------- host helpers

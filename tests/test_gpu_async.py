@@ -216,3 +216,41 @@ def test_reports_as_arrays_equal_the_dicts():
     arr = t.wait(as_array=True)
     assert arr.shape == (1,) and {f: arr[0][f].item() for f in arr.dtype.names} == t.wait()
     assert sv.compare_batched([], as_array=True).shape == (0,)
+
+
+def test_deferred_reductions_are_finished_by_whatever_comes_next():
+    # A submitted single-tensor check leaves its reduction to the next check on
+    # its stream (or to the wait / readiness query / a drain): chains of them,
+    # an empty check in between, a batched and a synchronous check taking over,
+    # each report equal to the synchronous one.
+    big = [_pair(n, 90 + k, p=0.01) for k, n in enumerate([(1 << 20) + 5, 1 << 22, (1 << 21) + 3])]
+    small = _pair(4099, 95, p=0.01)                                  # one workgroup: no separate reduction
+    z = empty(0, "f32")
+    want = [sv.compare(r, c, 1e-8, 0.0) for r, c in big]
+    want_small = sv.compare(*small, 1e-8, 0.0)
+    batch = [(big[0][0], big[0][1], 1e-8, 0.0, False), (small[0], small[1], 1e-8, 0.0, False)]
+    want_batch = sv.compare_batched(batch)
+    torch.cuda.synchronize()
+    print("deferred chain", flush=True)
+    for rounds in range(3):
+        t = [sv.compare_submit(*big[k % 3], 1e-8, 0.0) for k in range(7)]        # each finishes the one before
+        assert [x.wait() for x in reversed(t)] == [want[k % 3] for k in reversed(range(7))]
+    print("deferred then empty then check", flush=True)
+    t1 = sv.compare_submit(*big[0], 1e-8, 0.0)
+    t2 = sv.compare_submit(z, z, 1e-8, 0.0)                                     # launches nothing
+    t3 = sv.compare_submit(*big[1], 1e-8, 0.0)                                  # finishes t1
+    t4 = sv.compare_submit(*small, 1e-8, 0.0)                                   # queues t3's reduction first
+    t5 = sv.compare_submit(*big[2], 1e-8, 0.0)
+    t6 = sv.compare_batched_submit(batch)                                       # queues t5's reduction first
+    t7 = sv.compare_submit(*big[0], 1e-8, 0.0)
+    assert sv.compare(*big[1], 1e-8, 0.0) == want[1]                            # finishes t7
+    t8 = sv.compare_submit(*big[2], 1e-8, 0.0)
+    assert t8.wait() == want[2] and t7.wait() == want[0] and t6.wait() == want_batch
+    assert t5.wait() == want[2] and t4.wait() == want_small and t3.wait() == want[1]
+    assert t2.wait() == sv.compare(z, z, 1e-8, 0.0) and t1.wait() == want[0]
+    print("deferred ready polling", flush=True)
+    t = sv.compare_submit(*big[1], 1e-8, 0.0)
+    for _ in range(200_000):                                                    # ready() queues the reduction
+        if t.ready():
+            break
+    assert t.ready() and t.wait() == want[1]
