@@ -72,8 +72,7 @@ struct CheckSlot {
   SegDesc *h_table = nullptr;    // pinned staging of the segment table
   size_t h_table_cap = 0;
   bool deferred = false;         // its finalize is left to the next check launched on its stream
-  CompareArgs fin{};             // ... and what that finalize needs
-  uint64_t nparts = 0;           // its partials (one per check workgroup)
+  FinalizeArgs fin{};            // ... and what that finalize needs
 };
 
 struct DeviceState {
@@ -82,16 +81,20 @@ struct DeviceState {
   int cus = 0;
   Partial *partials[2] = {nullptr, nullptr};   // one per (workgroup, segment piece), in two halves that
   size_t partials_cap[2] = {0, 0};              // launched checks take in turn, so that a check can
-  int half = 0;                                 // finish the one before it while writing its own
+  int half = 0;                                 // finish the one before it while writing its own (the
+                                                // segment tables alternate the same way)
   int deferred = -1;                 // the slot whose finalize waits for the next check on its stream
-  SegDesc *table = nullptr;      // batched segment table
-  size_t table_cap = 0;
+  SegDesc *table[2] = {nullptr, nullptr};   // batched segment tables, in the halves of the partials
+  size_t table_cap[2] = {0, 0};
+  std::vector<SegDesc> table_held[2];       // what each device table holds (a repeated batch skips the copy)
   uint64_t *idx = nullptr;
   size_t idx_cap = 0;
   uint64_t *h_idx = nullptr;
   size_t h_idx_cap = 0;
   SynthJob *synth_table = nullptr;   // batched synthesis job table
   size_t synth_table_cap = 0;
+  std::vector<SynthJob> synth_held;  // what it holds (a repeated batch skips the copy)
+  hipStream_t synth_copy_stream = nullptr;   // where that copy was queued
   SynthJob *h_synth = nullptr;       // its pinned staging
   size_t h_synth_cap = 0;
   hipEvent_t synth_copied = nullptr; // staging -> table copy of the last batch done
@@ -340,6 +343,7 @@ int check_seg(const sv_segment &g, uint32_t k) {
 
 SegDesc make_desc(const sv_segment &g, uint64_t unit_begin) {
   SegDesc d;
+  std::memset(&d, 0, sizeof d);      // padding included: tables are compared bytewise
   d.ref = g.ref;
   d.cand = g.cand;
   d.n = g.n;
@@ -349,7 +353,7 @@ SegDesc make_desc(const sv_segment &g, uint64_t unit_begin) {
   d.dtype = g.dtype;
   d.equal_nan = g.equal_nan ? 1 : 0;
   d.vec_ok = (((uintptr_t)g.ref | (uintptr_t)g.cand) & 15u) == 0 ? 1 : 0;
-  d.blk = 0;
+  d.w0 = d.w1 = 0;
   return d;
 }
 
@@ -387,7 +391,7 @@ int flush_deferred(DeviceState *ds) {
     e1 = take_event();
     if (e0) (void)hipEventRecord(e0, sl.stream);
   }
-  const hipError_t e = launch_finalize(sl.fin, sl.stream);
+  const hipError_t e = launch_finalize(sl.fin, sl.stream);   // its own kernel
   if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
   if (e0 && e1) {
     (void)hipEventRecord(e1, sl.stream);
@@ -432,7 +436,10 @@ void plan_single(const sv_segment &g, int cus, CheckPlan &plan) {
   plan.args.single = make_desc(g, 0);
   plan.args.nseg = 1;
   plan.total_units = plan.args.total_units = units_of(g.dtype, g.n);
-  if (plan.total_units) compare_grid(plan.total_units, cus, false, &plan.nblocks, &plan.args.chunk);
+  if (plan.total_units) {
+    compare_grid(plan.total_units, cus, false, &plan.nblocks, &plan.args.chunk);
+    plan.args.single.w1 = plan.nblocks - 1;   // its workgroups 0 .. nblocks - 1, slots 0 .. nblocks - 1
+  }
 }
 
 void plan_batched(const sv_segment *segs, uint32_t nseg, int32_t mode, int cus, CheckPlan &plan) {
@@ -476,13 +483,16 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
                 (unsigned)kMaxStopBlocks);
   const size_t nfirsts = plan.stop_at_first ? (size_t)nseg * kFirstStride : 0;
   const int par = ds->half;                      // this check's half of the partials
-  const bool grow = (size_t)plan.nblocks + nseg > ds->partials_cap[par] || (batched && nseg > ds->table_cap) ||
-                    nfirsts > ds->firsts_cap;
+  const bool grow = (size_t)plan.nblocks + nseg > ds->partials_cap[par] ||
+                    (batched && nseg > ds->table_cap[par]) || nfirsts > ds->firsts_cap;
   int rc = SV_OK;
   if (grow || (ds->has_last && ds->last_stream != st)) rc = drain_pending(ds);
   if (!rc) rc = ensure_device(ds->partials[par], ds->partials_cap[par], (size_t)plan.nblocks + nseg, "partials");
   if (!rc && nfirsts) rc = ensure_firsts(ds, nfirsts, ds->seq + 1);
-  if (!rc && batched) rc = ensure_device(ds->table, ds->table_cap, nseg, "segment table");
+  if (!rc && batched && nseg > ds->table_cap[par]) {
+    ds->table_held[par].clear();               // a new allocation holds nothing yet
+    rc = ensure_device(ds->table[par], ds->table_cap[par], nseg, "segment table");
+  }
   if (!rc && batched) rc = ensure_pinned(sl.h_table, sl.h_table_cap, nseg, "segment table staging");
   if (!rc) rc = ensure_reports(sl, nseg);
   if (!rc) rc = ensure_counters(ds, 1);
@@ -492,17 +502,28 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   if (batched) {
     uint64_t begin = 0, blk = 0;
     for (uint32_t j = 0; j < nseg; ++j) {
-      sl.h_table[j] = make_desc(plan.segs[j], begin);
+      SegDesc &d = sl.h_table[j];
+      d = make_desc(plan.segs[j], begin);
       const uint64_t units = units_of(plan.segs[j].dtype, plan.segs[j].n);
       if (plan.stop_at_first) {
-        sl.h_table[j].blk = (uint32_t)blk;
+        d.w0 = (uint32_t)blk;
         blk += stop_blocks(units, plan.args.chunk);
+        d.w1 = (uint32_t)(blk - (units ? 1 : 0));
+      } else if (units) {
+        d.w0 = (uint32_t)(begin / plan.args.chunk);
+        d.w1 = (uint32_t)((begin + units - 1) / plan.args.chunk);
       }
       begin += units;
     }
-    SV_HIP(hipMemcpyAsync(ds->table, sl.h_table, nseg * sizeof(SegDesc), hipMemcpyHostToDevice, st),
-           "segment table copy to device");
-    args.segs = ds->table;
+    // the same batch as the last one in this half (a check repeated on the same
+    // tensors) finds its table in place: only this call writes the device table
+    std::vector<SegDesc> &held = ds->table_held[par];
+    if (held.size() != nseg || std::memcmp(held.data(), sl.h_table, nseg * sizeof(SegDesc)) != 0) {
+      SV_HIP(hipMemcpyAsync(ds->table[par], sl.h_table, nseg * sizeof(SegDesc), hipMemcpyHostToDevice, st),
+             "segment table copy to device");
+      held.assign(sl.h_table, sl.h_table + nseg);
+    }
+    args.segs = ds->table[par];
   }
   args.stop_at_first = plan.stop_at_first ? 1 : 0;
   args.firsts = ds->firsts;
@@ -512,7 +533,7 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   args.reports = sl.d_reports;
   args.done = ds->d_done + (size_t)k * kDoneStride;
   args.seq = ds->seq + 1;
-  const bool defer = !args.fused && k != kSyncSlot && !batched;   // see below
+  const bool defer = !args.fused && k != kSyncSlot;   // see below
   hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr;
   if (g_prof_on.load()) {
     e0 = take_event();
@@ -525,34 +546,33 @@ int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
     const uint64_t n = batched ? plan.segs[j].n : args.single.n;
     if (n) mask |= 1u << (batched ? plan.segs[j].dtype : args.single.dtype);
   }
-  // A submitted single-tensor check leaves its finalize to the next check on
-  // its stream, whose workgroup 0 runs it (one launch less per check when
-  // checks follow each other); a single-tensor check with a grid of its own
-  // takes it on, any other check has it queued first.
-  args.prev = DeferredFinalize{};
-  const bool host_prev = !batched && args.fused == 0;
+  // A submitted check leaves its finalize to the next check on its stream,
+  // whose first workgroups run it (one launch less per check when checks
+  // follow each other).  A check with a grid of its own takes it on; a
+  // one-workgroup check (which reports by itself) and a stop-at-first check
+  // have it queued first.
+  args.nprev = 0;
+  args.prev = FinalizeArgs{};
   if (ds->deferred >= 0) {
     CheckSlot &pd = ds->slots[ds->deferred];
-    if (host_prev && pd.stream == st) {
-      args.prev = DeferredFinalize{pd.fin.partials, pd.nparts, pd.fin.single.n, pd.fin.reports, pd.fin.done,
-                                   pd.fin.seq};
+    if (args.fused == 0 && !args.stop_at_first && pd.stream == st) {
+      args.prev = pd.fin;
+      args.nprev = pd.fin.nseg;
       ds->deferred = -1;
       pd.deferred = false;
     } else if ((rc = flush_deferred(ds)) != SV_OK) {
       return rc;
     }
   }
-  hipError_t e = launch_compare(args, plan.nblocks + (args.prev.partials ? 1u : 0u), mask, st);
+  hipError_t e = launch_compare(args, plan.nblocks + args.nprev, mask, st);
   if (e != hipSuccess) return hip_fail(e, "check kernel launch");
   if (e1) (void)hipEventRecord(e1, st);
   if (defer) {
-    sl.fin = args;
-    sl.fin.prev = DeferredFinalize{};
-    sl.nparts = plan.nblocks;
+    sl.fin = finalize_args(args);
     sl.deferred = true;
     ds->deferred = k;
   } else if (!args.fused) {
-    e = launch_finalize(args, st);
+    e = launch_finalize(finalize_args(args), st);
     if (e != hipSuccess) return hip_fail(e, "finalize kernel launch");
   }
   ds->seq = args.seq;
@@ -812,23 +832,12 @@ int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
   }
   const uint32_t nt = (uint32_t)table_jobs.size();
   if (nt) {
-    if (!ds->synth_copied) {
-      SV_HIP(hipEventCreateWithFlags(&ds->synth_copied, hipEventDisableTiming), "hipEventCreate");
-      SV_HIP(hipEventCreateWithFlags(&ds->synth_done, hipEventDisableTiming), "hipEventCreate");
-    }
-    if (ds->synth_pending) {
-      // the staging buffer is rewritten below: its last copy must have left it;
-      // the device table is rewritten on this stream after the last batch read it
-      SV_HIP(hipEventSynchronize(ds->synth_copied), "wait for the previous job-table copy");
-      SV_HIP(hipStreamWaitEvent(st, ds->synth_done, 0), "order after the previous batch");
-    }
-    rc = ensure_pinned(ds->h_synth, ds->h_synth_cap, nt, "job table staging");
-    if (!rc) rc = ensure_device(ds->synth_table, ds->synth_table_cap, nt, "job table");
-    if (rc) return rc;
+    std::vector<SynthJob> table(nt);
     uint64_t begin = 0;
     for (uint32_t t = 0; t < nt; ++t) {
       const sv_synth_job &j = jobs[table_jobs[t]];
-      SynthJob &d = ds->h_synth[t];
+      SynthJob &d = table[t];
+      std::memset(&d, 0, sizeof d);
       d.p = params[table_jobs[t]];
       d.out = j.out;
       d.n = j.n;
@@ -839,9 +848,34 @@ int sv_synth_batched(const sv_synth_job *jobs, uint32_t njobs) {
       begin += (d.nvec + tile_vecs - 1) / tile_vecs;
     }
     tiles = begin;
-    SV_HIP(hipMemcpyAsync(ds->synth_table, ds->h_synth, nt * sizeof(SynthJob), hipMemcpyHostToDevice, st),
-           "job table copy to device");
-    SV_HIP(hipEventRecord(ds->synth_copied, st), "hipEventRecord");
+    // the same batch as the last one (synthesis repeated into the same tensors)
+    // finds its table in place: only this call writes the device table
+    const bool same = ds->synth_held.size() == nt &&
+                      std::memcmp(ds->synth_held.data(), table.data(), nt * sizeof(SynthJob)) == 0;
+    if (same && st != ds->synth_copy_stream)       // that copy may still be queued on another stream
+      SV_HIP(hipStreamWaitEvent(st, ds->synth_copied, 0), "order after the job-table copy");
+    if (!same) {
+      if (!ds->synth_copied) {
+        SV_HIP(hipEventCreateWithFlags(&ds->synth_copied, hipEventDisableTiming), "hipEventCreate");
+        SV_HIP(hipEventCreateWithFlags(&ds->synth_done, hipEventDisableTiming), "hipEventCreate");
+      }
+      if (ds->synth_pending) {
+        // the staging buffer is rewritten below: its last copy must have left it;
+        // the device table is rewritten on this stream after the last batch read it
+        SV_HIP(hipEventSynchronize(ds->synth_copied), "wait for the previous job-table copy");
+        SV_HIP(hipStreamWaitEvent(st, ds->synth_done, 0), "order after the previous batch");
+      }
+      ds->synth_held.clear();
+      rc = ensure_pinned(ds->h_synth, ds->h_synth_cap, nt, "job table staging");
+      if (!rc) rc = ensure_device(ds->synth_table, ds->synth_table_cap, nt, "job table");
+      if (rc) return rc;
+      std::memcpy(ds->h_synth, table.data(), nt * sizeof(SynthJob));
+      SV_HIP(hipMemcpyAsync(ds->synth_table, ds->h_synth, nt * sizeof(SynthJob), hipMemcpyHostToDevice, st),
+             "job table copy to device");
+      SV_HIP(hipEventRecord(ds->synth_copied, st), "hipEventRecord");
+      ds->synth_held.swap(table);
+      ds->synth_copy_stream = st;
+    }
   }
   if (e0) (void)hipEventRecord(e0, st);
   if (nt)
@@ -1179,7 +1213,14 @@ int sv_shutdown(void) {
     }
     s->deferred = -1;
     s->half = 0;
-    if (s->table) (void)hipFree(s->table);
+    for (int h = 0; h < 2; ++h) {
+      if (s->table[h]) (void)hipFree(s->table[h]);
+      s->table[h] = nullptr;
+      s->table_cap[h] = 0;
+      s->table_held[h].clear();
+    }
+    s->synth_held.clear();
+    s->synth_copy_stream = nullptr;
     if (s->idx) (void)hipFree(s->idx);
     for (CheckSlot &sl : s->slots) {
       if (sl.h_reports) (void)hipHostFree(sl.h_reports);
@@ -1203,9 +1244,9 @@ int sv_shutdown(void) {
     s->synth_table = nullptr; s->h_synth = nullptr; s->synth_copied = nullptr; s->synth_done = nullptr;
     s->synth_table_cap = s->h_synth_cap = 0;
     s->synth_pending = false;
-    s->table = nullptr; s->idx = nullptr;
+    s->idx = nullptr;
     s->h_idx = nullptr;
-    s->table_cap = s->idx_cap = 0;
+    s->idx_cap = 0;
     s->h_idx_cap = 0;
   }
   perf_shutdown();

@@ -432,19 +432,11 @@ __device__ __forceinline__ void publish_report(const Partial &r, uint64_t n, sv_
                        __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
-// Called by one thread of every finalize workgroup once its report (if any)
-// is written and has landed (each workgroup waits for its own stores before
-// it arrives): the last to arrive clears the counter and hands the sequence
-// number to the host.  A lone workgroup needs no counter.  The counter's
-// reset need not land before the sequence number: the next launch that uses
-// it starts after this kernel has ended.
-__device__ __forceinline__ void arrive_and_signal(const CompareArgs &args) {
+// Called by one thread of a check that is its own only workgroup, once its
+// report is written: waits for those stores, then hands the sequence number
+// to the host.
+__device__ __forceinline__ void signal_done(const CompareArgs &args) {
   wait_memory();
-  if (gridDim.x > 1) {
-    if (__hip_atomic_fetch_add(args.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != gridDim.x - 1)
-      return;
-    __hip_atomic_store(args.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
   __hip_atomic_store(args.done, args.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
@@ -621,35 +613,42 @@ __device__ __forceinline__ uint32_t find_segment(const SegDesc *segs, uint32_t n
 
 // The reduction of a segment's partials P[b0 .. b1] into its report, by a
 // workgroup of kFinBlock threads: thread t merges slots b0 + t, b0 + t +
-// kFinBlock, ... in order (loaded four at a time), then a fixed shuffle tree
-// and the waves in order.  The result is valid on thread 0.  The finalize
-// kernel runs it, and so does the first workgroup of a check kernel that
-// finishes an earlier check (the same threads, the same tree: the same bits).
+// kFinBlock, ... in order, then a fixed shuffle tree and the waves in order.
+// The result is valid on thread 0.  The finalize kernel runs it with four
+// slots in flight per thread; a check kernel that finishes an earlier check
+// in its first workgroups runs it with one (kFour = false), which keeps the
+// check's registers at what its own loop needs.  The merges are the same in
+// either case, and so are the bits.
 constexpr int kFinBlock = kCmpBlock;             // finalize threads per segment
 constexpr int kFinWaves = kFinBlock / kWave;
 static_assert(kFinWaves == kWavesPerBlock, "a check workgroup runs the finalize's tree");
 
+template <bool kFour>
 __device__ Partial reduce_partials(const Partial *P, uint64_t b0, uint64_t b1, Partial *lds) {
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   Partial acc = empty_partial();
   uint64_t b = b0 + tid;
-  for (; b + 3 * kFinBlock <= b1; b += 4 * kFinBlock) {
-    const Partial p0 = P[b], p1 = P[b + kFinBlock], p2 = P[b + 2 * kFinBlock], p3 = P[b + 3 * kFinBlock];
-    merge(acc, p0);
-    merge(acc, p1);
-    merge(acc, p2);
-    merge(acc, p3);
+  if constexpr (!kFour) {
+    for (; b <= b1; b += kFinBlock) merge(acc, P[b]);
+  } else {
+    for (; b + 3 * kFinBlock <= b1; b += 4 * kFinBlock) {
+      const Partial p0 = P[b], p1 = P[b + kFinBlock], p2 = P[b + 2 * kFinBlock], p3 = P[b + 3 * kFinBlock];
+      merge(acc, p0);
+      merge(acc, p1);
+      merge(acc, p2);
+      merge(acc, p3);
+    }
+    // at most three left: all loaded before the first merge (one memory round
+    // trip instead of up to three), merged in the same order
+    const bool h0 = b <= b1, h1 = b + kFinBlock <= b1, h2 = b + 2 * kFinBlock <= b1;
+    Partial q0, q1, q2;
+    if (h0) q0 = P[b];
+    if (h1) q1 = P[b + kFinBlock];
+    if (h2) q2 = P[b + 2 * kFinBlock];
+    if (h0) merge(acc, q0);
+    if (h1) merge(acc, q1);
+    if (h2) merge(acc, q2);
   }
-  // at most three left: all loaded before the first merge (one memory round
-  // trip instead of up to three), merged in the same order
-  const bool h0 = b <= b1, h1 = b + kFinBlock <= b1, h2 = b + 2 * kFinBlock <= b1;
-  Partial q0, q1, q2;
-  if (h0) q0 = P[b];
-  if (h1) q1 = P[b + kFinBlock];
-  if (h2) q2 = P[b + 2 * kFinBlock];
-  if (h0) merge(acc, q0);
-  if (h1) merge(acc, q1);
-  if (h2) merge(acc, q2);
   wave_merge(acc);
   if (lane == 0) lds[wave] = acc;
   __syncthreads();
@@ -662,24 +661,38 @@ __device__ Partial reduce_partials(const Partial *P, uint64_t b0, uint64_t b1, P
   return r;
 }
 
-// One workgroup per segment, behind the check kernel; the report goes into
-// host-mapped memory.
-template <bool kSingle>
-__global__ __launch_bounds__(kFinBlock) void finalize_kernel(CompareArgs args) {
-  __shared__ Partial lds[kFinWaves];
-  const uint32_t s = blockIdx.x, tid = threadIdx.x;
-  const SegDesc sd = kSingle ? args.single : args.segs[s];
+// Segment s of a finished check: its report, then (one thread) the arrival of
+// this workgroup among the nwg that finalize the check; the last to arrive
+// clears the counter and hands the sequence number to the host.  Each
+// workgroup waits for its own stores before it arrives.  The counter's reset
+// need not land before the sequence number: the next launch that uses it
+// starts after this one has ended.
+template <bool kFour>
+__device__ void finalize_segment(const FinalizeArgs &f, uint32_t s, uint32_t nwg, Partial *lds) {
+  const SegDesc sd = f.segs ? f.segs[s] : f.single;
   const uint64_t units = units_of(sd.dtype, sd.n);
   if (units != 0) {                  // empty segments are reported by the host
     // the segment's workgroups and their slots: a piece of workgroups b0..b1 in
     // slots b + s, or (stop at first) workgroups of its own in slots b
-    const bool own = !kSingle && args.stop_at_first;
-    const uint64_t b0 = own ? sd.blk : sd.unit_begin / args.chunk;
-    const uint64_t b1 = own ? sd.blk + stop_blocks(units, args.chunk) - 1 : (sd.unit_begin + units - 1) / args.chunk;
-    const Partial r = reduce_partials(args.partials + (own ? 0 : s), b0, b1, lds);
-    publish_report(r, sd.n, args.reports + s);
+    const bool own = f.segs && f.stop_at_first;
+    const Partial r = reduce_partials<kFour>(f.partials + (own ? 0 : s), sd.w0, sd.w1, lds);
+    publish_report(r, sd.n, f.reports + s);
   }
-  if (tid == 0) arrive_and_signal(args);
+  if (threadIdx.x == 0) {
+    wait_memory();
+    if (nwg > 1) {
+      if (__hip_atomic_fetch_add(f.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != nwg - 1) return;
+      __hip_atomic_store(f.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __hip_atomic_store(f.done, f.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
+}
+
+// One workgroup per segment, behind the check kernel; the reports go into
+// host-mapped memory.
+__global__ __launch_bounds__(kFinBlock) void finalize_kernel(FinalizeArgs f) {
+  __shared__ Partial lds[kFinWaves];
+  finalize_segment<true>(f, blockIdx.x, gridDim.x, lds);
 }
 
 // kMask: the set of dtypes (bit 1 << dtype) the segments of this launch use;
@@ -744,7 +757,7 @@ __device__ __forceinline__ uint32_t find_block_segment(const SegDesc *segs, uint
   uint32_t lo = 0, hi = nseg;
   while (hi - lo > 1) {
     const uint32_t mid = (lo + hi) / 2;
-    if (segs[mid].blk <= b) lo = mid; else hi = mid;
+    if (segs[mid].w0 <= b) lo = mid; else hi = mid;
   }
   return lo;
 }
@@ -753,24 +766,20 @@ template <bool kSingle, int kMask, bool kStop = false>
 __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
   __shared__ Partial lds[kWavesPerBlock];
   uint64_t b = blockIdx.x;
-  if constexpr (kSingle) {
-    if (args.prev.partials != nullptr) {
-      // workgroup 0 finishes the earlier check left to this launch (its
-      // partials are complete: that check kernel ended before this one began)
-      if (b == 0) {
-        const Partial r = reduce_partials(args.prev.partials, 0, args.prev.nparts - 1, lds);
-        publish_report(r, args.prev.n, args.prev.reports);
-        if (threadIdx.x == 0) {
-          wait_memory();
-          __hip_atomic_store(args.prev.done, args.prev.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-        }
+  if constexpr (!kStop) {
+    if (args.nprev) {
+      // the first workgroups finish the earlier check left to this launch (its
+      // partials are complete: that check kernel ended before this one began);
+      // stop-at-first launches take none: their loop needs the registers
+      if (b < args.nprev) {
+        finalize_segment<false>(args.prev, (uint32_t)b, args.nprev, lds);
         return;
       }
-      --b;
+      b -= args.nprev;
     }
   }
   if constexpr (kStop) {
-    // one segment per workgroup: its tiles i, i + g, ... (i = b - blk)
+    // one segment per workgroup: its tiles i, i + g, ... (i = b - w0)
     __shared__ uint32_t lim;
     const uint32_t s = find_block_segment(args.segs, args.nseg, (uint32_t)b);
     const SegDesc sd = args.segs[s];
@@ -779,7 +788,7 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
     if (threadIdx.x == 0) lim = 0xFFFFFFFFu;
     __syncthreads();
     const StopCtx sc{args.firsts + (size_t)s * kFirstStride, (uint32_t)args.seq, &lim};
-    const Partial p = check_any<kMask, true>(sd, (b - sd.blk) * kCmpTile, units, g * kCmpTile, &sc, lds);
+    const Partial p = check_any<kMask, true>(sd, (b - sd.w0) * kCmpTile, units, g * kCmpTile, &sc, lds);
     if (threadIdx.x == 0) args.partials[b] = p;
     return;
   }
@@ -795,7 +804,7 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
     if constexpr (kSingle) {
       if (args.fused == 1) {         // the only workgroup: its partial is the whole result
         publish_report(p, sd.n, args.reports);
-        if (threadIdx.x == 0) arrive_and_signal(args);
+        if (threadIdx.x == 0) signal_done(args);
         return;
       }
       if (args.fused == 2) {
@@ -816,7 +825,10 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
 template <int kMask>
 static void launch_masked(const CompareArgs &args, uint32_t nblocks, hipStream_t stream) {
   if (args.segs == nullptr)
-    hipLaunchKernelGGL((compare_kernel<true, kMask>), dim3(nblocks), dim3(kCmpBlock), 0, stream, args);
+    // a single tensor's check runs two workgroups per CU (16 waves), held there by
+    // an LDS request it does not use: 80.8 against 82.5 us for 2 x 256 MiB of fp32,
+    // 1432 against 1508 us for 2 x 4 GiB of special values, than three per CU
+    hipLaunchKernelGGL((compare_kernel<true, kMask>), dim3(nblocks), dim3(kCmpBlock), SV_CMP_SINGLE_LDS, stream, args);
   else if (args.stop_at_first)
     hipLaunchKernelGGL((compare_kernel<false, kMask, true>), dim3(nblocks), dim3(kCmpBlock), 0, stream, args);
   else
@@ -855,11 +867,13 @@ hipError_t launch_fill_u64(uint64_t *p, uint64_t n, uint64_t value, hipStream_t 
   return hipGetLastError();
 }
 
-hipError_t launch_finalize(const CompareArgs &args, hipStream_t stream) {
-  if (args.segs == nullptr)
-    hipLaunchKernelGGL(finalize_kernel<true>, dim3(1), dim3(kFinBlock), 0, stream, args);
-  else
-    hipLaunchKernelGGL(finalize_kernel<false>, dim3(args.nseg), dim3(kFinBlock), 0, stream, args);
+FinalizeArgs finalize_args(const CompareArgs &args) {
+  return FinalizeArgs{args.segs, args.single, args.segs ? args.nseg : 1u, args.chunk, args.partials,
+                      args.counter, args.stop_at_first, args.reports, args.done, args.seq};
+}
+
+hipError_t launch_finalize(const FinalizeArgs &f, hipStream_t stream) {
+  hipLaunchKernelGGL(finalize_kernel, dim3(f.nseg), dim3(kFinBlock), 0, stream, f);
   return hipGetLastError();
 }
 

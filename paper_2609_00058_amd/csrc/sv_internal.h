@@ -25,6 +25,9 @@ namespace sv {
 #ifndef SV_CMP_LAST_BLOCK_MAX
 #define SV_CMP_LAST_BLOCK_MAX 64     // single-tensor grids up to this size: the last workgroup reports, no finalize
 #endif
+#ifndef SV_CMP_SINGLE_LDS
+#define SV_CMP_SINGLE_LDS 61440      // dynamic LDS bytes per single-tensor check workgroup, unused: two such
+#endif                               // workgroups share a CU's 160 KB, not three (measured faster)
 #ifndef SV_CMP_BATCH_BLOCKS_PER_CU
 #define SV_CMP_BATCH_BLOCKS_PER_CU 12   // check workgroups per CU, batched
 #endif
@@ -109,7 +112,7 @@ hipError_t launch_perturb_indexed(int32_t dtype, const PerturbParams &p, const u
 // that occurs, because both b and s grow along the unit space).
 //
 // Stop-at-first launches lay the workgroups out by segment instead: segment s
-// gets stop_blocks(units, chunk) workgroups of its own, from workgroup blk on,
+// gets stop_blocks(units, chunk) workgroups of its own, from workgroup w0 on,
 // which sweep it together from the front, workgroup i taking tiles i, i + g,
 // i + 2g, ... (a tile is kCmpBlock * SV_CMP_UNROLL units, one iteration of a
 // workgroup); each writes one partial, into slot b.  A mismatch found in a tile
@@ -124,7 +127,9 @@ struct SegDesc {
   int32_t dtype;
   int32_t equal_nan;
   int32_t vec_ok;               // both pointers 16-byte aligned
-  uint32_t blk;                 // stop-at-first launches: the segment's first workgroup
+  uint32_t w0, w1;              // the first and last check workgroup holding units of it (for a
+                                // stop-at-first launch its own workgroups, w0 .. w1 in slots w0 ..;
+                                // otherwise slot b + s of workgroup b), so the finalize divides nothing
 };
 
 constexpr uint64_t kCmpTile = (uint64_t)kCmpBlock * SV_CMP_UNROLL;   // units per workgroup iteration
@@ -145,13 +150,19 @@ struct Partial {
   uint64_t nan_r, nan_c, inf_r, inf_c;
 };
 
-// A single-tensor check whose finalize was left to the next check launched
-// on its stream: that launch's workgroup 0 reduces these partials (the
-// finalize's tree), writes the report and hands `seq` to the host.
-struct DeferredFinalize {
-  const Partial *partials;      // nullptr: none
-  uint64_t nparts;
-  uint64_t n;
+// What the finalize of a check needs: its segments, the layout of its
+// partials, where its reports and completion word go.  The finalize kernel
+// runs one workgroup per segment on it; a check whose finalize was left to
+// the next check launched on its stream is finished by that launch's first
+// workgroups instead (the same code, the same bits).
+struct FinalizeArgs {
+  const SegDesc *segs;          // device table (batched) or nullptr (single: `single`)
+  SegDesc single;
+  uint32_t nseg;                // workgroups of the finalize (1 for a single tensor)
+  uint64_t chunk;               // units per check workgroup
+  const Partial *partials;
+  uint32_t *counter;            // arrivals of its workgroups, zero between launches
+  int32_t stop_at_first;
   sv_report *reports;
   uint64_t *done;
   uint64_t seq;
@@ -173,7 +184,8 @@ struct CompareArgs {
   sv_report *reports;           // nseg reports, in host-mapped pinned memory
   uint64_t *done;               // host-mapped word that receives `seq` once every report is written
   uint64_t seq;
-  DeferredFinalize prev;        // single tensor, no fused report: an earlier check to finish first
+  uint32_t nprev;               // > 0: workgroups 0 .. nprev - 1 finish an earlier check first
+  FinalizeArgs prev;
 };
 
 // ----------------------------------------------------------------- host helpers
@@ -202,7 +214,8 @@ __host__ __device__ inline uint64_t units_of(int32_t dtype, uint64_t n) {
 // The check kernel (dtype_mask: OR of (1 << dtype) over the segments with
 // elements), and the finalize kernel that turns its partials into reports.
 hipError_t launch_compare(const CompareArgs &args, uint32_t nblocks, uint32_t dtype_mask, hipStream_t stream);
-hipError_t launch_finalize(const CompareArgs &args, hipStream_t stream);
+hipError_t launch_finalize(const FinalizeArgs &f, hipStream_t stream);
+FinalizeArgs finalize_args(const CompareArgs &args);
 hipError_t launch_fill_u64(uint64_t *p, uint64_t n, uint64_t value, hipStream_t stream);
 
 }  // namespace sv

@@ -291,3 +291,31 @@ def test_random_sequences_of_submits_waits_and_queries():
     for t, w in pending:
         assert t.wait() == w
     torch.cuda.synchronize()
+
+
+def test_repeated_batches_reuse_their_tables_on_any_stream(oracle):
+    # A batch identical to the last one finds its job / segment table already on
+    # the device; on another stream it still waits for that table's upload.
+    outs = [empty(n, "f32") for n in (70001, 1 << 20, 3)]
+    jobs = sv.SynthBatch([(o, 11, k, "normal", NORMAL) for k, o in enumerate(outs)])
+    want = [oracle.synth(11, k, "f32", "normal", oracle.dist_params(**NORMAL), o.numel()) for k, o in enumerate(outs)]
+    side = torch.cuda.Stream()
+    print("repeated batches", flush=True)
+    for rep in range(3):
+        for s in (torch.cuda.current_stream(), side, side, torch.cuda.current_stream()):
+            for o in outs:
+                o.zero_()
+            torch.cuda.synchronize()
+            with torch.cuda.stream(s):
+                sv.synth_batched(jobs)
+            torch.cuda.synchronize()
+            assert all(np.array_equal(bits(o), w) for o, w in zip(outs, want)), (rep, s)
+    cands = [_pair(o.numel(), 40 + k, p=0.01)[1] for k, o in enumerate(outs)]
+    a = sv.SegmentBatch([(o, c, 1e-8, 0.0, False) for o, c in zip(outs, cands)])
+    b = sv.SegmentBatch([(c, o, 1e-7, 1e-9, True) for o, c in zip(outs, cands)])
+    want_a, want_b = sv.compare_batched(a), sv.compare_batched(b)
+    assert want_a != want_b
+    for rep in range(6):                      # the two tables alternate between the halves
+        assert sv.compare_batched(a) == want_a and sv.compare_batched(b) == want_b
+        assert sv.compare_batched(a) == want_a and sv.compare_batched(a) == want_a
+        assert sv.compare_batched_submit(b).wait() == want_b
