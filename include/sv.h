@@ -422,8 +422,10 @@ const char *sv_last_error(void);
  * add a few microseconds between launches).  sv_profile_read() waits for the
  * recorded events of one kind, returns their count and total milliseconds,
  * and forgets them.  Kinds: 0 synthesis, 1 check (the streaming kernel of
- * sv_compare / sv_compare_batched), 2 candidate derivation, 3 the check's
- * finalize kernel (per-segment reduction and report).
+ * sv_compare / sv_compare_batched; it includes the reduction of an earlier
+ * submitted check that it finishes), 2 candidate derivation, 3 the check's
+ * finalize kernel (per-segment reduction and report, when it runs as a
+ * kernel of its own).
  */
 enum { SV_PROF_SYNTH = 0, SV_PROF_COMPARE = 1, SV_PROF_PERTURB = 2, SV_PROF_FINALIZE = 3 };
 int sv_profile_enable(int32_t on);

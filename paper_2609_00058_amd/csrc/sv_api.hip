@@ -461,8 +461,9 @@ void plan_batched(const sv_segment *segs, uint32_t nseg, int32_t mode, int cus, 
 
 // Queues the kernels of `plan` into slot k on the selected stream and marks
 // the slot pending under a new sequence number.  The check kernel and its
-// finalize kernel write the reports into the slot's host-mapped memory, then
-// the sequence number into the slot's completion word.
+// finalize write the reports into the slot's host-mapped memory, then the
+// sequence number into the slot's completion word; a submitted check leaves
+// its finalize to the next check on its stream (see below).
 int submit_check(DeviceState *ds, int k, CheckPlan &plan) {
   hipStream_t st = t_stream;
   CheckSlot &sl = ds->slots[k];

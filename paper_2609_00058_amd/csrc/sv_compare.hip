@@ -31,14 +31,16 @@
 //
 // Reduction.  Lanes -> wave by DPP moves and xor shuffles, waves ->
 // workgroup through LDS, one 72-byte partial per (workgroup, segment piece)
-// in scratch slot b + s.  The finalize kernel -- one workgroup per segment,
-// launched behind the check -- combines a segment's partials in a fixed order
-// and writes the report straight into host-mapped pinned memory, then the
-// last finalize workgroup writes the launch's sequence number, which the host
-// spins on.  No floating-point atomics: reports are bit-reproducible run to
-// run for a given device.  A small single tensor needs no finalize: one
-// workgroup, or the last of a few dozen, writes the report itself
-// (last_block_report), by the same reduction tree.
+// in scratch slot b + s.  The finalize -- one workgroup per segment, after
+// the check -- combines a segment's partials in a fixed order and writes the
+// report straight into host-mapped pinned memory, then its last workgroup
+// writes the launch's sequence number, which the host spins on.  It runs as
+// a kernel of its own behind the check, or, for a submitted check followed
+// by another on its stream, in the first workgroups of that next check.  No
+// floating-point atomics: reports are bit-reproducible run to run for a
+// given device.  A small single tensor needs no finalize: one workgroup, or
+// the last of a few dozen, writes the report itself (last_block_report), by
+// the same reduction tree.
 //
 // The partials of a large grid need no device-scope fence inside the check:
 // the finalize runs after it.  (On gfx950 such a fence writes back the whole
