@@ -365,9 +365,9 @@ void zero_report(sv_report *r, uint64_t n) {
 
 // grid for a check over `units` 16-byte units: at most SV_CMP_BLOCKS_PER_CU
 // workgroups per CU, each owning whole waves of units
-void compare_grid(uint64_t units, int cus, bool batched, uint32_t *nblocks, uint64_t *chunk) {
+void compare_grid(uint64_t units, int cus, bool batched, bool stop, uint32_t *nblocks, uint64_t *chunk) {
   const uint64_t per_iter = (uint64_t)kCmpBlock;
-  const uint64_t per_cu = batched ? SV_CMP_BATCH_BLOCKS_PER_CU : SV_CMP_BLOCKS_PER_CU;
+  const uint64_t per_cu = stop ? SV_CMP_STOP_BLOCKS_PER_CU : batched ? SV_CMP_BATCH_BLOCKS_PER_CU : SV_CMP_BLOCKS_PER_CU;
   uint64_t nb = std::min<uint64_t>((units + per_iter - 1) / per_iter, (uint64_t)cus * per_cu);
   if (!batched && units <= SV_CMP_FUSE_UNITS) nb = 1;   // small: one workgroup reports by itself
   if (nb == 0) nb = 1;
@@ -437,7 +437,7 @@ void plan_single(const sv_segment &g, int cus, CheckPlan &plan) {
   plan.args.nseg = 1;
   plan.total_units = plan.args.total_units = units_of(g.dtype, g.n);
   if (plan.total_units) {
-    compare_grid(plan.total_units, cus, false, &plan.nblocks, &plan.args.chunk);
+    compare_grid(plan.total_units, cus, false, false, &plan.nblocks, &plan.args.chunk);
     plan.args.single.w1 = plan.nblocks - 1;   // its workgroups 0 .. nblocks - 1, slots 0 .. nblocks - 1
   }
 }
@@ -451,7 +451,7 @@ void plan_batched(const sv_segment *segs, uint32_t nseg, int32_t mode, int cus, 
   for (uint32_t k = 0; k < nseg; ++k) total += units_of(segs[k].dtype, segs[k].n);
   plan.args.nseg = nseg;
   plan.total_units = plan.args.total_units = total;
-  if (total) compare_grid(total, cus, true, &plan.nblocks, &plan.args.chunk);
+  if (total) compare_grid(total, cus, true, plan.stop_at_first, &plan.nblocks, &plan.args.chunk);
   if (total && plan.stop_at_first) {   // workgroups of their own per segment
     uint64_t blocks = 0;
     for (uint32_t k = 0; k < nseg; ++k) blocks += stop_blocks(units_of(segs[k].dtype, segs[k].n), plan.args.chunk);

@@ -29,7 +29,10 @@ namespace sv {
 #define SV_CMP_SINGLE_LDS 61440      // dynamic LDS bytes per single-tensor check workgroup, unused: two such
 #endif                               // workgroups share a CU's 160 KB, not three (measured faster)
 #ifndef SV_CMP_BATCH_BLOCKS_PER_CU
-#define SV_CMP_BATCH_BLOCKS_PER_CU 12   // check workgroups per CU, batched
+#define SV_CMP_BATCH_BLOCKS_PER_CU 16   // check workgroups per CU, batched
+#endif
+#ifndef SV_CMP_STOP_BLOCKS_PER_CU
+#define SV_CMP_STOP_BLOCKS_PER_CU 12    // ... batched, stop at first mismatch
 #endif
 #ifndef SV_SYNTH_BLOCKS_PER_CU
 #define SV_SYNTH_BLOCKS_PER_CU 64    // synthesis workgroups per CU
