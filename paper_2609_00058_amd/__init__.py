@@ -334,7 +334,10 @@ class CheckTicket:
     """A submitted check (compare_submit, compare_batched_submit).  It keeps its
     tensors alive until waited for; wait() returns what compare() or
     compare_batched() would have returned (with as_array, the reports as a numpy
-    array of REPORT_DTYPE, one record per segment, also for a single tensor)."""
+    array of REPORT_DTYPE, one record per segment, also for a single tensor).
+    The check's last reduction step may be left to the next check submitted on
+    the same stream; ready() and wait() queue it themselves when none comes, so
+    poll ready() (or wait) rather than relying on a stream synchronization."""
 
     def __init__(self, ticket: int, nreports: int, batched: bool, keep):
         self.ticket, self.nreports, self.batched, self._keep = ticket, nreports, batched, keep
