@@ -266,6 +266,7 @@ def test_random_sequences_of_submits_waits_and_queries():
     batch = [(r, c, 1e-8, 0.0, False) for r, c in pairs[:4]]
     want = [sv.compare(r, c, 1e-8, 0.0) for r, c in pairs]
     want_b = sv.compare_batched(batch)
+    want_s = sv.compare_batched(batch, stop_at_first=True)
     torch.cuda.synchronize()
     streams = [torch.cuda.current_stream(), torch.cuda.Stream()]
     pending = []                                                     # (ticket, expected)
@@ -278,7 +279,8 @@ def test_random_sequences_of_submits_waits_and_queries():
                 k = int(rng.integers(0, len(pairs)))
                 pending.append((sv.compare_submit(*pairs[k], 1e-8, 0.0), want[k]))
             elif op == 5 and len(pending) < sv.SV_MAX_PENDING_CHECKS:
-                pending.append((sv.compare_batched_submit(batch), want_b))
+                stop = bool(rng.integers(0, 2))              # a stop-at-first batch's reduction is finished
+                pending.append((sv.compare_batched_submit(batch, stop_at_first=stop), want_s if stop else want_b))
             elif op == 6:
                 k = int(rng.integers(0, len(pairs)))
                 assert sv.compare(*pairs[k], 1e-8, 0.0) == want[k], step
