@@ -440,6 +440,8 @@ int sv_shutdown(void);
  * number themselves per device; the stop-at-first mode tags words in device
  * memory with the low 32 bits of that number and clears them when the high
  * bits change, and this lets a test cross that boundary without 2^32 checks.
+ * Numbers may be set back and repeat.  Tickets of checks waited for before
+ * the call must not be used after it.
  * INVALID_ARG while submitted checks of the device are not yet waited for, or
  * for last >= 2^56 - 2^32 (tickets hold 56 bits of it).
  */

@@ -1193,6 +1193,12 @@ int sv_testing_set_sequence(uint64_t last) {
   if (ds->npending)
     return fail(SV_ERR_INVALID_ARG, "sv_testing_set_sequence: %d submitted checks not yet waited for", ds->npending);
   ds->seq = last;
+  // numbers may repeat: no completion word may still hold one of them (none is
+  // pending, so the host may write them), and the next stop-at-first check
+  // clears the tagged words
+  if (ds->h_done)
+    for (int k = 0; k < kSlots; ++k) ds->h_done[(size_t)k * kDoneStride] = ~0ull;
+  ds->firsts_hi = ~0ull;
   return SV_OK;
 }
 

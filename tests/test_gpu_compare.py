@@ -330,7 +330,7 @@ def test_stop_at_first_words_from_2_32_checks_ago_count_for_nothing(oracle):
     fail, clean = [(R, B, 1e-6, 0.0, False)], [(R, N, 1e-6, 0.0, False)]
     print("stop-at-first tags", flush=True)
     for before, after, plain_between in ((9, (1 << 32) + 9, False), ((1 << 32) - 3, (2 << 32) - 3, True),
-                                         ((3 << 32) + 100, 100, False)):
+                                         ((3 << 32) + 100, 100, False), (500, 500, False)):   # same number again
         assert L.sv_testing_set_sequence(before) == 0
         same_report(sv.compare_batched(fail, stop_at_first=True)[0], want_bad)       # posts tile 0
         assert L.sv_testing_set_sequence(after) == 0
