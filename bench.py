@@ -34,6 +34,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0   # MI355X HBM3E, AMD public figure
 ELEMENTWISE = ("copy", "ulp", "scale", "special_flip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+# the workloads of workloads.py (listed here so that a wrong name fails before the GPU is touched)
+WORKLOAD_NAMES = ("uniform_small", "normal_ulp", "bf16_batch", "ragged_batch", "special_stream", "candidates_round")
 KERNEL_NAMES = {"synth": "void sv::synth_vec_kernel<1, 0, true>", "compare": "void sv::compare_kernel<true, 1, false>"}
 
 
@@ -74,7 +76,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="normal_ulp")
+    ap.add_argument("--workload", default="normal_ulp", choices=WORKLOAD_NAMES)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--full-check", action="store_true",
                     help="check failing segments in full even where the workload stops at the first mismatch")
@@ -266,7 +268,7 @@ def files_stage(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU: the path runs on a single MI355X and this build has no "
+        print("bench.py measures one GPU: the library runs the path on a single MI355X and has no "
               "multi-GPU execution; rerun with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if args.perf_stage:
