@@ -10,7 +10,8 @@ and check are queued (sv_compare_submit) before the host waits for step k-1's
 reports (sv_compare_wait), so the GPU does not idle while a report travels to
 the host; every report of the K steps is on the host before the clock stops.
 sync_ms_per_step times the same steps with each one waited for before the
-next is queued.
+next is queued.  The W warm-up steps are followed by more untimed steps until
+the warm-up has lasted 100 ms (the GPU raises its clocks under load).
 
 value = (bytes synthesized + bytes checked) / time per step, in GB/s
 (1e9 bytes/s): synthesis writes n * itemsize bytes, the check reads
@@ -342,6 +343,11 @@ def main():
         return reports(prev) if prev is not None else last
 
     pipelined(args.warmup)
+    # the GPU raises its clocks over tens of milliseconds of load: after the W
+    # warm-up steps, keep stepping (untimed) until 100 ms of warm-up have run
+    t_w = time.perf_counter()
+    while time.perf_counter() - t_w < 0.1:
+        pipelined(20)
     # timed region: K steps, no event markers
     torch.cuda.synchronize()
     t0 = time.perf_counter()
