@@ -834,10 +834,17 @@ int or_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
       double rel = (d == 0.0) ? 0.0 : d / fabs(y);   /* y = 0, d > 0 gives +Inf */
       if (rel > r->max_rel_err) r->max_rel_err = rel;
       double t = sum + d;
-      if (fabs(sum) >= fabs(d))
+      if (isinf(t)) {
+        /* the running sum (or d itself) has overflowed: every d is >= 0, so
+         * the fp64 sum is +Inf from here on in any order; the compensation
+         * term has no meaning past this point (it would turn Inf - Inf into
+         * NaN) and is dropped */
+        comp = 0.0;
+      } else if (fabs(sum) >= fabs(d)) {
         comp += (sum - t) + d;
-      else
+      } else {
         comp += (d - t) + sum;
+      }
       sum = t;
     }
   }

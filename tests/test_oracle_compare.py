@@ -178,3 +178,36 @@ def test_invalid_tolerances_rejected(oracle):
     for rtol, atol in [(-1e-5, 0.0), (0.0, -1.0), (math.nan, 0.0), (math.inf, 0.0)]:
         with pytest.raises(oracle.OracleError):
             oracle.compare(x, x, "f32", rtol, atol, False)
+
+
+# The largest finite fp64 value plus half an ulp: every exact real at or above
+# it rounds to +Inf under round-to-nearest-even.
+OVERFLOW_AT = Fraction(2) ** 1024 - Fraction(2) ** 970
+
+
+def test_err_sum_overflow_is_inf(oracle):
+    """An fp64 error sum whose exact value passes the overflow threshold is +Inf
+    (every d is >= 0, so no summation order brings it back), never NaN; a
+    difference that overflows by itself (both values finite) makes d, the
+    maxima and the sum +Inf.  Pinned by exact rationals."""
+    cases = [
+        ([1e308], [-1e308]),                            # d itself overflows
+        ([1e308, 1e308], [-7e307, -7e307]),             # each d finite, the total overflows
+        ([1.5e308, 0.0, 1.0], [0.0, 1.5e308, 2.0]),     # overflow at the second term, finite terms after
+        ([1e308, 5.0], [0.0, 5.0]),                     # near the edge, finite: a check that stays finite
+    ]
+    for ref, cand in cases:
+        y = np.array(ref, np.float64)
+        a = np.array(cand, np.float64)
+        rep = oracle.compare(y.view(np.uint64), a.view(np.uint64), "f64", 1e-7, 0.0, False)
+        exact = [abs(Fraction(float(p)) - Fraction(float(q))) for p, q in zip(cand, ref)]
+        total = sum(exact)
+        assert not math.isnan(rep["err_sum"])
+        if total >= OVERFLOW_AT:
+            assert rep["err_sum"] == math.inf
+        else:
+            assert rep["err_sum"] == float(total)
+        dmax = max(exact)
+        assert rep["max_abs_err"] == (math.inf if dmax >= OVERFLOW_AT else float(dmax))
+        if dmax >= OVERFLOW_AT:
+            assert rep["max_rel_err"] == math.inf
