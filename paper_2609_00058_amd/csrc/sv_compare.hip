@@ -27,7 +27,8 @@
 // sees (a wave visits its units in increasing order).  The fp64 maxima and
 // the sum stay per lane; d / |y| is divided out only when it can beat the
 // lane's running maximum m (the test d > fp64(m (1 - 2^-50)) |y| never
-// rejects a quotient that rounds above m).
+// rejects a quotient that rounds above m while that product is a normal
+// number; fp64 inputs also divide where it is not, see may_beat).
 //
 // Reduction.  Lanes -> wave by DPP moves and xor shuffles, waves ->
 // workgroup through LDS, one 72-byte partial per (workgroup, segment piece)
@@ -145,6 +146,24 @@ struct WaveAcc {                      // wave-uniform
   uint64_t mism, first, nan_r, nan_c, inf_r, inf_c;
 };
 
+// Whether d / |y| may round above the lane's running maximum m: d > fp64(mrc
+// |y|) never rejects such a quotient while that product is a normal fp64
+// number (its relative rounding error, at most 2^-53, is inside the 2^-50
+// margin of mrc).  Widened fp32, bf16 and fp16 values and int64 differences
+// keep it normal (m |y| >= 2^-426 once both are nonzero).  fp64 inputs do
+// not: below 2^-1022 the product is rounded to a multiple of 2^-1074, an
+// absolute error the margin does not cover, and a difference of two finite
+// values can overflow to +Inf, whose quotient beats any finite m even where
+// the product has overflowed too.  There the quotient is always formed.
+template <int DT>
+__device__ __forceinline__ bool may_beat(const LaneAcc &L, double d, double ay) {
+  const double b = L.mrc * ay;
+  if constexpr (DT == SV_F64)
+    return d > b || (d > 0.0 && b < 0x1p-1022) || d == __builtin_inf();
+  else
+    return d > b;
+}
+
 __device__ __forceinline__ void update_rel(LaneAcc &L, double d, double y) {
   const double rel = d / fabs(y);    // y = 0 < d gives +Inf
   if (rel > L.maxrel) {
@@ -196,7 +215,7 @@ __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, in
       bad[j] = __ballot(!(D[j] <= atol + rtol * ay));
       L.sum += D[j];
       L.maxabs = fmax(L.maxabs, D[j]);
-      f[j] = D[j] > L.mrc * ay;
+      f[j] = may_beat<DT>(L, D[j], ay);
       anyf |= f[j];
     }
   } else {
@@ -229,7 +248,7 @@ __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, in
       const double dj = fin ? D[j] : 0.0;
       L.sum += dj;
       L.maxabs = fmax(L.maxabs, dj);
-      f[j] = dj > L.mrc * ay;
+      f[j] = may_beat<DT>(L, dj, ay);
       anyf |= f[j];
     }
   }

@@ -55,11 +55,12 @@ def bits_at(t, idx):
 
 
 def same_report(got, want, sum_rel=1e-12):
-    """Bit-exact on every field except err_sum (within sum_rel relative)."""
+    """Bit-exact on every field except err_sum (within sum_rel relative; an
+    exact 0 or an overflow to +Inf must match exactly)."""
     for k in want:
         if k == "err_sum":
-            if want[k] == 0.0:
-                assert got[k] == 0.0, (k, got[k], want[k])
+            if want[k] == 0.0 or want[k] == float("inf"):
+                assert got[k] == want[k], (k, got[k], want[k])
             else:
                 assert abs(got[k] - want[k]) <= sum_rel * abs(want[k]), (k, got[k], want[k])
         else:
