@@ -18,7 +18,8 @@
  *    the paper (it only points to general-purpose numerical libraries).  They
  *    follow the conventions recorded in the design notes: Philox4x32-10 (Salmon, Moraes,
  *    Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11) keyed
- *    by the seed with counter (block, stream); uniform from the top 24 bits;
+ *    by the seed with counter (block, stream); uniform from the top 24 bits
+ *    of a word (from a 16-bit half-word for bf16 outputs);
  *    Box-Muller (1958) with ln, sin and cos written as fixed sequences of fp32
  *    operations (a Chebyshev polynomial for ln, Taylor series in powers of
  *    pi/2 over factorials for sin and cos, coefficients rounded to fp32,
@@ -494,6 +495,19 @@ static uint64_t element_value(uint64_t seed, uint64_t stream, int32_t dtype, int
     double U = (double)(R >> 11) * 0x1p-53;
     double t = q->span64 * U;
     return d2u(q->a64 + t);
+  }
+  if (dist == OR_UNIFORM && dtype == OR_BF16) {
+    /* bf16: one 16-bit draw per element, eight elements per block: element i
+     * takes half i mod 2 (the low half first) of word (i mod 8) / 2 of block
+     * i / 8; U = h 2^-16 in [0, 1); a + span U in fp32, two roundings, then
+     * rounded to bf16.  Sixteen bits reach every bf16 value of the top eight
+     * binades of the range; fp16, with three more significand bits, keeps the
+     * 24-bit draws below. */
+    or_philox_block(seed, stream, i / 8u, w);
+    uint32_t h = (w[(i % 8u) / 2u] >> (16u * (unsigned)(i % 2u))) & 0xFFFFu;
+    float U = (float)h * 0x1p-16f;
+    float t = q->span * U;
+    return f2u(q->a + t);
   }
   if (dist == OR_UNIFORM) {
     /* four elements per block: element i takes word i mod 4 of block i / 4 */

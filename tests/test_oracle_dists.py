@@ -103,16 +103,82 @@ def test_uniform_half_open_and_moments(oracle):
     assert d < 1.95 / math.sqrt(n)
 
 
-def test_uniform_bf16_is_rne_of_fp32(oracle):
+def _bf16_of_exact_fp32(vals):
+    """torch's fp32 -> bf16 rounding (round to nearest even) of fp32 values."""
     import torch
+    return torch.from_numpy(np.asarray(vals, np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def _half_words(oracle, seed, stream, n):
+    """The 16-bit halves of the Philox words in element order: block c gives
+    elements 8c .. 8c + 7 from words 0..3, low half first."""
+    w = oracle.philox_blocks(seed, stream, 0, -(-n // 8)).reshape(-1)
+    return np.stack([w & 0xFFFF, w >> 16], axis=1).reshape(-1)[:n]
+
+
+@pytest.mark.parametrize("a,b", [(-4.0, 4.0), (-1.0, 1.0), (0.0, 1.0), (-0.5, 0.25)])
+def test_uniform_bf16_closed_form_from_half_words(oracle, a, b):
+    """bf16 uniform: element i = RNE_bf16(a + (b - a) k 2^-16) with k the 16-bit
+    half-word of element i; on power-of-two spans a + (b - a) k 2^-16 is an fp32
+    value exactly (checked with Fractions), so the oracle's two fp32 roundings
+    vanish and the result is torch's bf16 rounding of the exact value."""
+    n = 1 << 15
+    got = oracle.synth(4, 11, "bf16", "uniform", oracle.dist_params(a=a, b=b), n)
+    k = _half_words(oracle, 4, 11, n)
+    table = np.array([float(Fraction(a) + Fraction(b - a) * Fraction(j, 1 << 16)) for j in range(1 << 16)])
+    for j in (0, 1, 12345, (1 << 16) - 1):
+        assert Fraction(float(np.float32(table[j]))) == Fraction(a) + Fraction(b - a) * Fraction(j, 1 << 16)
+    assert np.array_equal(table.astype(np.float32).astype(np.float64), table)   # every value exact in fp32
+    want = _bf16_of_exact_fp32(table.astype(np.float32))[k]
+    assert np.array_equal(got, want)
+
+
+def test_uniform_bf16_general_span_is_rne_of_the_fp32_value(oracle):
+    """On a span that is not a power of two: the fp32 value is the rounding of
+    a + rounding(span U) (two roundings, checked with Fractions), then bf16."""
+    a, b = -3.0, 7.5
+    n = 1 << 14
+    got = oracle.synth(6, 2, "bf16", "uniform", oracle.dist_params(a=a, b=b), n)
+    k = _half_words(oracle, 6, 2, n)
+    span = np.float32(b) - np.float32(a)
+    v = np.array([rne32_exact(Fraction(a) + Fraction(rne32_exact(Fraction(float(span)) * Fraction(int(j), 1 << 16))))
+                  for j in k], np.float32)
+    assert np.array_equal(got, _bf16_of_exact_fp32(v))
+
+
+def test_uniform_bf16_distribution(oracle):
+    """2^22 draws on [-4, 4): each bf16 value occurs with the probability the
+    65,536 equally likely half-words give it (chi-square), the moments of a
+    uniform variable, no correlation between the two halves of a word or
+    between neighbouring words, and the bounds (rounding may reach b)."""
+    import torch
+    a, b = -4.0, 4.0
+    n = 1 << 22
+    out = oracle.synth(1, 7, "bf16", "uniform", oracle.dist_params(a=a, b=b), n)
+    vals = (out.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    assert vals.min() >= a and vals.max() <= b
+    exact = np.array([a + (b - a) * j / 65536 for j in range(1 << 16)], np.float32)
+    keys = _bf16_of_exact_fp32(exact)
+    uk, cnt = np.unique(keys, return_counts=True)
+    p = cnt / 65536.0
+    assert np.isin(out, uk).all()                           # nothing outside the reachable set
+    obs = np.bincount(np.searchsorted(uk, out), minlength=uk.size)
+    chi2 = ((obs - n * p) ** 2 / (n * p)).sum()
+    dof = uk.size - 1
+    assert chi2 < dof + 5 * math.sqrt(2 * dof)
+    mean_sigma = (b - a) / math.sqrt(12 * n)
+    assert abs(vals.mean() - (a + b) / 2) < 5 * mean_sigma
+    for lag in (1, 2):                                      # halves of one word; neighbouring words
+        r = np.corrcoef(vals[:-lag], vals[lag:])[0, 1]
+        assert abs(r) < 5 / math.sqrt(n)
+
+
+def test_uniform_bf16_windows_are_slices(oracle):
     p = oracle.dist_params(a=-4.0, b=4.0)
-    n = 1 << 16
-    v32 = oracle.synth(9, 3, "f32", "uniform", p, n)
-    v16 = oracle.synth(9, 3, "bf16", "uniform", p, n)
-    want = torch.from_numpy(v32.view(np.float32)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
-    assert np.array_equal(v16, want)
-    # bf16 rounding may reach the closed end b = 4 (the interval is [a, b] after rounding)
-    assert f32(v16.astype(np.uint32) << 16).max() <= 4.0
+    full = oracle.synth(3, 3, "bf16", "uniform", p, 4096)
+    for off in (1, 7, 8, 9, 1001):
+        assert np.array_equal(oracle.synth(3, 3, "bf16", "uniform", p, 500, offset=off), full[off:off + 500])
+    assert np.array_equal(oracle.synth(3, 3, "bf16", "uniform", p, 100), full[:100])
 
 
 # --------------------------------------------------------------- ln / sincos / Box-Muller
