@@ -65,21 +65,29 @@ def _windows(n, parts):
     return [(o, min(step, n - o)) for o in range(0, n, step)]
 
 
-def oracle_ref_parallel(spec):
-    out = np.empty(spec.n, dtype=O.NP_STORAGE[spec.dtype])
+def windowed(n, size):
+    """(offset, length) of consecutive windows of at most `size` elements."""
+    return [(o, min(size, n - o)) for o in range(0, n, size)]
+
+
+def oracle_ref_parallel(spec, offset=0, n=None):
+    """Elements [offset, offset + n) of the reference (default: all of it)."""
+    n = spec.n - offset if n is None else n
+    out = np.empty(n, dtype=O.NP_STORAGE[spec.dtype])
     def run(w):
         o, m = w
-        out[o:o + m] = oracle_ref(spec, o, m)
+        out[o:o + m] = oracle_ref(spec, offset + o, m)
     with ThreadPoolExecutor(workers()) as ex:
-        list(ex.map(run, _windows(spec.n, 4 * workers())))
+        list(ex.map(run, _windows(n, 4 * workers())))
     return out
 
 
-def oracle_cand_parallel(case, ref):
+def oracle_cand_parallel(case, ref, offset=0):
+    """The candidate over the window of `ref`, which starts at element `offset`."""
     cand = np.empty_like(ref)
     def run(w):
         o, m = w
-        cand[o:o + m] = oracle_cand(case, ref[o:o + m], offset=o)
+        cand[o:o + m] = oracle_cand(case, ref[o:o + m], offset=offset + o)
     with ThreadPoolExecutor(workers()) as ex:
         list(ex.map(run, _windows(ref.size, 4 * workers())))
     return cand

@@ -1,11 +1,23 @@
-"""The five synthetic workloads at full size, in the launch configuration the
-benchmark times, against the CPU oracle.
+"""The synthetic workloads at full size against the CPU oracle, synthesized
+and checked by the same calls the benchmark times.
 
-Where the oracle finishes in seconds (chunked over host threads) it runs in
-full and the GPU must match it bit for bit (sum within 1e-12 relative); for
-the 2 GiB and 4 GiB workloads it checks sampled elements one by one plus
-whole segments, and the reports are pinned by closed forms and by the
-oracle's class counts.
+Single tensors are synthesized with sv_synth and checked with sv_compare; the
+batched workloads are synthesized with one sv_synth_batched over the
+benchmark's job list (at these sizes 32 vectors per thread in a tile: the lean
+32-bit loop of the batched kernel) and checked with one submitted batched
+check.  What is compared, bit for bit (the fp64 error sum within 1e-12
+relative):
+  - uniform_small, normal_ulp: every element of reference and candidate, the report;
+  - bf16_batch: every element of all 64 references and candidates, three reports;
+  - ragged_batch: every element of all 256 references and candidates, all reports;
+  - special_stream: every element of the 2^30-element reference and candidate,
+    streamed through the oracle in windows; the report against the oracle's
+    class counts and closed form (zero errors);
+  - candidates_round: the first mismatch of every failing segment and two
+    whole reports.
+The oracle runs chunked over host threads (the serial oracle on windows).
+A batched synthesis job whose Philox counters pass 2^32 (outside the lean
+loop) is checked on sampled elements and against the single-tensor kernel.
 """
 import numpy as np
 import pytest
@@ -13,10 +25,25 @@ import torch
 
 import paper_2609_00058_amd as sv
 import workloads as W
-from gpu_run import bits, bits_at, gpu_cand, gpu_ref, same_report
-from oracle_run import (oracle_case, oracle_case_parallel, oracle_elements, special_counts_parallel)
+from gpu_run import bits, bits_at, empty, gpu_cand, gpu_ref, same_report
+from oracle_run import (oracle_case, oracle_case_parallel, oracle_cand_parallel, oracle_elements,
+                        oracle_ref_parallel, special_counts_parallel, windowed)
 
 pytestmark = pytest.mark.gpu
+
+
+def bench_synth(wl):
+    """The references of a batched workload, synthesized as the benchmark does:
+    one sv_synth_batched over the distinct reference tensors."""
+    uniq, which = wl.ref_groups()
+    refs = [empty(s.n, s.dtype) for s in uniq]
+    sv.synth_batched(sv.SynthBatch([(r, s.seed, s.stream, s.dist, s.params) for s, r in zip(uniq, refs)]))
+    return refs, which
+
+
+def bench_check(wl, refs, which, cands):
+    batch = sv.SegmentBatch([(refs[j], c, k.rtol, k.atol, k.equal_nan) for c, k, j in zip(cands, wl.cases, which)])
+    return sv.compare_batched_submit(batch, stop_at_first=wl.stop_at_first).wait()
 
 
 def test_uniform_small_full(oracle):
@@ -46,41 +73,35 @@ def test_normal_ulp_full(oracle):
 
 def test_bf16_batch_full(oracle):
     wl = W.bf16_batch()
-    refs, cands = [], []
     print("bf16 batch: gpu", flush=True)
-    for case in wl.cases:
-        r = gpu_ref(case.ref)
-        refs.append(r)
-        cands.append(gpu_cand(case, r))
-    segs = [(r, c, case.rtol, case.atol, case.equal_nan) for r, c, case in zip(refs, cands, wl.cases)]
-    got = sv.compare_batched(segs)
+    refs, which = bench_synth(wl)
+    cands = [gpu_cand(case, refs[j]) for case, j in zip(wl.cases, which)]
+    got = bench_check(wl, refs, which, cands)
     for rep in got:   # |a - y| <= 2^-7 |y| < atol + rtol |y|: clean by construction
         assert rep["mismatches"] == 0 and rep["first_mismatch"] == -1 and rep["max_rel_err"] <= 2.0 ** -7
-    for k in (0, 37, 63):
-        print("bf16 batch: oracle segment", k, flush=True)
-        r, c, want = oracle_case_parallel(wl.cases[k])
-        assert np.array_equal(bits(refs[k]), r) and np.array_equal(bits(cands[k]), c)
-        same_report(got[k], want)
-    rng = np.random.default_rng(5)
-    for k in rng.choice(64, 8, replace=False):
-        idx = rng.integers(0, wl.cases[k].ref.n, 2000)
-        r, c = oracle_elements(wl.cases[k], idx)
-        assert np.array_equal(bits_at(refs[k], idx), r) and np.array_equal(bits_at(cands[k], idx), c)
-    del refs, cands, segs
+    for k, case in enumerate(wl.cases):
+        print("bf16 batch: oracle tensor", k, flush=True)
+        r = oracle_ref_parallel(case.ref)
+        assert np.array_equal(bits(refs[which[k]]), r), k
+        c = oracle_cand_parallel(case, r)
+        assert np.array_equal(bits(cands[k]), c), k
+        if k in (0, 37, 63):
+            same_report(got[k], oracle.compare(r, c, case.ref.dtype, case.rtol, case.atol, case.equal_nan))
+    del refs, cands
     torch.cuda.empty_cache()
 
 
 def test_ragged_batch_full(oracle):
     wl = W.ragged_batch()
     print("ragged batch: gpu", flush=True)
-    refs = [gpu_ref(c.ref) for c in wl.cases]
-    cands = [gpu_cand(c, r) for c, r in zip(wl.cases, refs)]
-    got = sv.compare_batched([(r, c, k.rtol, k.atol, k.equal_nan) for r, c, k in zip(refs, cands, wl.cases)])
+    refs, which = bench_synth(wl)
+    cands = [gpu_cand(c, refs[j]) for c, j in zip(wl.cases, which)]
+    got = bench_check(wl, refs, which, cands)
     faults = wl.expect["faults"]
     print("ragged batch: oracle", flush=True)
     for k, case in enumerate(wl.cases):
         r, c, want = oracle_case_parallel(case)
-        assert np.array_equal(bits(refs[k]), r), k
+        assert np.array_equal(bits(refs[which[k]]), r), k
         assert np.array_equal(bits(cands[k]), c), k
         same_report(got[k], want)
         if k in faults:
@@ -88,6 +109,32 @@ def test_ragged_batch_full(oracle):
         else:
             assert got[k]["mismatches"] == 0
     del refs, cands
+    torch.cuda.empty_cache()
+
+
+def test_batched_job_with_counters_past_2_pow_32(oracle):
+    """An int32 job of 2^33 + 2^20 elements (two per Philox block): its block
+    indices pass 2^32, so the batched kernel takes its general 64-bit loop;
+    batched beside a small job as a second tile size would."""
+    n = (1 << 33) + (1 << 20)
+    params = dict(lo=-(1 << 20), hi=1 << 20)
+    big = empty(n, "i32")
+    small = empty(1000, "f32")
+    print("counters past 2^32: batched synthesis of 32 GiB", flush=True)
+    sv.synth_batched([(big, 3, 9, "int_range", params), (small, 3, 10, "normal", dict(mean=5.0, std=10.0))])
+    p = oracle.dist_params(**params)
+    rng = np.random.default_rng(33)
+    edge = np.arange((1 << 33) - 4096, (1 << 33) + 4096, dtype=np.uint64)
+    idx = np.concatenate([edge, np.arange(n - 2048, n, dtype=np.uint64), np.arange(2048, dtype=np.uint64),
+                          rng.integers(0, n, 50000).astype(np.uint64)])
+    assert np.array_equal(bits_at(big, idx), oracle.synth_at(3, 9, "i32", "int_range", p, idx))
+    assert np.array_equal(bits(small), oracle.synth(3, 10, "f32", "normal", oracle.dist_params(mean=5.0, std=10.0),
+                                                    1000))
+    print("counters past 2^32: single-tensor kernel", flush=True)
+    one = empty(n, "i32")
+    sv.synth(one, 3, 9, "int_range", **params)
+    assert torch.equal(one, big)
+    del big, one
     torch.cuda.empty_cache()
 
 
@@ -104,10 +151,13 @@ def test_special_stream_full(oracle):
     assert got["max_abs_err"] == 0.0 and got["max_rel_err"] == 0.0 and got["err_sum"] == 0.0
     assert got["nan_ref"] == got["nan_cand"] == counts[0]
     assert got["inf_ref"] == got["inf_cand"] == counts[1]
-    rng = np.random.default_rng(6)
-    idx = np.concatenate([np.arange(2048), case.ref.n - 1 - np.arange(2048), rng.integers(0, case.ref.n, 20000)])
-    r, c = oracle_elements(case, idx)
-    assert np.array_equal(bits_at(ref, idx), r) and np.array_equal(bits_at(cand, idx), c)
+    # every element of reference and candidate, 2^26 at a time
+    for off, m in windowed(case.ref.n, 1 << 26):
+        print("special 2^30: oracle window at", off, flush=True)
+        r = oracle_ref_parallel(case.ref, off, m)
+        assert np.array_equal(bits(ref[off:off + m]), r), off
+        c = oracle_cand_parallel(case, r, off)
+        assert np.array_equal(bits(cand[off:off + m]), c), off
     del ref, cand
     torch.cuda.empty_cache()
 
