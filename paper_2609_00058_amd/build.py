@@ -26,9 +26,7 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", "--offload-arch=" + ARCH,
          "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = ["hipcc", *FLAGS, *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -39,6 +37,20 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed (%d):\n%s" % (res.returncode, err))
     if verbose and err.strip():
         print(err, file=sys.stderr)
+
+
+def build(verbose: bool = False) -> str:
+    """Compiles every source to an object (in parallel), then links the library."""
+    import tempfile
+    from concurrent.futures import ThreadPoolExecutor
+    tmp = LIB + ".tmp%d" % os.getpid()
+    with tempfile.TemporaryDirectory(prefix="sv_build_") as d:
+        objs = [os.path.join(d, os.path.splitext(s)[0] + ".o") for s in SOURCES]
+        compile_flags = [f for f in FLAGS if f != "-shared"]
+        jobs = [["hipcc", *compile_flags, "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
+        with ThreadPoolExecutor(min(len(jobs), os.cpu_count() or 1)) as ex:
+            list(ex.map(lambda c: _run(c, verbose), jobs))
+        _run(["hipcc", "-shared", "-fPIC", "--offload-arch=" + ARCH, *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 
