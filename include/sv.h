@@ -193,6 +193,30 @@ int sv_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
                double rtol, double atol, int32_t equal_nan, sv_report *report);
 
 /*
+ * sv_compare_noalloc -- sv_compare for callers that cannot allocate memory
+ * (code under HIP graph capture that prepares its work beforehand, tight
+ * serving loops, harnesses that forbid hipMalloc): the same check, the same
+ * kernels and the same report bits as sv_compare, but its scratch (workgroup
+ * partials, arrival counter, report staging) is a fixed array of 295,168
+ * bytes in device memory that the library holds on each GPU it runs on until
+ * the process ends.  The call allocates nothing: no hipMalloc, hipFree or
+ * pinned host memory, on its first call or any other.
+ *
+ * ref, cand : device pointers to n elements of dtype (any element alignment);
+ *             n is limited only as for sv_compare (at most 2^60).
+ * report    : host pointer, written on success.
+ * Synchronous: the report is copied to the host and the stream synchronised
+ * before the call returns.  Calls on one device share its array and are
+ * serialised by a lock; two calls that overlapped on one GPU would race on
+ * it, which the lock and the synchronous return rule out within a process.
+ * Errors as sv_compare, plus UNSUPPORTED when the device's check grid would
+ * need more than the 4,095 workgroup partials the array holds (a GPU of more
+ * than 511 compute units) or the device index is 64 or more.
+ */
+int sv_compare_noalloc(const void *ref, const void *cand, uint64_t n, int32_t dtype,
+                       double rtol, double atol, int32_t equal_nan, sv_report *report);
+
+/*
  * sv_compare_batched -- sv_compare on nseg independent segments in one launch.
  *
  * Each segment carries its own dtype, tolerances and equal_nan; indices in

@@ -35,7 +35,7 @@ SYMBOLS = ("sv_synth", "sv_synth_batched", "sv_synth_window", "sv_compare", "sv_
            "sv_compare_submit", "sv_compare_batched_submit", "sv_compare_ready", "sv_compare_wait", "sv_perturb",
            "sv_eval_transform", "sv_synth_file", "sv_compare_file", "sv_kernel_load", "sv_kernel_free", "sv_kernel_launch", "sv_kernel_time",
            "sv_reward", "sv_set_stream", "sv_last_error", "sv_profile_enable", "sv_profile_read", "sv_shutdown",
-           "sv_testing_set_sequence", "sv_abi_version")
+           "sv_testing_set_sequence", "sv_abi_version", "sv_compare_noalloc")
 
 
 class DistParams(ctypes.Structure):
@@ -110,6 +110,7 @@ _lib.sv_synth.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u
 _lib.sv_synth_batched.argtypes = [ctypes.POINTER(SynthJob), ctypes.c_uint32]
 _lib.sv_synth_window.argtypes = [_u64, _u64, _i32, _i32, ctypes.POINTER(DistParams), _u64, _u64, _vp]
 _lib.sv_compare.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(Report)]
+_lib.sv_compare_noalloc.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(Report)]
 _lib.sv_compare_batched.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, ctypes.POINTER(Report)]
 _lib.sv_compare_batched_mode.argtypes = [ctypes.POINTER(Segment), ctypes.c_uint32, _i32, ctypes.POINTER(Report)]
 _lib.sv_compare_submit.argtypes = [_vp, _vp, _u64, _i32, _dbl, _dbl, _i32, ctypes.POINTER(_u64)]
@@ -283,6 +284,17 @@ def compare(ref, cand, rtol: float, atol: float, equal_nan: bool = False) -> dic
         raise SVError(SV_ERR_INVALID_ARG, "ref and cand must have the same dtype and size")
     rep = Report()
     _run(ref, _lib.sv_compare, _dev_ptr(ref, "ref"), _dev_ptr(cand, "cand"), ref.numel(), dtype_code(ref),
+         rtol, atol, int(bool(equal_nan)), ctypes.byref(rep))
+    return rep.as_dict()
+
+
+def compare_noalloc(ref, cand, rtol: float, atol: float, equal_nan: bool = False) -> dict:
+    """compare() through sv_compare_noalloc: the library's fixed device scratch,
+    nothing allocated (synchronous)."""
+    if ref.dtype != cand.dtype or ref.numel() != cand.numel():
+        raise SVError(SV_ERR_INVALID_ARG, "ref and cand must have the same dtype and size")
+    rep = Report()
+    _run(ref, _lib.sv_compare_noalloc, _dev_ptr(ref, "ref"), _dev_ptr(cand, "cand"), ref.numel(), dtype_code(ref),
          rtol, atol, int(bool(equal_nan)), ctypes.byref(rep))
     return rep.as_dict()
 

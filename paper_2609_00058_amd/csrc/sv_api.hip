@@ -737,6 +737,49 @@ int api_fail(int code, const char *msg) { return fail(code, "%s", msg); }
 int api_hip_fail(hipError_t e, const char *what) { return hip_fail(e, what); }
 }  // namespace sv
 
+// ------------------------------------------------------------ sv_compare_noalloc
+// The single-tensor check with its scratch in a fixed device array instead of
+// memory the library allocates: the workgroup partials, the arrival counter,
+// the report and the completion word that the check kernel and its finalize
+// write.  The array is a host-side stand-in in host code: its device address
+// on each GPU comes from hipGetSymbolAddress, taken once per device with that
+// device current, and only that address is handed to kernels and copies.
+constexpr size_t kNaPartials = 4096;            // workgroup partials the array holds
+constexpr size_t kNaCounterOff = 0;             // uint32 arrival counter (zero between launches)
+constexpr size_t kNaDoneOff = 64;               // uint64 completion word
+constexpr size_t kNaReportOff = 128;            // sv_report
+constexpr size_t kNaPartialsOff = 256;
+constexpr size_t kNaBytes = kNaPartialsOff + kNaPartials * sizeof(Partial);
+static_assert(kNaReportOff + sizeof(sv_report) <= kNaPartialsOff, "scratch layout");
+constexpr int kNaMaxDevices = 64;
+
+static __device__ __align__(256) unsigned char scratch[kNaBytes];
+
+namespace {
+struct NoAllocDevice {
+  std::mutex mu;                 // one check at a time per device: they share the array
+  bool ready = false;
+  unsigned char *ptr = nullptr;  // device address of `scratch` on this device
+  int cus = 0;
+};
+NoAllocDevice g_noalloc[kNaMaxDevices];
+
+// Set-up on the current device (first call there): the array's device
+// address and the CU count.  The caller holds d.mu.
+int noalloc_setup(NoAllocDevice &d, int dev) {
+  if (d.ready) return SV_OK;
+  void *p = nullptr;
+  SV_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+  int cus = 0;
+  SV_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev),
+         "hipDeviceGetAttribute(multiProcessorCount)");
+  d.ptr = (unsigned char *)p;
+  d.cus = cus > 0 ? cus : 1;
+  d.ready = true;
+  return SV_OK;
+}
+}  // namespace
+
 // =================================================================== C ABI
 extern "C" {
 
@@ -1199,6 +1242,54 @@ int sv_testing_set_sequence(uint64_t last) {
   if (ds->h_done)
     for (int k = 0; k < kSlots; ++k) ds->h_done[(size_t)k * kDoneStride] = ~0ull;
   ds->firsts_hi = ~0ull;
+  return SV_OK;
+}
+
+int sv_compare_noalloc(const void *ref, const void *cand, uint64_t n, int32_t dtype, double rtol, double atol,
+                       int32_t equal_nan, sv_report *report) {
+  t_error.clear();
+  if (!report) return fail(SV_ERR_INVALID_ARG, "sv_compare_noalloc: report is NULL");
+  const sv_segment g{ref, cand, n, dtype, rtol, atol, equal_nan};
+  int rc = check_seg(g, 0);
+  if (rc) return rc;
+  if (!n) {
+    zero_report(report, 0);
+    return SV_OK;
+  }
+  int dev = 0;
+  SV_HIP(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= kNaMaxDevices)
+    return fail(SV_ERR_UNSUPPORTED, "sv_compare_noalloc: device %d beyond the %d it keeps scratch for", dev,
+                kNaMaxDevices);
+  NoAllocDevice &d = g_noalloc[dev];
+  std::lock_guard<std::mutex> lock(d.mu);
+  rc = noalloc_setup(d, dev);
+  if (rc) return rc;
+  CheckPlan plan;
+  plan_single(g, d.cus, plan);
+  if ((size_t)plan.nblocks + 1 > kNaPartials)
+    return fail(SV_ERR_UNSUPPORTED, "sv_compare_noalloc: the check needs %u workgroup partials, the fixed scratch "
+                "holds %zu", plan.nblocks + 1, kNaPartials);
+  hipStream_t st = t_stream;
+  CompareArgs &args = plan.args;
+  args.stop_at_first = 0;
+  args.firsts = nullptr;
+  args.fused = plan.nblocks == 1 ? 1 : plan.nblocks <= SV_CMP_LAST_BLOCK_MAX ? 2 : 0;
+  args.partials = (Partial *)(d.ptr + kNaPartialsOff);
+  args.counter = (uint32_t *)(d.ptr + kNaCounterOff);
+  args.reports = (sv_report *)(d.ptr + kNaReportOff);
+  args.done = (uint64_t *)(d.ptr + kNaDoneOff);
+  args.seq = 1;
+  args.nprev = 0;
+  args.prev = FinalizeArgs{};
+  // the arrival counter must start at zero: cleared by a kernel (the 8-byte
+  // word holding it), not a memset, before every check
+  SV_HIP(launch_fill_u64((uint64_t *)(d.ptr + kNaCounterOff), 1, 0, st), "clearing the arrival counter");
+  SV_HIP(launch_compare(args, plan.nblocks, 1u << dtype, st), "check kernel launch");
+  if (!args.fused) SV_HIP(launch_finalize(finalize_args(args), st), "finalize kernel launch");
+  SV_HIP(hipMemcpyAsync(report, d.ptr + kNaReportOff, sizeof(sv_report), hipMemcpyDeviceToHost, st),
+         "report copy to host");
+  SV_HIP(hipStreamSynchronize(st), "waiting for the check");
   return SV_OK;
 }
 

@@ -140,8 +140,10 @@ def test_synth_batched_argument_errors(svlib):
     assert L.sv_synth_batched(jobs, 3) == svlib.SV_ERR_UNSUPPORTED
 
 
-def test_compare_argument_errors_and_empty(svlib):
+@pytest.mark.parametrize("entry", ["sv_compare", "sv_compare_noalloc"])
+def test_compare_argument_errors_and_empty(svlib, entry):
     L = svlib.lib()
+    check = getattr(L, entry)
     INV = svlib.SV_ERR_INVALID_ARG
     rep = svlib.Report()
     assert L.sv_compare(0x1000, 0x2000, 4, 0, 1e-5, 1e-8, 0, None) == INV
