@@ -19,6 +19,13 @@ value = (bytes synthesized + bytes checked) / time per step, in GB/s
 (candidates_round) a failing segment counts only the bytes up to and
 including its first mismatch.
 
+The default workload is the 2^30-element fp32 special-value stream (4 GiB
+reference, 12 GiB of algorithmic traffic per step).  After the timed passes a
+cold pass repeats the steps with a 1 GiB write before each one (evicting the
+256 MB Infinity Cache and the L2) and reports the kernels' durations there
+(`cold`): the warm figures of workloads that fit the cache are not HBM
+figures.
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
                        [--no-cpu-baseline] [--copy-probe] [--perf-stage]
 """
@@ -37,7 +44,7 @@ ELEMENTWISE = ("copy", "ulp", "scale", "special_flip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 # the workloads of workloads.py (listed here so that a wrong name fails before the GPU is touched)
 WORKLOAD_NAMES = ("uniform_small", "normal_ulp", "bf16_batch", "ragged_batch", "special_stream", "candidates_round")
-KERNEL_NAMES = {"synth": "void sv::synth_vec_kernel<1, 0, true>", "compare": "void sv::compare_kernel<true, 1, false>"}
+EVICT_BYTES = 1 << 30     # written before each step of the cold pass
 
 
 def kernel_source_hash():
@@ -58,17 +65,18 @@ def kernel_source_hash():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload, kernel):
-    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary, or None when it was taken on other sources or another workload."""
+def measured_traffic(workload, role):
+    """HBM bytes per launch of the workload's synthesis or check kernel (role
+    "synth" / "compare") from the committed rocprofv3 counter summary, or None
+    when the counters were taken on other sources or not on this workload."""
     try:
         with open(TRAFFIC_FILE) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("source_hash") != kernel_source_hash() or t.get("workload") != workload:
+    if t.get("source_hash") != kernel_source_hash():
         return None
-    k = t["kernels"].get(KERNEL_NAMES.get(kernel, ""))
+    k = t.get("workloads", {}).get(workload, {}).get(role)
     return k["hbm_bytes"] if k else None
 
 
@@ -77,7 +85,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", default="normal_ulp", choices=WORKLOAD_NAMES)
+    ap.add_argument("--workload", default="special_stream", choices=WORKLOAD_NAMES)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--full-check", action="store_true",
                     help="check failing segments in full even where the workload stops at the first mismatch")
@@ -112,14 +120,63 @@ def stream_copy_GBps(torch):
     return round(2 * (1 << 29) / (best * 1e-3) / 1e9, 1)
 
 
-def cpu_baseline(wl, min_seconds=10.0, max_elems=1 << 26):
-    """The oracle, as it stands (serial C, one thread), timed on a bounded
-    sample of one step of the workload: synthesis + check of the first
-    max_elems elements of each of the first two tensors (a prefix synthesizes
-    the same bits as the tensor's; the candidate is derived untimed, index
-    faults past the prefix dropped), repeated until min_seconds of oracle work
-    have been timed (at most 1000 times)."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def host_threads():
+    """Threads for the all-core leg: the CPUs this process may run on, at most
+    16 (the host share of one GPU)."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def merge_reports(parts):
+    """Reports of consecutive windows of one tensor, (offset, report) in order,
+    merged into the tensor's: counts add, the first index is the earliest
+    window's, maxima take the maximum, the fp64 sums are added in window order
+    with Neumaier's compensation."""
+    out = dict(parts[0][1])
+    out["first_mismatch"] = -1
+    out["n"] = out["mismatches"] = out["nan_ref"] = out["nan_cand"] = out["inf_ref"] = out["inf_cand"] = 0
+    out["max_abs_err"] = out["max_rel_err"] = 0.0
+    s = c = 0.0
+    for off, r in parts:
+        if out["first_mismatch"] < 0 and r["first_mismatch"] >= 0:
+            out["first_mismatch"] = off + r["first_mismatch"]
+        for k in ("n", "mismatches", "nan_ref", "nan_cand", "inf_ref", "inf_cand"):
+            out[k] += r[k]
+        out["max_abs_err"] = max(out["max_abs_err"], r["max_abs_err"])
+        out["max_rel_err"] = max(out["max_rel_err"], r["max_rel_err"])
+        d = r["err_sum"]
+        t = s + d
+        c += ((s - t) + d) if abs(s) >= abs(d) else ((d - t) + s)
+        s = t
+    out["err_sum"] = s + c
+    return out
+
+
+def cpu_baseline(wl, min_seconds=6.0, max_elems=1 << 24):
+    """The oracle, as it stands (serial C), timed on a bounded sample of one
+    step of the workload: synthesis + check of the first max_elems elements of
+    each of the first two tensors (a prefix synthesizes the same bits as the
+    tensor's; the candidate is derived untimed, index faults past the prefix
+    dropped).  Two legs, each repeated until min_seconds have been timed (at
+    most 1000 times): one thread, and all host threads (up to 16), each
+    thread running the serial oracle on its own window of every tensor, the
+    windows' reports merged in order.  `value` is the all-threads leg."""
     import numpy as np
+    from concurrent.futures import ThreadPoolExecutor
     import oracle as O
     cases = wl.cases if not wl.batched else wl.cases[:2]
     work = []
@@ -138,18 +195,46 @@ def cpu_baseline(wl, min_seconds=10.0, max_elems=1 << 26):
                 cand = O.perturb(st.seed, st.stream, spec.dtype, st.op, ref, cand, value=st.value, bits=st.bits,
                                  idx=idx[idx < n])
         work.append((case, spec, p, n, cand))
-    nbytes, secs, reps, elems = 0, 0.0, 0, sum(w[3] for w in work)
-    while reps < 1000 and (reps == 0 or secs < min_seconds):
+    elems = sum(w[3] for w in work)
+    nbytes_rep = sum(3 * w[3] * w[1].itemsize for w in work)
+
+    def one_thread():
         for case, spec, p, n, cand in work:
-            t0 = time.perf_counter()
             ref = O.synth(spec.seed, spec.stream, spec.dtype, spec.dist, p, n)
             O.compare(ref, cand, spec.dtype, case.rtol, case.atol, case.equal_nan)
+
+    threads = host_threads()
+    pool = ThreadPoolExecutor(threads)
+
+    def all_threads():
+        for case, spec, p, n, cand in work:
+            step = -(-n // threads)
+            wins = [(o, min(step, n - o)) for o in range(0, n, step)]
+
+            def run(w):
+                o, m = w
+                ref = O.synth(spec.seed, spec.stream, spec.dtype, spec.dist, p, m, offset=o)
+                return o, O.compare(ref, cand[o:o + m], spec.dtype, case.rtol, case.atol, case.equal_nan)
+            merge_reports(list(pool.map(run, wins)))
+
+    def timed(fn):
+        secs, reps = 0.0, 0
+        while reps < 1000 and (reps == 0 or secs < min_seconds):
+            t0 = time.perf_counter()
+            fn()
             secs += time.perf_counter() - t0
-            nbytes += 3 * n * spec.itemsize
-        reps += 1
-    return {"value": round(nbytes / secs / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": "%d x (synthesis + check of %d elements of %d tensor(s))" % (reps, elems, len(work)),
-            "seconds": round(secs, 3), "cpu": platform.processor() or platform.machine()}
+            reps += 1
+        return reps, secs
+
+    r1, s1 = timed(one_thread)
+    rn, sn = timed(all_threads)
+    pool.shutdown()
+    return {"value": round(rn * nbytes_rep / sn / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": "synthesis + check of the first %d elements of %d tensor(s) (%d bytes of algorithmic "
+                      "traffic), %d times on %d threads (each on its window) in %.1f s; %d times on one thread "
+                      "in %.1f s" % (max_elems, len(work), nbytes_rep, rn, threads, sn, r1, s1),
+            "value_1_thread": round(r1 * nbytes_rep / s1 / 1e9, 4),
+            "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
 def perf_stage(args):
@@ -375,6 +460,19 @@ def main():
     t3 = time.perf_counter()
     sv.profile_enable(False)
     kt = {k: sv.profile_read(k) for k in kinds}
+    # cold: the same K steps, each after a 1 GiB write on the same stream (it
+    # evicts the Infinity Cache and the L2), the kernels timed by the same events
+    evict = torch.empty(EVICT_BYTES // 4, dtype=torch.int32, device="cuda")
+    sv.profile_enable(True)
+    for k in kinds:
+        sv.profile_read(k)
+    for i in range(args.steps):
+        evict.fill_(i)
+        step()
+    torch.cuda.synchronize()
+    sv.profile_enable(False)
+    kc = {k: sv.profile_read(k) for k in kinds}
+    del evict
 
     ms = (t1 - t0) / args.steps * 1e3
     sbytes, cbytes = wl.synth_bytes, wl.compare_bytes
@@ -398,6 +496,15 @@ def main():
     kernels["synth_and_check_frac"] = round(kernels["synth_and_check_GBps"] / HBM_PEAK_GBS, 4)
     kernel_ms = sum(kt[k][1] for k in kinds) / args.steps
     kernels["tensors_per_s"] = round(len(wl.cases) / (kernel_ms / 1e3), 1)   # kernel time only
+    cold = {"evict_bytes": EVICT_BYTES}
+    for k, nbytes in (("synth", sbytes), ("compare", cbytes), ("finalize", 0)):
+        cnt, tot = kc[k]
+        cold[k + "_ms"] = round(tot / args.steps, 6)
+        if nbytes:
+            cold[k + "_GBps"] = round(nbytes / (tot / args.steps / 1e3) / 1e9, 1)
+    kc_ms = (kc["synth"][1] + kc["compare"][1]) / args.steps
+    cold["synth_and_check_GBps"] = round((sbytes + cbytes) / (kc_ms / 1e3) / 1e9, 1)
+    cold["synth_and_check_frac"] = round(cold["synth_and_check_GBps"] / HBM_PEAK_GBS, 4)
     copy = stream_copy_GBps(torch)
     dom = max(("synth", "compare"), key=lambda k: kernels[k]["ms_per_step"])
     achieved = kernels[dom]["GBps"]
@@ -412,12 +519,12 @@ def main():
         "config": {"workload": wl.name, "description": wl.description, "tensors": len(wl.cases),
                    "elements": wl.total_elems, "synth_bytes": sbytes, "check_bytes": cbytes,
                    "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
-                   "stream_copy_GBps": copy, "frac_of_stream_copy": round(value / copy, 4),
-                   "tensors_per_s": round(len(wl.cases) / (ms / 1e3), 1)},
+                   "stream_copy_GBps": copy, "tensors_per_s": round(len(wl.cases) / (ms / 1e3), 1)},
         "kernels": kernels,
+        "cold": cold,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic(wl.name, dom) if not wl.batched else None},
+                     "traffic": measured_traffic(wl.name, dom)},
         "mismatches": [int(r["mismatches"]) for r in reps][:8],
         "failing_segments": sum(1 for r in reps if r["mismatches"]),
     }
