@@ -811,6 +811,7 @@ int sv_synth_window(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t di
   const uint64_t per_block =
       dist == SV_PERMUTATION ? 1
       : ((dist == SV_INT_RANGE && dtype != SV_U8) || (dist == SV_UNIFORM && dtype == SV_F64)) ? 2
+      : (dist == SV_UNIFORM && dtype == SV_BF16)                                              ? 8
                                                                                             : 4;
   p.e0 = offset;
   p.c0 = offset / per_block;

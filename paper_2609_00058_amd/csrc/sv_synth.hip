@@ -4,8 +4,10 @@
 // thread can produce any element and any slice can be regenerated alone.  The
 // fast path gives every thread one 16-byte output vector per iteration (4
 // fp32 / int32 or 8 bf16 elements), computes the Philox blocks that cover it
-// (one block for uniform / normal fp32, two for bf16 and the integer range,
-// four or eight for the special mix) and writes it with one dwordx4 store.
+// (one for uniform and normal fp32 and for uniform bf16, whose elements take
+// 16-bit draws; two for normal bf16 and the integer range; three for special
+// fp32 and six for special bf16: the normal values plus the class and payload
+// words) and writes it with one dwordx4 store.
 // The grid is a fixed multiple of the CU count with a grid-stride loop; the
 // ragged tail (fewer than one vector) is written element by element by the
 // first threads of the same launch.  Outputs that are not 16-byte aligned, and
@@ -89,6 +91,29 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
   }
 }
 
+// Elements per Philox block of the 4-byte-value kernels (fp32, bf16, int32
+// outputs): bf16 uniform values take a 16-bit half-word each, eight per
+// block; the others as DistTraits.
+template <int DIST, int DT> struct PerBlock { static constexpr int E = DistTraits<DIST>::E; };
+template <> struct PerBlock<SV_UNIFORM, SV_BF16> { static constexpr int E = 8; };
+
+// The E = PerBlock<DIST, DT>::E values (fp32 bits or int32 bits) of Philox
+// block `block`.  bf16 uniform: element 2j + h of the block takes half h (low
+// first) of word j, U = half 2^-16 (exact), a + span U in fp32.
+template <int DIST, int DT>
+__device__ __forceinline__ void values_of(const SynthParams &p, uint64_t block, uint32_t *v) {
+  if constexpr (DIST == SV_UNIFORM && DT == SV_BF16) {
+    const u32x4 w = philox_block(Key{p.k0, p.k1, p.s0, p.s1}, block);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[2 * j] = as_u32(p.a + p.span * ((float)(w[j] & 0xFFFFu) * 0x1p-16f));
+      v[2 * j + 1] = as_u32(p.a + p.span * ((float)(w[j] >> 16) * 0x1p-16f));
+    }
+  } else {
+    block_values<DIST>(p, block, v);
+  }
+}
+
 // Two elements as bf16 in one word.  Uniform and normal values are never
 // NaN, so the hardware conversion applies; special values go through
 // bf16_rne and its NaN rule.
@@ -119,7 +144,7 @@ __device__ __forceinline__ void store_elem(void *out, uint64_t i, uint32_t x) {
 template <int DIST, int DT, bool kNarrow>
 __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                            u32x4 *__restrict__ out, uint32_t rounds) {
-  constexpr int E = DistTraits<DIST>::E;
+  constexpr int E = PerBlock<DIST, DT>::E;
   constexpr int V = DT == SV_BF16 ? 8 : 4;   // elements per 16-byte vector
   constexpr int B = V / E;                   // Philox blocks per vector
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
@@ -132,7 +157,7 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
     if (u >= (Idx)nvec) break;
     uint32_t v[V];
 #pragma unroll
-    for (int b = 0; b < B; ++b) block_values<DIST>(p, (uint64_t)(c0 + u * B + b), v + b * E);
+    for (int b = 0; b < B; ++b) values_of<DIST, DT>(p, (uint64_t)(c0 + u * B + b), v + b * E);
     u32x4 o;
     if constexpr (DT == SV_BF16) {
       o.x = bf16_pair<DIST>(v[0], v[1]);
@@ -151,7 +176,7 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
   if (i < n) {
     const uint64_t g = p.e0 + i;
     uint32_t v[E];
-    block_values<DIST>(p, g / E, v);
+    values_of<DIST, DT>(p, g / E, v);
     store_elem<DIST, DT>(out, i, v[g % E]);
   }
 }
@@ -159,12 +184,12 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
 // Every element, one per thread (outputs that are not 16-byte aligned).
 template <int DIST, int DT>
 __global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint64_t n, void *__restrict__ out) {
-  constexpr int E = DistTraits<DIST>::E;
+  constexpr int E = PerBlock<DIST, DT>::E;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
     const uint64_t g = p.e0 + i;
     uint32_t v[E];
-    block_values<DIST>(p, g / E, v);
+    values_of<DIST, DT>(p, g / E, v);
     store_elem<DIST, DT>(out, i, v[g % E]);
   }
 }
@@ -173,9 +198,9 @@ template <int DIST, int DT>
 static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
   constexpr uint64_t V = DT == SV_BF16 ? 8 : 4;
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
-  if (((uintptr_t)out & 15u) == 0 && p.e0 % DistTraits<DIST>::E == 0) {
+  if (((uintptr_t)out & 15u) == 0 && p.e0 % PerBlock<DIST, DT>::E == 0) {
     const uint64_t nvec = n / V;
-    constexpr uint64_t B = V / DistTraits<DIST>::E;
+    constexpr uint64_t B = V / PerBlock<DIST, DT>::E;
     const uint32_t rounds = synth_tile_rounds(nvec, cus);   // vectors per thread in a tile, as for batches
     const uint64_t tile = (uint64_t)rounds * kBlock;
     const uint64_t tblocks = std::max<uint64_t>(std::min<uint64_t>((nvec + tile - 1) / tile, max_blocks),
@@ -472,12 +497,12 @@ hipError_t launch_eval_transform(int32_t which, const uint32_t *in, uint64_t n, 
 template <int DIST, int DT>
 __device__ __forceinline__ void synth_vector(const SynthParams &p, void *out, uint64_t n, uint64_t u,
                                              bool vec_ok) {
-  constexpr int E = DistTraits<DIST>::E;
+  constexpr int E = PerBlock<DIST, DT>::E;
   constexpr int V = DT == SV_BF16 ? 8 : 4;
   constexpr int B = V / E;
   uint32_t v[V];
 #pragma unroll
-  for (int b = 0; b < B; ++b) block_values<DIST>(p, u * B + b, v + b * E);
+  for (int b = 0; b < B; ++b) values_of<DIST, DT>(p, u * B + b, v + b * E);
   if (vec_ok && (u + 1) * V <= n) {
     u32x4 o;
     if constexpr (DT == SV_BF16) {
@@ -514,7 +539,7 @@ __device__ __forceinline__ uint32_t find_job(const SynthJob *jobs, uint32_t njob
 // unaligned outputs, take the general one.
 template <int DIST, int DT>
 __device__ __forceinline__ void synth_tile(const SynthJob &job, uint64_t u0, uint32_t rounds, bool ok) {
-  constexpr int E = DistTraits<DIST>::E;
+  constexpr int E = PerBlock<DIST, DT>::E;
   constexpr int V = DT == SV_BF16 ? 8 : 4;
   constexpr uint32_t B = V / E;
   const uint64_t whole = job.n / V;
@@ -524,7 +549,7 @@ __device__ __forceinline__ void synth_tile(const SynthJob &job, uint64_t u0, uin
       const uint32_t u = (uint32_t)u0 + r * (uint32_t)kBlock;
       uint32_t v[V];
 #pragma unroll
-      for (uint32_t b = 0; b < B; ++b) block_values<DIST>(job.p, (uint64_t)(u * B + b), v + b * E);
+      for (uint32_t b = 0; b < B; ++b) values_of<DIST, DT>(job.p, (uint64_t)(u * B + b), v + b * E);
       u32x4 o;
       if constexpr (DT == SV_BF16) {
         o.x = bf16_pair<DIST>(v[0], v[1]);

@@ -14,7 +14,7 @@ pytestmark = pytest.mark.gpu
 SPECIAL = dict(mean=0.0, std=1e3, p_nan=0.01, p_inf=0.005, p_denorm=0.01, p_zero=0.01)
 WINDOW_CASES = [("uniform", "f32", dict(a=-1.0, b=1.0)), ("normal", "bf16", dict(mean=5.0, std=10.0)),
                 ("int_range", "i32", dict(lo=-1000, hi=1000)), ("special", "f32", SPECIAL),
-                ("normal", "f32", dict(mean=0.0, std=1.0))]
+                ("normal", "f32", dict(mean=0.0, std=1.0)), ("uniform", "bf16", dict(a=-4.0, b=4.0))]
 
 
 @pytest.mark.parametrize("dist,dtype,params", WINDOW_CASES)
@@ -22,7 +22,8 @@ def test_window_is_the_slice_of_the_tensor(oracle, dist, dtype, params):
     full = empty(300_000, dtype)
     sv.synth(full, 7, 3, dist, **params)
     fb = bits(full)
-    for off, n in [(0, 1), (4, 1000), (5, 777), (1, 3), (131_071, 100_000), (299_990, 10)]:
+    for off, n in [(0, 1), (4, 1000), (5, 777), (1, 3), (8, 4097), (131_071, 100_000), (131_072, 5000),
+                   (299_990, 10)]:
         print("window", dist, dtype, off, n, flush=True)
         big = empty(n + 8, dtype)
         for shift in (0, 1):                        # 16-byte aligned and not

@@ -19,6 +19,7 @@ CASES = [
     ("uniform", "f32", dict(a=-1.0, b=1.0)),
     ("uniform", "f32", dict(a=-3.0, b=7.5)),
     ("uniform", "bf16", dict(a=-4.0, b=4.0)),
+    ("uniform", "bf16", dict(a=-3.0, b=7.5)),
     ("normal", "f32", dict(mean=0.0, std=1.0)),
     ("normal", "f32", dict(mean=5.0, std=10.0)),
     ("normal", "bf16", dict(mean=5.0, std=10.0)),
@@ -50,7 +51,7 @@ def test_synth_bit_exact(oracle, dist, dtype, params):
         assert np.array_equal(got, want), _diff(got, want)
 
 
-@pytest.mark.parametrize("dist,dtype,params", [CASES[0], CASES[2], CASES[4], CASES[6], CASES[10], CASES[11]])
+@pytest.mark.parametrize("dist,dtype,params", [CASES[0], CASES[2], CASES[3], CASES[5], CASES[7], CASES[11], CASES[12]])
 def test_synth_unaligned_outputs_and_guard(oracle, dist, dtype, params):
     n = 5003
     per = 8 if dtype == "bf16" else 4
