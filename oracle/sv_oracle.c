@@ -349,10 +349,18 @@ typedef struct {
   int64_t lo;              /* integer range, permutation                 */
   uint64_t range;          /* hi - lo + 1 (0 stands for 2^64)            */
   unsigned half;           /* permutation: bits of each Feistel half     */
+  uint32_t gate;           /* special: candidates have a gate byte below this */
   uint64_t t_nan, t_inf, t_den, t_zero;   /* cumulative class thresholds */
 } prepared;
 
 static uint64_t width32(double p) { return (uint64_t)floor(p * 4294967296.0); }
+
+/* The width of a special class among the candidates: floor(p 2^32 256 / S),
+ * evaluated as floor(fp64(p 2^40) / S) (p 2^40 is exact), at most 2^32. */
+static uint64_t class_width(double p, uint32_t gate) {
+  uint64_t w = (uint64_t)floor(p * 1099511627776.0 / (double)gate);
+  return w < (1ull << 32) ? w : (1ull << 32);
+}
 
 static int is_float(int32_t dtype) {
   return dtype == OR_F32 || dtype == OR_BF16 || dtype == OR_F16 || dtype == OR_F64;
@@ -395,10 +403,19 @@ static int prepare(int32_t dtype, int32_t dist, const or_dist_params *p, prepare
         tot += ps[k];
       }
       if (!(tot <= 1.0)) return -1;
-      q->t_nan = width32(p->p_nan);
-      q->t_inf = q->t_nan + width32(p->p_inf);
-      q->t_den = q->t_inf + width32(p->p_denorm);
-      q->t_zero = q->t_den + width32(p->p_zero);
+      /* a share S / 256 >= tot of the elements are candidates (S = ceil(256 tot));
+       * within them the classes take widths p / (S / 256) of the class word */
+      q->gate = (uint32_t)ceil(256.0 * tot);
+      if (q->gate) {
+        const uint64_t full = 1ull << 32;
+        q->t_nan = class_width(p->p_nan, q->gate);
+        q->t_inf = q->t_nan + class_width(p->p_inf, q->gate);
+        q->t_den = q->t_inf + class_width(p->p_denorm, q->gate);
+        q->t_zero = q->t_den + class_width(p->p_zero, q->gate);
+        if (q->t_inf > full) q->t_inf = full;
+        if (q->t_den > full) q->t_den = full;
+        if (q->t_zero > full) q->t_zero = full;
+      }
     }
     return 0;
   }
@@ -478,7 +495,6 @@ static uint64_t permute(uint64_t seed, uint64_t stream, const prepared *q, uint6
 }
 
 #define SPECIAL_CLASS_BLOCKS (1ull << 62)
-#define SPECIAL_PAYLOAD_BLOCKS ((1ull << 62) + (1ull << 61))
 
 /* Value of element i: fp32 bits (UNIFORM, NORMAL, SPECIAL; fp64 uniform gives
  * fp64 bits) or the integer (INT_RANGE), in the low bits of a 64-bit word. */
@@ -544,17 +560,23 @@ static uint64_t element_value(uint64_t seed, uint64_t stream, int32_t dtype, int
     return (uint64_t)q->lo + off;                   /* two's complement wrap-around: exact */
   }
   /* SPECIAL: the normal sequence above with some elements replaced.  Element
-   * i = 4c + k takes its class from word k of Philox block 2^62 + c, against
-   * cumulative thresholds in the order NaN, Inf, denormal, zero, normal, and
-   * its sign and payload / mantissa from word k of block 2^62 + 2^61 + c
-   * (block indices that the sequence of normal values, below 2^58, never
-   * reaches); an element of the normal class keeps the normal value. */
-  uint32_t cls[4], pay[4];
+   * i = 4c + k is a candidate when its gate, the low byte of word k of normal
+   * block c (the eight bits Box-Muller leaves unused), is below S = ceil(256
+   * p), p the total probability of the four special classes.  A candidate
+   * takes its class from x = word k of Philox block 2^62 + c (block indices
+   * the normal values, below 2^58, never reach), against cumulative
+   * thresholds of widths floor(p_class 2^32 256 / S) in the order NaN, Inf,
+   * denormal, zero; x at or above the last keeps the normal value.  Its sign
+   * and payload / mantissa come from r = x 0x9E3779B9 mod 2^32 (Fibonacci
+   * hashing, Knuth, TAOCP vol. 3, 6.4): the low bits of r are a bijection of
+   * the low bits of x, its top bit mixes all of x's bits. */
+  or_philox_block(seed, stream, i / 4u, w);
+  if ((w[i % 4u] & 0xFFu) >= q->gate) return element_value(seed, stream, dtype, OR_NORMAL, q, i);
+  uint32_t cls[4];
   or_philox_block(seed, stream, SPECIAL_CLASS_BLOCKS + i / 4u, cls);
   const uint64_t x = cls[i % 4u];
   if (x >= q->t_zero) return element_value(seed, stream, dtype, OR_NORMAL, q, i);
-  or_philox_block(seed, stream, SPECIAL_PAYLOAD_BLOCKS + i / 4u, pay);
-  const uint32_t r = pay[i % 4u];
+  const uint32_t r = (uint32_t)x * 0x9E3779B9u;
   const uint32_t sign = r & 0x80000000u;
   if (x < q->t_nan) return sign | 0x7FC00000u | (r & 0x003FFFFFu);
   if (x < q->t_inf) return sign | 0x7F800000u;
@@ -613,6 +635,11 @@ int or_special_class_counts(uint64_t seed, uint64_t stream, const or_dist_params
   for (int k = 0; k < 5; k++) counts[k] = 0;
   for (uint64_t i = offset; i < offset + n; i++) {
     uint32_t w[4];
+    or_philox_block(seed, stream, i / 4u, w);
+    if ((w[i % 4u] & 0xFFu) >= q.gate) {           /* not a candidate */
+      counts[4]++;
+      continue;
+    }
     or_philox_block(seed, stream, SPECIAL_CLASS_BLOCKS + i / 4u, w);
     uint64_t x = w[i % 4u];
     int cls = x < q.t_nan ? 0 : x < q.t_inf ? 1 : x < q.t_den ? 2 : x < q.t_zero ? 3 : 4;

@@ -308,19 +308,37 @@ def test_int_range_bounds_endpoints_and_chi_square(oracle):
 SPECIAL = dict(mean=0.0, std=1e3, p_nan=0.01, p_inf=0.005, p_denorm=0.01, p_zero=0.01)
 
 
-def test_special_classes_follow_thresholds_and_bit_rules(oracle):
-    # element i = 4c + k: class from word k of block 2^62 + c, sign and payload
-    # from word k of block 2^62 + 2^61 + c; the normal class keeps element i of
-    # the normal distribution with the same (seed, stream, mean, std)
+FIB = 0x9E3779B9   # Fibonacci hashing multiplier: 2^32 / golden ratio, odd
+
+
+def _special_layout(oracle, seed, stream, n, probs):
+    """Class of every element as the reading defines it, from the Philox words:
+    a candidate when the low byte of its normal word is below S = ceil(256 p),
+    then its class word against widths floor(p_class 2^32 256 / S) (exact
+    rationals), 0 NaN, 1 Inf, 2 denormal, 3 zero, 4 normal; and the hashed word
+    that gives the sign and payload."""
+    S = math.ceil(Fraction(256) * sum(Fraction(p) for p in probs))
+    w = oracle.philox_blocks(seed, stream, 0, n // 4).reshape(-1)
+    q = oracle.philox_blocks(seed, stream, 1 << 62, n // 4).reshape(-1)
+    widths = [math.floor(Fraction(p) * 2 ** 40 / S) for p in probs]
+    t = np.cumsum(widths)
+    cls = np.where((w & 0xFF) < S, np.searchsorted(t, q.astype(np.int64), side="right"), 4)
+    cls = np.minimum(cls, 4)
+    r = (q.astype(np.uint64) * FIB) & 0xFFFFFFFF
+    return S, widths, cls, r.astype(np.uint32)
+
+
+def test_special_classes_follow_gate_thresholds_and_bit_rules(oracle):
+    """Element i = 4c + k: a candidate when the low byte of word k of normal
+    block c (bits Box-Muller leaves unused) is below S = ceil(256 p); its class
+    from word k of block 2^62 + c; sign and payload / mantissa from that word
+    times 0x9E3779B9 mod 2^32; every other element keeps element i of the
+    normal distribution with the same (seed, stream, mean, std)."""
     n = 1 << 16
     bits = oracle.synth(0, 0, "f32", "special", oracle.dist_params(**SPECIAL), n)
-    q = oracle.philox_blocks(0, 0, 1 << 62, n // 4).reshape(-1)
-    r = oracle.philox_blocks(0, 0, (1 << 62) + (1 << 61), n // 4).reshape(-1)
-    widths = [math.floor(p * 2 ** 32) for p in (0.01, 0.005, 0.01, 0.01)]
-    assert widths == [42949672, 21474836, 42949672, 42949672]
-    t = np.cumsum(widths)
+    S, widths, cls, r = _special_layout(oracle, 0, 0, n, (0.01, 0.005, 0.01, 0.01))
+    assert S == 9 and widths == [1221679586, 610839793, 1221679586, 1221679586]
     sign = r & 0x80000000
-    cls = np.searchsorted(t, q.astype(np.int64), side="right")   # 0 nan 1 inf 2 den 3 zero 4 normal
     mag = bits & 0x7FFFFFFF
     spec = cls < 4
     assert np.all((bits[spec] & 0x80000000) == sign[spec])
@@ -345,6 +363,57 @@ def test_special_classes_follow_thresholds_and_bit_rules(oracle):
     assert np.all(np.isnan(x[nan])) and np.all(np.isinf(x[inf]))
     assert np.all(np.isfinite(x[cls >= 2]))
     assert np.all(np.abs(x[den]) < np.finfo(np.float32).tiny) and np.all(x[den] != 0)
+
+
+def test_special_class_probabilities_are_the_given_ones(oracle):
+    """The share of each class is (S / 256) floor(p 2^32 256 / S) / 2^32: p
+    itself, short by less than 2^-32 (exact rationals); and the extremes: no
+    special classes gives the normal distribution bit for bit, probabilities
+    summing to 1 leave no normal element."""
+    for probs in ((0.01, 0.005, 0.01, 0.01), (0.2, 0.1, 0.2, 0.2), (0.25, 0.25, 0.25, 0.25), (1e-6, 0.0, 0.0, 0.3)):
+        S = math.ceil(Fraction(256) * sum(Fraction(p) for p in probs))
+        for p in probs:
+            share = Fraction(S, 256) * math.floor(Fraction(p) * 2 ** 40 / S) / 2 ** 32
+            assert 0 <= Fraction(p) - share < Fraction(1, 2 ** 32)
+    n = 1 << 14
+    none = oracle.synth(3, 1, "f32", "special", oracle.dist_params(mean=5.0, std=10.0), n)
+    assert np.array_equal(none, oracle.synth(3, 1, "f32", "normal", oracle.dist_params(mean=5.0, std=10.0), n))
+    allp = dict(mean=5.0, std=10.0, p_nan=0.25, p_inf=0.25, p_denorm=0.25, p_zero=0.25)
+    x = f32(oracle.synth(3, 1, "f32", "special", oracle.dist_params(**allp), n))
+    ax = np.abs(x)
+    assert np.all(np.isnan(x) | np.isinf(x) | (ax < np.finfo(np.float32).tiny))
+    for cnt in (np.isnan(x).sum(), np.isinf(x).sum(), ((ax > 0) & (ax < np.finfo(np.float32).tiny)).sum(),
+                (x == 0).sum()):
+        assert abs(cnt - n / 4) < 5 * math.sqrt(n * 3 / 16)
+
+
+def test_special_signs_payloads_and_independence(oracle):
+    """Signs are balanced in every class, each NaN payload bit and the top
+    denormal mantissa bits are uniform, and whether an element is special does
+    not depend on the normal value it replaces (the normal values at special
+    positions follow N(mean, std), KS)."""
+    n = 1 << 21
+    heavy = dict(mean=0.0, std=1.0, p_nan=0.05, p_inf=0.05, p_denorm=0.05, p_zero=0.05)
+    bits = oracle.synth(2, 8, "f32", "special", oracle.dist_params(**heavy), n)
+    x = f32(bits)
+    ax = np.abs(x)
+    tiny = np.finfo(np.float32).tiny
+    classes = [np.isnan(x), np.isinf(x), (ax > 0) & (ax < tiny), x == 0]
+    for c in classes:
+        k = int(c.sum())
+        neg = int((bits[c] >> 31).sum())
+        assert abs(neg - k / 2) < 5 * math.sqrt(k / 4)
+    nanp = bits[classes[0]] & 0x3FFFFF
+    for b in range(22):
+        ones = int(((nanp >> b) & 1).sum())
+        assert abs(ones - nanp.size / 2) < 5 * math.sqrt(nanp.size / 4), b
+    top = (bits[classes[2]] & 0x7FFFFF) >> 19                  # top 4 mantissa bits of denormals
+    cnt = np.bincount(top, minlength=16)
+    e = top.size / 16
+    assert ((cnt - e) ** 2 / e).sum() < 15 + 5 * math.sqrt(30)
+    spec = ~np.isfinite(x) | (ax < tiny)
+    z = f32(oracle.synth(2, 8, "f32", "normal", oracle.dist_params(mean=0.0, std=1.0), n))[spec].astype(np.float64)
+    assert st.kstest(z, "norm").statistic < 1.95 / math.sqrt(z.size)
 
 
 def test_special_class_frequencies(oracle):
