@@ -332,6 +332,12 @@ int check_tolerances(double rtol, double atol) {
 
 uint64_t width32(double p) { return (uint64_t)std::floor(p * 4294967296.0); }
 
+// floor(p 2^40 / gate) (p 2^40 exact, the quotient rounded to fp64), at most 2^32
+uint64_t class_width(double p, uint32_t gate) {
+  const uint64_t w = (uint64_t)std::floor(p * 1099511627776.0 / (double)gate);
+  return std::min<uint64_t>(w, 1ull << 32);
+}
+
 int check_seg(const sv_segment &g, uint32_t k) {
   if (!valid_dtype(g.dtype)) return fail(SV_ERR_UNSUPPORTED, "segment %u: unknown dtype %d", k, g.dtype);
   int rc = check_tensor(g.ref, g.n, g.dtype, "segment ref");
@@ -699,10 +705,16 @@ int prepare_synth(uint64_t seed, uint64_t stream_id, int32_t dtype, int32_t dist
         tot += q;
       }
       if (!(tot <= 1.0)) return fail(SV_ERR_INVALID_ARG, "sv_synth: class probabilities sum to %g > 1", tot);
-      p.t_nan = width32(params->p_nan);
-      p.t_inf = p.t_nan + width32(params->p_inf);
-      p.t_den = p.t_inf + width32(params->p_denorm);
-      p.t_zero = p.t_den + width32(params->p_zero);
+      // S / 256 of the elements (S = ceil(256 tot)) are candidates; among them each
+      // class takes a width floor(p 2^32 256 / S) of the class word, cumulative
+      p.gate = (uint32_t)std::ceil(256.0 * tot);
+      if (p.gate) {
+        const uint64_t full = 1ull << 32;
+        p.t_nan = class_width(params->p_nan, p.gate);
+        p.t_inf = std::min(full, p.t_nan + class_width(params->p_inf, p.gate));
+        p.t_den = std::min(full, p.t_inf + class_width(params->p_denorm, p.gate));
+        p.t_zero = std::min(full, p.t_den + class_width(params->p_zero, p.gate));
+      }
     }
   } else {
     const int64_t lo = params->lo, hi = params->hi;

@@ -60,7 +60,8 @@ struct SynthParams {
   int64_t lo;                   // integer range
   uint64_t range;               // hi - lo + 1 (0 stands for 2^64: the whole int64 range)
   uint32_t half;                // permutation: bits of each Feistel half
-  uint64_t t_nan, t_inf, t_den, t_zero;   // cumulative class thresholds on w0
+  uint32_t gate;                // special: an element is a candidate when its gate byte is below this
+  uint64_t t_nan, t_inf, t_den, t_zero;   // special: cumulative class thresholds on a candidate's class word
   double a64, span64;           // fp64 uniform: a + span U53
   uint64_t e0;                  // tensor index of out[0] (a window of the tensor; 0 for a whole tensor)
   uint64_t c0;                  // e0 / E, the first Philox block (used when E divides e0)

@@ -29,14 +29,20 @@ template <> struct DistTraits<SV_NORMAL> { static constexpr int E = 4; };
 template <> struct DistTraits<SV_INT_RANGE> { static constexpr int E = 2; };
 template <> struct DistTraits<SV_SPECIAL> { static constexpr int E = 4; };
 
-// Special values: the normal sequence with some elements replaced, their
-// class and payload words from Philox blocks that the normal values (block
-// indices below 2^58) never reach.
+// Special values: the normal sequence with some elements replaced.  Element
+// 4c + k is a candidate when its gate, the low byte of word k of normal
+// block c (bits Box-Muller leaves unused), is below p.gate; a candidate's
+// class word is word k of Philox block 2^62 + c (block indices the normal
+// values, below 2^58, never reach), its sign and payload bits that word
+// times 0x9E3779B9 (Fibonacci hashing).
 constexpr uint64_t kSpecialClassBlocks = 1ull << 62;
-constexpr uint64_t kSpecialPayloadBlocks = (1ull << 62) + (1ull << 61);
+constexpr uint32_t kPayloadHash = 0x9E3779B9u;
 
-__device__ __forceinline__ void special_overlay(const SynthParams &p, uint32_t x, uint32_t r, uint32_t &v) {
+// Candidate `x`-word element: its class (cumulative thresholds NaN, Inf,
+// denormal, zero; at or above the last it keeps the normal value v).
+__device__ __forceinline__ void special_overlay(const SynthParams &p, uint32_t x, uint32_t &v) {
   if (x < p.t_zero) {
+    const uint32_t r = x * kPayloadHash;
     const uint32_t sign = r & 0x80000000u;
     const uint32_t m = r & 0x007FFFFFu;
     v = x < p.t_nan   ? sign | 0x7FC00000u | (r & 0x003FFFFFu)
@@ -44,6 +50,22 @@ __device__ __forceinline__ void special_overlay(const SynthParams &p, uint32_t x
         : x < p.t_den ? sign | (m ? m : 1u)
                       : sign;
   }
+}
+
+// Bit k set: element k of a block whose words are w is a special candidate.
+__device__ __forceinline__ uint32_t candidates(const SynthParams &p, const u32x4 &w) {
+  return ((w.x & 0xFFu) < p.gate ? 1u : 0u) | ((w.y & 0xFFu) < p.gate ? 2u : 0u) |
+         ((w.z & 0xFFu) < p.gate ? 4u : 0u) | ((w.w & 0xFFu) < p.gate ? 8u : 0u);
+}
+
+// The special elements among the four values v of normal block `block`,
+// whose candidates are the set bits of c.
+__device__ __forceinline__ void apply_overlay(const SynthParams &p, uint64_t block, uint32_t c, uint32_t *v) {
+  const u32x4 q = philox_block(Key{p.k0, p.k1, p.s0, p.s1}, kSpecialClassBlocks + block);
+  if (c & 1u) special_overlay(p, q.x, v[0]);
+  if (c & 2u) special_overlay(p, q.y, v[1]);
+  if (c & 4u) special_overlay(p, q.z, v[2]);
+  if (c & 8u) special_overlay(p, q.w, v[3]);
 }
 
 // The E element values (fp32 bits or int32 bits) of Philox block `block`.
@@ -71,10 +93,7 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
     v[0] = (uint32_t)(int32_t)(p.lo + (int64_t)__umul64hi(r0, p.range));
     v[1] = (uint32_t)(int32_t)(p.lo + (int64_t)__umul64hi(r1, p.range));
   } else {
-    // the normal values of the block, then the overlay: element k of the
-    // block takes its class from word k of block 2^62 + block (cumulative
-    // thresholds: NaN, Inf, denormal, zero, normal) and its sign and payload
-    // / mantissa from word k of block 2^62 + 2^61 + block
+    // the normal values of the block, then the overlay of its candidates
     float c0, s0, c1, s1;
     box_muller(w.x, w.y, c0, s0);
     box_muller(w.z, w.w, c1, s1);
@@ -82,12 +101,8 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
     v[1] = as_u32(__builtin_fmaf(p.std, s0, p.mean));
     v[2] = as_u32(__builtin_fmaf(p.std, c1, p.mean));
     v[3] = as_u32(__builtin_fmaf(p.std, s1, p.mean));
-    const u32x4 q = philox_block(key, kSpecialClassBlocks + block);
-    const u32x4 r = philox_block(key, kSpecialPayloadBlocks + block);
-    special_overlay(p, q.x, r.x, v[0]);
-    special_overlay(p, q.y, r.y, v[1]);
-    special_overlay(p, q.z, r.z, v[2]);
-    special_overlay(p, q.w, r.w, v[3]);
+    const uint32_t c = candidates(p, w);
+    if (c) apply_overlay(p, block, c, v);
   }
 }
 
@@ -181,6 +196,96 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
   }
 }
 
+// Special values, fp32, 16-byte aligned output, window starting on a block:
+// the path of the special-value stream.  One vector = one normal block, and
+// every vector is stored at once with its normal values, in order.  A vector
+// with candidates (each element is one with probability gate / 256) needs
+// the class block as well; rather than every lane computing one whenever any
+// lane of its wave needs it, a wave collects its candidate vectors (index,
+// candidate bits, normal values) in a ring in LDS and, 64 at a time, its 64
+// lanes take one each: class block, overlay, and the vector stored again.
+// A wave's vector memory operations are performed in program order, so the
+// second store of a vector lands after the first.  (Leaving the candidate
+// vectors out of the first stores measured much slower, 1686 against 1254 us
+// for 2^30 elements: cache lines written in two pieces far apart in time.)
+// Loops are uniform across the wave (lanes past the end only compute), so
+// every lane takes part in every pass over the ring.
+constexpr uint32_t kRing = 128;      // ring slots per wave: 64 pending + up to 64 new
+
+template <class Idx>
+__device__ __forceinline__ void overlay_ring(const SynthParams &p, Idx c0, u32x4 *__restrict__ out,
+                                             const u32x4 *rv, const Idx *ru, const uint32_t *rc, uint32_t head,
+                                             uint32_t count, uint32_t lane) {
+  if (lane < count) {
+    const uint32_t slot = (head + lane) % kRing;
+    const u32x4 w = rv[slot];
+    const Idx u = ru[slot];
+    uint32_t v[4] = {w.x, w.y, w.z, w.w};
+    apply_overlay(p, (uint64_t)(c0 + u), rc[slot], v);
+    out[u] = u32x4{v[0], v[1], v[2], v[3]};
+  }
+}
+
+template <bool kNarrow>
+__global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, uint64_t nvec, uint64_t n,
+                                                               u32x4 *__restrict__ out, uint32_t rounds) {
+  using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
+  constexpr int kWaves = kBlock / kWave;
+  __shared__ u32x4 ring_v[kWaves][kRing];
+  __shared__ Idx ring_u[kWaves][kRing];
+  __shared__ uint32_t ring_c[kWaves][kRing];
+  const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  u32x4 *rv = ring_v[wave];
+  Idx *ru = ring_u[wave];
+  uint32_t *rc = ring_c[wave];
+  const Key key{p.k0, p.k1, p.s0, p.s1};
+  const Idx tile = (Idx)rounds * kBlock;
+  const Idx c0 = (Idx)p.c0;
+  uint32_t head = 0, tail = 0;       // wave-uniform: slots [head, tail) (mod kRing) are pending
+  for (Idx t0 = (Idx)blockIdx.x * tile; t0 < (Idx)nvec; t0 += (Idx)gridDim.x * tile)
+  for (uint32_t r = 0; r < rounds; ++r) {
+    const Idx u = t0 + (Idx)r * kBlock + threadIdx.x;
+    const bool valid = u < (Idx)nvec;
+    const u32x4 w = philox_block(key, (uint64_t)(c0 + u));
+    float zc0, zs0, zc1, zs1;
+    box_muller(w.x, w.y, zc0, zs0);
+    box_muller(w.z, w.w, zc1, zs1);
+    const u32x4 v{as_u32(__builtin_fmaf(p.std, zc0, p.mean)), as_u32(__builtin_fmaf(p.std, zs0, p.mean)),
+                  as_u32(__builtin_fmaf(p.std, zc1, p.mean)), as_u32(__builtin_fmaf(p.std, zs1, p.mean))};
+    const uint32_t c = valid ? candidates(p, w) : 0u;
+    if (valid) out[u] = v;
+    const uint64_t m = __ballot(c != 0u);
+    if (c != 0u) {
+      const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      const uint32_t slot = (tail + below) % kRing;
+      rv[slot] = v;
+      ru[slot] = u;
+      rc[slot] = c;
+    }
+    tail += (uint32_t)__popcll(m);
+    if (tail - head >= (uint32_t)kWave) {   // a full pass: every lane takes one pending vector
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      overlay_ring<Idx>(p, c0, out, rv, ru, rc, head, kWave, lane);
+      head += kWave;
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  // what is left in the ring (fewer than 64)
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  overlay_ring<Idx>(p, c0, out, rv, ru, rc, head, tail - head, lane);
+  // the ragged tail elements, one per thread of the first threads of the grid
+  const uint64_t i = nvec * 4 + (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (i < n) {
+    const uint64_t g = p.e0 + i;
+    uint32_t e[4];
+    block_values<SV_SPECIAL>(p, g / 4, e);
+    ((uint32_t *)out)[i] = e[g % 4];
+  }
+}
+
 // Every element, one per thread (outputs that are not 16-byte aligned).
 template <int DIST, int DT>
 __global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint64_t n, void *__restrict__ out) {
@@ -206,6 +311,15 @@ static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int 
     const uint64_t tblocks = std::max<uint64_t>(std::min<uint64_t>((nvec + tile - 1) / tile, max_blocks),
                                                 (n - nvec * V + kBlock - 1) / kBlock);   // the tail needs < V threads
     const bool narrow = p.c0 + (nvec + tile) * B < (1ull << 32) && tblocks * tile + nvec < (1ull << 32);
+    if constexpr (DIST == SV_SPECIAL && DT == SV_F32) {
+      if (narrow)
+        hipLaunchKernelGGL(synth_special_kernel<true>, dim3((unsigned)tblocks), dim3(kBlock), 0, stream, p, nvec, n,
+                           (u32x4 *)out, rounds);
+      else
+        hipLaunchKernelGGL(synth_special_kernel<false>, dim3((unsigned)tblocks), dim3(kBlock), 0, stream, p, nvec, n,
+                           (u32x4 *)out, rounds);
+      return hipGetLastError();
+    }
     if (narrow)
       hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, true>), dim3((unsigned)tblocks), dim3(kBlock), 0, stream, p,
                          nvec, n, (u32x4 *)out, rounds);
