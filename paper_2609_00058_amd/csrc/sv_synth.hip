@@ -197,33 +197,35 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
 }
 
 // Special values, fp32, 16-byte aligned output, window starting on a block:
-// the path of the special-value stream.  One vector = one normal block, and
-// every vector is stored at once with its normal values, in order.  A vector
-// with candidates (each element is one with probability gate / 256) needs
-// the class block as well; rather than every lane computing one whenever any
-// lane of its wave needs it, a wave collects its candidate vectors (index,
-// candidate bits, normal values) in a ring in LDS and, 64 at a time, its 64
-// lanes take one each: class block, overlay, and the vector stored again.
-// A wave's vector memory operations are performed in program order, so the
-// second store of a vector lands after the first.  (Leaving the candidate
-// vectors out of the first stores measured much slower, 1686 against 1254 us
-// for 2^30 elements: cache lines written in two pieces far apart in time.)
-// Loops are uniform across the wave (lanes past the end only compute), so
-// every lane takes part in every pass over the ring.
-constexpr uint32_t kRing = 128;      // ring slots per wave: 64 pending + up to 64 new
+// the path of the special-value stream.  One vector = one normal block.  A
+// vector with candidates (each element is one with probability gate / 256)
+// needs the class block as well; rather than every lane computing one
+// whenever any lane of its wave needs it, each lane holds its next kGroup
+// vectors in registers while the wave lists their candidate vectors in LDS
+// (index and candidate bits, about 13 % of them on the special-value
+// stream); then the wave's lanes take the listed vectors 64 at a time, one
+// class block each, and leave the special values in LDS; each lane merges
+// them into its vectors and stores all kGroup of them once, in order.
+// (Storing the candidate vectors late, when a ring of them filled up,
+// measured much slower: cache lines written in two pieces far apart in
+// time; storing them twice, with normal values first, wrote 1.33 times the
+// bytes.)  Loops are uniform across the wave (lanes past the end only
+// compute), so every lane takes part in every pass over the list.
+constexpr uint32_t kGroup = 4;       // vectors a lane holds before their candidates are overlaid
 
-template <class Idx>
-__device__ __forceinline__ void overlay_ring(const SynthParams &p, Idx c0, u32x4 *__restrict__ out,
-                                             const u32x4 *rv, const Idx *ru, const uint32_t *rc, uint32_t head,
-                                             uint32_t count, uint32_t lane) {
-  if (lane < count) {
-    const uint32_t slot = (head + lane) % kRing;
-    const u32x4 w = rv[slot];
-    const Idx u = ru[slot];
-    uint32_t v[4] = {w.x, w.y, w.z, w.w};
-    apply_overlay(p, (uint64_t)(c0 + u), rc[slot], v);
-    out[u] = u32x4{v[0], v[1], v[2], v[3]};
+// The special values of candidate elements (bits c) given their class words
+// q, and which of them replace the normal value (bits of the result's .w).
+__device__ __forceinline__ u32x4 overlay_values(const SynthParams &p, const u32x4 &q, uint32_t c, uint32_t &m) {
+  uint32_t v[4] = {0u, 0u, 0u, 0u};
+  m = 0u;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    if (((c >> k) & 1u) && q[k] < p.t_zero) {
+      special_overlay(p, q[k], v[k]);
+      m |= 1u << k;
+    }
   }
+  return u32x4{v[0], v[1], v[2], v[3]};
 }
 
 template <bool kNarrow>
@@ -231,51 +233,67 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
                                                                u32x4 *__restrict__ out, uint32_t rounds) {
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
   constexpr int kWaves = kBlock / kWave;
-  __shared__ u32x4 ring_v[kWaves][kRing];
-  __shared__ Idx ring_u[kWaves][kRing];
-  __shared__ uint32_t ring_c[kWaves][kRing];
+  constexpr uint32_t kSlots = kGroup * kWave;     // every vector of a group may be a candidate
+  __shared__ u32x4 list_v[kWaves][kSlots];        // in: (index lo, index hi, candidate bits); out: values
+  __shared__ uint32_t list_m[kWaves][kSlots];     // out: which values replace normal ones
   const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  u32x4 *rv = ring_v[wave];
-  Idx *ru = ring_u[wave];
-  uint32_t *rc = ring_c[wave];
+  u32x4 *lv = list_v[wave];
+  uint32_t *lm = list_m[wave];
   const Key key{p.k0, p.k1, p.s0, p.s1};
-  const Idx tile = (Idx)rounds * kBlock;
+  const Idx tile = (Idx)rounds * kBlock;          // rounds: a multiple of kGroup
   const Idx c0 = (Idx)p.c0;
-  uint32_t head = 0, tail = 0;       // wave-uniform: slots [head, tail) (mod kRing) are pending
   for (Idx t0 = (Idx)blockIdx.x * tile; t0 < (Idx)nvec; t0 += (Idx)gridDim.x * tile)
-  for (uint32_t r = 0; r < rounds; ++r) {
-    const Idx u = t0 + (Idx)r * kBlock + threadIdx.x;
-    const bool valid = u < (Idx)nvec;
-    const u32x4 w = philox_block(key, (uint64_t)(c0 + u));
-    float zc0, zs0, zc1, zs1;
-    box_muller(w.x, w.y, zc0, zs0);
-    box_muller(w.z, w.w, zc1, zs1);
-    const u32x4 v{as_u32(__builtin_fmaf(p.std, zc0, p.mean)), as_u32(__builtin_fmaf(p.std, zs0, p.mean)),
-                  as_u32(__builtin_fmaf(p.std, zc1, p.mean)), as_u32(__builtin_fmaf(p.std, zs1, p.mean))};
-    const uint32_t c = valid ? candidates(p, w) : 0u;
-    if (valid) out[u] = v;
-    const uint64_t m = __ballot(c != 0u);
-    if (c != 0u) {
-      const uint32_t below = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-      const uint32_t slot = (tail + below) % kRing;
-      rv[slot] = v;
-      ru[slot] = u;
-      rc[slot] = c;
+  for (uint32_t r0 = 0; r0 < rounds; r0 += kGroup) {
+    u32x4 v[kGroup];
+    uint32_t c[kGroup], slot[kGroup];
+    uint32_t count = 0;                           // wave-uniform
+#pragma unroll
+    for (uint32_t g = 0; g < kGroup; ++g) {
+      const Idx u = t0 + (Idx)(r0 + g) * kBlock + threadIdx.x;
+      const u32x4 w = philox_block(key, (uint64_t)(c0 + u));
+      float zc0, zs0, zc1, zs1;
+      box_muller(w.x, w.y, zc0, zs0);
+      box_muller(w.z, w.w, zc1, zs1);
+      v[g] = u32x4{as_u32(__builtin_fmaf(p.std, zc0, p.mean)), as_u32(__builtin_fmaf(p.std, zs0, p.mean)),
+                   as_u32(__builtin_fmaf(p.std, zc1, p.mean)), as_u32(__builtin_fmaf(p.std, zs1, p.mean))};
+      c[g] = u < (Idx)nvec ? candidates(p, w) : 0u;
+      const uint64_t m = __ballot(c[g] != 0u);
+      slot[g] = count + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (c[g] != 0u) lv[slot[g]] = u32x4{(uint32_t)u, (uint32_t)((uint64_t)u >> 32), c[g], 0u};
+      count += (uint32_t)__popcll(m);
     }
-    tail += (uint32_t)__popcll(m);
-    if (tail - head >= (uint32_t)kWave) {   // a full pass: every lane takes one pending vector
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      overlay_ring<Idx>(p, c0, out, rv, ru, rc, head, kWave, lane);
-      head += kWave;
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    for (uint32_t base = 0; base < count; base += kWave) {   // the listed vectors, one per lane
+      const uint32_t e = base + lane;
+      if (e < count) {
+        const u32x4 in = lv[e];
+        const uint64_t u = ((uint64_t)in.y << 32) | in.x;
+        const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)c0 + u);
+        uint32_t m;
+        lv[e] = overlay_values(p, q, in.z, m);
+        lm[e] = m;
+      }
     }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (uint32_t g = 0; g < kGroup; ++g) {
+      const Idx u = t0 + (Idx)(r0 + g) * kBlock + threadIdx.x;
+      if (c[g] != 0u) {
+        const u32x4 sv = lv[slot[g]];
+        const uint32_t m = lm[slot[g]];
+        v[g].x = (m & 1u) ? sv.x : v[g].x;
+        v[g].y = (m & 2u) ? sv.y : v[g].y;
+        v[g].z = (m & 4u) ? sv.z : v[g].z;
+        v[g].w = (m & 8u) ? sv.w : v[g].w;
+      }
+      if (u < (Idx)nvec) out[u] = v[g];
+    }
+    // the list is rewritten by the next group only after every lane has read it
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
   }
-  // what is left in the ring (fewer than 64)
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  overlay_ring<Idx>(p, c0, out, rv, ru, rc, head, tail - head, lane);
   // the ragged tail elements, one per thread of the first threads of the grid
   const uint64_t i = nvec * 4 + (uint64_t)blockIdx.x * kBlock + threadIdx.x;
   if (i < n) {
@@ -310,16 +328,22 @@ static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int 
     const uint64_t tile = (uint64_t)rounds * kBlock;
     const uint64_t tblocks = std::max<uint64_t>(std::min<uint64_t>((nvec + tile - 1) / tile, max_blocks),
                                                 (n - nvec * V + kBlock - 1) / kBlock);   // the tail needs < V threads
-    const bool narrow = p.c0 + (nvec + tile) * B < (1ull << 32) && tblocks * tile + nvec < (1ull << 32);
     if constexpr (DIST == SV_SPECIAL && DT == SV_F32) {
-      if (narrow)
-        hipLaunchKernelGGL(synth_special_kernel<true>, dim3((unsigned)tblocks), dim3(kBlock), 0, stream, p, nvec, n,
-                           (u32x4 *)out, rounds);
+      // whole groups of kGroup vectors per thread in a tile
+      const uint32_t r4 = (rounds + kGroup - 1) / kGroup * kGroup;
+      const uint64_t tile4 = (uint64_t)r4 * kBlock;
+      const uint64_t blocks4 = std::max<uint64_t>(std::min<uint64_t>((nvec + tile4 - 1) / tile4, max_blocks),
+                                                  (n - nvec * V + kBlock - 1) / kBlock);
+      const bool narrow4 = p.c0 + nvec + tile4 < (1ull << 32) && blocks4 * tile4 + nvec < (1ull << 32);
+      if (narrow4)
+        hipLaunchKernelGGL(synth_special_kernel<true>, dim3((unsigned)blocks4), dim3(kBlock), 0, stream, p, nvec, n,
+                           (u32x4 *)out, r4);
       else
-        hipLaunchKernelGGL(synth_special_kernel<false>, dim3((unsigned)tblocks), dim3(kBlock), 0, stream, p, nvec, n,
-                           (u32x4 *)out, rounds);
+        hipLaunchKernelGGL(synth_special_kernel<false>, dim3((unsigned)blocks4), dim3(kBlock), 0, stream, p, nvec, n,
+                           (u32x4 *)out, r4);
       return hipGetLastError();
     }
+    const bool narrow = p.c0 + (nvec + tile) * B < (1ull << 32) && tblocks * tile + nvec < (1ull << 32);
     if (narrow)
       hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, true>), dim3((unsigned)tblocks), dim3(kBlock), 0, stream, p,
                          nvec, n, (u32x4 *)out, rounds);
