@@ -37,8 +37,8 @@ namespace sv {
 #ifndef SV_SYNTH_BLOCKS_PER_CU
 #define SV_SYNTH_BLOCKS_PER_CU 64    // synthesis workgroups per CU
 #endif
-#ifndef SV_SYNTH_NT_STORE
-#define SV_SYNTH_NT_STORE 0          // 1: non-temporal output stores
+#ifndef SV_SYNTH_NT_BYTES
+#define SV_SYNTH_NT_BYTES (1ull << 30)   // single-tensor outputs of at least this many bytes: non-temporal stores
 #endif
 
 constexpr int kBlock = 256;          // threads per workgroup of every streaming kernel

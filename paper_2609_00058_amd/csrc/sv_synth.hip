@@ -129,6 +129,23 @@ __device__ __forceinline__ void values_of(const SynthParams &p, uint64_t block, 
   }
 }
 
+// One 16-byte output vector.  Outputs much larger than the 256 MB Infinity
+// Cache are written with non-temporal stores (p.nt, set per launch): cached
+// stores leave the output's last-written part in the caches, and the check
+// that reads it next measured 8-12 % slower for it (2^30 fp32:
+// 1422 against 1241 us after a normal-value synthesis, 1452 against 1307 us
+// after special values); outputs that fit the cache keep cached stores, so
+// that the check finds them there (2^26 fp32 pairs: 4702 against 4631 GB/s).
+// (A compile-time choice: with a run-time branch the compiler merges the two
+// stores into one plain store.)
+template <bool kNT>
+__device__ __forceinline__ void store_vec(u32x4 *out, uint64_t u, const u32x4 &o) {
+  if constexpr (kNT)
+    __builtin_nontemporal_store(o, out + u);
+  else
+    out[u] = o;
+}
+
 // Two elements as bf16 in one word.  Uniform and normal values are never
 // NaN, so the hardware conversion applies; special values go through
 // bf16_rne and its NaN rule.
@@ -156,7 +173,7 @@ __device__ __forceinline__ void store_elem(void *out, uint64_t i, uint32_t x) {
 // every block index and byte offset of the launch fits 32 bits (the launch
 // checks), so the loop counts, the Philox counter and the addresses are
 // 32-bit (the counter's high word is 0).
-template <int DIST, int DT, bool kNarrow>
+template <int DIST, int DT, bool kNarrow, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                            u32x4 *__restrict__ out, uint32_t rounds) {
   constexpr int E = PerBlock<DIST, DT>::E;
@@ -182,10 +199,7 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
     } else {
       o = u32x4{v[0], v[1], v[2], v[3]};
     }
-    if constexpr (SV_SYNTH_NT_STORE)
-      __builtin_nontemporal_store(o, out + u);
-    else
-      out[u] = o;
+    store_vec<kNT>(out, u, o);
   }
   const uint64_t i = nvec * V + (uint64_t)gid;
   if (i < n) {
@@ -228,7 +242,7 @@ __device__ __forceinline__ u32x4 overlay_values(const SynthParams &p, const u32x
   return u32x4{v[0], v[1], v[2], v[3]};
 }
 
-template <bool kNarrow>
+template <bool kNarrow, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                                u32x4 *__restrict__ out, uint32_t rounds) {
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
@@ -288,7 +302,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
         v[g].z = (m & 4u) ? sv.z : v[g].z;
         v[g].w = (m & 8u) ? sv.w : v[g].w;
       }
-      if (u < (Idx)nvec) out[u] = v[g];
+      if (u < (Idx)nvec) store_vec<kNT>(out, u, v[g]);
     }
     // the list is rewritten by the next group only after every lane has read it
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -318,8 +332,10 @@ __global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint6
 }
 
 template <int DIST, int DT>
-static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
+static hipError_t launch_typed(const SynthParams &p0, uint64_t n, void *out, int cus, hipStream_t stream) {
   constexpr uint64_t V = DT == SV_BF16 ? 8 : 4;
+  const SynthParams &p = p0;
+  const bool nt = n * (16 / V) >= SV_SYNTH_NT_BYTES;
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
   if (((uintptr_t)out & 15u) == 0 && p.e0 % PerBlock<DIST, DT>::E == 0) {
     const uint64_t nvec = n / V;
@@ -335,21 +351,27 @@ static hipError_t launch_typed(const SynthParams &p, uint64_t n, void *out, int 
       const uint64_t blocks4 = std::max<uint64_t>(std::min<uint64_t>((nvec + tile4 - 1) / tile4, max_blocks),
                                                   (n - nvec * V + kBlock - 1) / kBlock);
       const bool narrow4 = p.c0 + nvec + tile4 < (1ull << 32) && blocks4 * tile4 + nvec < (1ull << 32);
-      if (narrow4)
-        hipLaunchKernelGGL(synth_special_kernel<true>, dim3((unsigned)blocks4), dim3(kBlock), 0, stream, p, nvec, n,
-                           (u32x4 *)out, r4);
+      const dim3 g4((unsigned)blocks4), b4(kBlock);
+      if (narrow4 && nt)
+        hipLaunchKernelGGL((synth_special_kernel<true, true>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
+      else if (narrow4)
+        hipLaunchKernelGGL((synth_special_kernel<true, false>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
+      else if (nt)
+        hipLaunchKernelGGL((synth_special_kernel<false, true>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
       else
-        hipLaunchKernelGGL(synth_special_kernel<false>, dim3((unsigned)blocks4), dim3(kBlock), 0, stream, p, nvec, n,
-                           (u32x4 *)out, r4);
+        hipLaunchKernelGGL((synth_special_kernel<false, false>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
       return hipGetLastError();
     }
     const bool narrow = p.c0 + (nvec + tile) * B < (1ull << 32) && tblocks * tile + nvec < (1ull << 32);
-    if (narrow)
-      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, true>), dim3((unsigned)tblocks), dim3(kBlock), 0, stream, p,
-                         nvec, n, (u32x4 *)out, rounds);
+    const dim3 g((unsigned)tblocks), b(kBlock);
+    if (narrow && nt)
+      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, true, true>), g, b, 0, stream, p, nvec, n, (u32x4 *)out, rounds);
+    else if (narrow)
+      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, true, false>), g, b, 0, stream, p, nvec, n, (u32x4 *)out, rounds);
+    else if (nt)
+      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, false, true>), g, b, 0, stream, p, nvec, n, (u32x4 *)out, rounds);
     else
-      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, false>), dim3((unsigned)tblocks), dim3(kBlock), 0, stream, p,
-                         nvec, n, (u32x4 *)out, rounds);
+      hipLaunchKernelGGL((synth_vec_kernel<DIST, DT, false, false>), g, b, 0, stream, p, nvec, n, (u32x4 *)out, rounds);
   } else {
     const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, max_blocks);
     hipLaunchKernelGGL((synth_elem_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n, out);
@@ -436,7 +458,7 @@ __device__ __forceinline__ uint64_t wide_elem(const SynthParams &p, uint64_t g) 
 // block, so that no Philox word is wasted.  Then the n - groups W ragged tail
 // elements, one per thread of the first threads of the grid (the window
 // starts on a block).
-template <int DIST, int DT>
+template <int DIST, int DT, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_wide_vec_kernel(SynthParams p, uint64_t ngroups, uint64_t n,
                                                                 u32x4 *__restrict__ out) {
   constexpr int E = Wide<DIST, DT>::E, V = Wide<DIST, DT>::V;
@@ -467,7 +489,7 @@ __global__ __launch_bounds__(kBlock) void synth_wide_vec_kernel(SynthParams p, u
       } else {
         o = u32x4{(uint32_t)x[0], (uint32_t)(x[0] >> 32), (uint32_t)x[1], (uint32_t)(x[1] >> 32)};
       }
-      out[g * G + j] = o;
+      store_vec<kNT>(out, g * G + j, o);
     }
   }
   const uint64_t i = ngroups * W + gid;
@@ -482,16 +504,22 @@ __global__ __launch_bounds__(kBlock) void synth_wide_elem_kernel(SynthParams p, 
 }
 
 template <int DIST, int DT>
-static hipError_t launch_wide(const SynthParams &p, uint64_t n, void *out, int cus, hipStream_t stream) {
+static hipError_t launch_wide(const SynthParams &p0, uint64_t n, void *out, int cus, hipStream_t stream) {
   constexpr uint64_t E = Wide<DIST, DT>::E, V = Wide<DIST, DT>::V;
+  const SynthParams &p = p0;
+  const bool nt = n * (16 / V) >= SV_SYNTH_NT_BYTES;
   constexpr uint64_t W = V >= E ? V : E;          // elements per group of vectors
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
   if (((uintptr_t)out & 15u) == 0 && p.e0 % E == 0) {
     const uint64_t ngroups = n / W;
     const uint64_t threads = std::max<uint64_t>(ngroups, n - ngroups * W);   // the tail needs < W threads
     const uint64_t blocks = std::min<uint64_t>((threads + kBlock - 1) / kBlock, max_blocks);
-    hipLaunchKernelGGL((synth_wide_vec_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
-                       ngroups, n, (u32x4 *)out);
+    if (nt)
+      hipLaunchKernelGGL((synth_wide_vec_kernel<DIST, DT, true>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
+                         ngroups, n, (u32x4 *)out);
+    else
+      hipLaunchKernelGGL((synth_wide_vec_kernel<DIST, DT, false>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p,
+                         ngroups, n, (u32x4 *)out);
   } else {
     const uint64_t blocks = std::min<uint64_t>((n + kBlock - 1) / kBlock, max_blocks);
     hipLaunchKernelGGL((synth_wide_elem_kernel<DIST, DT>), dim3((unsigned)blocks), dim3(kBlock), 0, stream, p, n,
