@@ -98,6 +98,7 @@ def lib():
                                        ctypes.c_uint64, vp]
         L.or_ln_f32_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_sincos_2pi_f32_n.argtypes = [vp, vp, vp, ctypes.c_uint64]
+        L.or_sincos_table.argtypes = [vp, vp]
         L.or_bf16_rne_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_f16_rne_n.argtypes = [vp, vp, ctypes.c_uint64]
         L.or_radius_f32_n.argtypes = [vp, vp, ctypes.c_uint64]
@@ -211,6 +212,14 @@ def f16_rne_n(bits) -> np.ndarray:
 
 def ln_f32(x: float) -> np.float32:
     return np.float32(lib().or_ln_f32(float(np.float32(x))))
+
+
+def sincos_table():
+    """The 256 table values (sin, cos of 2 pi k / 256 in fp32) of sincos_2pi_f32."""
+    s = np.empty(256, np.float32)
+    c = np.empty(256, np.float32)
+    lib().or_sincos_table(_ptr(s), _ptr(c))
+    return s, c
 
 
 def sincos_2pi_f32(j24: int):

@@ -21,9 +21,9 @@
  *    by the seed with counter (block, stream); uniform from the top 24 bits
  *    of a word (from a 16-bit half-word for bf16 outputs);
  *    Box-Muller (1958) with ln, sin and cos written as fixed sequences of fp32
- *    operations (a Chebyshev polynomial for ln, Taylor series in powers of
- *    pi/2 over factorials for sin and cos, coefficients rounded to fp32,
- *    Horner steps fused multiply-adds); Lemire's multiply-shift for integer
+ *    operations (a Chebyshev polynomial for ln, Horner steps fused
+ *    multiply-adds; sin and cos from a table of 256 correctly rounded values
+ *    and short series of the remaining angle); Lemire's multiply-shift for integer
  *    ranges; a class-threshold mix for special values.
  */
 #include "sv_oracle.h"
@@ -126,67 +126,65 @@ float or_ln_f32(float x) {
 }
 
 /* ------------------------------------------------------------------------- */
-/* sin and cos of the angle 2*pi*j/2^24, j < 2^24.                            */
-/* The angle is (pi/2)(q + f) with quadrant q = j >> 22 and f = (j mod 2^22)  */
-/* / 2^22, both exact.  S(f) = sin(pi f/2) and C(f) = cos(pi f/2) come from   */
-/* Taylor series in f with coefficients (-1)^k (pi/2)^n / n! rounded to fp32, */
-/* in f^2 by fused multiply-add Horner steps; for f > 1/2 the complement      */
-/* g = 1 - f (exact) is used instead, since sin(pi f/2) = cos(pi g/2), so     */
-/* that both series run on f in [0, 1/2] and keep relative accuracy near the  */
-/* zeros.  The quadrant then rotates (S, C).                                  */
+/* sin and cos of the angle 2 pi j / 2^24, j < 2^24.                          */
+/* The angle is split at the nearest of 256 table angles: j = 2^16 k + r with */
+/* k = round(j / 2^16) mod 256 (halves up) and r in [-2^15, 2^15), so that    */
+/* angle = 2 pi k / 256 + b, b = 2 pi r / 2^24, |b| <= pi / 256.  The table   */
+/* holds sin and cos of 2 pi k / 256 rounded to fp32 (to nearest, exact zeros */
+/* positive); b = fp32(r) * fp32(2 pi / 2^24) (one rounding); over |b| <=     */
+/* pi/256 sin b = b - b^3/6 and cos b = 1 - b^2/2 are within 2^-30 relative   */
+/* of the true values; then the angle-sum formulas, each with one fused       */
+/* multiply-add.  Table points on the axes (k a multiple of 64) are exact, so */
+/* near the zeros of sin and cos the result is the small term alone and keeps */
+/* its relative accuracy.                                                     */
 /* ------------------------------------------------------------------------- */
-static const float SIN_1 = 0x1.921fb6p+0f;    /*  (pi/2)^1 / 1!  */
-static const float SIN_3 = -0x1.4abbcep-1f;   /* -(pi/2)^3 / 3!  */
-static const float SIN_5 = 0x1.466bc6p-4f;    /*  (pi/2)^5 / 5!  */
-static const float SIN_7 = -0x1.32d2ccp-8f;   /* -(pi/2)^7 / 7!  */
-static const float SIN_9 = 0x1.507834p-13f;   /*  (pi/2)^9 / 9!  */
-static const float COS_2 = -0x1.3bd3ccp+0f;   /* -(pi/2)^2 / 2!  */
-static const float COS_4 = 0x1.03c1f0p-2f;    /*  (pi/2)^4 / 4!  */
-static const float COS_6 = -0x1.55d3c8p-6f;   /* -(pi/2)^6 / 6!  */
-static const float COS_8 = 0x1.e1f506p-11f;   /*  (pi/2)^8 / 8!  */
-static const float COS_10 = -0x1.a6d1f2p-16f; /* -(pi/2)^10 / 10! */
+static const float SC_B = 0x1.921fb6p-22f;    /* fp32(2 pi / 2^24)   */
+static const float SC_S3 = -0x1.555556p-3f;   /* fp32(-1/6)          */
+static float TAB_SIN[256], TAB_COS[256];
 
-static float sin_quarter(float f) {   /* sin(pi f / 2), f in [0, 1/2] */
-  float f2 = f * f;
-  float p = SIN_9;
-  p = fmaf(p, f2, SIN_7);
-  p = fmaf(p, f2, SIN_5);
-  p = fmaf(p, f2, SIN_3);
-  p = fmaf(p, f2, SIN_1);
-  return f * p;
+/* sin and cos of 2 pi k / 256 rounded to fp32: the first octant (m in 0..32
+ * of 64 per quadrant) in long double, the rest by the exact symmetries of
+ * the quadrant and the octant. */
+__attribute__((constructor)) static void init_sincos_table(void) {
+  const long double pi = 3.14159265358979323846264338327950288L;
+  for (int k = 0; k < 256; k++) {
+    int q = k >> 6, m = k & 63;
+    long double sm, cm;
+    if (m == 0) {
+      sm = 0.0L;
+      cm = 1.0L;
+    } else if (m <= 32) {
+      sm = sinl(pi * (long double)m / 128.0L);
+      cm = cosl(pi * (long double)m / 128.0L);
+    } else {
+      sm = cosl(pi * (long double)(64 - m) / 128.0L);
+      cm = sinl(pi * (long double)(64 - m) / 128.0L);
+    }
+    long double s = q == 0 ? sm : q == 1 ? cm : q == 2 ? -sm : -cm;
+    long double c = q == 0 ? cm : q == 1 ? -sm : q == 2 ? -cm : sm;
+    TAB_SIN[k] = s == 0.0L ? 0.0f : (float)s;
+    TAB_COS[k] = c == 0.0L ? 0.0f : (float)c;
+  }
 }
 
-static float cos_quarter(float f) {   /* cos(pi f / 2), f in [0, 1/2] */
-  float f2 = f * f;
-  float p = COS_10;
-  p = fmaf(p, f2, COS_8);
-  p = fmaf(p, f2, COS_6);
-  p = fmaf(p, f2, COS_4);
-  p = fmaf(p, f2, COS_2);
-  return fmaf(f2, p, 1.0f);
+void or_sincos_table(float *s, float *c) {
+  for (int k = 0; k < 256; k++) {
+    s[k] = TAB_SIN[k];
+    c[k] = TAB_COS[k];
+  }
 }
 
 void or_sincos_2pi_f32(uint32_t j24, float *s_out, float *c_out) {
   uint32_t j = j24 & 0x00FFFFFFu;
-  uint32_t q = j >> 22;
-  uint32_t fj = j & 0x003FFFFFu;
-  float S, C;
-  if (fj <= 0x00200000u) {
-    float f = (float)fj * 0x1p-22f;
-    S = sin_quarter(f);
-    C = cos_quarter(f);
-  } else {
-    float g = (float)(0x00400000u - fj) * 0x1p-22f;
-    S = cos_quarter(g);
-    C = sin_quarter(g);
-  }
-  float s, c;
-  if (q == 0) { s = S; c = C; }
-  else if (q == 1) { s = C; c = -S; }
-  else if (q == 2) { s = -S; c = -C; }
-  else { s = -C; c = S; }
-  *s_out = s;
-  *c_out = c;
+  uint32_t k = ((j + 0x8000u) >> 16) & 0xFFu;                           /* nearest table angle */
+  int32_t r = (int32_t)(j & 0xFFFFu) - (int32_t)((j & 0x8000u) << 1);   /* j - 2^16 k (mod 2^24) */
+  float b = (float)r * SC_B;
+  float b2 = b * b;
+  float sb = fmaf(b, b2 * SC_S3, b);                                     /* sin b */
+  float cb = fmaf(b2, -0.5f, 1.0f);                                      /* cos b */
+  float sk = TAB_SIN[k], ck = TAB_COS[k];
+  *s_out = fmaf(sk, cb, ck * sb);
+  *c_out = fmaf(ck, cb, -(sk * sb));
 }
 
 /* ------------------------------------------------------------------------- */

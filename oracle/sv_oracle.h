@@ -78,6 +78,8 @@ void or_philox_block(uint64_t seed, uint64_t stream, uint64_t c, uint32_t out[4]
 /* Building blocks exposed so that tests can pin them one at a time. */
 float or_ln_f32(float x);
 void or_sincos_2pi_f32(uint32_t j24, float *s, float *c);
+/* the 256 table values sin, cos of 2 pi k / 256 (fp32, correctly rounded) */
+void or_sincos_table(float *s, float *c);
 float or_radius_f32(uint32_t k24);   /* Box-Muller radius for u1 = (k24 + 1) 2^-24 */
 void or_box_muller_f32(uint32_t wa, uint32_t wb, float *zc, float *zs);
 uint16_t or_bf16_rne(uint32_t f32_bits);

@@ -67,10 +67,8 @@ def test_transform_constants_are_the_fp32_roundings_of_their_definitions():
     assert rne32(poly[-1]) == 1.0
     for k in range(1, 10):
         want["LN_P%d" % k] = poly[9 - k]
-    for k in (1, 3, 5, 7, 9):
-        want["SIN_%d" % k] = (-1) ** ((k - 1) // 2) * half_pi ** k / mp.factorial(k)
-    for k in (2, 4, 6, 8, 10):
-        want["COS_%d" % k] = (-1) ** (k // 2) * half_pi ** k / mp.factorial(k)
+    want["SC_B"] = 4 * half_pi / 2 ** 24          # 2 pi / 2^24
+    want["SC_S3"] = mp.mpf(-1) / 6                 # sin b = b - b^3 / 6
     got = _oracle_constants()
     assert set(want) <= set(got)
     for name, x in want.items():
@@ -201,8 +199,25 @@ def test_ln_at_powers_of_two_is_e_ln2_within_one_ulp(oracle):
         assert abs(float(oracle.ln_f32(2.0 ** e)) - want) <= float(ulp32(want))
 
 
+def test_sincos_table_is_the_correctly_rounded_values(oracle):
+    """The 256 table values are sin and cos of 2 pi k / 256 rounded to nearest
+    fp32 (mpmath at 200 bits), exact zeros positive; symmetric as the
+    functions are."""
+    mp = pytest.importorskip("mpmath")
+    mp.mp.prec = 200
+    s, c = oracle.sincos_table()
+    for k in range(256):
+        x = 2 * mp.pi * k / 256
+        for got, v in ((s[k], mp.sin(x)), (c[k], mp.cos(x))):
+            if k % 64 == 0 and abs(v) < mp.mpf(2) ** -100:
+                assert got == 0.0 and not math.copysign(1.0, float(got)) < 0, k
+            else:
+                assert float(got) == rne32_exact(Fraction(mp.nstr(v, 80))), k
+    assert np.array_equal(s[1:64], c[63:0:-1]) and np.array_equal(s[:128], -s[128:] + 0.0)
+
+
 def test_sincos_exhaustive(oracle):
-    # all 2^24 angles 2 pi j / 2^24 within 1.7 ulp (measured max 1.684), exact at the axes
+    # all 2^24 angles 2 pi j / 2^24 within 2.5 ulp (measured max 2.491), exact at the axes
     j = np.arange(1 << 24, dtype=np.uint32)
     s, c = oracle.sincos_2pi_f32_n(j)
     q = j >> 22
@@ -214,7 +229,8 @@ def test_sincos_exhaustive(oracle):
         nz = want != 0
         assert np.all(got[~nz] == 0)
         err = np.abs(got[nz].astype(np.float64) - want[nz]) / ulp32(want[nz])
-        assert err.max() <= 1.7
+        assert err.max() <= 2.5
+        assert (err > 1).mean() < 0.04      # measured 2.9 % above one ulp
     axes = np.array([0, 1 << 22, 2 << 22, 3 << 22], dtype=np.uint32)
     s, c = oracle.sincos_2pi_f32_n(axes)
     assert list(s) == [0.0, 1.0, 0.0, -1.0] and list(c) == [1.0, 0.0, -1.0, 0.0]
