@@ -146,42 +146,83 @@ __device__ __forceinline__ float sqrt_rn(float v) {
   return s;
 }
 
-// sin(pi f / 2) and cos(pi f / 2) for f in [0, 1/2]: Taylor series in f whose
-// coefficients are (-1)^k (pi/2)^n / n! rounded to fp32, Horner in f^2 with
-// fused multiply-adds.
-__device__ __forceinline__ float sin_q(float f, float f2) {
-  float p = 0x1.507834p-13f;                     //  (pi/2)^9 / 9!
-  p = __builtin_fmaf(p, f2, -0x1.32d2ccp-8f);    // -(pi/2)^7 / 7!
-  p = __builtin_fmaf(p, f2, 0x1.466bc6p-4f);     //  (pi/2)^5 / 5!
-  p = __builtin_fmaf(p, f2, -0x1.4abbcep-1f);    // -(pi/2)^3 / 3!
-  p = __builtin_fmaf(p, f2, 0x1.921fb6p+0f);     //  pi/2
-  return f * p;
+// ---------------------------------------------------------------------------
+// sin and cos of 2 pi j / 2^24 for j < 2^24: j = 2^16 k + r at the nearest of
+// 256 table angles (k = round(j / 2^16) mod 256, r in [-2^15, 2^15) the low
+// half of j as a signed 16-bit number), b = fp32(r) fp32(2 pi / 2^24),
+// sin b = b + b (b^2 fp32(-1/6)), cos b = 1 - b^2 / 2 (within 2^-30 of the
+// true values for |b| <= pi / 256), then the angle-sum formulas, one fused
+// multiply-add each.  The table holds sin and cos of 2 pi k / 256 rounded to
+// nearest fp32 (exact zeros positive); it lives in LDS, filled at the start of
+// every kernel that draws normal values (load_sincos_table).
+// ---------------------------------------------------------------------------
+static __shared__ f32x2_t sincos_tab[256];
+
+// sin x and cos x for 0 <= x <= pi / 4 in fp64: Taylor series through x^19
+// and x^20 (the first omitted terms are below 2^-60 relative).
+__device__ inline double sin_series_f64(double x) {
+  const double x2 = x * x;
+  double p = 1.0 / 121645100408832000.0;                 // 1 / 19!
+  p = __builtin_fma(p, -x2, 1.0 / 355687428096000.0);    // 1 / 17!
+  p = __builtin_fma(p, -x2, 1.0 / 1307674368000.0);      // 1 / 15!
+  p = __builtin_fma(p, -x2, 1.0 / 6227020800.0);         // 1 / 13!
+  p = __builtin_fma(p, -x2, 1.0 / 39916800.0);           // 1 / 11!
+  p = __builtin_fma(p, -x2, 1.0 / 362880.0);             // 1 / 9!
+  p = __builtin_fma(p, -x2, 1.0 / 5040.0);               // 1 / 7!
+  p = __builtin_fma(p, -x2, 1.0 / 120.0);                // 1 / 5!
+  p = __builtin_fma(p, -x2, 1.0 / 6.0);                  // 1 / 3!
+  p = __builtin_fma(p, -x2, 1.0);
+  return x * p;
 }
 
-__device__ __forceinline__ float cos_q(float f2) {
-  float p = -0x1.a6d1f2p-16f;                    // -(pi/2)^10 / 10!
-  p = __builtin_fmaf(p, f2, 0x1.e1f506p-11f);    //  (pi/2)^8 / 8!
-  p = __builtin_fmaf(p, f2, -0x1.55d3c8p-6f);    // -(pi/2)^6 / 6!
-  p = __builtin_fmaf(p, f2, 0x1.03c1f0p-2f);     //  (pi/2)^4 / 4!
-  p = __builtin_fmaf(p, f2, -0x1.3bd3ccp+0f);    // -(pi/2)^2 / 2!
-  return __builtin_fmaf(f2, p, 1.0f);
+__device__ inline double cos_series_f64(double x) {
+  const double x2 = x * x;
+  double p = 1.0 / 2432902008176640000.0;                // 1 / 20!
+  p = __builtin_fma(p, -x2, 1.0 / 6402373705728000.0);   // 1 / 18!
+  p = __builtin_fma(p, -x2, 1.0 / 20922789888000.0);     // 1 / 16!
+  p = __builtin_fma(p, -x2, 1.0 / 87178291200.0);        // 1 / 14!
+  p = __builtin_fma(p, -x2, 1.0 / 479001600.0);          // 1 / 12!
+  p = __builtin_fma(p, -x2, 1.0 / 3628800.0);            // 1 / 10!
+  p = __builtin_fma(p, -x2, 1.0 / 40320.0);              // 1 / 8!
+  p = __builtin_fma(p, -x2, 1.0 / 720.0);                // 1 / 6!
+  p = __builtin_fma(p, -x2, 1.0 / 24.0);                 // 1 / 4!
+  p = __builtin_fma(p, -x2, 1.0 / 2.0);                  // 1 / 2!
+  return __builtin_fma(p, -x2, 1.0);
 }
 
-// sin and cos of 2 pi j / 2^24 for j < 2^24: quadrant q = j >> 22, fraction
-// f = (j mod 2^22) / 2^22; above f = 1/2 the series run on the exact
-// complement 1 - f.  The magnitudes are the two series values, exchanged when
-// exactly one of "odd quadrant" and "complement" holds; sine is negative in
-// quadrants 2 and 3, cosine in 1 and 2 (sign bits set by XOR, as negation).
+// Entry k of the table: the first octant (m in 0..32 of the 64 steps of a
+// quadrant) from the series, the rest by the exact symmetries of the octant
+// and the quadrant; fp64 rounded to nearest fp32.
+__device__ inline f32x2_t sincos_entry(uint32_t k) {
+  const uint32_t q = k >> 6, m = k & 63u;
+  double sm = 0.0, cm = 1.0;
+  if (m != 0u) {
+    const double x = (double)(m <= 32u ? m : 64u - m) * (3.141592653589793 / 128.0);
+    const double sx = sin_series_f64(x), cx = cos_series_f64(x);
+    sm = m <= 32u ? sx : cx;
+    cm = m <= 32u ? cx : sx;
+  }
+  const double sv = q == 0 ? sm : q == 1 ? cm : q == 2 ? -sm : -cm;
+  const double cv = q == 0 ? cm : q == 1 ? -sm : q == 2 ? -cm : sm;
+  return f32x2_t{sv == 0.0 ? 0.0f : (float)sv, cv == 0.0 ? 0.0f : (float)cv};
+}
+
+// Fills the table; reached by every thread of the workgroup, before any use.
+__device__ inline void load_sincos_table() {
+  for (uint32_t k = threadIdx.x; k < 256u; k += blockDim.x) sincos_tab[k] = sincos_entry(k);
+  __syncthreads();
+}
+
 __device__ __forceinline__ void sincos_2pi(uint32_t j, float &s, float &c) {
-  const uint32_t q = j >> 22;
-  const uint32_t fj = j & 0x003FFFFFu;
-  const bool upper = fj > 0x00200000u;
-  const float f = (float)(upper ? 0x00400000u - fj : fj) * 0x1p-22f;
-  const float f2 = f * f;
-  const float a = sin_q(f, f2), b = cos_q(f2);
-  const bool swap = ((q & 1u) != 0u) != upper;
-  s = as_f32(as_u32(swap ? b : a) ^ ((q & 2u) << 30));
-  c = as_f32(as_u32(swap ? a : b) ^ (((q + 1u) & 2u) << 30));
+  const uint32_t k = ((j + 0x8000u) >> 16) & 0xFFu;
+  const int32_t r = (int32_t)(int16_t)(uint16_t)(j & 0xFFFFu);
+  const float b = (float)r * 0x1.921fb6p-22f;          // fp32(2 pi / 2^24)
+  const float b2 = b * b;
+  const float sb = __builtin_fmaf(b, b2 * -0x1.555556p-3f, b);   // fp32(-1/6)
+  const float cb = __builtin_fmaf(b2, -0.5f, 1.0f);
+  const f32x2_t t = sincos_tab[k];
+  s = __builtin_fmaf(t.x, cb, t.y * sb);
+  c = __builtin_fmaf(t.y, cb, -(t.x * sb));
 }
 
 // Box-Muller pair from two words: u1 = ((wa >> 8) + 1) 2^-24 in (0, 1],

@@ -24,6 +24,14 @@
 namespace sv {
 
 template <int DIST> struct DistTraits;
+
+// Kernels that draw normal values (normal and special distributions) fill the
+// sine / cosine table of the Box-Muller transform first, every thread of the
+// workgroup taking part.
+template <int DIST>
+__device__ __forceinline__ void prepare_distribution() {
+  if constexpr (DIST == SV_NORMAL || DIST == SV_SPECIAL) load_sincos_table();
+}
 template <> struct DistTraits<SV_UNIFORM> { static constexpr int E = 4; };
 template <> struct DistTraits<SV_NORMAL> { static constexpr int E = 4; };
 template <> struct DistTraits<SV_INT_RANGE> { static constexpr int E = 2; };
@@ -176,6 +184,7 @@ __device__ __forceinline__ void store_elem(void *out, uint64_t i, uint32_t x) {
 template <int DIST, int DT, bool kNarrow, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                            u32x4 *__restrict__ out, uint32_t rounds) {
+  prepare_distribution<DIST>();
   constexpr int E = PerBlock<DIST, DT>::E;
   constexpr int V = DT == SV_BF16 ? 8 : 4;   // elements per 16-byte vector
   constexpr int B = V / E;                   // Philox blocks per vector
@@ -245,6 +254,7 @@ __device__ __forceinline__ u32x4 overlay_values(const SynthParams &p, const u32x
 template <bool kNarrow, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                                u32x4 *__restrict__ out, uint32_t rounds) {
+  load_sincos_table();
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
   constexpr int kWaves = kBlock / kWave;
   constexpr uint32_t kSlots = kGroup * kWave;     // every vector of a group may be a candidate
@@ -321,6 +331,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
 // Every element, one per thread (outputs that are not 16-byte aligned).
 template <int DIST, int DT>
 __global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint64_t n, void *__restrict__ out) {
+  prepare_distribution<DIST>();
   constexpr int E = PerBlock<DIST, DT>::E;
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
@@ -461,6 +472,7 @@ __device__ __forceinline__ uint64_t wide_elem(const SynthParams &p, uint64_t g) 
 template <int DIST, int DT, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_wide_vec_kernel(SynthParams p, uint64_t ngroups, uint64_t n,
                                                                 u32x4 *__restrict__ out) {
+  prepare_distribution<DIST>();
   constexpr int E = Wide<DIST, DT>::E, V = Wide<DIST, DT>::V;
   constexpr int G = V >= E ? 1 : E / V;
   constexpr int W = G * V;
@@ -498,6 +510,7 @@ __global__ __launch_bounds__(kBlock) void synth_wide_vec_kernel(SynthParams p, u
 
 template <int DIST, int DT>
 __global__ __launch_bounds__(kBlock) void synth_wide_elem_kernel(SynthParams p, uint64_t n, void *__restrict__ out) {
+  prepare_distribution<DIST>();
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride)
     store_wide<DT>(out, i, wide_elem<DIST, DT>(p, p.e0 + i));
@@ -624,6 +637,7 @@ hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint6
 // ------------------------------------------------------------ diagnostics
 __global__ __launch_bounds__(kBlock) void eval_transform_kernel(int32_t which, const uint32_t *__restrict__ in,
                                                                 uint64_t n, uint32_t *__restrict__ out) {
+  load_sincos_table();
   const uint64_t stride = (uint64_t)gridDim.x * kBlock;
   for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride) {
     if (which == SV_EVAL_F16) {
@@ -746,6 +760,7 @@ __device__ __forceinline__ void synth_tile(const SynthJob &job, uint64_t u0, uin
 // the GPU.
 __global__ __launch_bounds__(kBlock) void synth_batched_kernel(const SynthJob *__restrict__ jobs, uint32_t njobs,
                                                                uint64_t total_tiles, uint32_t rounds) {
+  load_sincos_table();   // the jobs may draw normal values
   uint32_t j = 0;
   uint64_t lo = 1, hi = 0;           // tiles [lo, hi) belong to job j (none yet)
   for (uint64_t t = blockIdx.x; t < total_tiles; t += gridDim.x) {
