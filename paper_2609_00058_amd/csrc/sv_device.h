@@ -53,8 +53,38 @@ __device__ __forceinline__ u32x4 philox_block(const Key &key, uint64_t block) {
     x0 = n0;
     x2 = n2;
   }
+  {
+    // second round: word 1 is the low half of the first round's uniform
+    // product, so (word 1 ^ key) is one scalar and a plain XOR leaves the
+    // compiler free to keep uniform operands scalar
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+    const uint64_t a = (uint64_t)0xD2511F53u * x0;
+    const uint64_t b = (uint64_t)0xCD9E8D57u * x2;
+    const uint32_t n0 = (uint32_t)(b >> 32) ^ (x1 ^ k0);
+    const uint32_t n2 = ((uint32_t)(a >> 32) ^ k1) ^ x3;
+    x1 = (uint32_t)b;
+    x3 = (uint32_t)a;
+    x0 = n0;
+    x2 = n2;
+  }
+  {
+    // third round: in a launch whose block indices stay below 2^32, word 3
+    // (the low half of the second round's product of a uniform word) is
+    // uniform too; a plain XOR costs no more when it is not
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+    const uint64_t a = (uint64_t)0xD2511F53u * x0;
+    const uint64_t b = (uint64_t)0xCD9E8D57u * x2;
+    const uint32_t n0 = xor3((uint32_t)(b >> 32), x1, k0);
+    const uint32_t n2 = (uint32_t)(a >> 32) ^ (x3 ^ k1);
+    x1 = (uint32_t)b;
+    x3 = (uint32_t)a;
+    x0 = n0;
+    x2 = n2;
+  }
 #pragma unroll
-  for (int r = 1; r < 10; ++r) {
+  for (int r = 3; r < 10; ++r) {
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
     const uint64_t a = (uint64_t)0xD2511F53u * x0;
@@ -67,6 +97,15 @@ __device__ __forceinline__ u32x4 philox_block(const Key &key, uint64_t block) {
     x2 = n2;
   }
   return u32x4{x0, x1, x2, x3};
+}
+
+// A wave-uniform value copied once into a vector register: for an operand
+// that a loop would otherwise move there again on every iteration (a VOP3
+// instruction reads at most one scalar register).
+__device__ __forceinline__ float in_vgpr(float x) {
+  float r;
+  asm("v_mov_b32 %0, %1" : "=v"(r) : "s"(x));
+  return r;
 }
 
 // ---------------------------------------------------------------------------
@@ -213,9 +252,12 @@ __device__ inline void load_sincos_table() {
   __syncthreads();
 }
 
-__device__ __forceinline__ void sincos_2pi(uint32_t j, float &s, float &c) {
-  const uint32_t k = ((j + 0x8000u) >> 16) & 0xFFu;
-  const int32_t r = (int32_t)(int16_t)(uint16_t)(j & 0xFFFFu);
+// j = w >> 8 for a 32-bit word w: k = ((j + 2^15) >> 16) mod 256 is the top
+// byte of w + 2^23 (the carry out of bit 31 is the mod 256), and r is bits
+// 8..23 of w as a signed number.
+__device__ __forceinline__ void sincos_2pi_word(uint32_t w, float &s, float &c) {
+  const uint32_t k = (w + 0x800000u) >> 24;
+  const int32_t r = (int32_t)(int16_t)(uint16_t)(w >> 8);
   const float b = (float)r * 0x1.921fb6p-22f;          // fp32(2 pi / 2^24)
   const float b2 = b * b;
   const float sb = __builtin_fmaf(b, b2 * -0x1.555556p-3f, b);   // fp32(-1/6)
@@ -225,17 +267,47 @@ __device__ __forceinline__ void sincos_2pi(uint32_t j, float &s, float &c) {
   c = __builtin_fmaf(t.y, cb, -(t.x * sb));
 }
 
+__device__ __forceinline__ void sincos_2pi(uint32_t j, float &s, float &c) {   // j < 2^24
+  sincos_2pi_word(j << 8, s, c);
+}
+
 // Box-Muller pair from two words: u1 = ((wa >> 8) + 1) 2^-24 in (0, 1],
 // u2 = (wb >> 8) 2^-24; r = sqrt(-2 ln u1); (r cos 2 pi u2, r sin 2 pi u2).
+//
+// The radius takes ln_f32's steps with two exact rescalings folded in:
+// u1's bits are those of the integer k24 + 1 (converted exactly) less 24 in
+// the exponent field, so the offset subtracted from them absorbs the 2^-24;
+// and -2 ln u1 is ln_f32 with every Horner coefficient and both ln 2 parts
+// times -2 -- scaling by a power of two commutes with each rounding here (no
+// intermediate is denormal or overflows), so the bits equal
+// sqrt_rn(-2 * ln_f32(u1)) for every k24 (compared on all 2^24 of them).
+__device__ __forceinline__ float bm_radicand(uint32_t k24) {
+  const int32_t ix = (int32_t)as_u32((float)(k24 + 1u)) - (0x3F3504F3 + (24 << 23));
+  const float ef = (float)(ix >> 23);
+  const float m = as_f32((uint32_t)(ix & 0x007FFFFF) + 0x3F3504F3u);
+  const float f = m - 1.0f;
+  float p = 0x1.31335ap-3f;                              // -2 x the coefficients of ln_f32
+  p = __builtin_fmaf(p, f, -0x1.064786p-2f);
+  p = __builtin_fmaf(p, f, 0x1.0fb036p-2f);
+  p = __builtin_fmaf(p, f, -0x1.22cf10p-2f);
+  p = __builtin_fmaf(p, f, 0x1.5423b0p-2f);
+  p = __builtin_fmaf(p, f, -0x1.999e86p-2f);
+  p = __builtin_fmaf(p, f, 0x1.000424p-1f);
+  p = __builtin_fmaf(p, f, -0x1.55555ep-1f);
+  p = __builtin_fmaf(p, f, 0x1.fffff8p-1f);
+  p = __builtin_fmaf(p, f, -2.0f);
+  const float lnm = f * p;
+  return __builtin_fmaf(ef, -0x1.62e4p+0f, __builtin_fmaf(ef, -0x1.7f7d1cp-19f, lnm));
+}
+
 __device__ __forceinline__ float bm_radius(uint32_t k24) {   // u1 = (k24 + 1) 2^-24
-  const float u1 = (float)(k24 + 1u) * 0x1p-24f;
-  return sqrt_rn(-2.0f * ln_f32(u1));
+  return sqrt_rn(bm_radicand(k24));
 }
 
 __device__ __forceinline__ void box_muller(uint32_t wa, uint32_t wb, float &zc, float &zs) {
   const float r = bm_radius(wa >> 8);
   float s, c;
-  sincos_2pi(wb >> 8, s, c);
+  sincos_2pi_word(wb, s, c);
   zc = r * c;
   zs = r * s;
 }

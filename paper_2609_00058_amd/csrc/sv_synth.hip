@@ -192,13 +192,12 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
   const Idx gid = (Idx)blockIdx.x * kBlock + threadIdx.x;
   const Idx tile = (Idx)rounds * kBlock;
   const Idx c0 = (Idx)p.c0;
-  for (Idx t0 = (Idx)blockIdx.x * tile; t0 < (Idx)nvec; t0 += (Idx)gridDim.x * tile)
-  for (uint32_t r = 0; r < rounds; ++r) {
-    const Idx u = t0 + (Idx)r * kBlock + threadIdx.x;
-    if (u >= (Idx)nvec) break;
+  SynthParams q = p;
+  if constexpr (DIST == SV_NORMAL) q.mean = in_vgpr(p.mean);   // the addend of mean + std z
+  const auto vector_at = [&](Idx u) {
     uint32_t v[V];
 #pragma unroll
-    for (int b = 0; b < B; ++b) values_of<DIST, DT>(p, (uint64_t)(c0 + u * B + b), v + b * E);
+    for (int b = 0; b < B; ++b) values_of<DIST, DT>(q, (uint64_t)(c0 + u * B + b), v + b * E);
     u32x4 o;
     if constexpr (DT == SV_BF16) {
       o.x = bf16_pair<DIST>(v[0], v[1]);
@@ -209,6 +208,18 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
       o = u32x4{v[0], v[1], v[2], v[3]};
     }
     store_vec<kNT>(out, u, o);
+  };
+  for (Idx t0 = (Idx)blockIdx.x * tile; t0 < (Idx)nvec; t0 += (Idx)gridDim.x * tile) {
+    if (t0 + tile <= (Idx)nvec) {
+      // a whole tile: a uniform trip count and no per-lane bound
+      for (uint32_t r = 0; r < rounds; ++r) vector_at(t0 + (Idx)r * kBlock + threadIdx.x);
+    } else {
+      for (uint32_t r = 0; r < rounds; ++r) {
+        const Idx u = t0 + (Idx)r * kBlock + threadIdx.x;
+        if (u >= (Idx)nvec) break;
+        vector_at(u);
+      }
+    }
   }
   const uint64_t i = nvec * V + (uint64_t)gid;
   if (i < n) {
@@ -225,30 +236,56 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
 // needs the class block as well; rather than every lane computing one
 // whenever any lane of its wave needs it, each lane holds its next kGroup
 // vectors in registers while the wave lists their candidate vectors in LDS
-// (index and candidate bits, about 13 % of them on the special-value
-// stream); then the wave's lanes take the listed vectors 64 at a time, one
-// class block each, and leave the special values in LDS; each lane merges
-// them into its vectors and stores all kGroup of them once, in order.
-// (Storing the candidate vectors late, when a ring of them filled up,
-// measured much slower: cache lines written in two pieces far apart in
-// time; storing them twice, with normal values first, wrote 1.33 times the
-// bytes.)  Loops are uniform across the wave (lanes past the end only
-// compute), so every lane takes part in every pass over the list.
-constexpr uint32_t kGroup = 4;       // vectors a lane holds before their candidates are overlaid
+// (the vector's offset in the tile, its four gate bytes and its normal
+// values; about 13 % of the vectors on the special-value stream); then the
+// wave's lanes take the listed vectors 64 at a time, one class block each,
+// and overwrite the special elements in LDS; each lane reads its listed
+// vectors back and stores all kGroup of them once, in order.  kGroup = 6
+// lists about 51 vectors on that stream, so one pass over the list nearly
+// always covers it and few of its lanes idle.  (Storing the candidate
+// vectors late, when a ring of them filled up, measured much slower: cache
+// lines written in two pieces far apart in time; storing them twice, with
+// normal values first, wrote 1.33 times the bytes.)  Loops are uniform across
+// the wave (lanes past the end only compute), so every lane takes part in
+// every pass over the list.
+#ifndef SV_SPECIAL_GROUP
+#define SV_SPECIAL_GROUP 6
+#endif
+constexpr uint32_t kGroup = SV_SPECIAL_GROUP;   // vectors a lane holds before their candidates are overlaid
 
-// The special values of candidate elements (bits c) given their class words
-// q, and which of them replace the normal value (bits of the result's .w).
-__device__ __forceinline__ u32x4 overlay_values(const SynthParams &p, const u32x4 &q, uint32_t c, uint32_t &m) {
-  uint32_t v[4] = {0u, 0u, 0u, 0u};
-  m = 0u;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    if (((c >> k) & 1u) && q[k] < p.t_zero) {
-      special_overlay(p, q[k], v[k]);
-      m |= 1u << k;
-    }
-  }
-  return u32x4{v[0], v[1], v[2], v[3]};
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// The class thresholds as 32-bit compares: a class word x is at or above
+// threshold t (at most 2^32) iff t < 2^32 and x >= t.
+struct SpecialClasses {
+  uint32_t nan, inf, den, zero;
+  bool nan_all, inf_all, den_all, zero_all;   // t = 2^32: no word reaches it
+};
+
+__device__ __forceinline__ SpecialClasses special_classes(const SynthParams &p) {
+  const auto lo = [](uint64_t t) { return (uint32_t)(t > 0xFFFFFFFFull ? 0xFFFFFFFFull : t); };
+  return SpecialClasses{lo(p.t_nan), lo(p.t_inf), lo(p.t_den), lo(p.t_zero),
+                        p.t_nan > 0xFFFFFFFFull, p.t_inf > 0xFFFFFFFFull, p.t_den > 0xFFFFFFFFull,
+                        p.t_zero > 0xFFFFFFFFull};
+}
+
+__device__ __forceinline__ bool at_or_above(uint32_t x, uint32_t t, bool all) { return !all && x >= t; }
+
+// A candidate element whose class word is x: its special value, or nv (its
+// normal value) when x is at or above the last threshold -- special_overlay's
+// values, with selects in place of branches.
+__device__ __forceinline__ uint32_t special_or_keep(const SpecialClasses &c, uint32_t x, uint32_t nv) {
+  const uint32_t r = x * kPayloadHash;
+  const uint32_t m = r & 0x007FFFFFu;
+  uint32_t e = at_or_above(x, c.den, c.den_all) ? 0u : (m > 1u ? m : 1u);      // zero : denormal
+  e = at_or_above(x, c.inf, c.inf_all) ? e : 0x7F800000u;                     // Inf
+  e = at_or_above(x, c.nan, c.nan_all) ? e : (0x7FC00000u | (r & 0x003FFFFFu));   // NaN
+  return at_or_above(x, c.zero, c.zero_all) ? nv : ((r & 0x80000000u) | e);
+}
+
+// The four gate bytes of a normal block, element k in byte k.
+__device__ __forceinline__ uint32_t gate_bytes(const u32x4 &w) {
+  return (w.x & 0xFFu) | ((w.y & 0xFFu) << 8) | ((w.z & 0xFFu) << 16) | (w.w << 24);
 }
 
 template <bool kNarrow, bool kNT>
@@ -258,32 +295,41 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
   constexpr int kWaves = kBlock / kWave;
   constexpr uint32_t kSlots = kGroup * kWave;     // every vector of a group may be a candidate
-  __shared__ u32x4 list_v[kWaves][kSlots];        // in: (index lo, index hi, candidate bits); out: values
-  __shared__ uint32_t list_m[kWaves][kSlots];     // out: which values replace normal ones
+  __shared__ u32x4 list_val[kWaves][kSlots];      // a listed vector's normal values, then its final ones
+  __shared__ u32x2 list_key[kWaves][kSlots];      // its offset in the tile and its gate bytes
   const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  u32x4 *lv = list_v[wave];
-  uint32_t *lm = list_m[wave];
+  u32x4 *lv = list_val[wave];
+  u32x2 *lk = list_key[wave];
   const Key key{p.k0, p.k1, p.s0, p.s1};
+  const SpecialClasses cls = special_classes(p);
+  const uint32_t gate = p.gate;
+  const float mean = in_vgpr(p.mean);
   const Idx tile = (Idx)rounds * kBlock;          // rounds: a multiple of kGroup
   const Idx c0 = (Idx)p.c0;
-  for (Idx t0 = (Idx)blockIdx.x * tile; t0 < (Idx)nvec; t0 += (Idx)gridDim.x * tile)
-  for (uint32_t r0 = 0; r0 < rounds; r0 += kGroup) {
+  const auto group = [&](Idx t0, uint32_t r0, auto whole_tile) {
+    constexpr bool kWhole = decltype(whole_tile)::value;   // every vector of the tile is in range
     u32x4 v[kGroup];
-    uint32_t c[kGroup], slot[kGroup];
+    uint32_t slot[kGroup];
+    bool listed[kGroup];
     uint32_t count = 0;                           // wave-uniform
 #pragma unroll
     for (uint32_t g = 0; g < kGroup; ++g) {
-      const Idx u = t0 + (Idx)(r0 + g) * kBlock + threadIdx.x;
+      const uint32_t off = (r0 + g) * kBlock + threadIdx.x;
+      const Idx u = t0 + (Idx)off;
       const u32x4 w = philox_block(key, (uint64_t)(c0 + u));
       float zc0, zs0, zc1, zs1;
       box_muller(w.x, w.y, zc0, zs0);
       box_muller(w.z, w.w, zc1, zs1);
-      v[g] = u32x4{as_u32(__builtin_fmaf(p.std, zc0, p.mean)), as_u32(__builtin_fmaf(p.std, zs0, p.mean)),
-                   as_u32(__builtin_fmaf(p.std, zc1, p.mean)), as_u32(__builtin_fmaf(p.std, zs1, p.mean))};
-      c[g] = u < (Idx)nvec ? candidates(p, w) : 0u;
-      const uint64_t m = __ballot(c[g] != 0u);
-      slot[g] = count + __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-      if (c[g] != 0u) lv[slot[g]] = u32x4{(uint32_t)u, (uint32_t)((uint64_t)u >> 32), c[g], 0u};
+      v[g] = u32x4{as_u32(__builtin_fmaf(p.std, zc0, mean)), as_u32(__builtin_fmaf(p.std, zs0, mean)),
+                   as_u32(__builtin_fmaf(p.std, zc1, mean)), as_u32(__builtin_fmaf(p.std, zs1, mean))};
+      const uint32_t low = min(min(w.x & 0xFFu, w.y & 0xFFu), min(w.z & 0xFFu, w.w & 0xFFu));
+      listed[g] = low < gate && (kWhole || u < (Idx)nvec);
+      const uint64_t m = __ballot(listed[g]);
+      slot[g] = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, count));
+      if (listed[g]) {
+        lk[slot[g]] = u32x2{off, gate_bytes(w)};
+        lv[slot[g]] = v[g];
+      }
       count += (uint32_t)__popcll(m);
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -291,32 +337,34 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
     for (uint32_t base = 0; base < count; base += kWave) {   // the listed vectors, one per lane
       const uint32_t e = base + lane;
       if (e < count) {
-        const u32x4 in = lv[e];
-        const uint64_t u = ((uint64_t)in.y << 32) | in.x;
-        const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)c0 + u);
-        uint32_t m;
-        lv[e] = overlay_values(p, q, in.z, m);
-        lm[e] = m;
+        const u32x2 k = lk[e];
+        const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)(Idx)(c0 + t0 + (Idx)k.x));
+        u32x4 x = lv[e];
+        x.x = (k.y & 0xFFu) < gate ? special_or_keep(cls, q.x, x.x) : x.x;
+        x.y = ((k.y >> 8) & 0xFFu) < gate ? special_or_keep(cls, q.y, x.y) : x.y;
+        x.z = ((k.y >> 16) & 0xFFu) < gate ? special_or_keep(cls, q.z, x.z) : x.z;
+        x.w = (k.y >> 24) < gate ? special_or_keep(cls, q.w, x.w) : x.w;
+        lv[e] = x;
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (uint32_t g = 0; g < kGroup; ++g) {
-      const Idx u = t0 + (Idx)(r0 + g) * kBlock + threadIdx.x;
-      if (c[g] != 0u) {
-        const u32x4 sv = lv[slot[g]];
-        const uint32_t m = lm[slot[g]];
-        v[g].x = (m & 1u) ? sv.x : v[g].x;
-        v[g].y = (m & 2u) ? sv.y : v[g].y;
-        v[g].z = (m & 4u) ? sv.z : v[g].z;
-        v[g].w = (m & 8u) ? sv.w : v[g].w;
-      }
-      if (u < (Idx)nvec) store_vec<kNT>(out, u, v[g]);
+      const Idx u = t0 + (Idx)((r0 + g) * kBlock + threadIdx.x);
+      if (listed[g]) v[g] = lv[slot[g]];
+      if (kWhole || u < (Idx)nvec) store_vec<kNT>(out, u, v[g]);
     }
     // the list is rewritten by the next group only after every lane has read it
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
+  };
+  for (Idx t0 = (Idx)blockIdx.x * tile; t0 < (Idx)nvec; t0 += (Idx)gridDim.x * tile) {
+    if (t0 + tile <= (Idx)nvec) {
+      for (uint32_t r0 = 0; r0 < rounds; r0 += kGroup) group(t0, r0, std::true_type{});
+    } else {
+      for (uint32_t r0 = 0; r0 < rounds; r0 += kGroup) group(t0, r0, std::false_type{});
+    }
   }
   // the ragged tail elements, one per thread of the first threads of the grid
   const uint64_t i = nvec * 4 + (uint64_t)blockIdx.x * kBlock + threadIdx.x;
