@@ -5,9 +5,9 @@
 // fast path gives every thread one 16-byte output vector per iteration (4
 // fp32 / int32 or 8 bf16 elements), computes the Philox blocks that cover it
 // (one for uniform and normal fp32 and for uniform bf16, whose elements take
-// 16-bit draws; two for normal bf16 and the integer range; three for special
-// fp32 and six for special bf16: the normal values plus the class and payload
-// words) and writes it with one dwordx4 store.
+// 16-bit draws; two for normal bf16 and the integer range; special values
+// take the normal blocks plus one class block for each block that holds a
+// candidate element) and writes it with one dwordx4 store.
 // The grid is a fixed multiple of the CU count with a grid-stride loop; the
 // ragged tail (fewer than one vector) is written element by element by the
 // first threads of the same launch.  Outputs that are not 16-byte aligned, and
@@ -252,6 +252,15 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
 #define SV_SPECIAL_GROUP 6
 #endif
 constexpr uint32_t kGroup = SV_SPECIAL_GROUP;   // vectors a lane holds before their candidates are overlaid
+#ifndef SV_SPECIAL_LIST
+#define SV_SPECIAL_LIST 128
+#endif
+// List entries per wave (24 bytes each).  Listing a wave's next 64 vectors
+// when the list cannot take all of its candidates, each candidate computes its
+// class block itself instead: slower, but only for mixes in which most
+// vectors hold a candidate.  The special-value stream lists about 51 per
+// group of six vectors per lane, 11 standard deviations below 128.
+constexpr uint32_t kSpecialList = SV_SPECIAL_LIST;
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -288,13 +297,24 @@ __device__ __forceinline__ uint32_t gate_bytes(const u32x4 &w) {
   return (w.x & 0xFFu) | ((w.y & 0xFFu) << 8) | ((w.z & 0xFFu) << 16) | (w.w << 24);
 }
 
+// The final values of a vector with normal values x, gate bytes b and class
+// block q.
+__device__ __forceinline__ u32x4 overlay_vector(const SpecialClasses &cls, uint32_t gate, const u32x4 &q,
+                                                uint32_t b, u32x4 x) {
+  x.x = (b & 0xFFu) < gate ? special_or_keep(cls, q.x, x.x) : x.x;
+  x.y = ((b >> 8) & 0xFFu) < gate ? special_or_keep(cls, q.y, x.y) : x.y;
+  x.z = ((b >> 16) & 0xFFu) < gate ? special_or_keep(cls, q.z, x.z) : x.z;
+  x.w = (b >> 24) < gate ? special_or_keep(cls, q.w, x.w) : x.w;
+  return x;
+}
+
 template <bool kNarrow, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                                u32x4 *__restrict__ out, uint32_t rounds) {
   load_sincos_table();
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
   constexpr int kWaves = kBlock / kWave;
-  constexpr uint32_t kSlots = kGroup * kWave;     // every vector of a group may be a candidate
+  constexpr uint32_t kSlots = kSpecialList;       // list entries per wave
   __shared__ u32x4 list_val[kWaves][kSlots];      // a listed vector's normal values, then its final ones
   __shared__ u32x2 list_key[kWaves][kSlots];      // its offset in the tile and its gate bytes
   const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
@@ -325,12 +345,20 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
       const uint32_t low = min(min(w.x & 0xFFu, w.y & 0xFFu), min(w.z & 0xFFu, w.w & 0xFFu));
       listed[g] = low < gate && (kWhole || u < (Idx)nvec);
       const uint64_t m = __ballot(listed[g]);
-      slot[g] = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, count));
-      if (listed[g]) {
-        lk[slot[g]] = u32x2{off, gate_bytes(w)};
-        lv[slot[g]] = v[g];
+      const uint32_t nm = (uint32_t)__popcll(m);
+      if (count + nm <= kSlots) {
+        slot[g] = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, count));
+        if (listed[g]) {
+          lk[slot[g]] = u32x2{off, gate_bytes(w)};
+          lv[slot[g]] = v[g];
+        }
+        count += nm;
+      } else if (listed[g]) {
+        // the list is full (a mix with many candidates): this vector's class block here
+        const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)(c0 + u));
+        v[g] = overlay_vector(cls, gate, q, gate_bytes(w), v[g]);
+        listed[g] = false;
       }
-      count += (uint32_t)__popcll(m);
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -339,12 +367,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
       if (e < count) {
         const u32x2 k = lk[e];
         const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)(Idx)(c0 + t0 + (Idx)k.x));
-        u32x4 x = lv[e];
-        x.x = (k.y & 0xFFu) < gate ? special_or_keep(cls, q.x, x.x) : x.x;
-        x.y = ((k.y >> 8) & 0xFFu) < gate ? special_or_keep(cls, q.y, x.y) : x.y;
-        x.z = ((k.y >> 16) & 0xFFu) < gate ? special_or_keep(cls, q.z, x.z) : x.z;
-        x.w = (k.y >> 24) < gate ? special_or_keep(cls, q.w, x.w) : x.w;
-        lv[e] = x;
+        lv[e] = overlay_vector(cls, gate, q, k.y, lv[e]);
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");

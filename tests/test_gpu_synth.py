@@ -15,6 +15,10 @@ pytestmark = pytest.mark.gpu
 
 SPECIAL = dict(mean=0.0, std=1e3, p_nan=0.01, p_inf=0.005, p_denorm=0.01, p_zero=0.01)
 SPECIAL_HEAVY = dict(mean=5.0, std=10.0, p_nan=0.2, p_inf=0.1, p_denorm=0.2, p_zero=0.2)
+# about 60 % of the 16-byte vectors hold a candidate: a wave's list of them fills up part way through a group
+SPECIAL_MID = dict(mean=1.0, std=3.0, p_nan=0.05, p_inf=0.05, p_denorm=0.05, p_zero=0.05)
+# every element special: the last class threshold is 2^32 (no class word keeps its normal value)
+SPECIAL_ALL = dict(mean=0.0, std=1.0, p_nan=0.25, p_inf=0.25, p_denorm=0.25, p_zero=0.25)
 CASES = [
     ("uniform", "f32", dict(a=-1.0, b=1.0)),
     ("uniform", "f32", dict(a=-3.0, b=7.5)),
@@ -29,6 +33,9 @@ CASES = [
     ("special", "f32", SPECIAL),
     ("special", "f32", SPECIAL_HEAVY),
     ("special", "bf16", SPECIAL_HEAVY),
+    ("special", "f32", SPECIAL_MID),
+    ("special", "f32", SPECIAL_ALL),
+    ("special", "f32", dict(mean=0.0, std=1.0, p_nan=1.0)),
 ]
 SIZES = [1, 3, 4, 5, 8, 17, 1000, 4099, 65543, (1 << 20) + 3]
 
