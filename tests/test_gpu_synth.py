@@ -74,6 +74,20 @@ def test_synth_unaligned_outputs_and_guard(oracle, dist, dtype, params):
         assert np.all(allb[:off] == 0x5A5A) and np.all(allb[off + n:] == 0x5A5A)
 
 
+@pytest.mark.parametrize("dist,params", [("normal", dict(mean=5.0, std=10.0)), ("special", SPECIAL),
+                                         ("special", SPECIAL_MID)])
+def test_synth_far_window_with_64_bit_block_indices(oracle, dist, params):
+    # a window past element 2^40: Philox block indices above 2^32, so the kernels index in 64 bits;
+    # large enough for whole tiles and a ragged last one
+    n, off = (1 << 20) + 3, (1 << 40) + 12
+    print("far window", dist, params, flush=True)
+    g = empty(n, "f32")
+    sv.synth_window(g, 11, 5, dist, off, **params)
+    want = oracle.synth(11, 5, "f32", dist, oracle.dist_params(**params), n, off)
+    got = bits(g)
+    assert np.array_equal(got, want), _diff(got, want)
+
+
 def test_synth_is_deterministic_and_empty_ok():
     a, b = empty(1 << 20, "f32"), empty(1 << 20, "f32")
     sv.synth(a, 1, 2, "normal", mean=0.0, std=1.0)
