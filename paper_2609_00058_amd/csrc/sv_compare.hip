@@ -221,31 +221,41 @@ __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, in
   } else {
 #pragma unroll
     for (int j = 0; j < G; ++j) {
-      bool ny, na, iy, ia;
-      double aval;
+      // every decision as a wave mask (one ballot per compare), combined
+      // with scalar bit operations
+      uint64_t ny, na, iy, ia, same;
+      bool lane_fin;                     // this lane's pair is finite
       if constexpr (DT == SV_F64) {
-        ny = __builtin_isnan(Y[j]);
-        na = __builtin_isnan(A[j]);
-        iy = __builtin_isinf(Y[j]);
-        ia = __builtin_isinf(A[j]);
-        aval = A[j];
+        ny = __ballot(__builtin_isnan(Y[j]));
+        na = __ballot(__builtin_isnan(A[j]));
+        iy = __ballot(__builtin_isinf(Y[j]));
+        ia = __ballot(__builtin_isinf(A[j]));
+        same = __ballot(A[j] == Y[j]);
+        lane_fin = __builtin_isfinite(Y[j]) && __builtin_isfinite(A[j]);   // (their difference may overflow)
       } else {
+        // the fp32 values (bf16 and fp16 widened exactly) have the classes,
+        // and compare equal exactly when, the fp64 ones do; their difference
+        // is finite exactly when both are
         const float yf = as_f32(elem_bits<DT>(yv, G * g + j)), af = as_f32(elem_bits<DT>(av, G * g + j));
-        ny = __builtin_isnan(yf);
-        na = __builtin_isnan(af);
-        iy = __builtin_isinf(yf);
-        ia = __builtin_isinf(af);
-        aval = (double)af;
+        ny = __ballot(__builtin_isnan(yf));
+        na = __ballot(__builtin_isnan(af));
+        iy = __ballot(__builtin_fabsf(yf) > 0x1.fffffep+127f);
+        ia = __ballot(__builtin_fabsf(af) > 0x1.fffffep+127f);
+        same = __ballot(af == yf);
+        lane_fin = __builtin_fabs(D[j]) <= 0x1.fffffffffffffp+1023;   // a compare the ballot takes as it is
       }
-      W.nan_r += __popcll(__ballot(ny));
-      W.nan_c += __popcll(__ballot(na));
-      W.inf_r += __popcll(__ballot(iy));
-      W.inf_c += __popcll(__ballot(ia));
-      const bool fin = !(ny | na | iy | ia);
+      const uint64_t fin = __ballot(lane_fin);
+      W.nan_r += __popcll(ny);
+      W.nan_c += __popcll(na);
+      W.inf_r += __popcll(iy);
+      W.inf_c += __popcll(ia);
       const double ay = fabs(Y[j]);
-      const bool match = fin ? (D[j] <= atol + rtol * ay) : ((aval == Y[j]) || (eqn && ny && na));
-      bad[j] = __ballot(!match);
-      const double dj = fin ? D[j] : 0.0;
+      const uint64_t within = __ballot(D[j] <= atol + rtol * ay);
+      // a pair holding a NaN or an infinity matches when the values are equal
+      // (equal infinities) or, with equal_nan, both are NaN
+      const uint64_t match = (fin & within) | (~fin & (same | (eqn ? ny & na : 0ull)));
+      bad[j] = ~match & __ballot(true);
+      const double dj = lane_fin ? D[j] : 0.0;
       L.sum += dj;
       L.maxabs = fmax(L.maxabs, dj);
       f[j] = may_beat<DT>(L, dj, ay);
