@@ -178,7 +178,12 @@ __device__ __forceinline__ void update_rel(LaneAcc &L, double d, double y) {
 // Reached by every lane of the wave (ballots).  int64 differences are formed
 // exactly and rounded once (fp64 cannot hold every int64); with the zero
 // tolerances of integer types the test d <= 0 is then exact equality.
-template <int DT>
+// Pairs holding a NaN or an infinity are decided with wave masks and scalar
+// bit operations (kMasks), or with per-lane selects and branches: the
+// stop-at-first kernel, whose loop measured faster that way (the candidates
+// round's check 285 against 308 us; the single and the batched check faster
+// with masks, e.g. 1262 against 1356 us for 2^30 special values).
+template <int DT, bool kMasks = true>
 __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, int g, double rtol, double atol,
                                             bool eqn, LaneAcc &L, WaveAcc &W, uint64_t *bad) {
   constexpr int G = Elem<DT>::G;
@@ -216,6 +221,38 @@ __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, in
       L.sum += D[j];
       L.maxabs = fmax(L.maxabs, D[j]);
       f[j] = may_beat<DT>(L, D[j], ay);
+      anyf |= f[j];
+    }
+  } else if constexpr (!kMasks) {
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      bool ny, na, iy, ia, same;
+      if constexpr (DT == SV_F64) {
+        ny = __builtin_isnan(Y[j]);
+        na = __builtin_isnan(A[j]);
+        iy = __builtin_isinf(Y[j]);
+        ia = __builtin_isinf(A[j]);
+        same = A[j] == Y[j];
+      } else {
+        const float yf = as_f32(elem_bits<DT>(yv, G * g + j)), af = as_f32(elem_bits<DT>(av, G * g + j));
+        ny = __builtin_isnan(yf);
+        na = __builtin_isnan(af);
+        iy = __builtin_isinf(yf);
+        ia = __builtin_isinf(af);
+        same = af == yf;
+      }
+      W.nan_r += __popcll(__ballot(ny));
+      W.nan_c += __popcll(__ballot(na));
+      W.inf_r += __popcll(__ballot(iy));
+      W.inf_c += __popcll(__ballot(ia));
+      const bool fin = !(ny | na | iy | ia);
+      const double ay = fabs(Y[j]);
+      const bool match = fin ? (D[j] <= atol + rtol * ay) : (same || (eqn && ny && na));
+      bad[j] = __ballot(!match);
+      const double dj = fin ? D[j] : 0.0;
+      L.sum += dj;
+      L.maxabs = fmax(L.maxabs, dj);
+      f[j] = may_beat<DT>(L, dj, ay);
       anyf |= f[j];
     }
   } else {
@@ -317,7 +354,7 @@ __device__ __forceinline__ void fold_int_sum(LaneAcc &L) {
 
 // One unit: its groups, then the mismatch count and, for the first
 // mismatching unit a wave sees, the smallest mismatching index.
-template <int DT>
+template <int DT, bool kMasks = true>
 __device__ __forceinline__ void check_unit(const u32x4 &yv, const u32x4 &av, uint64_t wave_e0, double rtol,
                                            double atol, bool eqn, LaneAcc &L, WaveAcc &W) {
   constexpr int V = Elem<DT>::V;
@@ -333,7 +370,7 @@ __device__ __forceinline__ void check_unit(const u32x4 &yv, const u32x4 &av, uin
     if constexpr (kSmallInt<DT>)
       check_group_int<DT>(yv, av, g, L, bad + G * g);
     else
-      check_group<DT>(yv, av, g, rtol, atol, eqn, L, W, bad + G * g);
+      check_group<DT, kMasks>(yv, av, g, rtol, atol, eqn, L, W, bad + G * g);
   }
   uint64_t any = 0;
 #pragma unroll
@@ -529,7 +566,7 @@ __device__ __forceinline__ bool leave_segment(const StopCtx &sc, uint64_t t, uin
 // the segment; ulo and step multiples of kCmpTile) -> a workgroup partial,
 // valid on thread 0.  A plain launch passes its contiguous piece with step =
 // kCmpTile; a stop-at-first launch its share of the segment's tiles.
-template <int DT, bool kStop = false>
+template <int DT, bool kStop = false, bool kMasks = true>
 __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, uint64_t step, const StopCtx *sc,
                                Partial *lds) {
   constexpr int V = Elem<DT>::V;
@@ -562,7 +599,7 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, ui
     }
 #pragma unroll
     for (int k = 0; k < kUnroll; ++k)
-      check_unit<DT>(yv[k], av[k], (base + (uint64_t)k * kCmpBlock) * V, rtol, atol, eqn, L, W);
+      check_unit<DT, kMasks>(yv[k], av[k], (base + (uint64_t)k * kCmpBlock) * V, rtol, atol, eqn, L, W);
     if constexpr (kSmallInt<DT>) fold_int_sum(L);
   }
   // the rest, one sub-iteration at a time, guarded (same unit order); a plain
@@ -588,7 +625,7 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, ui
         }
       }
     }
-    check_unit<DT>(yv, av, base * V, rtol, atol, eqn, L, W);
+    check_unit<DT, kMasks>(yv, av, base * V, rtol, atol, eqn, L, W);
     if constexpr (kSmallInt<DT>) fold_int_sum(L);
     if constexpr (kStop)
       base += (k % kUnroll == kUnroll - 1) ? step - (uint64_t)(kUnroll - 1) * kCmpBlock : (uint64_t)kCmpBlock;
@@ -731,18 +768,18 @@ __global__ __launch_bounds__(kFinBlock) void finalize_kernel(FinalizeArgs f) {
 // what the widest of them needs.
 // The check of one piece for the element types in kMask (bit 1 << dtype):
 // with one type the code of that type only, else a branch on the segment's.
-template <int kMask, bool kStop, int DT = 0>
+template <int kMask, bool kStop, bool kMasks, int DT = 0>
 __device__ __forceinline__ Partial check_any(const SegDesc &sd, uint64_t ulo, uint64_t uhi, uint64_t step,
                                              const StopCtx *sc, Partial *lds) {
   if constexpr (DT > SV_I64) {
     return empty_partial();                         // not reached: the host passes types in kMask only
   } else if constexpr ((kMask & (1 << DT)) == 0) {
-    return check_any<kMask, kStop, DT + 1>(sd, ulo, uhi, step, sc, lds);
+    return check_any<kMask, kStop, kMasks, DT + 1>(sd, ulo, uhi, step, sc, lds);
   } else if constexpr ((kMask >> (DT + 1)) == 0) {
-    return check_piece<DT, kStop>(sd, ulo, uhi, step, sc, lds);   // the last type in the mask
+    return check_piece<DT, kStop, kMasks>(sd, ulo, uhi, step, sc, lds);   // the last type in the mask
   } else {
-    if (sd.dtype == DT) return check_piece<DT, kStop>(sd, ulo, uhi, step, sc, lds);
-    return check_any<kMask, kStop, DT + 1>(sd, ulo, uhi, step, sc, lds);
+    if (sd.dtype == DT) return check_piece<DT, kStop, kMasks>(sd, ulo, uhi, step, sc, lds);
+    return check_any<kMask, kStop, kMasks, DT + 1>(sd, ulo, uhi, step, sc, lds);
   }
 }
 
@@ -819,10 +856,9 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
     if (threadIdx.x == 0) lim = 0xFFFFFFFFu;
     __syncthreads();
     const StopCtx sc{args.firsts + (size_t)s * kFirstStride, (uint32_t)args.seq, &lim};
-    const Partial p = check_any<kMask, true>(sd, (b - sd.w0) * kCmpTile, units, g * kCmpTile, &sc, lds);
+    const Partial p = check_any<kMask, true, false>(sd, (b - sd.w0) * kCmpTile, units, g * kCmpTile, &sc, lds);
     if (threadIdx.x == 0) args.partials[b] = p;
-    return;
-  }
+  } else {
   uint64_t lo = b * args.chunk;
   const uint64_t hi = lo + args.chunk < args.total_units ? lo + args.chunk : args.total_units;
   uint32_t s = kSingle ? 0u : find_segment(args.segs, args.nseg, lo);
@@ -831,7 +867,7 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
     const uint64_t seg_end = sd.unit_begin + units_of(sd.dtype, sd.n);
     const uint64_t piece_hi = hi < seg_end ? hi : seg_end;
     const uint64_t ulo = lo - sd.unit_begin, uhi = piece_hi - sd.unit_begin;
-    const Partial p = check_any<kMask, false>(sd, ulo, uhi, kCmpTile, nullptr, lds);
+    const Partial p = check_any<kMask, false, true>(sd, ulo, uhi, kCmpTile, nullptr, lds);
     if constexpr (kSingle) {
       if (args.fused == 1) {         // the only workgroup: its partial is the whole result
         publish_report(p, sd.n, args.reports);
@@ -850,6 +886,7 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
       ++s;
       while (s < args.nseg && lo < hi && args.segs[s].n == 0) ++s;
     }
+  }
   }
 }
 
