@@ -104,15 +104,20 @@ typedef struct {
  * Element i is a function of (seed, stream_id, i) only: Philox4x32-10
  * (Salmon et al., SC'11) keyed by the seed, with counter (block index,
  * stream_id), where block = i / E and E = 4 (uniform, normal, special, uint8
- * range) or 2 (int32 / int64 range).  Uniform: a + (b - a) * (top 24 bits) * 2^-24 in
- * fp32.  Normal: Box-Muller with ln, sin, cos evaluated as fixed fp32
- * operation sequences, so the bits are reproducible on any IEEE-754 machine.
+ * range), 8 (bf16 uniform) or 2 (int32 / int64 range).  Uniform: a + (b - a) *
+ * (top 24 bits) * 2^-24 in fp32; a bf16 element takes a 16-bit half-word
+ * (the low half first), U = h * 2^-16.  Normal: Box-Muller with ln, sin, cos
+ * evaluated as fixed fp32 operation sequences (sin and cos from a table of
+ * 256 angles), so the bits are reproducible on any IEEE-754 machine.
  * Integer range: lo + floor(R * (hi - lo + 1) / 2^64), R a 64-bit word.
- * Special: the normal sequence, element 4c + k replaced when word k of
- * block 2^62 + c falls below the cumulative class thresholds floor(p * 2^32)
- * (NaN, Inf, denormal, zero), by the bit pattern of its class (quiet NaN
- * with a random payload, Inf, denormal, zero), sign and payload from word k
- * of block 2^62 + 2^61 + c.  bf16
+ * Special: the normal sequence with some elements replaced.  Element 4c + k
+ * is a candidate when the low byte of word k of normal block c is below
+ * S = ceil(256 * (p_nan + p_inf + p_denorm + p_zero)); a candidate takes its
+ * class from x = word k of block 2^62 + c against the cumulative thresholds
+ * min(floor(p * 2^40 / S), 2^32) (NaN, Inf, denormal, zero; at or above the
+ * last it keeps its normal value), and its sign and payload from
+ * x * 0x9E3779B9 mod 2^32 (quiet NaN with that payload, Inf, denormal, zero).
+ * bf16
  * and fp16 outputs are the round-to-nearest-even of the fp32 value (an fp16
  * NaN keeps its sign and the top 10 fraction bits, bit 0 set if they are all
  * 0).  fp64 outputs: uniform from 53 random bits, U = (R >> 11) 2^-53 with R
