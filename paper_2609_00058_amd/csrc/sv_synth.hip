@@ -255,7 +255,7 @@ constexpr uint32_t kGroup = SV_SPECIAL_GROUP;   // vectors a lane holds before t
 #ifndef SV_SPECIAL_LIST
 #define SV_SPECIAL_LIST 128
 #endif
-// List entries per wave (24 bytes each).  Listing a wave's next 64 vectors
+// List entries per wave (32 bytes each).  Listing a wave's next 64 vectors
 // when the list cannot take all of its candidates, each candidate computes its
 // class block itself instead: slower, but only for mixes in which most
 // vectors hold a candidate.  The special-value stream lists about 51 per
@@ -292,9 +292,11 @@ __device__ __forceinline__ uint32_t special_or_keep(const SpecialClasses &c, uin
   return at_or_above(x, c.zero, c.zero_all) ? nv : ((r & 0x80000000u) | e);
 }
 
-// The four gate bytes of a normal block, element k in byte k.
+// The four gate bytes of a normal block, element k in byte k: two byte
+// permutes (v_perm_b32 picks bytes 0-3 of its second operand with selectors
+// 0-3, of its first with 4-7, and 0x0C gives a zero byte) and an OR.
 __device__ __forceinline__ uint32_t gate_bytes(const u32x4 &w) {
-  return (w.x & 0xFFu) | ((w.y & 0xFFu) << 8) | ((w.z & 0xFFu) << 16) | (w.w << 24);
+  return __builtin_amdgcn_perm(w.y, w.x, 0x0C0C0400u) | __builtin_amdgcn_perm(w.w, w.z, 0x04000C0Cu);
 }
 
 // The final values of a vector with normal values x, gate bytes b and class
@@ -315,11 +317,11 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
   constexpr int kWaves = kBlock / kWave;
   constexpr uint32_t kSlots = kSpecialList;       // list entries per wave
-  __shared__ u32x4 list_val[kWaves][kSlots];      // a listed vector's normal values, then its final ones
-  __shared__ u32x2 list_key[kWaves][kSlots];      // its offset in the tile and its gate bytes
+  // entry: [0] a listed vector's normal values, then its final ones; [1].xy
+  // its offset in the tile and its gate bytes (one address serves both)
+  __shared__ u32x4 list[kWaves][kSlots][2];
   const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  u32x4 *lv = list_val[wave];
-  u32x2 *lk = list_key[wave];
+  u32x4 (*lw)[2] = list[wave];
   const Key key{p.k0, p.k1, p.s0, p.s1};
   const SpecialClasses cls = special_classes(p);
   const uint32_t gate = p.gate;
@@ -329,7 +331,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
   const auto group = [&](Idx t0, uint32_t r0, auto whole_tile) {
     constexpr bool kWhole = decltype(whole_tile)::value;   // every vector of the tile is in range
     u32x4 v[kGroup];
-    uint32_t slot[kGroup];
+    u32x4 *ent[kGroup];                           // the listed vectors' entries
     bool listed[kGroup];
     uint32_t count = 0;                           // wave-uniform
 #pragma unroll
@@ -347,10 +349,10 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
       const uint64_t m = __ballot(listed[g]);
       const uint32_t nm = (uint32_t)__popcll(m);
       if (count + nm <= kSlots) {
-        slot[g] = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, count));
+        ent[g] = lw[__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, count))];
         if (listed[g]) {
-          lk[slot[g]] = u32x2{off, gate_bytes(w)};
-          lv[slot[g]] = v[g];
+          ent[g][0] = v[g];
+          *(u32x2 *)&ent[g][1] = u32x2{off, gate_bytes(w)};
         }
         count += nm;
       } else if (listed[g]) {
@@ -365,9 +367,9 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
     for (uint32_t base = 0; base < count; base += kWave) {   // the listed vectors, one per lane
       const uint32_t e = base + lane;
       if (e < count) {
-        const u32x2 k = lk[e];
+        const u32x2 k = *(const u32x2 *)&lw[e][1];
         const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)(Idx)(c0 + t0 + (Idx)k.x));
-        lv[e] = overlay_vector(cls, gate, q, k.y, lv[e]);
+        lw[e][0] = overlay_vector(cls, gate, q, k.y, lw[e][0]);
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -375,7 +377,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
 #pragma unroll
     for (uint32_t g = 0; g < kGroup; ++g) {
       const Idx u = t0 + (Idx)((r0 + g) * kBlock + threadIdx.x);
-      if (listed[g]) v[g] = lv[slot[g]];
+      if (listed[g]) v[g] = ent[g][0];
       if (kWhole || u < (Idx)nvec) store_vec<kNT>(out, u, v[g]);
     }
     // the list is rewritten by the next group only after every lane has read it
