@@ -9,7 +9,7 @@ substream ids, tolerances -- and draws the host-side layout of the faults
 seeded per workload.  Both sides then synthesize and derive candidates
 themselves from these descriptions.
 
-The five workloads stand in for the paper's benchmark test data (not
+The six workloads stand in for the paper's benchmark test data (not
 available here), following its advice to draw inputs from a broad numeric
 range (Sec. 4.2.1; a Gaussian with mean 5 and std 10 is its example, used for
 the float segments of the ragged batch).
