@@ -127,6 +127,24 @@ def test_synth_full_size_sampled(oracle, dist, dtype, n, params):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("dist,params", [("normal", dict(mean=0.0, std=1.0)), ("special", SPECIAL)])
+def test_synth_far_window_of_1_gib_sampled(oracle, dist, params):
+    # 2^28 + 5 fp32 values past element 2^40: 64-bit block indices and the non-temporal stores of
+    # outputs of 1 GiB or more, together; sampled against the oracle element by element
+    n, off = (1 << 28) + 5, (1 << 40) + 12
+    print("far window 1 GiB", dist, flush=True)
+    g = empty(n, "f32")
+    sv.synth_window(g, 3, 9, dist, off, **params)
+    rng = np.random.default_rng(77)
+    idx = np.unique(np.concatenate([np.arange(4096), np.arange(n - 4096, n),
+                                    rng.integers(0, n, 60000)])).astype(np.uint64)
+    got = bits_at(g, idx)
+    want = oracle.synth_at(3, 9, "f32", dist, oracle.dist_params(**params), idx + np.uint64(off))
+    assert np.array_equal(got, want), _diff(got, want)
+    del g
+    torch.cuda.empty_cache()
+
+
 def test_synth_batched_matches_single_calls_and_oracle(oracle):
     rng = np.random.default_rng(12)
     jobs, singles = [], []
