@@ -164,6 +164,10 @@ __device__ __forceinline__ bool may_beat(const LaneAcc &L, double d, double ay) 
     return d > b;
 }
 
+// Gives every lane the wave's largest relative error so far (defined with the
+// cross-lane steps below).
+__device__ __forceinline__ void share_rel(LaneAcc &L);
+
 __device__ __forceinline__ void update_rel(LaneAcc &L, double d, double y) {
   const double rel = d / fabs(y);    // y = 0 < d gives +Inf
   if (rel > L.maxrel) {
@@ -303,6 +307,10 @@ __device__ __forceinline__ void check_group(const u32x4 &yv, const u32x4 &av, in
 #pragma unroll
     for (int j = 0; j < G; ++j)
       if (f[j]) update_rel(L, D[j], Y[j]);
+    // the report needs only the largest quotient of all: filtering every lane
+    // against the wave's largest divides far less often where most pairs
+    // differ (a lane alone sees few pairs, so its own maximum keeps rising)
+    share_rel(L);
   }
 }
 
@@ -462,6 +470,18 @@ __device__ __forceinline__ void wave_merge(Partial &acc) {
   merge_step<3>(acc);
   merge_step<4>(acc);
   merge_step<5>(acc);
+}
+
+__device__ __forceinline__ void share_rel(LaneAcc &L) {
+  double m = L.maxrel;
+  m = fmax(m, lane_pair<0>(m));
+  m = fmax(m, lane_pair<1>(m));
+  m = fmax(m, lane_pair<2>(m));
+  m = fmax(m, lane_pair<3>(m));
+  m = fmax(m, lane_pair<4>(m));
+  m = fmax(m, lane_pair<5>(m));
+  L.maxrel = m;
+  L.mrc = m * 0x1.ffffffffffff8p-1;   // 1 - 2^-50, as in update_rel
 }
 
 __device__ __forceinline__ uint64_t dbits(double x) { return (uint64_t)__double_as_longlong(x); }
