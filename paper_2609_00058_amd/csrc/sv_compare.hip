@@ -146,7 +146,8 @@ struct WaveAcc {                      // wave-uniform
   uint64_t mism, first, nan_r, nan_c, inf_r, inf_c;
 };
 
-// Whether d / |y| may round above the lane's running maximum m: d > fp64(mrc
+// Whether d / |y| may round above the running maximum m the lane holds (the
+// wave's, as of its last rise): d > fp64(mrc
 // |y|) never rejects such a quotient while that product is a normal fp64
 // number (its relative rounding error, at most 2^-53, is inside the 2^-50
 // margin of mrc).  Widened fp32, bf16 and fp16 values and int64 differences
