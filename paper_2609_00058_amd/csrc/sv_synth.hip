@@ -14,8 +14,10 @@
 // windows that start inside a Philox block, go through a one-element-per-thread
 // kernel.  A window of a tensor (out[0] = element e0) is the same bits as the
 // slice of the whole tensor: only the counter base moves.  The path is ALU-bound (Philox is
-// 20 64-bit multiply-adds and 20 three-input XORs per block; Box-Muller adds a
-// logarithm, a square root and a sine / cosine pair per two elements).
+// 20 32x32->64-bit products and 20 XOR pairs per block, of which the uniform
+// substream words leave 18 products and 15 three-input XORs per lane when the
+// block indices fit 32 bits; Box-Muller adds a logarithm, a square root and a
+// sine / cosine pair per two elements).
 #include <type_traits>
 
 #include "sv_device.h"
