@@ -56,6 +56,7 @@
 namespace sv {
 
 constexpr int kUnroll = SV_CMP_UNROLL;   // units per thread in flight
+constexpr int kStopUnroll = SV_CMP_STOP_UNROLL;   // ... in a stop-at-first launch (its tile: kStopTile)
 constexpr int kWavesPerBlock = kCmpBlock / kWave;
 
 // V elements per 16-byte unit, checked in groups of G.
@@ -560,7 +561,7 @@ __device__ __forceinline__ bool leave_segment(const StopCtx &sc, uint64_t t, uin
                                               bool &told, uint32_t it, uint32_t wave, uint32_t lane) {
   if (W.first != kNone && !told) {
     told = true;
-    const uint32_t f = (uint32_t)(W.first / V / kCmpTile);
+    const uint32_t f = (uint32_t)(W.first / V / kStopTile);
     if (lane == 0) {
       const uint32_t old = __hip_atomic_fetch_min(sc.lim, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
       if (f < old)
@@ -580,17 +581,19 @@ __device__ __forceinline__ bool leave_segment(const StopCtx &sc, uint64_t t, uin
       }
     }
   }
-  return t / kCmpTile > __builtin_amdgcn_readfirstlane(lim);
+  return t / kStopTile > __builtin_amdgcn_readfirstlane(lim);
 }
 
 // The tiles ulo, ulo + step, ... below uhi of one segment (units, relative to
-// the segment; ulo and step multiples of kCmpTile) -> a workgroup partial,
-// valid on thread 0.  A plain launch passes its contiguous piece with step =
-// kCmpTile; a stop-at-first launch its share of the segment's tiles.
+// the segment; ulo and step multiples of the tile, kCmpTile units, or
+// kStopTile for a stop-at-first launch) -> a workgroup partial, valid on
+// thread 0.  A plain launch passes its contiguous piece with step = kCmpTile;
+// a stop-at-first launch its share of the segment's tiles.
 template <int DT, bool kStop = false, bool kMasks = true>
 __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, uint64_t step, const StopCtx *sc,
                                Partial *lds) {
   constexpr int V = Elem<DT>::V;
+  constexpr int kU = kStop ? kStopUnroll : kUnroll;   // units per thread per tile
   const uint32_t tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
   const kGlobal u32x4 *yv4 = (const kGlobal u32x4 *)sd.ref;
   const kGlobal u32x4 *av4 = (const kGlobal u32x4 *)sd.cand;
@@ -605,21 +608,21 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, ui
   bool told = false;
   uint32_t it = 0;
   uint64_t t = ulo;
-  // whole tiles: kUnroll sub-iterations of kCmpBlock units, every unit full
-  for (; t + wofs + (uint64_t)(kUnroll - 1) * kCmpBlock + kWave <= full_end; t += step, ++it) {
+  // whole tiles: kU sub-iterations of kCmpBlock units, every unit full
+  for (; t + wofs + (uint64_t)(kU - 1) * kCmpBlock + kWave <= full_end; t += step, ++it) {
     if constexpr (kStop) {
       if (leave_segment<V>(*sc, t, t + wofs, W, told, it, wave, lane)) break;
     }
     const uint64_t base = t + wofs;
-    u32x4 yv[kUnroll], av[kUnroll];
+    u32x4 yv[kU], av[kU];
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
+    for (int k = 0; k < kU; ++k) {
       const uint64_t u = base + (uint64_t)k * kCmpBlock + lane;
       yv[k] = __builtin_nontemporal_load(yv4 + u);
       av[k] = __builtin_nontemporal_load(av4 + u);
     }
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k)
+    for (int k = 0; k < kU; ++k)
       check_unit<DT, kMasks>(yv[k], av[k], (base + (uint64_t)k * kCmpBlock) * V, rtol, atol, eqn, L, W);
     if constexpr (kSmallInt<DT>) fold_int_sum(L);
   }
@@ -628,7 +631,7 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, ui
   // after each tile's last sub-iteration
   for (uint64_t base = t + wofs, k = 0; base < uhi; ++k) {
     if constexpr (kStop) {
-      if (k % kUnroll == 0 && leave_segment<V>(*sc, base - wofs, base, W, told, it++, wave, lane)) break;
+      if (k % kU == 0 && leave_segment<V>(*sc, base - wofs, base, W, told, it++, wave, lane)) break;
       if (base * V > W.first) break;
     }
     const uint64_t u = base + lane;
@@ -649,14 +652,14 @@ __device__ Partial check_piece(const SegDesc &sd, uint64_t ulo, uint64_t uhi, ui
     check_unit<DT, kMasks>(yv, av, base * V, rtol, atol, eqn, L, W);
     if constexpr (kSmallInt<DT>) fold_int_sum(L);
     if constexpr (kStop)
-      base += (k % kUnroll == kUnroll - 1) ? step - (uint64_t)(kUnroll - 1) * kCmpBlock : (uint64_t)kCmpBlock;
+      base += (k % kU == kU - 1) ? step - (uint64_t)(kU - 1) * kCmpBlock : (uint64_t)kCmpBlock;
     else
       base += kCmpBlock;
   }
   if constexpr (kStop) {
     // a mismatch in the wave's last tile: post it for the segment's other workgroups
     if (W.first != kNone && !told && lane == 0) {
-      const uint32_t f = (uint32_t)(W.first / V / kCmpTile);
+      const uint32_t f = (uint32_t)(W.first / V / kStopTile);
       __hip_atomic_fetch_max(sc->word, ((uint64_t)sc->epoch << 32) | (0xFFFFFFFFu - f), __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
     }
@@ -877,7 +880,7 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
     if (threadIdx.x == 0) lim = 0xFFFFFFFFu;
     __syncthreads();
     const StopCtx sc{args.firsts + (size_t)s * kFirstStride, (uint32_t)args.seq, &lim};
-    const Partial p = check_any<kMask, true, false>(sd, (b - sd.w0) * kCmpTile, units, g * kCmpTile, &sc, lds);
+    const Partial p = check_any<kMask, true, false>(sd, (b - sd.w0) * kStopTile, units, g * kStopTile, &sc, lds);
     if (threadIdx.x == 0) args.partials[b] = p;
   } else {
   uint64_t lo = b * args.chunk;

@@ -13,6 +13,9 @@ namespace sv {
 #ifndef SV_CMP_UNROLL
 #define SV_CMP_UNROLL 4              // 16-byte units per thread in flight in the check
 #endif
+#ifndef SV_CMP_STOP_UNROLL
+#define SV_CMP_STOP_UNROLL 2         // ... in a stop-at-first check: smaller tiles, less read past a mismatch
+#endif
 #ifndef SV_CMP_BLOCK
 #define SV_CMP_BLOCK 512             // threads per check workgroup
 #endif
@@ -118,8 +121,8 @@ hipError_t launch_perturb_indexed(int32_t dtype, const PerturbParams &p, const u
 // Stop-at-first launches lay the workgroups out by segment instead: segment s
 // gets stop_blocks(units, chunk) workgroups of its own, from workgroup w0 on,
 // which sweep it together from the front, workgroup i taking tiles i, i + g,
-// i + 2g, ... (a tile is kCmpBlock * SV_CMP_UNROLL units, one iteration of a
-// workgroup); each writes one partial, into slot b.  A mismatch found in a tile
+// i + 2g, ... (a tile is kStopTile = kCmpBlock * SV_CMP_STOP_UNROLL units, one
+// iteration of a workgroup); each writes one partial, into slot b.  A mismatch found in a tile
 // is posted to the segment's word in `firsts`, so that the segment's other
 // workgroups, which are all near that tile, stop there too.
 struct SegDesc {
@@ -137,13 +140,14 @@ struct SegDesc {
 };
 
 constexpr uint64_t kCmpTile = (uint64_t)kCmpBlock * SV_CMP_UNROLL;   // units per workgroup iteration
+constexpr uint64_t kStopTile = (uint64_t)kCmpBlock * SV_CMP_STOP_UNROLL;   // ... of a stop-at-first launch
 constexpr uint64_t kMaxStopBlocks = 0xFFFFFFFFull / kCmpBlock;   // a grid's work-items fit in 32 bits
 constexpr size_t kFirstStride = 16;   // uint64 words between the segments' words in `firsts` (128 bytes)
 
 // Workgroups of one segment in a stop-at-first launch: a share of about
 // `chunk` units each, and no more workgroups than tiles.
 __host__ __device__ inline uint64_t stop_blocks(uint64_t units, uint64_t chunk) {
-  const uint64_t by_chunk = (units + chunk - 1) / chunk, tiles = (units + kCmpTile - 1) / kCmpTile;
+  const uint64_t by_chunk = (units + chunk - 1) / chunk, tiles = (units + kStopTile - 1) / kStopTile;
   return by_chunk < tiles ? by_chunk : tiles;
 }
 

@@ -246,7 +246,7 @@ def test_batched_stop_at_first(oracle):
     assert e.value.code == sv.SV_ERR_UNSUPPORTED
 
 
-TILE = 512 * 4          # units per workgroup iteration of the check (threads x units in flight)
+TILE = 512 * 2          # units per workgroup iteration of a stop-at-first check (threads x units in flight)
 
 
 def test_stop_at_first_shared_between_workgroups(oracle):
