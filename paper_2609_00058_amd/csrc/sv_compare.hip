@@ -883,34 +883,34 @@ __global__ __launch_bounds__(kCmpBlock) void compare_kernel(CompareArgs args) {
     const Partial p = check_any<kMask, true, false>(sd, (b - sd.w0) * kStopTile, units, g * kStopTile, &sc, lds);
     if (threadIdx.x == 0) args.partials[b] = p;
   } else {
-  uint64_t lo = b * args.chunk;
-  const uint64_t hi = lo + args.chunk < args.total_units ? lo + args.chunk : args.total_units;
-  uint32_t s = kSingle ? 0u : find_segment(args.segs, args.nseg, lo);
-  while (lo < hi) {
-    const SegDesc sd = kSingle ? args.single : args.segs[s];
-    const uint64_t seg_end = sd.unit_begin + units_of(sd.dtype, sd.n);
-    const uint64_t piece_hi = hi < seg_end ? hi : seg_end;
-    const uint64_t ulo = lo - sd.unit_begin, uhi = piece_hi - sd.unit_begin;
-    const Partial p = check_any<kMask, false, true>(sd, ulo, uhi, kCmpTile, nullptr, lds);
-    if constexpr (kSingle) {
-      if (args.fused == 1) {         // the only workgroup: its partial is the whole result
-        publish_report(p, sd.n, args.reports);
-        if (threadIdx.x == 0) signal_done(args);
-        return;
+    uint64_t lo = b * args.chunk;
+    const uint64_t hi = lo + args.chunk < args.total_units ? lo + args.chunk : args.total_units;
+    uint32_t s = kSingle ? 0u : find_segment(args.segs, args.nseg, lo);
+    while (lo < hi) {
+      const SegDesc sd = kSingle ? args.single : args.segs[s];
+      const uint64_t seg_end = sd.unit_begin + units_of(sd.dtype, sd.n);
+      const uint64_t piece_hi = hi < seg_end ? hi : seg_end;
+      const uint64_t ulo = lo - sd.unit_begin, uhi = piece_hi - sd.unit_begin;
+      const Partial p = check_any<kMask, false, true>(sd, ulo, uhi, kCmpTile, nullptr, lds);
+      if constexpr (kSingle) {
+        if (args.fused == 1) {         // the only workgroup: its partial is the whole result
+          publish_report(p, sd.n, args.reports);
+          if (threadIdx.x == 0) signal_done(args);
+          return;
+        }
+        if (args.fused == 2) {
+          last_block_report(args, p, sd.n);
+          return;
+        }
       }
-      if (args.fused == 2) {
-        last_block_report(args, p, sd.n);
-        return;
+      if (threadIdx.x == 0) args.partials[b + s] = p;
+      if constexpr (kSingle) return;   // one segment: the chunk is a single piece
+      lo = piece_hi;
+      if constexpr (!kSingle) {
+        ++s;
+        while (s < args.nseg && lo < hi && args.segs[s].n == 0) ++s;
       }
     }
-    if (threadIdx.x == 0) args.partials[b + s] = p;
-    if constexpr (kSingle) return;   // one segment: the chunk is a single piece
-    lo = piece_hi;
-    if constexpr (!kSingle) {
-      ++s;
-      while (s < args.nseg && lo < hi && args.segs[s].n == 0) ++s;
-    }
-  }
   }
 }
 
