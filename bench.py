@@ -519,7 +519,8 @@ def main():
         "config": {"workload": wl.name, "description": wl.description, "tensors": len(wl.cases),
                    "elements": wl.total_elems, "synth_bytes": sbytes, "check_bytes": cbytes,
                    "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
-                   "stream_copy_GBps": copy, "tensors_per_s": round(len(wl.cases) / (ms / 1e3), 1)},
+                   "stream_copy_GBps": copy, "tensors_per_s": round(len(wl.cases) / (ms / 1e3), 1),
+                   "elements_per_s": round(wl.total_elems / (ms / 1e3), 1)},
         "kernels": kernels,
         "cold": cold,
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
