@@ -36,6 +36,13 @@
  * first use, grows when needed and releases in sv_shutdown(); calls that use
  * it on the same device are serialised by a lock, and checks of one device
  * run in submission order.
+ *
+ * One HIP runtime per process.  The library links libamdhip64.so.7 by that
+ * name.  A process that also uses another copy of the runtime (PyTorch ships
+ * its own) must load that copy first, so that the library binds to it: with
+ * the library loaded first, the process ends up with two runtimes, and the
+ * library's sees no device (every call fails with SV_ERR_HIP).  The Python
+ * binding imports torch before it loads the library.
  */
 #ifndef SV_H
 #define SV_H

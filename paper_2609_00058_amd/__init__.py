@@ -20,6 +20,13 @@ if not os.path.exists(LIB_PATH):
     raise ImportError("libsynthverify.so is not built (run paper_2609_00058_amd/build.py or "
                       "__graft_entry__.build())")
 
+# torch first: the library must run on the HIP runtime that torch loads (its
+# own libamdhip64.so.7), which the library's dependency of the same name then
+# binds to.  Loaded before torch, the library would bring in the system's copy,
+# and the process would hold two HIP runtimes, of which the library's finds no
+# device (measured: "no ROCm-capable device is detected" on every call).
+import torch  # noqa: E402,F401
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 SV_OK, SV_ERR_INVALID_ARG, SV_ERR_UNSUPPORTED, SV_ERR_HIP, SV_ERR_ALLOC, SV_ERR_IO = 0, -1, -2, -3, -4, -5

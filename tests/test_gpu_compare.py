@@ -341,3 +341,19 @@ def test_stop_at_first_words_from_2_32_checks_ago_count_for_nothing(oracle):
     t = sv.compare_submit(R, N, 1e-6, 0.0)
     assert L.sv_testing_set_sequence(7) == sv.SV_ERR_INVALID_ARG                 # a check is pending
     same_report(t.wait(), want_near)
+
+
+def test_package_imported_before_torch_shares_torchs_runtime():
+    """Regression: the package imported before torch used to load the
+    system's HIP runtime beside torch's, and every call then failed with "no
+    ROCm-capable device"; the binding now loads torch first."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("import paper_2609_00058_amd as sv\nimport torch\n"
+            "x = torch.zeros(1000, device='cuda')\ny = x.clone(); y[7] = 1.0\n"
+            "r = sv.compare(x, y, 0.0, 0.0)\nprint(r['mismatches'], r['first_mismatch'])\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stderr[-3000:]
+    assert r.stdout.split() == ["1", "7"], r.stdout
