@@ -28,7 +28,7 @@ def code():
 
 def wall_clock_mhz():
     rate = ctypes.c_int()
-    hip = ctypes.CDLL("libamdhip64.so")
+    hip = ctypes.CDLL("libamdhip64.so.7")   # by its soname: the runtime torch has loaded, not a second copy
     assert hip.hipDeviceGetAttribute(ctypes.byref(rate), WALL_CLOCK_RATE_ATTR, 0) == 0
     return rate.value / 1e3
 
