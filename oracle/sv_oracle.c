@@ -16,7 +16,7 @@
  *    the normal distribution with explicit mean and std below.
  *  - The generator, the word-to-element mapping and the transforms are not in
  *    the paper (it only points to general-purpose numerical libraries).  They
- *    follow the conventions recorded in the design notes: Philox4x32-10 (Salmon, Moraes,
+ *    follow these conventions: Philox4x32-10 (Salmon, Moraes,
  *    Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC'11) keyed
  *    by the seed with counter (block, stream); uniform from the top 24 bits
  *    of a word (from a 16-bit half-word for bf16 outputs);

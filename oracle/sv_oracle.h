@@ -11,8 +11,8 @@
  * struct and constant here is the oracle's own.
  *
  * Conventions the paper leaves open (generator, word-to-element mapping,
- * distribution transforms, NaN/Inf rules, report fields) are fixed once in the
- * design notes and followed here step by step.
+ * distribution transforms, NaN/Inf rules, report fields) are stated with the
+ * functions below and in sv_oracle.c, and followed there step by step.
  */
 #ifndef SV_ORACLE_H
 #define SV_ORACLE_H
