@@ -296,3 +296,19 @@ def test_file_entry_points_reject_bad_arguments_without_a_device(svlib, tmp_path
         svlib.SV_ERR_INVALID_ARG                      # 16 bytes are not 0 values
     q = svlib.dist_params(a=-1.0, b=1.0)
     assert L.sv_synth_window(0, 0, 0, 0, ctypes.byref(q), 1 << 60, 1, 0x1000) == svlib.SV_ERR_INVALID_ARG
+
+
+def test_one_hip_runtime_per_process_with_torch():
+    """The package loads torch before the library, so the library binds to
+    the HIP runtime torch ships and the process maps one copy of it (two
+    copies left the library without a device)."""
+    code = ("import paper_2609_00058_amd\n"
+            "paths = sorted({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l})\n"
+            "print('\\n'.join(paths))\n")
+    r = subprocess.run([__import__("sys").executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    paths = r.stdout.split()
+    assert len(paths) == 1, paths
+    import torch
+    assert os.path.dirname(paths[0]) == os.path.join(os.path.dirname(torch.__file__), "lib"), paths
