@@ -85,3 +85,31 @@ def test_random_batches_match_the_oracle(oracle, seed):
             assert g["first_mismatch"] == w["first_mismatch"]
     for j in rng.choice(len(segs), size=min(2, len(segs)), replace=False):
         same_report(sv.compare(*segs[int(j)]), want[int(j)])
+
+
+def test_twenty_thousand_small_segments(oracle):
+    """A batch far longer than the grid: 20,000 segments of 0 to 50 elements
+    of every type, in one buffer per type, both check modes."""
+    rng = np.random.default_rng(9100)
+    pools = {}
+    for dtype in TYPES:
+        y, a = _values(rng, 600_000, dtype)
+        pools[dtype] = (y, a, dev_bits(y, dtype), dev_bits(a, dtype))
+    segs, want = [], []
+    for k in range(20000):
+        dtype = TYPES[k % len(TYPES)]
+        y, a, Y, A = pools[dtype]
+        n = int(rng.integers(0, 51))
+        o = int(rng.integers(0, 600_000 - n))
+        rtol, atol, eqn = _tolerance(rng)
+        segs.append((Y[o:o + n], A[o:o + n], rtol, atol, eqn))
+        want.append(oracle.compare(y[o:o + n], a[o:o + n], dtype, rtol, atol, eqn))
+    print("twenty thousand segments", flush=True)
+    got = sv.compare_batched(segs)
+    for g, w in zip(got, want):
+        same_report(g, w)
+    for g, w in zip(sv.compare_batched(segs, stop_at_first=True), want):
+        if w["mismatches"] == 0:
+            same_report(g, w)
+        else:
+            assert g["mismatches"] == 1 and g["first_mismatch"] == w["first_mismatch"], (g, w)
