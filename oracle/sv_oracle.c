@@ -744,14 +744,23 @@ static uint64_t index_op(int32_t dtype, const or_perturb_plan *plan, uint64_t b)
     float v = (float)plan->value;
     return from_f32(dtype, as_f32(dtype, b) + v);
   }
-  /* FAULT_AT: integers + 1 (wrapping in their width), floats x + (1 + |x|) */
+  /* FAULT_AT: integers + 1 (wrapping in their width), floats x + (1 + |x|).
+   * IEEE 754 leaves open which NaN a sum of two NaNs returns, and x + t has
+   * two when x is a NaN (t = 1 + |x| is |x|'s NaN); so a NaN x gives |x| with
+   * the quiet bit set, stated here rather than left to the order of the
+   * operands.  x = -Inf gives -Inf + Inf, the invalid operation: the quiet
+   * NaN with the sign bit set and no payload. */
   if (is_int(dtype)) return b + 1u;
   if (dtype == OR_F64) {
     double x = u2d(b);
+    if (isnan(x)) return (b & 0x7FFFFFFFFFFFFFFFull) | 0x0008000000000000ull;
+    if (isinf(x) && x < 0) return 0xFFF8000000000000ull;
     double t = 1.0 + fabs(x);
     return d2u(x + t);
   }
   float x = as_f32(dtype, b);
+  if (isnan(x)) return from_f32(dtype, u2f((f2u(x) & 0x7FFFFFFFu) | 0x00400000u));
+  if (isinf(x) && x < 0) return from_f32(dtype, u2f(0xFFC00000u));
   float t = 1.0f + fabsf(x);
   return from_f32(dtype, x + t);
 }

@@ -137,3 +137,35 @@ def test_window_equals_slice_of_full(oracle):
         for off, m in [(0, 7), (999, 5), (3999, 97)]:
             part = oracle.perturb(1, 2, "f32", op, ref[off:off + m], offset=off, **kw)
             assert np.array_equal(part, full[off:off + m]), (op, off)
+
+
+def test_fault_step_on_nan_and_infinite_references(oracle):
+    """The fault step x + (1 + |x|) on references that are not finite, per
+    element format: +Inf stays +Inf; -Inf gives the invalid operation's quiet
+    NaN with the sign bit set and no payload; a NaN gives its magnitude with
+    the quiet bit set (signalling NaNs quieted, sign cleared, payload kept),
+    then the format's NaN rule for bf16 and fp16 (their fp32 value narrowed).
+    Finite references: the sum in the element's arithmetic (numpy)."""
+    cases = {
+        "f64": (np.uint64, np.float64, 0x7FF0000000000000, 0xFFF0000000000000, 0xFFF8000000000000, 1 << 51,
+                [0x7FF8000000000000, 0xFFF8000000000000, 0x7FF8000000000001, 0xFFF4000000000000,
+                 0x7FF0000000000001, 0xFFF0000000000123]),
+        "f32": (np.uint32, np.float32, 0x7F800000, 0xFF800000, 0xFFC00000, 1 << 22,
+                [0x7FC00000, 0xFFC00000, 0x7FC00001, 0xFFA00000, 0x7F800001, 0xFF800123]),
+    }
+    for dtype, (st, ft, pinf, ninf, inv, quiet, nans) in cases.items():
+        finite = np.array([0.0, -0.0, 1.0, -1.5, 3e-300 if dtype == "f64" else 3e-38, -7.25], dtype=ft)
+        ref = np.concatenate([np.array([pinf, ninf] + nans, dtype=st), finite.view(st)])
+        c = oracle.perturb(0, 0, dtype, "fault_at", ref, idx=np.arange(ref.size, dtype=np.uint64))
+        sign = st(1) << st(8 * np.dtype(st).itemsize - 1)
+        assert c[0] == pinf and c[1] == inv
+        for k, v in enumerate(nans):
+            assert c[2 + k] == (st(v) & ~sign) | st(quiet), (dtype, hex(v), hex(int(c[2 + k])))
+        x = finite
+        assert np.array_equal(c[2 + len(nans):].view(ft), x + (ft(1) + np.abs(x)))
+    # bf16 and fp16: the fp32 result narrowed by the format's rules
+    for dtype, nan_in, want in (("bf16", [0xFF80, 0xFFC0, 0xFFA0, 0x7F81], [0xFFC0, 0x7FC0, 0x7FE0, 0x7FC1]),
+                                ("f16", [0xFC00, 0xFE00, 0xFD00, 0x7C01], [0xFE00, 0x7E00, 0x7F00, 0x7E01])):
+        ref = np.array(nan_in, dtype=np.uint16)
+        c = oracle.perturb(0, 0, dtype, "fault_at", ref, idx=np.arange(ref.size, dtype=np.uint64))
+        assert [int(v) for v in c] == want, (dtype, [hex(int(v)) for v in c])
