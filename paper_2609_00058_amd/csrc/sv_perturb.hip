@@ -103,14 +103,21 @@ __global__ __launch_bounds__(kBlock) void perturb_index_kernel(PerturbParams p, 
   } else if constexpr (DT == SV_I32 || DT == SV_U8 || DT == SV_I64) {
     out = y + 1u;                                   // FAULT_AT on integers, wrapping in their width
   } else if constexpr (DT == SV_F64) {
+    // FAULT_AT in fp64.  x + (1 + |x|) has two NaN operands when x is a NaN,
+    // and which one a sum returns is not fixed: the result is |x| quieted;
+    // -Inf + Inf is the invalid operation's NaN, sign set, no payload
     const double x = bits_f64(y);
     const double t = 1.0 + fabs(x);
-    out = f64_bits(x + t);                          // FAULT_AT in fp64
+    out = __builtin_isnan(x) ? ((y & 0x7FFFFFFFFFFFFFFFull) | 0x0008000000000000ull)
+          : x == -__builtin_inf() ? 0xFFF8000000000000ull : f64_bits(x + t);
   } else if (p.op == SV_OP_ADD_AT) {
     out = narrow<DT>(widen<DT>(y) + p.value);
   } else {
+    // FAULT_AT: always outside any sane tolerance; NaN and -Inf as for fp64
     const float x = widen<DT>(y);
-    out = narrow<DT>(x + (1.0f + fabsf(x)));        // FAULT_AT: always outside any sane tolerance
+    const float r = __builtin_isnan(x) ? as_f32((as_u32(x) & 0x7FFFFFFFu) | 0x00400000u)
+                    : x == -__builtin_inff() ? as_f32(0xFFC00000u) : x + (1.0f + fabsf(x));
+    out = narrow<DT>(r);
   }
   store_bits<DT>(cand, i, out);
 }
