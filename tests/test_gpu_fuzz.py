@@ -6,9 +6,10 @@ elements into their buffers (the element path), candidates equal to their
 reference, aliased to it, or differing with special values mixed in, and
 random tolerances and equal_nan.  Each batch goes through the plain batched
 check, the stop-at-first check, a submitted check waited for later, and two of
-its segments through the single-tensor check.  Reports must equal the
-oracle's (the fp64 error sum within 1e-12 relative); a failing segment of a
-stop-at-first check carries the exact first index.
+its segments through the single-tensor check and the check without
+allocation.  Reports must equal the oracle's (the fp64 error sum within 1e-12
+relative); a failing segment of a stop-at-first check carries the exact first
+index.
 """
 import numpy as np
 import pytest
@@ -85,6 +86,7 @@ def test_random_batches_match_the_oracle(oracle, seed):
             assert g["first_mismatch"] == w["first_mismatch"]
     for j in rng.choice(len(segs), size=min(2, len(segs)), replace=False):
         same_report(sv.compare(*segs[int(j)]), want[int(j)])
+        same_report(sv.compare_noalloc(*segs[int(j)]), want[int(j)])
 
 
 def test_twenty_thousand_small_segments(oracle):
