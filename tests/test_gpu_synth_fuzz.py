@@ -80,3 +80,39 @@ def test_random_requests_match_the_oracle(oracle):
     sv.synth_batched([(o, r["seed"], r["stream"], r["dist"], r["params"]) for o, r, _ in batch])
     for k, (o, r, w0) in enumerate(batch):
         assert np.array_equal(bits(o), w0.view(bits(o).dtype)), (k, r)
+
+
+EXTREME = [("uniform", "f32", dict(a=-3e38, b=3e38)), ("uniform", "f64", dict(a=-1.7e308, b=1.7e308)),
+           ("uniform", "bf16", dict(a=1.0, b=1.0)), ("uniform", "f32", dict(a=1.0, b=1.0000001)),
+           ("uniform", "f32", dict(a=0.0, b=1e-40)), ("uniform", "f16", dict(a=-1e6, b=1e6)),
+           ("uniform", "f64", dict(a=-1e-310, b=1e-310)), ("normal", "f32", dict(mean=0.0, std=1e38)),
+           ("normal", "f32", dict(mean=3e38, std=1e38)), ("normal", "bf16", dict(mean=-3e38, std=1e38)),
+           ("normal", "f16", dict(mean=0.0, std=1e5)), ("normal", "f64", dict(mean=1e300, std=1e38)),
+           ("normal", "f32", dict(mean=0.0, std=0.0)), ("normal", "f32", dict(mean=1e-45, std=1e-45)),
+           ("special", "f32", dict(mean=0.0, std=1e38, p_nan=0.25, p_inf=0.25, p_denorm=0.25, p_zero=0.25)),
+           ("special", "f16", dict(mean=6e4, std=1e4, p_nan=0.0, p_inf=0.0, p_denorm=0.5, p_zero=0.0)),
+           ("int_range", "i32", dict(lo=5, hi=5)), ("int_range", "u8", dict(lo=255, hi=255)),
+           ("int_range", "i64", dict(lo=-2 ** 63, hi=-2 ** 63 + 1)), ("permutation", "u8", dict(lo=7, hi=7))]
+
+
+@pytest.mark.parametrize("dist,dtype,params", EXTREME)
+def test_extreme_parameters_agree_with_the_oracle(oracle, dist, dtype, params):
+    """Spans and scales at the ends of the types: the library refuses exactly
+    what the oracle refuses, and otherwise writes the oracle's bits (values
+    that overflow to infinity included)."""
+    n = 40_001 if dist != "permutation" else 1
+    try:
+        want = oracle.synth(3, 4, dtype, dist, oracle.dist_params(**params), n)
+    except oracle.OracleError:
+        want = None
+    out = empty(n, dtype)
+    try:
+        sv.synth(out, 3, 4, dist, **params)
+        got = bits(out)
+    except sv.SVError:
+        got = None
+    if want is None:
+        assert got is None, "the library accepted what the oracle refuses"
+    else:
+        assert got is not None, "the library refused what the oracle accepts"
+        assert np.array_equal(got, want.view(got.dtype))
