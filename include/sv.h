@@ -314,7 +314,7 @@ enum {
 typedef struct {
   int32_t op;
   double p;             /* selection probability of ops 1..3, in [0, 1]           */
-  double value;         /* ADD_AT delta; SCALE half-width                         */
+  double value;         /* ADD_AT delta; SCALE half-width; a finite fp32 value    */
   uint32_t bits;        /* SET_AT pattern                                         */
   const uint64_t *idx;  /* host: element indices of ops 4..6, each < n            */
   uint64_t nidx;

@@ -787,6 +787,9 @@ int or_perturb(uint64_t seed, uint64_t stream, int32_t dtype,
   int op = plan->op;
   if (op < OR_OP_COPY || op > OR_OP_FAULT_AT) return -2;
   if (!op_supported(dtype, op)) return -2;
+  /* the scale width and the added delta are used as fp32 values: they must
+   * be finite there */
+  if ((op == OR_OP_SCALE || op == OR_OP_ADD_AT) && !isfinite((float)plan->value)) return -1;
   if (op <= OR_OP_SPECIAL_FLIP) {
     if (op != OR_OP_COPY && !(plan->p >= 0.0 && plan->p <= 1.0)) return -1;
     for (uint64_t k = 0; k < n; k++)

@@ -8,6 +8,7 @@ all bf16 values, and the Philox words that select elements.
 import math
 
 import numpy as np
+import pytest
 import torch
 
 F32_EDGE = np.array([0, 0x80000000, 1, 0x80000001, 0x007FFFFF, 0x807FFFFF, 0x00800000, 0x3F800000,
@@ -169,3 +170,16 @@ def test_fault_step_on_nan_and_infinite_references(oracle):
         ref = np.array(nan_in, dtype=np.uint16)
         c = oracle.perturb(0, 0, dtype, "fault_at", ref, idx=np.arange(ref.size, dtype=np.uint64))
         assert [int(v) for v in c] == want, (dtype, [hex(int(v)) for v in c])
+
+
+def test_scale_and_add_need_a_finite_fp32_value(oracle):
+    """The scale width and the added delta enter as fp32 values (fp32(1 + u)
+    with |u| <= value, fp32(y) + fp32(value)); a value that is NaN, infinite,
+    or overflows fp32 is refused, and the largest finite fp32 is accepted."""
+    ref = np.array([0x3F800000, 0x40000000], np.uint32)
+    idx = np.array([1], np.uint64)
+    for op in ("scale", "add_at"):
+        for bad in (float("nan"), float("inf"), -float("inf"), 1e300, -3.5e38):
+            with pytest.raises(oracle.OracleError):
+                oracle.perturb(0, 0, "f32", op, ref, p=1.0, value=bad, idx=idx)
+        oracle.perturb(0, 0, "f32", op, ref, p=1.0, value=float(np.finfo(np.float32).max), idx=idx)
