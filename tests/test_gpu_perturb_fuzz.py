@@ -73,3 +73,37 @@ def test_random_steps_match_the_oracle(oracle):
             done += 1
     print("perturb fuzz: %d steps compared, %d refused by both" % (done, refused), flush=True)
     assert done >= 30
+
+
+EXTREME = [("ulp", dict(p=-0.1)), ("ulp", dict(p=1.5)), ("ulp", dict(p=float("nan"))), ("ulp", dict(p=1.0)),
+           ("scale", dict(p=1.0, value=float("inf"))), ("scale", dict(p=1.0, value=float("nan"))),
+           ("scale", dict(p=1.0, value=-1e-3)), ("scale", dict(p=1.0, value=0.0)), ("scale", dict(p=1.0, value=3e38)),
+           ("add_at", dict(value=float("inf"))), ("add_at", dict(value=float("nan"))), ("add_at", dict(value=1e300)),
+           ("special_flip", dict(p=1.0)), ("set_at", dict(bits=0xFFFFFFFF))]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("op,kw", EXTREME)
+def test_extreme_plans_agree_with_the_oracle(oracle, dtype, op, kw):
+    """Probabilities outside [0, 1] or NaN, infinite and NaN widths and deltas:
+    refused by the library exactly where the oracle refuses them, otherwise
+    the oracle's bits."""
+    n = 5000
+    ref = _reference(oracle, np.random.default_rng(9500), dtype, n)
+    idx = np.array([0, 17, 4999], dtype=np.uint64) if op in ("add_at", "set_at", "fault_at") else None
+    try:
+        want = oracle.perturb(8, 9, dtype, op, ref, ref.copy(), idx=idx, **kw)
+    except oracle.OracleError:
+        want = None
+    R = dev_bits(ref, dtype)
+    C = R.clone()
+    try:
+        sv.perturb(R, C, 8, 9, op, idx=idx, **kw)
+        got = bits(C)
+    except sv.SVError:
+        got = None
+    if want is None:
+        assert got is None, "the library accepted what the oracle refuses"
+    else:
+        assert got is not None, "the library refused what the oracle accepts"
+        assert np.array_equal(got, want.view(got.dtype))
