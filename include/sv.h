@@ -101,7 +101,7 @@ typedef struct {
   const void *cand;   /* device: candidate output K(x), same dtype and n */
   uint64_t n;         /* elements; 0 allowed                           */
   int32_t dtype;      /* any SV_ element type                           */
-  double rtol, atol;  /* finite, >= 0; ignored for the integer types    */
+  double rtol, atol;  /* finite, >= 0; ignored (and not checked) for the integer types */
   int32_t equal_nan;  /* nonzero: NaN vs NaN agrees                     */
 } sv_segment;
 

@@ -827,7 +827,9 @@ int or_compare(const void *ref, const void *cand, uint64_t n, int32_t dtype,
   if (!r) return -1;
   if (!valid_dtype(dtype)) return -2;
   if (n && (!ref || !cand)) return -1;
-  if (!(rtol >= 0.0) || !(atol >= 0.0) || isinf(rtol) || isinf(atol)) return -1;
+  /* integer types compare exactly and ignore the tolerances, which are then
+   * not checked either */
+  if (!is_int(dtype) && (!(rtol >= 0.0) || !(atol >= 0.0) || isinf(rtol) || isinf(atol))) return -1;
   memset(r, 0, sizeof(*r));
   r->n = n;
   r->first_mismatch = -1;

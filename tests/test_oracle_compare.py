@@ -180,6 +180,18 @@ def test_invalid_tolerances_rejected(oracle):
             oracle.compare(x, x, "f32", rtol, atol, False)
 
 
+def test_integer_types_ignore_the_tolerances_entirely(oracle):
+    """Integer elements agree only when equal: the tolerances play no part, and
+    values that a float check refuses (negative, NaN, infinite) are not refused
+    either; the report is the one of rtol = atol = 0."""
+    y = np.array([5, -7, 2 ** 31 - 1, 0], np.int32).view(np.uint32)
+    a = np.array([5, -6, 2 ** 31 - 1, 3], np.int32).view(np.uint32)
+    want = oracle.compare(y, a, "i32", 0.0, 0.0, False)
+    assert want["mismatches"] == 2 and want["first_mismatch"] == 1
+    for rtol, atol in [(-1e-5, 0.0), (0.0, -1.0), (math.nan, 0.0), (0.0, math.inf), (1e300, 1e300)]:
+        assert oracle.compare(y, a, "i32", rtol, atol, False) == want
+
+
 # The largest finite fp64 value plus half an ulp: every exact real at or above
 # it rounds to +Inf under round-to-nearest-even.
 OVERFLOW_AT = Fraction(2) ** 1024 - Fraction(2) ** 970
