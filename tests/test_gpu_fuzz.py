@@ -115,3 +115,34 @@ def test_twenty_thousand_small_segments(oracle):
             same_report(g, w)
         else:
             assert g["mismatches"] == 1 and g["first_mismatch"] == w["first_mismatch"], (g, w)
+
+
+TOL_EXTREMES = [(0.0, 0.0), (1e308, 0.0), (0.0, 1e308), (1.7976931348623157e308, 1.7976931348623157e308),
+                (5e-324, 5e-324), (-0.0, -0.0), (-1e-9, 0.0), (0.0, -1e-9), (float("nan"), 0.0),
+                (0.0, float("nan")), (float("inf"), 0.0), (0.0, float("inf"))]
+
+
+@pytest.mark.parametrize("rtol,atol", TOL_EXTREMES)
+@pytest.mark.parametrize("dtype", ["f32", "f64", "i32"])
+def test_extreme_tolerances_agree_with_the_oracle(oracle, dtype, rtol, atol):
+    """Tolerances at the ends of fp64 and outside the allowed range: refused by
+    the library exactly where the oracle refuses them, otherwise the oracle's
+    report (single and batched)."""
+    rng = np.random.default_rng(9600)
+    y, a = _values(rng, 3001, dtype)
+    try:
+        want = oracle.compare(y, a, dtype, rtol, atol, True)
+    except oracle.OracleError:
+        want = None
+    Y, A = dev_bits(y, dtype), dev_bits(a, dtype)
+    for call in (lambda: sv.compare(Y, A, rtol, atol, True),
+                 lambda: sv.compare_batched([(Y, A, rtol, atol, True)])[0]):
+        try:
+            got = call()
+        except sv.SVError:
+            got = None
+        if want is None:
+            assert got is None, "the library accepted what the oracle refuses"
+        else:
+            assert got is not None, "the library refused what the oracle accepts"
+            same_report(got, want)
