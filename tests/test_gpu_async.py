@@ -259,8 +259,9 @@ def test_deferred_reductions_are_finished_by_whatever_comes_next():
 def test_random_sequences_of_submits_waits_and_queries():
     # Seeded random interleavings of everything that touches the pending checks:
     # submits of tensors with and without a separate reduction, empty and
-    # batched submits, synchronous checks, waits and readiness queries in any
-    # order, on two streams.  Every report must equal the synchronous one.
+    # batched submits, synchronous checks, checks without allocation, waits
+    # and readiness queries in any order, on two streams.  Every report must
+    # equal the synchronous one.
     rng = np.random.default_rng(123)
     pairs = [_pair(n, 200 + k, p=0.01) for k, n in enumerate([(1 << 20) + 1, 1 << 21, 70001, 4099, 0, (1 << 19) + 7])]
     batch = [(r, c, 1e-8, 0.0, False) for r, c in pairs[:4]]
@@ -272,7 +273,7 @@ def test_random_sequences_of_submits_waits_and_queries():
     pending = []                                                     # (ticket, expected)
     print("random sequences", flush=True)
     for step in range(600):
-        op = rng.integers(0, 10)
+        op = rng.integers(0, 11)
         s = streams[int(rng.integers(0, 2))] if rng.random() < 0.15 else streams[0]
         with torch.cuda.stream(s):
             if op <= 4 and len(pending) < sv.SV_MAX_PENDING_CHECKS:
@@ -287,6 +288,9 @@ def test_random_sequences_of_submits_waits_and_queries():
             elif op == 7 and pending:
                 t, w = pending[int(rng.integers(0, len(pending)))]
                 t.ready()
+            elif op == 10:                                   # the check without allocation, between them
+                k = int(rng.integers(0, len(pairs)))
+                assert sv.compare_noalloc(*pairs[k], 1e-8, 0.0) == want[k], step
             elif pending:
                 t, w = pending.pop(int(rng.integers(0, len(pending))))
                 assert t.wait() == w, step
