@@ -325,3 +325,52 @@ def test_repeated_batches_reuse_their_tables_on_any_stream(oracle):
         assert sv.compare_batched(a) == want_a and sv.compare_batched(b) == want_b
         assert sv.compare_batched(a) == want_a and sv.compare_batched(a) == want_a
         assert sv.compare_batched_submit(b).wait() == want_b
+
+
+def test_threads_synthesize_batches_on_their_own_streams(oracle):
+    """Four threads, each on a stream of its own, launch batched syntheses of
+    changing job lists (so the shared job table is rewritten while other
+    threads' batches may still read it), single-tensor syntheses and batched
+    checks, then every output is compared with the oracle."""
+    from concurrent.futures import ThreadPoolExecutor
+    from gpu_run import bits, empty
+    kinds = [("f32", "normal", dict(mean=5.0, std=10.0)), ("bf16", "uniform", dict(a=-4.0, b=4.0)),
+             ("i32", "int_range", dict(lo=-100, hi=10 ** 6)), ("f16", "special", dict(mean=0.0, std=1.0, p_nan=0.1)),
+             ("u8", "int_range", dict(lo=0, hi=255)), ("f64", "uniform", dict(a=0.0, b=1.0))]
+
+    def worker(k):
+        rng = np.random.default_rng(9700 + k)
+        stream = torch.cuda.Stream()
+        made = []
+        with torch.cuda.stream(stream):
+            for it in range(20):
+                jobs = []
+                for j in range(int(rng.integers(1, 7))):
+                    dtype, dist, params = kinds[int(rng.integers(0, len(kinds)))]
+                    n = int(rng.integers(0, 50000))
+                    out = empty(n, dtype)
+                    seed, sid = int(rng.integers(0, 2 ** 62)), int(rng.integers(0, 2 ** 62))
+                    jobs.append((out, seed, sid, dist, params))
+                    made.append((out, seed, sid, dtype, dist, params))
+                sv.synth_batched(jobs)
+                if it % 4 == 0:
+                    dtype, dist, params = kinds[int(rng.integers(0, len(kinds)))]
+                    out = empty(int(rng.integers(1, 30000)), dtype)
+                    seed = int(rng.integers(0, 2 ** 62))
+                    sv.synth(out, seed, 1, dist, **params)
+                    made.append((out, seed, 1, dtype, dist, params))
+                if it % 5 == 0:
+                    segs = [(o, o, 0.0, 0.0, True) for o, *_ in made[-3:]]
+                    assert all(r["mismatches"] == 0 for r in sv.compare_batched(segs))
+        stream.synchronize()
+        return made
+
+    print("threads synthesize", flush=True)
+    with ThreadPoolExecutor(4) as ex:
+        results = list(ex.map(worker, range(4)))
+    torch.cuda.synchronize()
+    for made in results:
+        for out, seed, sid, dtype, dist, params in made:
+            want = oracle.synth(seed, sid, dtype, dist, oracle.dist_params(**params), out.numel())
+            got = bits(out)
+            assert np.array_equal(got, want.view(got.dtype)), (dtype, dist, out.numel())
