@@ -467,7 +467,9 @@ enum { SV_PROF_SYNTH = 0, SV_PROF_COMPARE = 1, SV_PROF_PERTURB = 2, SV_PROF_FINA
 int sv_profile_enable(int32_t on);
 int sv_profile_read(int32_t kind, uint64_t *count, double *total_ms);
 
-/* Frees the scratch areas of every device.  Later calls allocate again. */
+/* Frees the scratch areas of every device, after waiting for the device's
+ * work.  Later calls allocate again.  Checks still pending are forgotten:
+ * sv_compare_wait on their tickets then fails with SV_ERR_INVALID_ARG. */
 int sv_shutdown(void);
 
 /*
