@@ -82,7 +82,7 @@ EXTREME = [("ulp", dict(p=-0.1)), ("ulp", dict(p=1.5)), ("ulp", dict(p=float("na
            ("special_flip", dict(p=1.0)), ("set_at", dict(bits=0xFFFFFFFF))]
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dtype", TYPES)
 @pytest.mark.parametrize("op,kw", EXTREME)
 def test_extreme_plans_agree_with_the_oracle(oracle, dtype, op, kw):
     """Probabilities outside [0, 1] or NaN, infinite and NaN widths and deltas:

@@ -92,15 +92,24 @@ EXTREME = [("uniform", "f32", dict(a=-3e38, b=3e38)), ("uniform", "f64", dict(a=
            ("special", "f32", dict(mean=0.0, std=1e38, p_nan=0.25, p_inf=0.25, p_denorm=0.25, p_zero=0.25)),
            ("special", "f16", dict(mean=6e4, std=1e4, p_nan=0.0, p_inf=0.0, p_denorm=0.5, p_zero=0.0)),
            ("int_range", "i32", dict(lo=5, hi=5)), ("int_range", "u8", dict(lo=255, hi=255)),
-           ("int_range", "i64", dict(lo=-2 ** 63, hi=-2 ** 63 + 1)), ("permutation", "u8", dict(lo=7, hi=7))]
+           ("int_range", "i64", dict(lo=-2 ** 63, hi=-2 ** 63 + 1)), ("permutation", "u8", dict(lo=7, hi=7)),
+           ("int_range", "i64", dict(lo=-2 ** 63, hi=2 ** 63 - 1)), ("int_range", "u8", dict(lo=0, hi=255)),
+           ("permutation", "u8", dict(lo=0, hi=255)), ("permutation", "i32", dict(lo=-2 ** 31, hi=2 ** 31 - 1)),
+           ("permutation", "i64", dict(lo=-2 ** 63, hi=-2 ** 63 + 2 ** 60 - 1)),
+           ("permutation", "i64", dict(lo=2 ** 63 - 2 ** 60, hi=2 ** 63 - 1)),
+           ("uniform", "f16", dict(a=-65504.0, b=65504.0)), ("uniform", "bf16", dict(a=-3e38, b=3e38)),
+           ("normal", "f64", dict(mean=0.0, std=3.4e38)),
+           ("special", "bf16", dict(mean=0.0, std=1.0, p_nan=0.0, p_inf=0.0, p_denorm=1.0, p_zero=0.0)),
+           ("special", "f64", dict(mean=0.0, std=1.0, p_nan=1.0, p_inf=0.0, p_denorm=0.0, p_zero=0.0))]
 
 
 @pytest.mark.parametrize("dist,dtype,params", EXTREME)
 def test_extreme_parameters_agree_with_the_oracle(oracle, dist, dtype, params):
-    """Spans and scales at the ends of the types: the library refuses exactly
-    what the oracle refuses, and otherwise writes the oracle's bits (values
-    that overflow to infinity included)."""
-    n = 40_001 if dist != "permutation" else 1
+    """Spans and scales at the ends of the types, whole-type integer ranges and
+    permutation domains up to 2^60 values: the library refuses exactly what
+    the oracle refuses, and otherwise writes the oracle's bits (values that
+    overflow to infinity included)."""
+    n = 40_001 if dist != "permutation" else min(40_001, params["hi"] - params["lo"] + 1)
     try:
         want = oracle.synth(3, 4, dtype, dist, oracle.dist_params(**params), n)
     except oracle.OracleError:
