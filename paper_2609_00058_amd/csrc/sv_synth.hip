@@ -312,15 +312,45 @@ __device__ __forceinline__ u32x4 overlay_vector(const SpecialClasses &cls, uint3
   return x;
 }
 
-template <bool kNarrow, bool kNT>
+// The two 16-bit values (first in the low half) of the fp32 values lo, hi in
+// a narrow output type: the hardware conversions for values that cannot be
+// NaN (the normal values of vectors without candidates), the conversions with
+// the NaN rules for the rest.
+template <int DT>
+__device__ __forceinline__ uint32_t narrow_pair_not_nan(uint32_t lo, uint32_t hi) {
+  if constexpr (DT == SV_BF16) {
+    return bf16x2_rne_not_nan(lo, hi);
+  } else {
+    asm("" : "+v"(lo), "+v"(hi));   // keep the fp32 rounding of the values
+    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)as_f32(lo)) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)as_f32(hi)) << 16);
+  }
+}
+template <int DT>
+__device__ __forceinline__ uint32_t narrow_pair(uint32_t lo, uint32_t hi) {
+  if constexpr (DT == SV_BF16) return bf16_rne(lo) | (bf16_rne(hi) << 16);
+  else return f16_rne(lo) | (f16_rne(hi) << 16);
+}
+
+// DT: fp32, bf16 or fp16 output.  A lane's kGroup slots are normal blocks:
+// for fp32 one block per 16-byte vector, so kGroup vectors; for the 16-bit
+// types two blocks per vector (eight elements), so kGroup / 2 vectors, slot g
+// being half g % 2 of vector g / 2.  The list is one of blocks either way;
+// for the 16-bit types the overlay pass leaves a listed block's four final
+// values in the entry already converted (two words).
+template <int DT, bool kNarrow, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                                u32x4 *__restrict__ out, uint32_t rounds) {
   load_sincos_table();
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
+  constexpr uint32_t kBpv = DT == SV_F32 ? 1 : 2;   // normal blocks per 16-byte vector
+  constexpr uint32_t kVecs = kGroup / kBpv;         // vectors per lane per group
+  static_assert(kGroup % kBpv == 0, "a group holds whole vectors");
   constexpr int kWaves = kBlock / kWave;
   constexpr uint32_t kSlots = kSpecialList;       // list entries per wave
-  // entry: [0] a listed vector's normal values, then its final ones; [1].xy
-  // its offset in the tile and its gate bytes (one address serves both)
+  // entry: [0] a listed block's normal values, then its final ones; [1].xy
+  // its offset in the tile (in blocks) and its gate bytes (one address
+  // serves both)
   __shared__ u32x4 list[kWaves][kSlots][2];
   const uint32_t lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   u32x4 (*lw)[2] = list[wave];
@@ -328,19 +358,22 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
   const SpecialClasses cls = special_classes(p);
   const uint32_t gate = p.gate;
   const float mean = in_vgpr(p.mean);
-  const Idx tile = (Idx)rounds * kBlock;          // rounds: a multiple of kGroup
+  const Idx tile = (Idx)rounds * kBlock;          // rounds: a multiple of kVecs
   const Idx c0 = (Idx)p.c0;
   const auto group = [&](Idx t0, uint32_t r0, auto whole_tile) {
     constexpr bool kWhole = decltype(whole_tile)::value;   // every vector of the tile is in range
     u32x4 v[kGroup];
-    u32x4 *ent[kGroup];                           // the listed vectors' entries
+    u32x4 *ent[kGroup];                           // the listed blocks' entries
     bool listed[kGroup];
+    bool done[kGroup];                            // 16-bit types: overlaid and converted here (list full)
     uint32_t count = 0;                           // wave-uniform
 #pragma unroll
     for (uint32_t g = 0; g < kGroup; ++g) {
-      const uint32_t off = (r0 + g) * kBlock + threadIdx.x;
-      const Idx u = t0 + (Idx)off;
-      const u32x4 w = philox_block(key, (uint64_t)(c0 + u));
+      const uint32_t vo = (r0 + g / kBpv) * kBlock + threadIdx.x;   // the vector's offset in the tile
+      const uint32_t off = vo * kBpv + g % kBpv;                     // the block's
+      const Idx u = t0 + (Idx)vo;
+      const Idx blk = c0 + t0 * (Idx)kBpv + (Idx)off;
+      const u32x4 w = philox_block(key, (uint64_t)blk);
       float zc0, zs0, zc1, zs1;
       box_muller(w.x, w.y, zc0, zs0);
       box_muller(w.z, w.w, zc1, zs1);
@@ -348,6 +381,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
                    as_u32(__builtin_fmaf(p.std, zc1, mean)), as_u32(__builtin_fmaf(p.std, zs1, mean))};
       const uint32_t low = min(min(w.x & 0xFFu, w.y & 0xFFu), min(w.z & 0xFFu, w.w & 0xFFu));
       listed[g] = low < gate && (kWhole || u < (Idx)nvec);
+      done[g] = false;
       const uint64_t m = __ballot(listed[g]);
       const uint32_t nm = (uint32_t)__popcll(m);
       if (count + nm <= kSlots) {
@@ -358,29 +392,52 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
         }
         count += nm;
       } else if (listed[g]) {
-        // the list is full (a mix with many candidates): this vector's class block here
-        const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)(c0 + u));
+        // the list is full (a mix with many candidates): this block's class block here
+        const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)blk);
         v[g] = overlay_vector(cls, gate, q, gate_bytes(w), v[g]);
+        if constexpr (DT != SV_F32) {
+          v[g].x = narrow_pair<DT>(v[g].x, v[g].y);
+          v[g].y = narrow_pair<DT>(v[g].z, v[g].w);
+          done[g] = true;
+        }
         listed[g] = false;
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    for (uint32_t base = 0; base < count; base += kWave) {   // the listed vectors, one per lane
+    for (uint32_t base = 0; base < count; base += kWave) {   // the listed blocks, one per lane
       const uint32_t e = base + lane;
       if (e < count) {
         const u32x2 k = *(const u32x2 *)&lw[e][1];
-        const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)(Idx)(c0 + t0 + (Idx)k.x));
-        lw[e][0] = overlay_vector(cls, gate, q, k.y, lw[e][0]);
+        const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)(Idx)(c0 + t0 * (Idx)kBpv + (Idx)k.x));
+        const u32x4 f = overlay_vector(cls, gate, q, k.y, lw[e][0]);
+        if constexpr (DT == SV_F32)
+          lw[e][0] = f;
+        else
+          *(u32x2 *)&lw[e][0] = u32x2{narrow_pair<DT>(f.x, f.y), narrow_pair<DT>(f.z, f.w)};
       }
     }
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (uint32_t g = 0; g < kGroup; ++g) {
-      const Idx u = t0 + (Idx)((r0 + g) * kBlock + threadIdx.x);
-      if (listed[g]) v[g] = ent[g][0];
-      if (kWhole || u < (Idx)nvec) store_vec<kNT>(out, u, v[g]);
+    for (uint32_t j = 0; j < kVecs; ++j) {
+      const Idx u = t0 + (Idx)((r0 + j) * kBlock + threadIdx.x);
+      u32x4 o;
+      if constexpr (DT == SV_F32) {
+        if (listed[j]) v[j] = ent[j][0];
+        o = v[j];
+      } else {
+        u32x2 h[2];
+#pragma unroll
+        for (uint32_t b = 0; b < 2; ++b) {
+          const uint32_t g = 2 * j + b;
+          h[b] = u32x2{narrow_pair_not_nan<DT>(v[g].x, v[g].y), narrow_pair_not_nan<DT>(v[g].z, v[g].w)};
+          if (done[g]) h[b] = u32x2{v[g].x, v[g].y};
+          if (listed[g]) h[b] = *(const u32x2 *)&ent[g][0];
+        }
+        o = u32x4{h[0].x, h[0].y, h[1].x, h[1].y};
+      }
+      if (kWhole || u < (Idx)nvec) store_vec<kNT>(out, u, o);
     }
     // the list is rewritten by the next group only after every lane has read it
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -388,19 +445,51 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
   };
   for (Idx t0 = (Idx)blockIdx.x * tile; t0 < (Idx)nvec; t0 += (Idx)gridDim.x * tile) {
     if (t0 + tile <= (Idx)nvec) {
-      for (uint32_t r0 = 0; r0 < rounds; r0 += kGroup) group(t0, r0, std::true_type{});
+      for (uint32_t r0 = 0; r0 < rounds; r0 += kVecs) group(t0, r0, std::true_type{});
     } else {
-      for (uint32_t r0 = 0; r0 < rounds; r0 += kGroup) group(t0, r0, std::false_type{});
+      for (uint32_t r0 = 0; r0 < rounds; r0 += kVecs) group(t0, r0, std::false_type{});
     }
   }
   // the ragged tail elements, one per thread of the first threads of the grid
-  const uint64_t i = nvec * 4 + (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+  constexpr uint32_t kPerVec = 4 * kBpv;
+  const uint64_t i = nvec * kPerVec + (uint64_t)blockIdx.x * kBlock + threadIdx.x;
   if (i < n) {
     const uint64_t g = p.e0 + i;
     uint32_t e[4];
     block_values<SV_SPECIAL>(p, g / 4, e);
-    ((uint32_t *)out)[i] = e[g % 4];
+    if constexpr (DT == SV_F32)
+      ((uint32_t *)out)[i] = e[g % 4];
+    else if constexpr (DT == SV_BF16)
+      ((uint16_t *)out)[i] = (uint16_t)bf16_rne(e[g % 4]);
+    else
+      ((uint16_t *)out)[i] = (uint16_t)f16_rne(e[g % 4]);
   }
+}
+
+// Special values into a 16-byte aligned output whose window starts on a
+// block, through synth_special_kernel: whole groups of vectors per thread in
+// a tile; 32-bit indices where every block index and vector offset fits.
+template <int DT>
+static hipError_t launch_special(const SynthParams &p, uint64_t n, void *out, int cus, bool nt, hipStream_t stream) {
+  constexpr uint64_t kBpv = DT == SV_F32 ? 1 : 2, V = 4 * kBpv, kVecs = kGroup / kBpv;
+  const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
+  const uint64_t nvec = n / V;
+  const uint32_t rounds = synth_tile_rounds(nvec, cus);
+  const uint32_t r4 = (uint32_t)((rounds + kVecs - 1) / kVecs * kVecs);
+  const uint64_t tile4 = (uint64_t)r4 * kBlock;
+  const uint64_t blocks4 = std::max<uint64_t>(std::min<uint64_t>((nvec + tile4 - 1) / tile4, max_blocks),
+                                              (n - nvec * V + kBlock - 1) / kBlock);   // the tail needs < V threads
+  const bool narrow4 = p.c0 + (nvec + tile4) * kBpv < (1ull << 32) && (blocks4 * tile4 + nvec) * kBpv < (1ull << 32);
+  const dim3 g4((unsigned)blocks4), b4(kBlock);
+  if (narrow4 && nt)
+    hipLaunchKernelGGL((synth_special_kernel<DT, true, true>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
+  else if (narrow4)
+    hipLaunchKernelGGL((synth_special_kernel<DT, true, false>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
+  else if (nt)
+    hipLaunchKernelGGL((synth_special_kernel<DT, false, true>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
+  else
+    hipLaunchKernelGGL((synth_special_kernel<DT, false, false>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
+  return hipGetLastError();
 }
 
 // Every element, one per thread (outputs that are not 16-byte aligned).
@@ -430,24 +519,7 @@ static hipError_t launch_typed(const SynthParams &p0, uint64_t n, void *out, int
     const uint64_t tile = (uint64_t)rounds * kBlock;
     const uint64_t tblocks = std::max<uint64_t>(std::min<uint64_t>((nvec + tile - 1) / tile, max_blocks),
                                                 (n - nvec * V + kBlock - 1) / kBlock);   // the tail needs < V threads
-    if constexpr (DIST == SV_SPECIAL && DT == SV_F32) {
-      // whole groups of kGroup vectors per thread in a tile
-      const uint32_t r4 = (rounds + kGroup - 1) / kGroup * kGroup;
-      const uint64_t tile4 = (uint64_t)r4 * kBlock;
-      const uint64_t blocks4 = std::max<uint64_t>(std::min<uint64_t>((nvec + tile4 - 1) / tile4, max_blocks),
-                                                  (n - nvec * V + kBlock - 1) / kBlock);
-      const bool narrow4 = p.c0 + nvec + tile4 < (1ull << 32) && blocks4 * tile4 + nvec < (1ull << 32);
-      const dim3 g4((unsigned)blocks4), b4(kBlock);
-      if (narrow4 && nt)
-        hipLaunchKernelGGL((synth_special_kernel<true, true>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
-      else if (narrow4)
-        hipLaunchKernelGGL((synth_special_kernel<true, false>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
-      else if (nt)
-        hipLaunchKernelGGL((synth_special_kernel<false, true>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
-      else
-        hipLaunchKernelGGL((synth_special_kernel<false, false>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
-      return hipGetLastError();
-    }
+    if constexpr (DIST == SV_SPECIAL) return launch_special<DT>(p, n, out, cus, nt, stream);
     const bool narrow = p.c0 + (nvec + tile) * B < (1ull << 32) && tblocks * tile + nvec < (1ull << 32);
     const dim3 g((unsigned)tblocks), b(kBlock);
     if (narrow && nt)
@@ -598,6 +670,8 @@ static hipError_t launch_wide(const SynthParams &p0, uint64_t n, void *out, int 
   const bool nt = n * (16 / V) >= SV_SYNTH_NT_BYTES;
   constexpr uint64_t W = V >= E ? V : E;          // elements per group of vectors
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
+  if constexpr (DIST == SV_SPECIAL && DT == SV_F16)
+    if (((uintptr_t)out & 15u) == 0 && p.e0 % 4 == 0) return launch_special<DT>(p, n, out, cus, nt, stream);
   if (((uintptr_t)out & 15u) == 0 && p.e0 % E == 0) {
     const uint64_t ngroups = n / W;
     const uint64_t threads = std::max<uint64_t>(ngroups, n - ngroups * W);   // the tail needs < W threads

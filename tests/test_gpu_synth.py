@@ -36,6 +36,17 @@ CASES = [
     ("special", "f32", SPECIAL_MID),
     ("special", "f32", SPECIAL_ALL),
     ("special", "f32", dict(mean=0.0, std=1.0, p_nan=1.0)),
+    # the 16-bit types through the listing kernel: two blocks per 16-byte vector
+    ("special", "bf16", SPECIAL),
+    ("special", "bf16", SPECIAL_MID),
+    ("special", "bf16", SPECIAL_ALL),
+    ("special", "bf16", dict(mean=0.0, std=1.0, p_nan=1.0)),
+    ("special", "bf16", dict(mean=0.0, std=1e38)),
+    ("special", "f16", SPECIAL_HEAVY),
+    ("special", "f16", SPECIAL_MID),
+    ("special", "f16", SPECIAL_ALL),
+    ("special", "f16", dict(mean=0.0, std=1.0, p_inf=1.0)),
+    ("special", "f16", dict(mean=0.0, std=1e5, p_denorm=0.02)),
 ]
 SIZES = [1, 3, 4, 5, 8, 17, 1000, 4099, 65543, (1 << 20) + 3]
 
@@ -74,16 +85,18 @@ def test_synth_unaligned_outputs_and_guard(oracle, dist, dtype, params):
         assert np.all(allb[:off] == 0x5A5A) and np.all(allb[off + n:] == 0x5A5A)
 
 
-@pytest.mark.parametrize("dist,params", [("normal", dict(mean=5.0, std=10.0)), ("special", SPECIAL),
-                                         ("special", SPECIAL_MID)])
-def test_synth_far_window_with_64_bit_block_indices(oracle, dist, params):
+@pytest.mark.parametrize("dist,dtype,params", [("normal", "f32", dict(mean=5.0, std=10.0)),
+                                               ("special", "f32", SPECIAL), ("special", "f32", SPECIAL_MID),
+                                               ("special", "bf16", SPECIAL), ("special", "bf16", SPECIAL_MID),
+                                               ("special", "f16", SPECIAL), ("special", "f16", SPECIAL_ALL)])
+def test_synth_far_window_with_64_bit_block_indices(oracle, dist, dtype, params):
     # a window past element 2^40: Philox block indices above 2^32, so the kernels index in 64 bits;
     # large enough for whole tiles and a ragged last one
     n, off = (1 << 20) + 3, (1 << 40) + 12
-    print("far window", dist, params, flush=True)
-    g = empty(n, "f32")
+    print("far window", dist, dtype, params, flush=True)
+    g = empty(n, dtype)
     sv.synth_window(g, 11, 5, dist, off, **params)
-    want = oracle.synth(11, 5, "f32", dist, oracle.dist_params(**params), n, off)
+    want = oracle.synth(11, 5, dtype, dist, oracle.dist_params(**params), n, off)
     got = bits(g)
     assert np.array_equal(got, want), _diff(got, want)
 
@@ -127,19 +140,22 @@ def test_synth_full_size_sampled(oracle, dist, dtype, n, params):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("dist,params", [("normal", dict(mean=0.0, std=1.0)), ("special", SPECIAL)])
-def test_synth_far_window_of_1_gib_sampled(oracle, dist, params):
-    # 2^28 + 5 fp32 values past element 2^40: 64-bit block indices and the non-temporal stores of
-    # outputs of 1 GiB or more, together; sampled against the oracle element by element
-    n, off = (1 << 28) + 5, (1 << 40) + 12
-    print("far window 1 GiB", dist, flush=True)
-    g = empty(n, "f32")
+@pytest.mark.parametrize("dist,dtype,params", [("normal", "f32", dict(mean=0.0, std=1.0)),
+                                               ("special", "f32", SPECIAL), ("special", "bf16", SPECIAL),
+                                               ("special", "f16", SPECIAL_MID)])
+def test_synth_far_window_of_1_gib_sampled(oracle, dist, dtype, params):
+    # 1 GiB of values (2^28 + 5 fp32, 2^29 + 5 bf16 / fp16) past element 2^40: 64-bit block indices and
+    # the non-temporal stores of outputs of 1 GiB or more, together; sampled against the oracle element
+    # by element
+    n, off = (1 << 30) // (4 if dtype == "f32" else 2) + 5, (1 << 40) + 12
+    print("far window 1 GiB", dist, dtype, flush=True)
+    g = empty(n, dtype)
     sv.synth_window(g, 3, 9, dist, off, **params)
     rng = np.random.default_rng(77)
     idx = np.unique(np.concatenate([np.arange(4096), np.arange(n - 4096, n),
                                     rng.integers(0, n, 60000)])).astype(np.uint64)
     got = bits_at(g, idx)
-    want = oracle.synth_at(3, 9, "f32", dist, oracle.dist_params(**params), idx + np.uint64(off))
+    want = oracle.synth_at(3, 9, dtype, dist, oracle.dist_params(**params), idx + np.uint64(off))
     assert np.array_equal(got, want), _diff(got, want)
     del g
     torch.cuda.empty_cache()
@@ -163,10 +179,9 @@ def test_synth_batched_matches_single_calls_and_oracle(oracle):
     for ref, seed, stream, dist, params in singles:
         sv.synth(ref, seed, stream, dist, **params)
     for (out, seed, stream, dist, params), (ref, *_rest) in zip(jobs, singles):
-        assert torch.equal(out.view(torch.int16 if out.dtype == torch.bfloat16 else torch.int32),
-                           ref.view(torch.int16 if ref.dtype == torch.bfloat16 else torch.int32))
-    for out, seed, stream, dist, params in jobs[:12]:
-        dtype = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32"}[out.dtype]
+        assert np.array_equal(bits(out), bits(ref))
+    for out, seed, stream, dist, params in jobs[:12] + jobs[-12:]:
+        dtype = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32", torch.float16: "f16"}[out.dtype]
         want = oracle.synth(seed, stream, dtype, dist, oracle.dist_params(**params), out.numel())
         assert np.array_equal(bits(out), want)
     # back-to-back batches reuse the job table: the second must not see the first's jobs
