@@ -332,19 +332,21 @@ __device__ __forceinline__ uint32_t narrow_pair(uint32_t lo, uint32_t hi) {
   else return f16_rne(lo) | (f16_rne(hi) << 16);
 }
 
-// DT: fp32, bf16 or fp16 output.  A lane's kGroup slots are normal blocks:
-// for fp32 one block per 16-byte vector, so kGroup vectors; for the 16-bit
-// types two blocks per vector (eight elements), so kGroup / 2 vectors, slot g
-// being half g % 2 of vector g / 2.  The list is one of blocks either way;
-// for the 16-bit types the overlay pass leaves a listed block's four final
-// values in the entry already converted (two words).
+// DT: fp32, bf16, fp16 or fp64 output.  The kernel works in units: one
+// 16-byte vector for fp32 (one block) and for the 16-bit types (two blocks,
+// eight elements), two vectors for fp64 (one block).  A lane's kGroup slots
+// are normal blocks: kGroup units for fp32 and fp64; kGroup / 2 for the
+// 16-bit types, slot g being half g % 2 of unit g / 2.  The list is one of
+// blocks either way; for the 16-bit types the overlay pass leaves a listed
+// block's four final values in the entry already converted (two words);
+// fp64 widens the four fp32 values of every block as it stores them.
 template <int DT, bool kNarrow, bool kNT>
 __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, uint64_t nvec, uint64_t n,
                                                                u32x4 *__restrict__ out, uint32_t rounds) {
   load_sincos_table();
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
-  constexpr uint32_t kBpv = DT == SV_F32 ? 1 : 2;   // normal blocks per 16-byte vector
-  constexpr uint32_t kVecs = kGroup / kBpv;         // vectors per lane per group
+  constexpr uint32_t kBpv = DT == SV_BF16 || DT == SV_F16 ? 2 : 1;   // normal blocks per unit
+  constexpr uint32_t kVecs = kGroup / kBpv;         // units per lane per group
   static_assert(kGroup % kBpv == 0, "a group holds whole vectors");
   constexpr int kWaves = kBlock / kWave;
   constexpr uint32_t kSlots = kSpecialList;       // list entries per wave
@@ -395,7 +397,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
         // the list is full (a mix with many candidates): this block's class block here
         const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)blk);
         v[g] = overlay_vector(cls, gate, q, gate_bytes(w), v[g]);
-        if constexpr (DT != SV_F32) {
+        if constexpr (DT == SV_BF16 || DT == SV_F16) {
           v[g].x = narrow_pair<DT>(v[g].x, v[g].y);
           v[g].y = narrow_pair<DT>(v[g].z, v[g].w);
           done[g] = true;
@@ -411,7 +413,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
         const u32x2 k = *(const u32x2 *)&lw[e][1];
         const u32x4 q = philox_block(key, kSpecialClassBlocks + (uint64_t)(Idx)(c0 + t0 * (Idx)kBpv + (Idx)k.x));
         const u32x4 f = overlay_vector(cls, gate, q, k.y, lw[e][0]);
-        if constexpr (DT == SV_F32)
+        if constexpr (DT == SV_F32 || DT == SV_F64)
           lw[e][0] = f;
         else
           *(u32x2 *)&lw[e][0] = u32x2{narrow_pair<DT>(f.x, f.y), narrow_pair<DT>(f.z, f.w)};
@@ -426,6 +428,13 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
       if constexpr (DT == SV_F32) {
         if (listed[j]) v[j] = ent[j][0];
         o = v[j];
+      } else if constexpr (DT == SV_F64) {
+        if (listed[j]) v[j] = ent[j][0];
+        const uint64_t w0 = widen_f32_bits(v[j].x), w1 = widen_f32_bits(v[j].y);
+        const uint64_t w2 = widen_f32_bits(v[j].z), w3 = widen_f32_bits(v[j].w);
+        if (kWhole || u < (Idx)nvec)
+          store_vec<kNT>(out, 2 * u, u32x4{(uint32_t)w0, (uint32_t)(w0 >> 32), (uint32_t)w1, (uint32_t)(w1 >> 32)});
+        o = u32x4{(uint32_t)w2, (uint32_t)(w2 >> 32), (uint32_t)w3, (uint32_t)(w3 >> 32)};
       } else {
         u32x2 h[2];
 #pragma unroll
@@ -437,7 +446,7 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
         }
         o = u32x4{h[0].x, h[0].y, h[1].x, h[1].y};
       }
-      if (kWhole || u < (Idx)nvec) store_vec<kNT>(out, u, o);
+      if (kWhole || u < (Idx)nvec) store_vec<kNT>(out, DT == SV_F64 ? 2 * u + 1 : u, o);
     }
     // the list is rewritten by the next group only after every lane has read it
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -459,6 +468,8 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
     block_values<SV_SPECIAL>(p, g / 4, e);
     if constexpr (DT == SV_F32)
       ((uint32_t *)out)[i] = e[g % 4];
+    else if constexpr (DT == SV_F64)
+      ((uint64_t *)out)[i] = widen_f32_bits(e[g % 4]);
     else if constexpr (DT == SV_BF16)
       ((uint16_t *)out)[i] = (uint16_t)bf16_rne(e[g % 4]);
     else
@@ -471,7 +482,8 @@ __global__ __launch_bounds__(kBlock) void synth_special_kernel(SynthParams p, ui
 // a tile; 32-bit indices where every block index and vector offset fits.
 template <int DT>
 static hipError_t launch_special(const SynthParams &p, uint64_t n, void *out, int cus, bool nt, hipStream_t stream) {
-  constexpr uint64_t kBpv = DT == SV_F32 ? 1 : 2, V = 4 * kBpv, kVecs = kGroup / kBpv;
+  constexpr uint64_t kBpv = DT == SV_BF16 || DT == SV_F16 ? 2 : 1, V = 4 * kBpv, kVecs = kGroup / kBpv;
+  constexpr uint64_t kVpu = DT == SV_F64 ? 2 : 1;   // 16-byte vectors per unit
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
   const uint64_t nvec = n / V;
   const uint32_t rounds = synth_tile_rounds(nvec, cus);
@@ -479,7 +491,8 @@ static hipError_t launch_special(const SynthParams &p, uint64_t n, void *out, in
   const uint64_t tile4 = (uint64_t)r4 * kBlock;
   const uint64_t blocks4 = std::max<uint64_t>(std::min<uint64_t>((nvec + tile4 - 1) / tile4, max_blocks),
                                               (n - nvec * V + kBlock - 1) / kBlock);   // the tail needs < V threads
-  const bool narrow4 = p.c0 + (nvec + tile4) * kBpv < (1ull << 32) && (blocks4 * tile4 + nvec) * kBpv < (1ull << 32);
+  const bool narrow4 = p.c0 + (nvec + tile4) * kBpv < (1ull << 32) &&
+                       (blocks4 * tile4 + nvec) * kBpv * kVpu < (1ull << 32);
   const dim3 g4((unsigned)blocks4), b4(kBlock);
   if (narrow4 && nt)
     hipLaunchKernelGGL((synth_special_kernel<DT, true, true>), g4, b4, 0, stream, p, nvec, n, (u32x4 *)out, r4);
@@ -670,7 +683,7 @@ static hipError_t launch_wide(const SynthParams &p0, uint64_t n, void *out, int 
   const bool nt = n * (16 / V) >= SV_SYNTH_NT_BYTES;
   constexpr uint64_t W = V >= E ? V : E;          // elements per group of vectors
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
-  if constexpr (DIST == SV_SPECIAL && DT == SV_F16)
+  if constexpr (DIST == SV_SPECIAL && (DT == SV_F16 || DT == SV_F64))
     if (((uintptr_t)out & 15u) == 0 && p.e0 % 4 == 0) return launch_special<DT>(p, n, out, cus, nt, stream);
   if (((uintptr_t)out & 15u) == 0 && p.e0 % E == 0) {
     const uint64_t ngroups = n / W;

@@ -47,6 +47,12 @@ CASES = [
     ("special", "f16", SPECIAL_ALL),
     ("special", "f16", dict(mean=0.0, std=1.0, p_inf=1.0)),
     ("special", "f16", dict(mean=0.0, std=1e5, p_denorm=0.02)),
+    # fp64: one block per two 16-byte vectors, every value widened with the NaN rule
+    ("special", "f64", SPECIAL),
+    ("special", "f64", SPECIAL_MID),
+    ("special", "f64", SPECIAL_ALL),
+    ("special", "f64", dict(mean=0.0, std=1.0, p_nan=1.0)),
+    ("special", "f64", dict(mean=-3e38, std=1e38, p_inf=0.1)),
 ]
 SIZES = [1, 3, 4, 5, 8, 17, 1000, 4099, 65543, (1 << 20) + 3]
 
@@ -88,7 +94,8 @@ def test_synth_unaligned_outputs_and_guard(oracle, dist, dtype, params):
 @pytest.mark.parametrize("dist,dtype,params", [("normal", "f32", dict(mean=5.0, std=10.0)),
                                                ("special", "f32", SPECIAL), ("special", "f32", SPECIAL_MID),
                                                ("special", "bf16", SPECIAL), ("special", "bf16", SPECIAL_MID),
-                                               ("special", "f16", SPECIAL), ("special", "f16", SPECIAL_ALL)])
+                                               ("special", "f16", SPECIAL), ("special", "f16", SPECIAL_ALL),
+                                               ("special", "f64", SPECIAL), ("special", "f64", SPECIAL_MID)])
 def test_synth_far_window_with_64_bit_block_indices(oracle, dist, dtype, params):
     # a window past element 2^40: Philox block indices above 2^32, so the kernels index in 64 bits;
     # large enough for whole tiles and a ragged last one
@@ -142,12 +149,12 @@ def test_synth_full_size_sampled(oracle, dist, dtype, n, params):
 
 @pytest.mark.parametrize("dist,dtype,params", [("normal", "f32", dict(mean=0.0, std=1.0)),
                                                ("special", "f32", SPECIAL), ("special", "bf16", SPECIAL),
-                                               ("special", "f16", SPECIAL_MID)])
+                                               ("special", "f16", SPECIAL_MID), ("special", "f64", SPECIAL)])
 def test_synth_far_window_of_1_gib_sampled(oracle, dist, dtype, params):
-    # 1 GiB of values (2^28 + 5 fp32, 2^29 + 5 bf16 / fp16) past element 2^40: 64-bit block indices and
-    # the non-temporal stores of outputs of 1 GiB or more, together; sampled against the oracle element
-    # by element
-    n, off = (1 << 30) // (4 if dtype == "f32" else 2) + 5, (1 << 40) + 12
+    # 1 GiB of values (2^28 + 5 fp32, 2^29 + 5 bf16 / fp16, 2^27 + 5 fp64) past element 2^40: 64-bit
+    # block indices and the non-temporal stores of outputs of 1 GiB or more, together; sampled against
+    # the oracle element by element
+    n, off = (1 << 30) // {"f32": 4, "bf16": 2, "f16": 2, "f64": 8}[dtype] + 5, (1 << 40) + 12
     print("far window 1 GiB", dist, dtype, flush=True)
     g = empty(n, dtype)
     sv.synth_window(g, 3, 9, dist, off, **params)
@@ -181,7 +188,8 @@ def test_synth_batched_matches_single_calls_and_oracle(oracle):
     for (out, seed, stream, dist, params), (ref, *_rest) in zip(jobs, singles):
         assert np.array_equal(bits(out), bits(ref))
     for out, seed, stream, dist, params in jobs[:12] + jobs[-12:]:
-        dtype = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32", torch.float16: "f16"}[out.dtype]
+        dtype = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32", torch.float16: "f16",
+                 torch.float64: "f64"}[out.dtype]
         want = oracle.synth(seed, stream, dtype, dist, oracle.dist_params(**params), out.numel())
         assert np.array_equal(bits(out), want)
     # back-to-back batches reuse the job table: the second must not see the first's jobs
