@@ -108,6 +108,21 @@ def test_synth_far_window_with_64_bit_block_indices(oracle, dist, dtype, params)
     assert np.array_equal(got, want), _diff(got, want)
 
 
+@pytest.mark.parametrize("dist,dtype,params", [("normal", "f32", dict(mean=0.0, std=1.0)), ("uniform", "bf16", dict(a=-4.0, b=4.0)),
+                                               ("special", "f32", SPECIAL_MID), ("special", "bf16", SPECIAL),
+                                               ("special", "f16", SPECIAL_MID), ("special", "f64", SPECIAL)])
+def test_synth_window_across_block_2_to_the_32(oracle, dist, dtype, params):
+    # a window whose Philox block indices cross 2^32 (element 2^34) part way through: the kernels must
+    # take 64-bit indices for the whole launch; ragged at both ends of a tile
+    n, off = (1 << 20) + 3, (1 << 34) - (1 << 19) + 4
+    print("window across block 2^32", dist, dtype, flush=True)
+    g = empty(n, dtype)
+    sv.synth_window(g, 21, 22, dist, off, **params)
+    want = oracle.synth(21, 22, dtype, dist, oracle.dist_params(**params), n, off)
+    got = bits(g)
+    assert np.array_equal(got, want), _diff(got, want)
+
+
 def test_synth_is_deterministic_and_empty_ok():
     a, b = empty(1 << 20, "f32"), empty(1 << 20, "f32")
     sv.synth(a, 1, 2, "normal", mean=0.0, std=1.0)
