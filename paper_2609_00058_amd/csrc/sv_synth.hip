@@ -167,10 +167,32 @@ __device__ __forceinline__ uint32_t bf16_pair(uint32_t lo, uint32_t hi) {
     return bf16_rne(lo) | (bf16_rne(hi) << 16);
 }
 
+// The two 16-bit values (first in the low half) of the fp32 values lo, hi in
+// a narrow output type: the hardware conversions for values that cannot be
+// NaN (the normal values of vectors without candidates), the conversions with
+// the NaN rules for the rest.
+template <int DT>
+__device__ __forceinline__ uint32_t narrow_pair_not_nan(uint32_t lo, uint32_t hi) {
+  if constexpr (DT == SV_BF16) {
+    return bf16x2_rne_not_nan(lo, hi);
+  } else {
+    asm("" : "+v"(lo), "+v"(hi));   // keep the fp32 rounding of the values
+    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)as_f32(lo)) |
+           ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)as_f32(hi)) << 16);
+  }
+}
+template <int DT>
+__device__ __forceinline__ uint32_t narrow_pair(uint32_t lo, uint32_t hi) {
+  if constexpr (DT == SV_BF16) return bf16_rne(lo) | (bf16_rne(hi) << 16);
+  else return f16_rne(lo) | (f16_rne(hi) << 16);
+}
+
 template <int DIST, int DT>
 __device__ __forceinline__ void store_elem(void *out, uint64_t i, uint32_t x) {
   if constexpr (DT == SV_BF16)
     ((uint16_t *)out)[i] = (uint16_t)bf16_rne(x);
+  else if constexpr (DT == SV_F16)
+    ((uint16_t *)out)[i] = (uint16_t)f16_rne(x);
   else
     ((uint32_t *)out)[i] = x;
 }
@@ -188,7 +210,7 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
                                                            u32x4 *__restrict__ out, uint32_t rounds) {
   prepare_distribution<DIST>();
   constexpr int E = PerBlock<DIST, DT>::E;
-  constexpr int V = DT == SV_BF16 ? 8 : 4;   // elements per 16-byte vector
+  constexpr int V = DT == SV_BF16 || DT == SV_F16 ? 8 : 4;   // elements per 16-byte vector
   constexpr int B = V / E;                   // Philox blocks per vector
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
   const Idx gid = (Idx)blockIdx.x * kBlock + threadIdx.x;
@@ -206,6 +228,12 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
       o.y = bf16_pair<DIST>(v[2], v[3]);
       o.z = bf16_pair<DIST>(v[4], v[5]);
       o.w = bf16_pair<DIST>(v[6], v[7]);
+    } else if constexpr (DT == SV_F16) {
+      static_assert(DIST == SV_UNIFORM || DIST == SV_NORMAL, "fp16 values here are never NaN");
+      o.x = narrow_pair_not_nan<SV_F16>(v[0], v[1]);
+      o.y = narrow_pair_not_nan<SV_F16>(v[2], v[3]);
+      o.z = narrow_pair_not_nan<SV_F16>(v[4], v[5]);
+      o.w = narrow_pair_not_nan<SV_F16>(v[6], v[7]);
     } else {
       o = u32x4{v[0], v[1], v[2], v[3]};
     }
@@ -310,26 +338,6 @@ __device__ __forceinline__ u32x4 overlay_vector(const SpecialClasses &cls, uint3
   x.z = ((b >> 16) & 0xFFu) < gate ? special_or_keep(cls, q.z, x.z) : x.z;
   x.w = (b >> 24) < gate ? special_or_keep(cls, q.w, x.w) : x.w;
   return x;
-}
-
-// The two 16-bit values (first in the low half) of the fp32 values lo, hi in
-// a narrow output type: the hardware conversions for values that cannot be
-// NaN (the normal values of vectors without candidates), the conversions with
-// the NaN rules for the rest.
-template <int DT>
-__device__ __forceinline__ uint32_t narrow_pair_not_nan(uint32_t lo, uint32_t hi) {
-  if constexpr (DT == SV_BF16) {
-    return bf16x2_rne_not_nan(lo, hi);
-  } else {
-    asm("" : "+v"(lo), "+v"(hi));   // keep the fp32 rounding of the values
-    return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)as_f32(lo)) |
-           ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)as_f32(hi)) << 16);
-  }
-}
-template <int DT>
-__device__ __forceinline__ uint32_t narrow_pair(uint32_t lo, uint32_t hi) {
-  if constexpr (DT == SV_BF16) return bf16_rne(lo) | (bf16_rne(hi) << 16);
-  else return f16_rne(lo) | (f16_rne(hi) << 16);
 }
 
 // DT: fp32, bf16, fp16 or fp64 output.  The kernel works in units: one
@@ -521,7 +529,7 @@ __global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint6
 
 template <int DIST, int DT>
 static hipError_t launch_typed(const SynthParams &p0, uint64_t n, void *out, int cus, hipStream_t stream) {
-  constexpr uint64_t V = DT == SV_BF16 ? 8 : 4;
+  constexpr uint64_t V = DT == SV_BF16 || DT == SV_F16 ? 8 : 4;
   const SynthParams &p = p0;
   const bool nt = n * (16 / V) >= SV_SYNTH_NT_BYTES;
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
@@ -781,9 +789,9 @@ hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint6
     case SV_INT_RANGE * 8 + SV_I32: return launch_typed<SV_INT_RANGE, SV_I32>(p, n, out, cus, stream);
     case SV_SPECIAL * 8 + SV_F32: return launch_typed<SV_SPECIAL, SV_F32>(p, n, out, cus, stream);
     case SV_SPECIAL * 8 + SV_BF16: return launch_typed<SV_SPECIAL, SV_BF16>(p, n, out, cus, stream);
-    case SV_UNIFORM * 8 + SV_F16: return launch_wide<SV_UNIFORM, SV_F16>(p, n, out, cus, stream);
+    case SV_UNIFORM * 8 + SV_F16: return launch_typed<SV_UNIFORM, SV_F16>(p, n, out, cus, stream);
     case SV_UNIFORM * 8 + SV_F64: return launch_wide<SV_UNIFORM, SV_F64>(p, n, out, cus, stream);
-    case SV_NORMAL * 8 + SV_F16: return launch_wide<SV_NORMAL, SV_F16>(p, n, out, cus, stream);
+    case SV_NORMAL * 8 + SV_F16: return launch_typed<SV_NORMAL, SV_F16>(p, n, out, cus, stream);
     case SV_NORMAL * 8 + SV_F64: return launch_wide<SV_NORMAL, SV_F64>(p, n, out, cus, stream);
     case SV_SPECIAL * 8 + SV_F16: return launch_wide<SV_SPECIAL, SV_F16>(p, n, out, cus, stream);
     case SV_SPECIAL * 8 + SV_F64: return launch_wide<SV_SPECIAL, SV_F64>(p, n, out, cus, stream);

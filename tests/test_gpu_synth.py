@@ -47,6 +47,11 @@ CASES = [
     ("special", "f16", SPECIAL_ALL),
     ("special", "f16", dict(mean=0.0, std=1.0, p_inf=1.0)),
     ("special", "f16", dict(mean=0.0, std=1e5, p_denorm=0.02)),
+    # fp16 uniform and normal values: two blocks per 16-byte vector, hardware conversions
+    ("uniform", "f16", dict(a=-4.0, b=4.0)),
+    ("uniform", "f16", dict(a=60000.0, b=65504.0)),
+    ("normal", "f16", dict(mean=5.0, std=10.0)),
+    ("normal", "f16", dict(mean=0.0, std=3e4)),
     # fp64: one block per two 16-byte vectors, every value widened with the NaN rule
     ("special", "f64", SPECIAL),
     ("special", "f64", SPECIAL_MID),
@@ -95,7 +100,9 @@ def test_synth_unaligned_outputs_and_guard(oracle, dist, dtype, params):
                                                ("special", "f32", SPECIAL), ("special", "f32", SPECIAL_MID),
                                                ("special", "bf16", SPECIAL), ("special", "bf16", SPECIAL_MID),
                                                ("special", "f16", SPECIAL), ("special", "f16", SPECIAL_ALL),
-                                               ("special", "f64", SPECIAL), ("special", "f64", SPECIAL_MID)])
+                                               ("special", "f64", SPECIAL), ("special", "f64", SPECIAL_MID),
+                                               ("uniform", "f16", dict(a=-1.0, b=3.0)),
+                                               ("normal", "f16", dict(mean=1.0, std=2.0))])
 def test_synth_far_window_with_64_bit_block_indices(oracle, dist, dtype, params):
     # a window past element 2^40: Philox block indices above 2^32, so the kernels index in 64 bits;
     # large enough for whole tiles and a ragged last one
@@ -110,7 +117,9 @@ def test_synth_far_window_with_64_bit_block_indices(oracle, dist, dtype, params)
 
 @pytest.mark.parametrize("dist,dtype,params", [("normal", "f32", dict(mean=0.0, std=1.0)), ("uniform", "bf16", dict(a=-4.0, b=4.0)),
                                                ("special", "f32", SPECIAL_MID), ("special", "bf16", SPECIAL),
-                                               ("special", "f16", SPECIAL_MID), ("special", "f64", SPECIAL)])
+                                               ("special", "f16", SPECIAL_MID), ("special", "f64", SPECIAL),
+                                               ("uniform", "f16", dict(a=-4.0, b=4.0)),
+                                               ("normal", "f16", dict(mean=0.0, std=1.0))])
 def test_synth_window_across_block_2_to_the_32(oracle, dist, dtype, params):
     # a window whose Philox block indices cross 2^32 (element 2^34) part way through: the kernels must
     # take 64-bit indices for the whole launch; ragged at both ends of a tile
@@ -164,7 +173,8 @@ def test_synth_full_size_sampled(oracle, dist, dtype, n, params):
 
 @pytest.mark.parametrize("dist,dtype,params", [("normal", "f32", dict(mean=0.0, std=1.0)),
                                                ("special", "f32", SPECIAL), ("special", "bf16", SPECIAL),
-                                               ("special", "f16", SPECIAL_MID), ("special", "f64", SPECIAL)])
+                                               ("special", "f16", SPECIAL_MID), ("special", "f64", SPECIAL),
+                                               ("normal", "f16", dict(mean=0.0, std=1.0))])
 def test_synth_far_window_of_1_gib_sampled(oracle, dist, dtype, params):
     # 1 GiB of values (2^28 + 5 fp32, 2^29 + 5 bf16 / fp16, 2^27 + 5 fp64) past element 2^40: 64-bit
     # block indices and the non-temporal stores of outputs of 1 GiB or more, together; sampled against
