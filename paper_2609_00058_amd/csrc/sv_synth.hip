@@ -121,6 +121,7 @@ __device__ __forceinline__ void block_values(const SynthParams &p, uint64_t bloc
 // block; the others as DistTraits.
 template <int DIST, int DT> struct PerBlock { static constexpr int E = DistTraits<DIST>::E; };
 template <> struct PerBlock<SV_UNIFORM, SV_BF16> { static constexpr int E = 8; };
+template <> struct PerBlock<SV_INT_RANGE, SV_U8> { static constexpr int E = 4; };
 
 // The E = PerBlock<DIST, DT>::E values (fp32 bits or int32 bits) of Philox
 // block `block`.  bf16 uniform: element 2j + h of the block takes half h (low
@@ -134,6 +135,11 @@ __device__ __forceinline__ void values_of(const SynthParams &p, uint64_t block, 
       v[2 * j] = as_u32(p.a + p.span * ((float)(w[j] & 0xFFFFu) * 0x1p-16f));
       v[2 * j + 1] = as_u32(p.a + p.span * ((float)(w[j] >> 16) * 0x1p-16f));
     }
+  } else if constexpr (DIST == SV_INT_RANGE && DT == SV_U8) {
+    // uint8: a range of at most 256 values from one 32-bit word per element
+    const u32x4 w = philox_block(Key{p.k0, p.k1, p.s0, p.s1}, block);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = (uint32_t)p.lo + __umulhi(w[k], (uint32_t)p.range);
   } else {
     block_values<DIST>(p, block, v);
   }
@@ -193,6 +199,8 @@ __device__ __forceinline__ void store_elem(void *out, uint64_t i, uint32_t x) {
     ((uint16_t *)out)[i] = (uint16_t)bf16_rne(x);
   else if constexpr (DT == SV_F16)
     ((uint16_t *)out)[i] = (uint16_t)f16_rne(x);
+  else if constexpr (DT == SV_U8)
+    ((uint8_t *)out)[i] = (uint8_t)x;
   else
     ((uint32_t *)out)[i] = x;
 }
@@ -210,7 +218,7 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
                                                            u32x4 *__restrict__ out, uint32_t rounds) {
   prepare_distribution<DIST>();
   constexpr int E = PerBlock<DIST, DT>::E;
-  constexpr int V = DT == SV_BF16 || DT == SV_F16 ? 8 : 4;   // elements per 16-byte vector
+  constexpr int V = DT == SV_U8 ? 16 : DT == SV_BF16 || DT == SV_F16 ? 8 : 4;   // elements per 16-byte vector
   constexpr int B = V / E;                   // Philox blocks per vector
   using Idx = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
   const Idx gid = (Idx)blockIdx.x * kBlock + threadIdx.x;
@@ -234,6 +242,9 @@ __global__ __launch_bounds__(kBlock) void synth_vec_kernel(SynthParams p, uint64
       o.y = narrow_pair_not_nan<SV_F16>(v[2], v[3]);
       o.z = narrow_pair_not_nan<SV_F16>(v[4], v[5]);
       o.w = narrow_pair_not_nan<SV_F16>(v[6], v[7]);
+    } else if constexpr (DT == SV_U8) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = v[4 * k] | (v[4 * k + 1] << 8) | (v[4 * k + 2] << 16) | (v[4 * k + 3] << 24);
     } else {
       o = u32x4{v[0], v[1], v[2], v[3]};
     }
@@ -529,7 +540,7 @@ __global__ __launch_bounds__(kBlock) void synth_elem_kernel(SynthParams p, uint6
 
 template <int DIST, int DT>
 static hipError_t launch_typed(const SynthParams &p0, uint64_t n, void *out, int cus, hipStream_t stream) {
-  constexpr uint64_t V = DT == SV_BF16 || DT == SV_F16 ? 8 : 4;
+  constexpr uint64_t V = DT == SV_U8 ? 16 : DT == SV_BF16 || DT == SV_F16 ? 8 : 4;
   const SynthParams &p = p0;
   const bool nt = n * (16 / V) >= SV_SYNTH_NT_BYTES;
   const uint64_t max_blocks = (uint64_t)cus * SV_SYNTH_BLOCKS_PER_CU;
@@ -795,7 +806,7 @@ hipError_t launch_synth(int32_t dtype, int32_t dist, const SynthParams &p, uint6
     case SV_NORMAL * 8 + SV_F64: return launch_wide<SV_NORMAL, SV_F64>(p, n, out, cus, stream);
     case SV_SPECIAL * 8 + SV_F16: return launch_wide<SV_SPECIAL, SV_F16>(p, n, out, cus, stream);
     case SV_SPECIAL * 8 + SV_F64: return launch_wide<SV_SPECIAL, SV_F64>(p, n, out, cus, stream);
-    case SV_INT_RANGE * 8 + SV_U8: return launch_wide<SV_INT_RANGE, SV_U8>(p, n, out, cus, stream);
+    case SV_INT_RANGE * 8 + SV_U8: return launch_typed<SV_INT_RANGE, SV_U8>(p, n, out, cus, stream);
     case SV_INT_RANGE * 8 + SV_I64: return launch_wide<SV_INT_RANGE, SV_I64>(p, n, out, cus, stream);
     case SV_PERMUTATION * 8 + SV_I32: return launch_perm<SV_I32>(p, n, out, cus, stream);
     case SV_PERMUTATION * 8 + SV_U8: return launch_perm<SV_U8>(p, n, out, cus, stream);

@@ -52,6 +52,10 @@ CASES = [
     ("uniform", "f16", dict(a=60000.0, b=65504.0)),
     ("normal", "f16", dict(mean=5.0, std=10.0)),
     ("normal", "f16", dict(mean=0.0, std=3e4)),
+    # uint8: four blocks per 16-byte vector, one 32-bit word per element
+    ("int_range", "u8", dict(lo=0, hi=255)),
+    ("int_range", "u8", dict(lo=3, hi=202)),
+    ("int_range", "u8", dict(lo=7, hi=7)),
     # fp64: one block per two 16-byte vectors, every value widened with the NaN rule
     ("special", "f64", SPECIAL),
     ("special", "f64", SPECIAL_MID),
@@ -102,7 +106,8 @@ def test_synth_unaligned_outputs_and_guard(oracle, dist, dtype, params):
                                                ("special", "f16", SPECIAL), ("special", "f16", SPECIAL_ALL),
                                                ("special", "f64", SPECIAL), ("special", "f64", SPECIAL_MID),
                                                ("uniform", "f16", dict(a=-1.0, b=3.0)),
-                                               ("normal", "f16", dict(mean=1.0, std=2.0))])
+                                               ("normal", "f16", dict(mean=1.0, std=2.0)),
+                                               ("int_range", "u8", dict(lo=10, hi=250))])
 def test_synth_far_window_with_64_bit_block_indices(oracle, dist, dtype, params):
     # a window past element 2^40: Philox block indices above 2^32, so the kernels index in 64 bits;
     # large enough for whole tiles and a ragged last one
@@ -119,7 +124,8 @@ def test_synth_far_window_with_64_bit_block_indices(oracle, dist, dtype, params)
                                                ("special", "f32", SPECIAL_MID), ("special", "bf16", SPECIAL),
                                                ("special", "f16", SPECIAL_MID), ("special", "f64", SPECIAL),
                                                ("uniform", "f16", dict(a=-4.0, b=4.0)),
-                                               ("normal", "f16", dict(mean=0.0, std=1.0))])
+                                               ("normal", "f16", dict(mean=0.0, std=1.0)),
+                                               ("int_range", "u8", dict(lo=0, hi=99))])
 def test_synth_window_across_block_2_to_the_32(oracle, dist, dtype, params):
     # a window whose Philox block indices cross 2^32 (element 2^34) part way through: the kernels must
     # take 64-bit indices for the whole launch; ragged at both ends of a tile
@@ -214,7 +220,7 @@ def test_synth_batched_matches_single_calls_and_oracle(oracle):
         assert np.array_equal(bits(out), bits(ref))
     for out, seed, stream, dist, params in jobs[:12] + jobs[-12:]:
         dtype = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32", torch.float16: "f16",
-                 torch.float64: "f64"}[out.dtype]
+                 torch.float64: "f64", torch.uint8: "u8"}[out.dtype]
         want = oracle.synth(seed, stream, dtype, dist, oracle.dist_params(**params), out.numel())
         assert np.array_equal(bits(out), want)
     # back-to-back batches reuse the job table: the second must not see the first's jobs
